@@ -1,0 +1,255 @@
+"""CPU oracle for the iterative NUTS hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It wraps ``nuts_oracle.c`` (plain C,
+fp64, sequential sums, no fused multiply-adds) with ctypes and adds the
+numpy-side statistics (ESS, MCSE) in ``oracle.ess``.  It shares no code with
+the HIP library and the library never imports it.
+
+What each function follows is stated in ``nuts_oracle.c``: Appendix A
+(Alg. 1 recursive BuildTree, Alg. 2 IterativeBuildTree) and Appendix B (the
+logistic-regression model) of arXiv 1912.11554, Hoffman & Gelman (2014)
+Alg. 6, Betancourt (2017) App. A, Salmon et al. (2011) for Philox.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "nuts_oracle.c")
+# NUTS_ORACLE_LIB lets a test run load a deliberately broken copy (mutation checks).
+_LIB = os.environ.get("NUTS_ORACLE_LIB", os.path.join(_HERE, "liboracle.so"))
+
+# Per-sample statistics; same layout as the library's nuts_stats record.
+STATS_DTYPE = np.dtype(
+    [
+        ("potential_energy", "<f8"),
+        ("energy", "<f8"),
+        ("accept_prob", "<f8"),
+        ("tree_depth", "<i4"),
+        ("num_steps", "<i4"),
+        ("proposal_index", "<i4"),
+        ("term_leaf", "<i4"),
+        ("direction_bits", "<u4"),
+        ("diverging", "u1"),
+        ("turning", "u1"),
+        ("hit_max_depth", "u1"),
+        ("_pad", "u1", (9,)),
+    ]
+)
+assert STATS_DTYPE.itemsize == 56
+
+TARGET_LOGISTIC = 0
+TARGET_LINGAUSS = 1
+BUILDER_ITERATIVE = 0
+BUILDER_RECURSIVE = 1
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain C, -ffp-contract=off)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+             "-Wall", "-o", tmp, _SRC, "-lm"]
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i64, u64, dbl, i32 = ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_int
+        L.orc_philox4x64_10.argtypes = [P, P, P]
+        L.orc_u53.argtypes = [u64]
+        L.orc_u53.restype = dbl
+        L.orc_normals.argtypes = [u64, u64, u64, i64, P]
+        L.orc_direction.argtypes = [u64, u64, u64, u64]
+        L.orc_direction.restype = i32
+        L.orc_u_merge.argtypes = [u64, u64, u64, u64]
+        L.orc_u_merge.restype = dbl
+        L.orc_u_leaf.argtypes = [u64, u64, u64, u64, u64]
+        L.orc_u_leaf.restype = dbl
+        L.orc_logistic_ug.argtypes = [P, P, i64, i64, dbl, P, P]
+        L.orc_logistic_ug.restype = dbl
+        L.orc_logistic_ug_f32.argtypes = [P, P, i64, i64, dbl, P, P]
+        L.orc_logistic_ug_f32.restype = dbl
+        L.orc_lingauss_ug.argtypes = [P, P, i64, i64, dbl, dbl, P, P]
+        L.orc_lingauss_ug.restype = dbl
+        L.orc_bitcount.argtypes = [u64]
+        L.orc_bitcount.restype = i32
+        L.orc_trailing_ones.argtypes = [u64]
+        L.orc_trailing_ones.restype = i32
+        L.orc_check_range.argtypes = [u64, P, P]
+        L.orc_nuts_chain.argtypes = [
+            i32, P, P, P, i64, i64, dbl, dbl, dbl, P, i32, i64, i64, u64, u64, i32, i32, P,
+            i64, P, P, P, P, P, i64, P, P, i64, P, u64,
+        ]
+        L.orc_nuts_chain.restype = i64
+        L.orc_leapfrog_steps.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, dbl, i64, P, P]
+        L.orc_leapfrog_steps.restype = dbl
+        L.orc_is_uturn_exported.argtypes = [P, P, P, P, i32, P, i64]
+        L.orc_is_uturn_exported.restype = i32
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _u8(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.uint8)
+
+
+# ---------------------------------------------------------------- RNG ------
+def philox4x64_10(counter, key):
+    c = np.ascontiguousarray(counter, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib().orc_philox4x64_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def u53(word: int) -> float:
+    return lib().orc_u53(int(word))
+
+
+def normals(seed, chain, t, D):
+    out = np.zeros(D, dtype=np.float64)
+    lib().orc_normals(seed, chain, t, D, _p(out))
+    return out
+
+
+def direction(seed, chain, t, j):
+    return lib().orc_direction(seed, chain, t, j)
+
+
+def u_merge(seed, chain, t, j):
+    return lib().orc_u_merge(seed, chain, t, j)
+
+
+def u_leaf(seed, chain, t, j, n):
+    return lib().orc_u_leaf(seed, chain, t, j, n)
+
+
+# ------------------------------------------------------------ targets ------
+def logistic_potential_grad(X, y, w, prior_scale=1.0):
+    """U(w) and dU/dw of the logistic log-joint (Appendix B model), fp64."""
+    X = _f64(X)
+    y = _u8(y)
+    w = _f64(w)
+    N, D = X.shape
+    g = np.zeros(D, dtype=np.float64)
+    U = lib().orc_logistic_ug(_p(X), _p(y), N, D, prior_scale, _p(w), _p(g))
+    return U, g
+
+
+def logistic_potential_grad_f32(Xf, y, w, prior_scale=1.0):
+    """Same values over an fp32 X, promoted to fp64 one row at a time."""
+    Xf = np.ascontiguousarray(Xf, dtype=np.float32)
+    y = _u8(y)
+    w = _f64(w)
+    N, D = Xf.shape
+    g = np.zeros(D, dtype=np.float64)
+    U = lib().orc_logistic_ug_f32(_p(Xf), _p(y), N, D, prior_scale, _p(w), _p(g))
+    return U, g
+
+
+def lingauss_potential_grad(X, yv, w, prior_scale=1.0, noise_scale=1.0):
+    X = _f64(X)
+    yv = _f64(yv)
+    w = _f64(w)
+    N, D = X.shape
+    g = np.zeros(D, dtype=np.float64)
+    U = lib().orc_lingauss_ug(_p(X), _p(yv), N, D, prior_scale, noise_scale, _p(w), _p(g))
+    return U, g
+
+
+# ------------------------------------------------------ index logic --------
+def bitcount(n):
+    return lib().orc_bitcount(n)
+
+
+def trailing_ones(n):
+    return lib().orc_trailing_ones(n)
+
+
+def check_range(n):
+    a = ctypes.c_int()
+    b = ctypes.c_int()
+    lib().orc_check_range(n, ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value
+
+
+# ---------------------------------------------------------- sampler --------
+def leapfrog(X, y, q, p, h, nsteps, inv_mass=None, prior_scale=1.0, target=TARGET_LOGISTIC,
+             yv=None, noise_scale=1.0):
+    X = _f64(X)
+    N, D = X.shape
+    q = _f64(q).copy()
+    p = _f64(p).copy()
+    im = _f64(np.ones(D) if inv_mass is None else inv_mass)
+    U = lib().orc_leapfrog_steps(target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale,
+                                 noise_scale, _p(im), h, nsteps, _p(q), _p(p))
+    return q, p, U
+
+
+def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chain=0,
+         prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
+         init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
+         trace_cap=0, leaves_cap=0, sel_salt=0):
+    """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
+    final_q [D], inv_mass [D], grad_evals; with trace_cap the U-turn check
+    trace as (first_leaf, last_leaf) pairs; with leaves_cap the generated
+    leaves as records (j, n, position, H - H0).  ``sel_salt`` (test only)
+    re-keys the proposal-selection draws and nothing else."""
+    X = _f64(X)
+    N, D = X.shape
+    samples = np.zeros((num_samples, D), dtype=np.float64)
+    stats = np.zeros(num_samples, dtype=STATS_DTYPE)
+    final_q = np.zeros(D, dtype=np.float64)
+    out_im = np.zeros(D, dtype=np.float64)
+    tr = np.zeros(max(2 * trace_cap, 1), dtype=np.int64)
+    trlen = ctypes.c_int64(0)
+    lv = np.zeros(max(4 * leaves_cap, 1), dtype=np.int64)
+    lvlen = ctypes.c_int64(0)
+    nev = lib().orc_nuts_chain(
+        target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale, noise_scale, step_size,
+        _p(_f64(inv_mass)), max_tree_depth, num_warmup, num_samples, seed, chain, builder,
+        1 if adapt_diag_mass else 0, _p(_f64(init_q)), first_iter, _p(samples), _p(stats),
+        _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
+        ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
+        ctypes.byref(lvlen), sel_salt,
+    )
+    out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im, grad_evals=nev)
+    if trace_cap:
+        out["trace"] = tr[: trlen.value].reshape(-1, 2)
+    if leaves_cap:
+        rec = lv[: lvlen.value].reshape(-1, 4)
+        out["leaves"] = dict(j=rec[:, 0].copy(), n=rec[:, 1].copy(), pos=rec[:, 2].copy(),
+                             dH=rec[:, 3].copy().view(np.float64))
+    return out
+
+
+def is_uturn(qa, pa, qb, pb, v, inv_mass=None):
+    qa, pa, qb, pb = (_f64(a) for a in (qa, pa, qb, pb))
+    D = qa.shape[0]
+    im = _f64(np.ones(D) if inv_mass is None else inv_mass)
+    return bool(lib().orc_is_uturn_exported(_p(qa), _p(pa), _p(qb), _p(pb), v, _p(im), D))

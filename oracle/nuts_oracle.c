@@ -1,0 +1,730 @@
+/*
+ * CPU oracle for the iterative No-U-Turn sampler on the Bayesian
+ * logistic-regression log-joint.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, plain, obviously correct
+ * reference that the GPU path is checked against.  Only the test suite, the
+ * package smoke check and the benchmark's CPU-baseline leg may load it.  It
+ * shares no source with the HIP library (no headers, no helpers, no tables)
+ * and the library never calls it.
+ *
+ * Everything is fp64, summed sequentially in index order, built with
+ * -ffp-contract=off so that no fused multiply-adds change the rounding.
+ *
+ * Sources restated here (no listing is copied):
+ *   - Phan, Pradhan, Jankowiak, "Composable Effects for Flexible and
+ *     Accelerated Probabilistic Programming in NumPyro" (arXiv 1912.11554):
+ *       Appendix B / Fig. 1a   the logistic-regression model,
+ *       Section 3.1            why the tree builder must be iterative,
+ *       Appendix A, Alg. 1     recursive BuildTree,
+ *       Appendix A, Alg. 2     IterativeBuildTree, the S array indexed by
+ *                              BitCount and the candidate set C(n).
+ *   - Hoffman & Gelman, "The No-U-Turn Sampler" (JMLR 2014), Alg. 6:
+ *       U-turn criterion on the endpoints, random direction per doubling,
+ *       divergence threshold Delta_max = 1000.
+ *   - Betancourt, "A Conceptual Introduction to Hamiltonian Monte Carlo"
+ *     (arXiv 1701.02434), App. A: multinomial trajectory sampling, biased
+ *     progressive sampling across doublings.
+ *   - Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2,
+ *     3" (SC'11): Philox4x64 with 10 rounds.
+ *   - Box & Muller (1958) for normal variates.
+ *
+ * Readings taken where the paper is silent (its Alg. 1/2 omit the proposal,
+ * the direction and the step size):
+ *   R1  TrailingBit(n) counts the trailing 1 bits of n (so C(11) = {10, 8}).
+ *   R2  the check loop of Alg. 2 runs from i_max DOWN to i_min; S has
+ *       max(d, 1) slots.
+ *   R3  IsUTurn is Hoffman & Gelman's endpoint test on time-ordered ends,
+ *       with velocities M^-1 p; a dot product of exactly 0 is not a U-turn.
+ *   R4  multinomial weights exp(-H): streaming selection inside a subtree,
+ *       biased progressive selection when a subtree is merged.
+ *   R5  direction uniform on {-1, +1} per doubling; fixed step size.
+ *   R6  a leaf diverges iff !(H - H0 <= 1000); that also catches NaN.
+ *   R8  Philox4x64-10, key (seed, chain), counter (t, tag<<32 | j, n, 0).
+ *   R13 optional diagonal inverse mass from warmup variance, normalised to
+ *       mean one.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x64-10 (Salmon et al. 2011).  Round: two 64x64->128 products of the
+ * even words with the round multipliers; the odd words and the key are xored
+ * into the high halves and the words are permuted.  The key is bumped by the
+ * two Weyl constants between rounds.                                         */
+
+#define ORC_PHILOX_M0 0xD2E7470EE14C6C93ULL
+#define ORC_PHILOX_M1 0xCA5A826395121157ULL
+#define ORC_PHILOX_W0 0x9E3779B97F4A7C15ULL
+#define ORC_PHILOX_W1 0xBB67AE8584CAA73BULL
+
+static void orc_mul128(uint64_t a, uint64_t b, uint64_t *hi, uint64_t *lo)
+{
+    unsigned __int128 p = (unsigned __int128)a * (unsigned __int128)b;
+    *hi = (uint64_t)(p >> 64);
+    *lo = (uint64_t)p;
+}
+
+void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4])
+{
+    uint64_t x0 = ctr_in[0], x1 = ctr_in[1], x2 = ctr_in[2], x3 = ctr_in[3];
+    uint64_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += ORC_PHILOX_W0;
+            k1 += ORC_PHILOX_W1;
+        }
+        uint64_t hi0, lo0, hi1, lo1;
+        orc_mul128(ORC_PHILOX_M0, x0, &hi0, &lo0);
+        orc_mul128(ORC_PHILOX_M1, x2, &hi1, &lo1);
+        uint64_t y0 = hi1 ^ x1 ^ k0;
+        uint64_t y1 = lo1;
+        uint64_t y2 = hi0 ^ x3 ^ k1;
+        uint64_t y3 = lo0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* Draw tags: which random quantity a Philox block feeds (reading R8). */
+enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4 };
+
+static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, uint64_t j,
+                      uint64_t n, uint64_t out[4])
+{
+    uint64_t ctr[4] = { t, (tag << 32) | j, n, 0 };
+    uint64_t key[2] = { seed, chain };
+    orc_philox4x64_10(ctr, key, out);
+}
+
+/* 53 high bits of a word -> uniform on [0, 1). */
+double orc_u53(uint64_t w) { return (double)(w >> 11) * (1.0 / 9007199254740992.0); }
+
+/* D standard normals for the momentum of iteration t: block b gives four
+ * uniforms, i.e. two Box-Muller pairs, i.e. normals 4b .. 4b+3. */
+void orc_normals(uint64_t seed, uint64_t chain, uint64_t t, int64_t D, double *out)
+{
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int64_t b = 0; 4 * b < D; ++b) {
+        uint64_t w[4];
+        orc_block(seed, chain, t, ORC_TAG_MOMENTUM, 0, (uint64_t)b, w);
+        for (int pair = 0; pair < 2; ++pair) {
+            double ua = orc_u53(w[2 * pair]);
+            double ub = orc_u53(w[2 * pair + 1]);
+            double r = sqrt(-2.0 * log(1.0 - ua));
+            double th = two_pi * ub;
+            int64_t i0 = 4 * b + 2 * pair;
+            if (i0 < D) out[i0] = r * cos(th);
+            if (i0 + 1 < D) out[i0 + 1] = r * sin(th);
+        }
+    }
+}
+
+/* +1 or -1 for doubling j of iteration t. */
+int orc_direction(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j)
+{
+    uint64_t w[4];
+    orc_block(seed, chain, t, ORC_TAG_DIR, j, 0, w);
+    return (w[0] & 1ULL) ? +1 : -1;
+}
+
+double orc_u_merge(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j)
+{
+    uint64_t w[4];
+    orc_block(seed, chain, t, ORC_TAG_MERGE, j, 0, w);
+    return orc_u53(w[0]);
+}
+
+double orc_u_leaf(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_t n)
+{
+    uint64_t w[4];
+    orc_block(seed, chain, t, ORC_TAG_LEAF, j, n, w);
+    return orc_u53(w[0]);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Targets: U(w) = -log joint and its gradient.                              */
+
+/* Bayesian logistic regression (Appendix B): weights m ~ N(0, 1) per feature,
+ * intercept b ~ N(0, 1), y_i ~ Bernoulli(logits = x_i . m + b).  The intercept
+ * is the last (or any) column of ones in X, sharing the N(0, s^2) prior, so
+ *   U(w)  = sum_i [softplus(eta_i) - y_i eta_i] + sum_j w_j^2 / (2 s^2)
+ *           + D (ln s + ln(2 pi) / 2),           eta = X w,
+ *   dU/dw = X^T (sigmoid(eta) - y) + w / s^2.
+ * Each row term is written as softplus((1 - 2 y_i) eta_i) >= 0 and the
+ * residual as (1 - 2 y_i) sigmoid((1 - 2 y_i) eta_i), which are the same
+ * numbers without cancellation.                                              */
+static double orc_softplus(double x) { return fmax(x, 0.0) + log1p(exp(-fabs(x))); }
+
+static double orc_sigmoid(double x)
+{
+    if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+    double e = exp(x);
+    return e / (1.0 + e);
+}
+
+double orc_logistic_ug(const double *X, const uint8_t *y, int64_t N, int64_t D, double s,
+                       const double *w, double *grad)
+{
+    for (int64_t j = 0; j < D; ++j) grad[j] = 0.0;
+    double U = 0.0;
+    for (int64_t i = 0; i < N; ++i) {
+        const double *xi = X + i * D;
+        double eta = 0.0;
+        for (int64_t j = 0; j < D; ++j) eta += xi[j] * w[j];
+        double sgn = y[i] ? -1.0 : 1.0;
+        double t = sgn * eta;
+        U += orc_softplus(t);
+        double r = sgn * orc_sigmoid(t);
+        for (int64_t j = 0; j < D; ++j) grad[j] += r * xi[j];
+    }
+    const double half_log_2pi = 0.91893853320467274178032973640562;
+    double inv_s2 = 1.0 / (s * s);
+    for (int64_t j = 0; j < D; ++j) {
+        U += 0.5 * w[j] * w[j] * inv_s2;
+        grad[j] += w[j] * inv_s2;
+    }
+    U += (double)D * (log(s) + half_log_2pi);
+    return U;
+}
+
+/* Conjugate linear-Gaussian target used to pin the sampler's statistics:
+ *   U(w) = sum_i (y_i - x_i . w)^2 / (2 sn^2) + sum_j w_j^2 / (2 s^2) + const,
+ * whose posterior is N(mu, Sigma), Sigma = (X^T X / sn^2 + I / s^2)^-1,
+ * mu = Sigma X^T y / sn^2.                                                   */
+double orc_lingauss_ug(const double *X, const double *yv, int64_t N, int64_t D, double s,
+                       double sn, const double *w, double *grad)
+{
+    for (int64_t j = 0; j < D; ++j) grad[j] = 0.0;
+    double U = 0.0, inv_n2 = 1.0 / (sn * sn), inv_s2 = 1.0 / (s * s);
+    for (int64_t i = 0; i < N; ++i) {
+        const double *xi = X + i * D;
+        double eta = 0.0;
+        for (int64_t j = 0; j < D; ++j) eta += xi[j] * w[j];
+        double res = yv[i] - eta;
+        U += 0.5 * res * res * inv_n2;
+        for (int64_t j = 0; j < D; ++j) grad[j] -= res * inv_n2 * xi[j];
+    }
+    for (int64_t j = 0; j < D; ++j) {
+        U += 0.5 * w[j] * w[j] * inv_s2;
+        grad[j] += w[j] * inv_s2;
+    }
+    return U;
+}
+
+enum { ORC_TARGET_LOGISTIC = 0, ORC_TARGET_LINGAUSS = 1 };
+
+typedef struct {
+    int kind;
+    const double *X;      /* N x D row-major */
+    const uint8_t *y;     /* logistic labels */
+    const double *yv;     /* linear-Gaussian responses */
+    int64_t N, D;
+    double s;             /* prior scale */
+    double sn;            /* noise scale (linear-Gaussian) */
+    int64_t nevals;       /* gradient evaluations performed */
+} orc_target;
+
+static double orc_eval(orc_target *tg, const double *w, double *grad)
+{
+    tg->nevals++;
+    if (tg->kind == ORC_TARGET_LINGAUSS)
+        return orc_lingauss_ug(tg->X, tg->yv, tg->N, tg->D, tg->s, tg->sn, w, grad);
+    return orc_logistic_ug(tg->X, tg->y, tg->N, tg->D, tg->s, w, grad);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Index arithmetic of Alg. 2.                                               */
+
+int orc_bitcount(uint64_t n)
+{
+    int c = 0;
+    while (n) { c += (int)(n & 1ULL); n >>= 1; }
+    return c;
+}
+
+int orc_trailing_ones(uint64_t n)
+{
+    int c = 0;
+    while (n & 1ULL) { ++c; n >>= 1; }
+    return c;
+}
+
+/* For odd n: the S slots holding the first leaves of every balanced subtree
+ * that ends at leaf n are i_max = BitCount(n-1) down to
+ * i_min = i_max - TrailingBit(n) + 1. */
+void orc_check_range(uint64_t n, int *i_max, int *i_min)
+{
+    int l = orc_trailing_ones(n);
+    *i_max = orc_bitcount(n - 1);
+    *i_min = *i_max - l + 1;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Phase-space nodes and the leapfrog integrator.                            */
+
+typedef struct {
+    double *q, *p, *g;
+    double U;
+} orc_node;
+
+static void orc_node_alloc(orc_node *z, int64_t D)
+{
+    z->q = (double *)calloc((size_t)D, sizeof(double));
+    z->p = (double *)calloc((size_t)D, sizeof(double));
+    z->g = (double *)calloc((size_t)D, sizeof(double));
+    z->U = 0.0;
+}
+
+static void orc_node_free(orc_node *z) { free(z->q); free(z->p); free(z->g); }
+
+static void orc_node_copy(orc_node *dst, const orc_node *src, int64_t D)
+{
+    memcpy(dst->q, src->q, (size_t)D * sizeof(double));
+    memcpy(dst->p, src->p, (size_t)D * sizeof(double));
+    memcpy(dst->g, src->g, (size_t)D * sizeof(double));
+    dst->U = src->U;
+}
+
+static double orc_kinetic(const double *p, const double *inv_mass, int64_t D)
+{
+    double k = 0.0;
+    for (int64_t j = 0; j < D; ++j) k += inv_mass[j] * p[j] * p[j];
+    return 0.5 * k;
+}
+
+/* Kick-drift-kick with the gradient carried in the node: one gradient
+ * evaluation per step (the form the paper's LeapFrog calls through grad). */
+static void orc_leapfrog(orc_target *tg, orc_node *z, double h, const double *inv_mass)
+{
+    int64_t D = tg->D;
+    for (int64_t j = 0; j < D; ++j) z->p[j] = z->p[j] - 0.5 * h * z->g[j];
+    for (int64_t j = 0; j < D; ++j) z->q[j] = z->q[j] + h * inv_mass[j] * z->p[j];
+    z->U = orc_eval(tg, z->q, z->g);
+    for (int64_t j = 0; j < D; ++j) z->p[j] = z->p[j] - 0.5 * h * z->g[j];
+}
+
+/* Hoffman & Gelman's endpoint criterion on time-ordered ends: a subtree whose
+ * first-generated node is a and last-generated node is b, built in direction
+ * v, has left end a and right end b if v > 0, else the reverse. */
+static int orc_is_uturn(const double *qa, const double *pa, const double *qb, const double *pb,
+                        int v, const double *inv_mass, int64_t D)
+{
+    const double *qL = v > 0 ? qa : qb, *pL = v > 0 ? pa : pb;
+    const double *qR = v > 0 ? qb : qa, *pR = v > 0 ? pb : pa;
+    double dl = 0.0, dr = 0.0;
+    for (int64_t j = 0; j < D; ++j) {
+        double dq = qR[j] - qL[j];
+        dl += dq * inv_mass[j] * pL[j];
+        dr += dq * inv_mass[j] * pR[j];
+    }
+    return (dl < 0.0) || (dr < 0.0);
+}
+
+int orc_is_uturn_exported(const double *qa, const double *pa, const double *qb, const double *pb,
+                          int v, const double *inv_mass, int64_t D)
+{
+    return orc_is_uturn(qa, pa, qb, pb, v, inv_mass, D);
+}
+
+static double orc_logaddexp(double a, double b)
+{
+    if (a == -INFINITY) return b;
+    if (b == -INFINITY) return a;
+    double m = fmax(a, b);
+    return m + log1p(exp(-fabs(a - b)));
+}
+
+/* ------------------------------------------------------------------------- */
+/* Tree building.                                                            */
+
+enum { ORC_OK = 0, ORC_TURNING = 1, ORC_DIVERGENT = 2 };
+
+/* Everything one iteration shares between the doubling loop and the two tree
+ * builders. */
+typedef struct {
+    orc_target *tg;
+    const double *inv_mass;
+    double eps;
+    uint64_t seed, chain, t;
+    double H0;
+    /* optional trace of U-turn checks inside subtrees: pairs (first, last) of
+     * leaf indices within the current subtree, in the order performed */
+    int64_t *trace;
+    int64_t trace_cap, trace_len;
+    /* optional trace of generated leaves: (doubling j, leaf n, signed
+     * position, H - H0 as raw bits) per leaf */
+    int64_t *leaves;
+    int64_t leaves_cap, leaves_len;
+    /* xored into the seed for the selection draws only (0 = the standard
+     * protocol); lets a test re-draw the choices over a fixed trajectory */
+    uint64_t sel_salt;
+    /* per-iteration totals */
+    int64_t nleaves;
+    double sum_accept;
+} orc_iter;
+
+/* What a subtree hands back: the streaming proposal and its log-weight. */
+typedef struct {
+    int status;
+    int64_t term_leaf;
+    double logw;          /* log of the summed exp(-(H - H0)) over the subtree */
+    orc_node prop;
+    int64_t prop_idx;     /* signed leaf offset of the proposal from q0 */
+    int has_prop;
+} orc_sub;
+
+static void orc_trace_check(orc_iter *it, int64_t first, int64_t last)
+{
+    if (it->trace && it->trace_len + 2 <= it->trace_cap) {
+        it->trace[it->trace_len++] = first;
+        it->trace[it->trace_len++] = last;
+    }
+}
+
+/* Energy bookkeeping and the streaming multinomial choice for the leaf that
+ * was just generated (leaf n of subtree j, whose start node sits at signed
+ * offset e and which grows in direction v).  Returns ORC_DIVERGENT or ORC_OK. */
+static int orc_leaf(orc_iter *it, orc_sub *sub, const orc_node *z, int j, int64_t n,
+                    int64_t e, int v)
+{
+    int64_t D = it->tg->D;
+    double H = z->U + orc_kinetic(z->p, it->inv_mass, D);
+    double dH = H - it->H0;
+    if (it->leaves && it->leaves_len + 4 <= it->leaves_cap) {
+        int64_t bits;
+        memcpy(&bits, &dH, sizeof(bits));
+        it->leaves[it->leaves_len++] = j;
+        it->leaves[it->leaves_len++] = n;
+        it->leaves[it->leaves_len++] = e + (int64_t)v * (n + 1);
+        it->leaves[it->leaves_len++] = bits;
+    }
+    it->nleaves++;
+    if (dH == dH) it->sum_accept += (dH > 0.0) ? exp(-dH) : 1.0;
+    if (!(dH <= 1000.0)) {
+        sub->status = ORC_DIVERGENT;
+        sub->term_leaf = n;
+        return ORC_DIVERGENT;
+    }
+    double lam = -dH;
+    double logw_new = orc_logaddexp(sub->logw, lam);
+    double u = orc_u_leaf(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j, (uint64_t)n);
+    if (u < exp(lam - logw_new)) {
+        orc_node_copy(&sub->prop, z, D);
+        sub->prop_idx = e + (int64_t)v * (n + 1);
+        sub->has_prop = 1;
+    }
+    sub->logw = logw_new;
+    return ORC_OK;
+}
+
+/* Alg. 2 (IterativeBuildTree): 2^j leapfrog steps from z in direction v.
+ * Even leaves are kept in S[BitCount(n)]; at odd leaves the U-turn test runs
+ * against the slots named by orc_check_range.  On return z holds the last
+ * leaf generated. */
+static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t e,
+                                orc_sub *sub)
+{
+    int64_t D = it->tg->D;
+    int nslots = j > 0 ? j : 1;
+    double *Sq = (double *)malloc((size_t)nslots * (size_t)D * sizeof(double));
+    double *Sp = (double *)malloc((size_t)nslots * (size_t)D * sizeof(double));
+    int64_t S_leaf[64];
+    int64_t nleaf = (int64_t)1 << j;
+    for (int64_t n = 0; n < nleaf; ++n) {
+        orc_leapfrog(it->tg, z, (double)v * it->eps, it->inv_mass);
+        if (orc_leaf(it, sub, z, j, n, e, v) != ORC_OK) break;
+        if ((n & 1) == 0) {
+            int i = orc_bitcount((uint64_t)n);
+            memcpy(Sq + (int64_t)i * D, z->q, (size_t)D * sizeof(double));
+            memcpy(Sp + (int64_t)i * D, z->p, (size_t)D * sizeof(double));
+            S_leaf[i] = n;
+        } else {
+            int i_max, i_min;
+            orc_check_range((uint64_t)n, &i_max, &i_min);
+            int turned = 0;
+            for (int k = i_max; k >= i_min; --k) {
+                orc_trace_check(it, S_leaf[k], n);
+                if (orc_is_uturn(Sq + (int64_t)k * D, Sp + (int64_t)k * D, z->q, z->p, v,
+                                 it->inv_mass, D)) {
+                    turned = 1;
+                    break;
+                }
+            }
+            if (turned) {
+                sub->status = ORC_TURNING;
+                sub->term_leaf = n;
+                break;
+            }
+        }
+    }
+    free(Sq);
+    free(Sp);
+}
+
+/* Alg. 1 (BuildTree), recursive: a depth-d subtree is a depth-(d-1) subtree
+ * followed by another one, then the U-turn test between the first leaf of
+ * the left half and the last leaf of the right half.  Leaves are numbered
+ * from `offset`; the first leaf's (q, p) is returned in fq/fp. */
+static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t offset, int v,
+                                int64_t e, orc_sub *sub, double *fq, double *fp)
+{
+    int64_t D = it->tg->D;
+    if (d == 0) {
+        orc_leapfrog(it->tg, z, (double)v * it->eps, it->inv_mass);
+        orc_leaf(it, sub, z, j, offset, e, v);
+        memcpy(fq, z->q, (size_t)D * sizeof(double));
+        memcpy(fp, z->p, (size_t)D * sizeof(double));
+        return;
+    }
+    orc_build_recursive(it, z, j, d - 1, offset, v, e, sub, fq, fp);
+    if (sub->status != ORC_OK) return;
+    double *rq = (double *)malloc((size_t)D * sizeof(double));
+    double *rp = (double *)malloc((size_t)D * sizeof(double));
+    int64_t half = (int64_t)1 << (d - 1);
+    orc_build_recursive(it, z, j, d - 1, offset + half, v, e, sub, rq, rp);
+    free(rq);
+    free(rp);
+    if (sub->status != ORC_OK) return;
+    int64_t last = offset + 2 * half - 1;
+    orc_trace_check(it, offset, last);
+    if (orc_is_uturn(fq, fp, z->q, z->p, v, it->inv_mass, D)) {
+        sub->status = ORC_TURNING;
+        sub->term_leaf = last;
+    }
+}
+
+/* Per-sample statistics; the layout matches the library's nuts_stats. */
+typedef struct {
+    double potential_energy;
+    double energy;
+    double accept_prob;
+    int32_t tree_depth;
+    int32_t num_steps;
+    int32_t proposal_index;
+    int32_t term_leaf;
+    uint32_t direction_bits;
+    uint8_t diverging, turning, hit_max_depth, pad[9];
+} orc_stats;
+
+enum { ORC_BUILDER_ITERATIVE = 0, ORC_BUILDER_RECURSIVE = 1 };
+
+/* One NUTS iteration from state (q, U, g) -- trajectory doubling (H&G Alg. 6
+ * with multinomial selection).  On return `cur` holds the new state. */
+static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builder,
+                          orc_stats *st)
+{
+    orc_target *tg = it->tg;
+    int64_t D = tg->D;
+    const double *im = it->inv_mass;
+
+    double *xi = (double *)malloc((size_t)D * sizeof(double));
+    orc_normals(it->seed, it->chain, it->t, D, xi);
+    for (int64_t j = 0; j < D; ++j) cur->p[j] = xi[j] / sqrt(im[j]);
+    free(xi);
+    it->H0 = cur->U + orc_kinetic(cur->p, im, D);
+    it->nleaves = 0;
+    it->sum_accept = 0.0;
+
+    orc_node left, right, prop, z;
+    orc_node_alloc(&left, D); orc_node_alloc(&right, D);
+    orc_node_alloc(&prop, D); orc_node_alloc(&z, D);
+    orc_node_copy(&left, cur, D);
+    orc_node_copy(&right, cur, D);
+    orc_node_copy(&prop, cur, D);
+    int64_t prop_idx = 0, Lpos = 0, Rpos = 0;
+    double logw_traj = 0.0;
+
+    orc_sub sub;
+    orc_node_alloc(&sub.prop, D);
+    double *fq = (double *)malloc((size_t)D * sizeof(double));
+    double *fp = (double *)malloc((size_t)D * sizeof(double));
+
+    memset(st, 0, sizeof(*st));
+    st->term_leaf = -1;
+    for (int j = 0; j < max_depth; ++j) {
+        int v = orc_direction(it->seed, it->chain, it->t, (uint64_t)j);
+        if (v > 0) st->direction_bits |= (1u << j);
+        orc_node_copy(&z, v > 0 ? &right : &left, D);
+        int64_t e = v > 0 ? Rpos : Lpos;
+        sub.status = ORC_OK;
+        sub.term_leaf = -1;
+        sub.logw = -INFINITY;
+        sub.prop_idx = 0;
+        sub.has_prop = 0;
+        if (builder == ORC_BUILDER_RECURSIVE)
+            orc_build_recursive(it, &z, j, j, 0, v, e, &sub, fq, fp);
+        else
+            orc_build_iterative(it, &z, j, v, e, &sub);
+        st->tree_depth = j + 1;
+        if (sub.status != ORC_OK) {
+            st->term_leaf = (int32_t)sub.term_leaf;
+            if (sub.status == ORC_DIVERGENT) st->diverging = 1;
+            else st->turning = 1;
+            break;
+        }
+        /* biased progressive selection between the old trajectory and the
+         * new subtree */
+        double u = orc_u_merge(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j);
+        if (u < exp(sub.logw - logw_traj)) {
+            orc_node_copy(&prop, &sub.prop, D);
+            prop_idx = sub.prop_idx;
+        }
+        logw_traj = orc_logaddexp(logw_traj, sub.logw);
+        if (v > 0) { orc_node_copy(&right, &z, D); Rpos += (int64_t)1 << j; }
+        else       { orc_node_copy(&left, &z, D);  Lpos -= (int64_t)1 << j; }
+        if (orc_is_uturn(left.q, left.p, right.q, right.p, +1, im, D)) {
+            st->turning = 1;
+            st->term_leaf = -2;
+            break;
+        }
+        if (j == max_depth - 1) st->hit_max_depth = 1;
+    }
+    st->num_steps = (int32_t)it->nleaves;
+    st->accept_prob = it->nleaves > 0 ? it->sum_accept / (double)it->nleaves : 0.0;
+    st->proposal_index = (int32_t)prop_idx;
+    orc_node_copy(cur, &prop, D);
+    st->potential_energy = cur->U;
+    st->energy = cur->U + orc_kinetic(cur->p, im, D);
+
+    free(fq); free(fp);
+    orc_node_free(&sub.prop);
+    orc_node_free(&left); orc_node_free(&right);
+    orc_node_free(&prop); orc_node_free(&z);
+}
+
+/* Diagonal inverse mass from warmup draws (reading R13): Welford mean and
+ * variance of the states after warmup iterations [W/2, W), shrunk towards
+ * 1e-3 with weight 5/(n+5), then scaled to mean one. */
+typedef struct {
+    int64_t n;
+    double *mean, *m2;
+} orc_welford;
+
+/* Full chain: init at q0, then num_warmup + num_samples iterations whose
+ * global indices start at first_iter.  Kept samples go to out_samples
+ * [num_samples][D] and out_stats [num_samples].  The final state goes to
+ * out_q (may be NULL); out_inv_mass receives the inverse mass in use at the
+ * end (may be NULL).  Returns the number of gradient evaluations. */
+int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double *yv, int64_t N,
+                       int64_t D, double s, double sn, double eps, const double *inv_mass_in,
+                       int max_depth, int64_t num_warmup, int64_t num_samples, uint64_t seed,
+                       uint64_t chain, int builder, int adapt_diag, const double *q0,
+                       int64_t first_iter, double *out_samples, orc_stats *out_stats,
+                       double *out_q, double *out_inv_mass, int64_t *trace,
+                       int64_t trace_cap, int64_t *trace_len, int64_t *leaves,
+                       int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt)
+{
+    orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
+    double *im = (double *)malloc((size_t)D * sizeof(double));
+    for (int64_t j = 0; j < D; ++j) im[j] = inv_mass_in ? inv_mass_in[j] : 1.0;
+
+    orc_node cur;
+    orc_node_alloc(&cur, D);
+    for (int64_t j = 0; j < D; ++j) cur.q[j] = q0 ? q0[j] : 0.0;
+    cur.U = orc_eval(&tg, cur.q, cur.g);
+
+    orc_iter it;
+    memset(&it, 0, sizeof(it));
+    it.tg = &tg;
+    it.inv_mass = im;
+    it.eps = eps;
+    it.seed = seed;
+    it.chain = chain;
+    it.trace = trace;
+    it.trace_cap = trace_cap;
+    it.leaves = leaves;
+    it.leaves_cap = leaves_cap;
+    it.sel_salt = sel_salt;
+
+    orc_welford wf = { 0, (double *)calloc((size_t)D, sizeof(double)),
+                       (double *)calloc((size_t)D, sizeof(double)) };
+
+    orc_stats st;
+    for (int64_t k = 0; k < num_warmup + num_samples; ++k) {
+        it.t = (uint64_t)(first_iter + k);
+        orc_iteration(&it, &cur, max_depth, builder, &st);
+        if (adapt_diag && k < num_warmup && k >= num_warmup / 2) {
+            wf.n++;
+            for (int64_t j = 0; j < D; ++j) {
+                double d1 = cur.q[j] - wf.mean[j];
+                wf.mean[j] += d1 / (double)wf.n;
+                wf.m2[j] += d1 * (cur.q[j] - wf.mean[j]);
+            }
+        }
+        if (adapt_diag && k == num_warmup - 1 && wf.n >= 2) {
+            double nn = (double)wf.n, tot = 0.0;
+            for (int64_t j = 0; j < D; ++j) {
+                double var = wf.m2[j] / (nn - 1.0);
+                im[j] = (nn / (nn + 5.0)) * var + 1e-3 * (5.0 / (nn + 5.0));
+                tot += im[j];
+            }
+            double mean = tot / (double)D;
+            for (int64_t j = 0; j < D; ++j) im[j] = im[j] / mean;
+        }
+        if (k >= num_warmup) {
+            int64_t o = k - num_warmup;
+            if (out_samples) memcpy(out_samples + o * D, cur.q, (size_t)D * sizeof(double));
+            if (out_stats) out_stats[o] = st;
+        }
+    }
+    if (out_q) memcpy(out_q, cur.q, (size_t)D * sizeof(double));
+    if (out_inv_mass) memcpy(out_inv_mass, im, (size_t)D * sizeof(double));
+    if (trace_len) *trace_len = it.trace_len;
+    if (leaves_len) *leaves_len = it.leaves_len;
+    free(wf.mean); free(wf.m2);
+    orc_node_free(&cur);
+    free(im);
+    return tg.nevals;
+}
+
+/* Exposed single leapfrog step for the integrator tests (position, momentum
+ * and gradient updated in place; returns the new potential). */
+double orc_leapfrog_steps(int kind, const double *X, const uint8_t *y, const double *yv,
+                          int64_t N, int64_t D, double s, double sn, const double *inv_mass,
+                          double h, int64_t nsteps, double *q, double *p)
+{
+    orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
+    orc_node z;
+    orc_node_alloc(&z, D);
+    memcpy(z.q, q, (size_t)D * sizeof(double));
+    memcpy(z.p, p, (size_t)D * sizeof(double));
+    z.U = orc_eval(&tg, z.q, z.g);
+    for (int64_t k = 0; k < nsteps; ++k) orc_leapfrog(&tg, &z, h, inv_mass);
+    memcpy(q, z.q, (size_t)D * sizeof(double));
+    memcpy(p, z.p, (size_t)D * sizeof(double));
+    double U = z.U;
+    orc_node_free(&z);
+    return U;
+}
+
+/* Timing helper for the CPU baseline: `reps` gradient evaluations at w over
+ * an fp32 X (promoted row by row, never copied whole), or fp64 X. */
+double orc_logistic_ug_f32(const float *Xf, const uint8_t *y, int64_t N, int64_t D, double s,
+                           const double *w, double *grad)
+{
+    double *row = (double *)malloc((size_t)D * sizeof(double));
+    for (int64_t j = 0; j < D; ++j) grad[j] = 0.0;
+    double U = 0.0;
+    for (int64_t i = 0; i < N; ++i) {
+        for (int64_t j = 0; j < D; ++j) row[j] = (double)Xf[i * D + j];
+        double eta = 0.0;
+        for (int64_t j = 0; j < D; ++j) eta += row[j] * w[j];
+        double sgn = y[i] ? -1.0 : 1.0;
+        double t = sgn * eta;
+        U += orc_softplus(t);
+        double r = sgn * orc_sigmoid(t);
+        for (int64_t j = 0; j < D; ++j) grad[j] += r * row[j];
+    }
+    free(row);
+    const double half_log_2pi = 0.91893853320467274178032973640562;
+    double inv_s2 = 1.0 / (s * s);
+    for (int64_t j = 0; j < D; ++j) {
+        U += 0.5 * w[j] * w[j] * inv_s2;
+        grad[j] += w[j] * inv_s2;
+    }
+    U += (double)D * (log(s) + half_log_2pi);
+    return U;
+}
