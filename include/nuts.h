@@ -1,0 +1,156 @@
+/*
+ * nuts.h -- C ABI of the MI355X (gfx950) iterative No-U-Turn sampler for
+ * Bayesian logistic regression.
+ *
+ * What is computed (arXiv 1912.11554):
+ *   - the model of Appendix B / Fig. 1a: weights m ~ N(0, 1), intercept
+ *     b ~ N(0, 1), y_i ~ Bernoulli(logits = x_i . m + b).  Here the intercept
+ *     is a column of ones inside X and every weight has prior N(0, s^2), so
+ *       U(w)  = sum_i [softplus(eta_i) - y_i eta_i] + |w|^2 / (2 s^2)
+ *               + D (ln s + ln(2 pi) / 2),                eta = X w,
+ *       dU/dw = X^T (sigmoid(eta) - y) + w / s^2;
+ *   - NUTS trajectory doubling with the iterative tree builder of
+ *     Appendix A, Alg. 2 (even leaves kept in S[BitCount(n)], U-turn checks
+ *     at odd leaves against the candidate set C(n)), the leapfrog integrator
+ *     (Section 3.1), Hoffman & Gelman's endpoint U-turn criterion and
+ *     divergence threshold 1000, multinomial selection inside subtrees and
+ *     biased progressive selection between doublings (Betancourt 2017);
+ *   - random draws from Philox4x64-10 keyed by (seed, chain) with counter
+ *     (iteration, tag << 32 | doubling, leaf or block, 0), so every draw is
+ *     reproducible per (chain, iteration, doubling, leaf).
+ *
+ * Conventions for every entry point:
+ *   - X is row-major N x D (float64 or float32 as `dtype` says), D counting
+ *     the ones column; y holds N bytes equal to 0 or 1.  With
+ *     NUTS_DATA_PER_CHAIN, X is [C][N][D] and y is [C][N].
+ *   - Every pointer argument may be host or device memory; the library
+ *     finds out which.  Inputs are borrowed for the call only and never
+ *     retained or freed.  Outputs are caller-allocated.
+ *   - Calls are synchronous: they return after the outputs are written.  Work
+ *     runs on the stream given to nuts_init.
+ *   - Every call returns NUTS_OK or a negative code; nuts_last_error gives a
+ *     message.  The library never aborts or exits.  A handle is used by one
+ *     thread at a time.
+ */
+#ifndef NUTS_H
+#define NUTS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nuts_handle nuts_handle;
+typedef struct nuts_data nuts_data;
+
+enum {
+    NUTS_OK = 0,
+    NUTS_EINVAL = -1,       /* bad argument: null pointer, bad size, non-finite scale, y not 0/1 */
+    NUTS_ENOMEM = -2,       /* device allocation failed */
+    NUTS_EDEVICE = -3,      /* HIP runtime error, or a kernel reported a failure */
+    NUTS_EUNSUPPORTED = -4  /* a shape no kernel path handles (see nuts_last_error) */
+};
+
+enum { NUTS_F64 = 0, NUTS_F32 = 1 };
+
+enum {
+    NUTS_DATA_PER_CHAIN = 1u << 0,  /* X is [C][N][D] and y is [C][N]; else one shared data set */
+    NUTS_ADAPT_DIAG_MASS = 1u << 1  /* set the diagonal inverse mass from warmup draws */
+};
+
+/* Kernel path selection for nuts_sample_data (opts->path). */
+enum {
+    NUTS_PATH_AUTO = 0,
+    NUTS_PATH_WAVE = 1,  /* one wavefront per chain, whole tree on device */
+    NUTS_PATH_GRID = 2   /* one chain over the whole GPU, grid barrier per leapfrog step */
+};
+
+/* One record per (chain, kept sample).  56 bytes, no implicit padding. */
+typedef struct {
+    double potential_energy;  /* U at the emitted sample */
+    double energy;            /* U + K of the emitted sample and its momentum */
+    double accept_prob;       /* mean over generated leaves of min(1, exp(H0 - H)) */
+    int32_t tree_depth;       /* doublings performed, counting a rejected last one */
+    int32_t num_steps;        /* leapfrog steps = gradient evaluations this iteration */
+    int32_t proposal_index;   /* signed leapfrog offset of the sample from the start point */
+    int32_t term_leaf;        /* leaf of the last subtree where it stopped; -1 none; -2 U-turn of the whole trajectory */
+    uint32_t direction_bits;  /* bit j set iff doubling j went forward in time */
+    uint8_t diverging;        /* the last subtree hit H - H0 > 1000 (or NaN) */
+    uint8_t turning;          /* stopped by a U-turn (inside the last subtree or across the trajectory) */
+    uint8_t hit_max_depth;    /* all max_tree_depth doublings completed */
+    uint8_t _pad[9];
+} nuts_stats;
+
+/* Create a handle on device `device_ordinal`.  `hip_stream` is a hipStream_t
+ * to run on (not owned), or NULL for a stream the handle creates. */
+int nuts_init(nuts_handle** out, int device_ordinal, void* hip_stream);
+
+/* Release a handle and every device buffer it owns.  NULL is a no-op. */
+void nuts_free(nuts_handle* h);
+
+/* Message describing the last failure on this handle ("" if none).  With a
+ * NULL handle, the message of the last failed nuts_init. */
+const char* nuts_last_error(const nuts_handle* h);
+
+/* Copy X and y into the library's device layout (64-row column blocks, the
+ * dtype kept) once, for repeated use.  num_datasets is 1 for shared data, or
+ * C for per-chain data ([C][N][D] and [C][N]).  The result belongs to the
+ * handle and must be released with nuts_data_free before nuts_free. */
+int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D,
+                     int dtype, int64_t num_datasets, nuts_data** out);
+void nuts_data_free(nuts_handle* h, nuts_data* d);
+
+/* Potential and gradient (Appendix B model) at K positions W [K][D].  With
+ * shared data every row of W is evaluated on the same X; with per-chain data
+ * row k uses data set k (K must equal num_datasets).  Writes out_U [K] and
+ * out_grad [K][D] (fp64).  U and the gradient are accumulated in fp64 also
+ * for fp32 X. */
+int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_scale,
+                             const double* W, int64_t K, double* out_U, double* out_grad);
+
+/* One-shot form of the above for a single position w [D]: lays out X and y,
+ * evaluates, releases.  N = 0 is allowed (the prior alone). */
+int nuts_potential_grad(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D,
+                        int dtype, double prior_scale, const double* w, double* out_U,
+                        double* out_grad);
+
+/* Options of nuts_sample_data; a NULL pointer means all defaults. */
+typedef struct {
+    const double* init_q;      /* [C][D] start positions, or NULL for zeros */
+    int64_t first_iter;        /* global index of the first iteration (the RNG counter) */
+    double* out_final_q;       /* [C][D] state after the last iteration, or NULL */
+    double* out_inv_mass;      /* [C][D] inverse mass in use at the end, or NULL */
+    int64_t* out_grad_evals;   /* [1] gradient evaluations of the whole call, or NULL */
+    int32_t path;              /* NUTS_PATH_* */
+    int32_t _reserved;
+} nuts_sample_opts;
+
+/* Run num_chains chains for num_warmup + num_samples iterations on prepared
+ * data, all on the device with no host round trip per leapfrog step.  Each
+ * chain starts at init_q (zeros by default) with the gradient evaluated
+ * there.  Iteration k of the call has global index first_iter + k; the first
+ * num_warmup iterations are not emitted.  inv_mass_diag is [D] (shared by
+ * all chains) or NULL for the identity; with NUTS_ADAPT_DIAG_MASS the
+ * inverse mass is re-set at the end of warmup from the variance of the
+ * warmup states in [num_warmup/2, num_warmup), shrunk towards 1e-3 with
+ * weight 5/(n+5) and scaled to mean one.  Writes out_samples [C][S][D] fp64
+ * and out_stats [C][S] (either may be NULL).  Divergences are not errors. */
+int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double prior_scale,
+                     double step_size, const double* inv_mass_diag, int max_tree_depth,
+                     int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed,
+                     double* out_samples, nuts_stats* out_stats, const nuts_sample_opts* opts);
+
+/* One-shot form: lays out X and y, samples, releases.  Argument order follows
+ * the problem statement: data, prior, step size, mass, depth, iterations,
+ * chains, seed, outputs. */
+int nuts_sample(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype,
+                uint32_t flags, double prior_scale, double step_size, const double* inv_mass_diag,
+                int max_tree_depth, int64_t num_warmup, int64_t num_samples, int64_t num_chains,
+                uint64_t seed, double* out_samples, nuts_stats* out_stats);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NUTS_H */

@@ -1,0 +1,245 @@
+"""MI355X (gfx950) iterative NUTS for Bayesian logistic regression.
+
+Thin ctypes binding over ``libnuts.so`` (C ABI in ``include/nuts.h``): it
+marshals numpy arrays or torch tensors (host or device) into pointers and
+passes torch's current HIP stream; every step of the sampler runs in the HIP
+kernels.  Build the library with ``python -m paper_1912_11554_amd.build``.
+There is no CPU fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnuts.so")
+
+NUTS_OK, NUTS_EINVAL, NUTS_ENOMEM, NUTS_EDEVICE, NUTS_EUNSUPPORTED = 0, -1, -2, -3, -4
+NUTS_F64, NUTS_F32 = 0, 1
+NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS = 1, 2
+NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID = 0, 1, 2
+
+EXPORTED = [
+    "nuts_init", "nuts_free", "nuts_last_error", "nuts_data_create", "nuts_data_free",
+    "nuts_data_potential_grad", "nuts_potential_grad", "nuts_sample_data", "nuts_sample",
+]
+
+STATS_DTYPE = np.dtype([
+    ("potential_energy", "<f8"), ("energy", "<f8"), ("accept_prob", "<f8"),
+    ("tree_depth", "<i4"), ("num_steps", "<i4"), ("proposal_index", "<i4"),
+    ("term_leaf", "<i4"), ("direction_bits", "<u4"), ("diverging", "u1"),
+    ("turning", "u1"), ("hit_max_depth", "u1"), ("_pad", "u1", (9,)),
+])
+assert STATS_DTYPE.itemsize == 56
+
+
+class NutsError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"NUTS error {code}: {msg}")
+        self.code = code
+
+
+class _Opts(ctypes.Structure):
+    _fields_ = [
+        ("init_q", ctypes.c_void_p),
+        ("first_iter", ctypes.c_int64),
+        ("out_final_q", ctypes.c_void_p),
+        ("out_inv_mass", ctypes.c_void_p),
+        ("out_grad_evals", ctypes.c_void_p),
+        ("path", ctypes.c_int32),
+        ("_reserved", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load_library():
+    """Load libnuts.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing; build it with "
+                           "`python -m paper_1912_11554_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i64, u64, i32, u32, dbl = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                  ctypes.c_int, ctypes.c_uint32, ctypes.c_double)
+    L.nuts_init.argtypes = [ctypes.POINTER(P), i32, P]
+    L.nuts_init.restype = i32
+    L.nuts_free.argtypes = [P]
+    L.nuts_free.restype = None
+    L.nuts_last_error.argtypes = [P]
+    L.nuts_last_error.restype = ctypes.c_char_p
+    L.nuts_data_create.argtypes = [P, P, P, i64, i64, i32, i64, ctypes.POINTER(P)]
+    L.nuts_data_create.restype = i32
+    L.nuts_data_free.argtypes = [P, P]
+    L.nuts_data_free.restype = None
+    L.nuts_data_potential_grad.argtypes = [P, P, dbl, P, i64, P, P]
+    L.nuts_data_potential_grad.restype = i32
+    L.nuts_potential_grad.argtypes = [P, P, P, i64, i64, i32, dbl, P, P, P]
+    L.nuts_potential_grad.restype = i32
+    L.nuts_sample_data.argtypes = [P, P, u32, dbl, dbl, P, i32, i64, i64, i64, u64, P, P,
+                                   ctypes.POINTER(_Opts)]
+    L.nuts_sample_data.restype = i32
+    L.nuts_sample.argtypes = [P, P, P, i64, i64, i32, u32, dbl, dbl, P, i32, i64, i64, i64,
+                              u64, P, P]
+    L.nuts_sample.restype = i32
+    _lib = L
+    return L
+
+
+def _ptr(a):
+    """Raw pointer of a numpy array or torch tensor (None stays None)."""
+    if a is None:
+        return None
+    if isinstance(a, np.ndarray):
+        assert a.flags.c_contiguous
+        return a.ctypes.data
+    assert a.is_contiguous()
+    return a.data_ptr()
+
+
+def _dtype_code(X):
+    name = str(X.dtype)
+    if name.endswith("float64"):
+        return NUTS_F64
+    if name.endswith("float32"):
+        return NUTS_F32
+    raise TypeError(f"X must be float64 or float32, got {X.dtype}")
+
+
+def _current_stream():
+    try:
+        import torch
+        if torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+    except Exception:
+        pass
+    return None
+
+
+class Sampler:
+    """A handle on one GPU.  ``stream`` defaults to torch's current stream."""
+
+    def __init__(self, device: int = 0, stream=None):
+        L = load_library()
+        h = ctypes.c_void_p()
+        if stream is None:
+            stream = _current_stream()
+        rc = L.nuts_init(ctypes.byref(h), device, stream)
+        if rc != NUTS_OK:
+            raise NutsError(rc, L.nuts_last_error(None).decode())
+        self._L = L
+        self._h = h
+
+    def close(self):
+        if self._h:
+            self._L.nuts_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc):
+        if rc != NUTS_OK:
+            raise NutsError(rc, self._L.nuts_last_error(self._h).decode())
+
+    # ------------------------------------------------------------------
+    def data(self, X, y, per_chain: bool = False):
+        """Lay out X ([N, D] or, per chain, [C, N, D]) and y once."""
+        if per_chain:
+            C, N, D = X.shape
+        else:
+            (N, D), C = X.shape, 1
+        out = ctypes.c_void_p()
+        self._check(self._L.nuts_data_create(self._h, _ptr(X), _ptr(y), N, D, _dtype_code(X),
+                                             C, ctypes.byref(out)))
+        return Data(self, out, N, D, C)
+
+    def potential_grad(self, X, y, w, prior_scale=1.0):
+        """U and grad U at one position w [D] (float64)."""
+        N, D = X.shape
+        U = np.zeros(1)
+        g = np.zeros(D)
+        w = np.ascontiguousarray(w, dtype=np.float64)
+        self._check(self._L.nuts_potential_grad(self._h, _ptr(X), _ptr(y), N, D, _dtype_code(X),
+                                                prior_scale, _ptr(w), _ptr(U), _ptr(g)))
+        return U[0], g
+
+    def sample(self, X, y, *, step_size, max_tree_depth, num_warmup, num_samples,
+               num_chains=1, seed=0, prior_scale=1.0, inv_mass=None, per_chain=False,
+               adapt_diag_mass=False, **kw):
+        """One-shot sampling; see ``Data.sample`` for the outputs."""
+        d = self.data(X, y, per_chain=per_chain)
+        try:
+            return d.sample(step_size=step_size, max_tree_depth=max_tree_depth,
+                            num_warmup=num_warmup, num_samples=num_samples,
+                            num_chains=num_chains, seed=seed, prior_scale=prior_scale,
+                            inv_mass=inv_mass, adapt_diag_mass=adapt_diag_mass, **kw)
+        finally:
+            d.free()
+
+
+class Data:
+    """Data set in the library's device layout (owned by a Sampler)."""
+
+    def __init__(self, sampler, handle, N, D, C):
+        self.s, self._d, self.N, self.D, self.num_sets = sampler, handle, N, D, C
+
+    def free(self):
+        if self._d:
+            self.s._L.nuts_data_free(self.s._h, self._d)
+            self._d = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+    def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None):
+        """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor)."""
+        if isinstance(W, np.ndarray):
+            W = np.ascontiguousarray(W, dtype=np.float64).reshape(-1, self.D)
+        K = W.shape[0]
+        if out_U is None:
+            out_U = np.zeros(K)
+        if out_grad is None:
+            out_grad = np.zeros((K, self.D))
+        self.s._check(self.s._L.nuts_data_potential_grad(self.s._h, self._d, prior_scale,
+                                                          _ptr(W), K, _ptr(out_U),
+                                                          _ptr(out_grad)))
+        return out_U, out_grad
+
+    def sample(self, *, step_size, max_tree_depth, num_warmup, num_samples, num_chains=1,
+               seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
+               first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None):
+        """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
+        (STATS_DTYPE), final_q [C, D], inv_mass [C, D], grad_evals.  Outputs
+        are numpy unless device tensors are passed in out_samples /
+        out_stats (then those are filled and returned)."""
+        C, D = num_chains, self.D
+        flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
+            NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0)
+        if out_samples is None:
+            out_samples = np.zeros((C, num_samples, D))
+        if out_stats is None:
+            out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
+        final_q = np.zeros((C, D))
+        out_im = np.zeros((C, D))
+        gev = np.zeros(1, dtype=np.int64)
+        im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)
+        iq = None if init_q is None else np.ascontiguousarray(init_q, dtype=np.float64)
+        opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), path, 0)
+        self.s._check(self.s._L.nuts_sample_data(
+            self.s._h, self._d, flags, prior_scale, step_size, _ptr(im), max_tree_depth,
+            num_warmup, num_samples, C, seed, _ptr(out_samples), _ptr(out_stats),
+            ctypes.byref(opts)))
+        return dict(samples=out_samples, stats=out_stats, final_q=final_q, inv_mass=out_im,
+                    grad_evals=int(gev[0]))

@@ -1,0 +1,456 @@
+// C ABI of the NUTS library: argument validation, host/device pointer
+// handling, device-layout data sets, path selection and launches.  No C++
+// exception or abort crosses this boundary; every failure is a status code
+// plus a message kept on the handle.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/nuts.h"
+#include "device.h"
+#include "launch.h"
+
+using namespace nuts;
+
+struct nuts_data {
+    DataView view;
+    void* X = nullptr;
+    uint8_t* y = nullptr;
+};
+
+struct nuts_handle {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    int num_cu = 0;
+    std::string err;
+};
+
+static thread_local std::string g_init_error;
+
+static int fail(nuts_handle* h, int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (h) h->err = buf;
+    else g_init_error = buf;
+    return code;
+}
+
+#define HIP_TRY(h, expr)                                                                         \
+    do {                                                                                         \
+        hipError_t e_ = (expr);                                                                  \
+        if (e_ != hipSuccess)                                                                    \
+            return fail((h), e_ == hipErrorOutOfMemory ? NUTS_ENOMEM : NUTS_EDEVICE, "%s: %s", \
+                        #expr, hipGetErrorString(e_));                                           \
+    } while (0)
+
+namespace {
+
+// Device memory owned for the duration of one call.
+struct DevBuf {
+    void* p = nullptr;
+    DevBuf() = default;
+    DevBuf(const DevBuf&) = delete;
+    DevBuf& operator=(const DevBuf&) = delete;
+    ~DevBuf()
+    {
+        if (p) (void)hipFree(p);
+    }
+    hipError_t alloc(size_t bytes)
+    {
+        return hipMalloc(&p, bytes ? bytes : 1);
+    }
+};
+
+// True if `p` is device-accessible memory allocated by HIP (device or
+// managed); plain or pinned host memory is copied explicitly instead.
+bool is_device_ptr(const void* p)
+{
+    if (!p) return false;
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // clear the sticky "invalid value" of unknown host memory
+        return false;
+    }
+    return attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged;
+}
+
+// Make a device copy of a host input (or pass a device input through).
+hipError_t stage_in(const void* src, size_t bytes, DevBuf& tmp, const void** dev, hipStream_t s)
+{
+    if (!src || bytes == 0) {
+        *dev = src;
+        return hipSuccess;
+    }
+    if (is_device_ptr(src)) {
+        *dev = src;
+        return hipSuccess;
+    }
+    hipError_t e = tmp.alloc(bytes);
+    if (e != hipSuccess) return e;
+    e = hipMemcpyAsync(tmp.p, src, bytes, hipMemcpyHostToDevice, s);
+    *dev = tmp.p;
+    return e;
+}
+
+// A caller output: written in place if on the device, else through `tmp`
+// and copied back by finish_out.
+hipError_t stage_out(void* dst, size_t bytes, DevBuf& tmp, void** dev)
+{
+    if (!dst) {
+        *dev = nullptr;
+        return hipSuccess;
+    }
+    if (is_device_ptr(dst)) {
+        *dev = dst;
+        return hipSuccess;
+    }
+    hipError_t e = tmp.alloc(bytes);
+    *dev = tmp.p;
+    return e;
+}
+
+hipError_t finish_out(void* dst, size_t bytes, const DevBuf& tmp, hipStream_t s)
+{
+    if (!dst || !tmp.p || bytes == 0) return hipSuccess;
+    return hipMemcpyAsync(dst, tmp.p, bytes, hipMemcpyDeviceToHost, s);
+}
+
+size_t elem_size(int dtype) { return dtype == NUTS_F64 ? 8 : 4; }
+
+bool finite_pos(double x) { return std::isfinite(x) && x > 0.0; }
+
+// hipSetDevice for the handle's device for the lifetime of a call.
+struct DeviceScope {
+    int prev = -1;
+    explicit DeviceScope(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        (void)hipSetDevice(dev);
+    }
+    ~DeviceScope()
+    {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace
+
+extern "C" {
+
+int nuts_init(nuts_handle** out, int device_ordinal, void* hip_stream)
+{
+    if (!out) return fail(nullptr, NUTS_EINVAL, "nuts_init: out is NULL");
+    *out = nullptr;
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count == 0)
+        return fail(nullptr, NUTS_EDEVICE, "nuts_init: no HIP device (%s)", hipGetErrorString(e));
+    if (device_ordinal < 0 || device_ordinal >= count)
+        return fail(nullptr, NUTS_EINVAL, "nuts_init: device %d out of range [0, %d)", device_ordinal, count);
+    DeviceScope ds(device_ordinal);
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, device_ordinal);
+    if (e != hipSuccess) return fail(nullptr, NUTS_EDEVICE, "nuts_init: %s", hipGetErrorString(e));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(nullptr, NUTS_EUNSUPPORTED, "nuts_init: built for gfx950, device is %s", prop.gcnArchName);
+    nuts_handle* h = new (std::nothrow) nuts_handle();
+    if (!h) return fail(nullptr, NUTS_ENOMEM, "nuts_init: out of host memory");
+    h->device = device_ordinal;
+    h->num_cu = prop.multiProcessorCount;
+    if (hip_stream) {
+        h->stream = (hipStream_t)hip_stream;
+    } else {
+        e = hipStreamCreate(&h->stream);
+        if (e != hipSuccess) {
+            delete h;
+            return fail(nullptr, NUTS_EDEVICE, "nuts_init: hipStreamCreate: %s", hipGetErrorString(e));
+        }
+        h->own_stream = true;
+    }
+    *out = h;
+    return NUTS_OK;
+}
+
+void nuts_free(nuts_handle* h)
+{
+    if (!h) return;
+    DeviceScope ds(h->device);
+    if (h->own_stream) (void)hipStreamDestroy(h->stream);
+    delete h;
+}
+
+const char* nuts_last_error(const nuts_handle* h)
+{
+    return h ? h->err.c_str() : g_init_error.c_str();
+}
+
+int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype,
+                     int64_t num_datasets, nuts_data** out)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!out) return fail(h, NUTS_EINVAL, "nuts_data_create: out is NULL");
+    *out = nullptr;
+    if (dtype != NUTS_F64 && dtype != NUTS_F32) return fail(h, NUTS_EINVAL, "dtype must be NUTS_F64 or NUTS_F32");
+    if (N < 0) return fail(h, NUTS_EINVAL, "N must be >= 0 (got %lld)", (long long)N);
+    if (D < 1) return fail(h, NUTS_EINVAL, "D must be >= 1 (got %lld)", (long long)D);
+    if (D > kMaxDim)
+        return fail(h, NUTS_EUNSUPPORTED, "D = %lld exceeds the %d columns the kernels support", (long long)D, kMaxDim);
+    if (num_datasets < 1) return fail(h, NUTS_EINVAL, "num_datasets must be >= 1");
+    if (N > 0 && (!X || !y)) return fail(h, NUTS_EINVAL, "X and y must be non-NULL when N > 0");
+
+    DeviceScope ds(h->device);
+    nuts_data* d = new (std::nothrow) nuts_data();
+    if (!d) return fail(h, NUTS_ENOMEM, "out of host memory");
+    d->view.N = N;
+    d->view.D = (int)D;
+    d->view.dtype = dtype;
+    d->view.nb = (N + kBlockRows - 1) / kBlockRows;
+    d->view.nds = num_datasets;
+    const size_t es = elem_size(dtype);
+    const size_t xblk = (size_t)d->view.nb * D * kBlockRows * num_datasets * es;
+    const size_t yblk = (size_t)d->view.nb * kBlockRows * num_datasets;
+    auto cleanup = [&](int code) {
+        if (d->X) (void)hipFree(d->X);
+        if (d->y) (void)hipFree(d->y);
+        delete d;
+        return code;
+    };
+    hipError_t e;
+    if (xblk) {
+        e = hipMalloc(&d->X, xblk);
+        if (e != hipSuccess) return cleanup(fail(h, NUTS_ENOMEM, "hipMalloc(%zu) for X: %s", xblk, hipGetErrorString(e)));
+        e = hipMalloc((void**)&d->y, yblk);
+        if (e != hipSuccess) return cleanup(fail(h, NUTS_ENOMEM, "hipMalloc(%zu) for y: %s", yblk, hipGetErrorString(e)));
+        DevBuf xs, ys, flag;
+        const void* Xd = nullptr;
+        const void* yd = nullptr;
+        e = stage_in(X, (size_t)N * D * num_datasets * es, xs, &Xd, h->stream);
+        if (e == hipSuccess) e = stage_in(y, (size_t)N * num_datasets, ys, &yd, h->stream);
+        if (e == hipSuccess) e = flag.alloc(sizeof(unsigned int));
+        if (e == hipSuccess) e = hipMemsetAsync(flag.p, 0, sizeof(unsigned int), h->stream);
+        if (e == hipSuccess)
+            e = launch_to_blocks(Xd, (const uint8_t*)yd, d->view, d->X, d->y, (unsigned int*)flag.p, h->stream);
+        unsigned int bad = 0;
+        if (e == hipSuccess) e = hipMemcpyAsync(&bad, flag.p, sizeof bad, hipMemcpyDeviceToHost, h->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+        if (e != hipSuccess)
+            return cleanup(fail(h, e == hipErrorOutOfMemory ? NUTS_ENOMEM : NUTS_EDEVICE, "data layout: %s",
+                                hipGetErrorString(e)));
+        if (bad) return cleanup(fail(h, NUTS_EINVAL, "y holds a value other than 0 or 1"));
+    }
+    d->view.X = d->X;
+    d->view.y = d->y;
+    *out = d;
+    return NUTS_OK;
+}
+
+void nuts_data_free(nuts_handle* h, nuts_data* d)
+{
+    if (!d) return;
+    if (h) {
+        DeviceScope ds(h->device);
+        (void)hipStreamSynchronize(h->stream);
+        if (d->X) (void)hipFree(d->X);
+        if (d->y) (void)hipFree(d->y);
+    } else {
+        if (d->X) (void)hipFree(d->X);
+        if (d->y) (void)hipFree(d->y);
+    }
+    delete d;
+}
+
+int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_scale, const double* W,
+                             int64_t K, double* out_U, double* out_grad)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (!W || !out_U || !out_grad) return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be non-NULL");
+    if (K < 1 || K > 65535) return fail(h, NUTS_EINVAL, "K must be in [1, 65535] (got %lld)", (long long)K);
+    if (d->view.nds > 1 && K != d->view.nds)
+        return fail(h, NUTS_EINVAL, "per-chain data: K (%lld) must equal the number of data sets (%lld)",
+                    (long long)K, (long long)d->view.nds);
+    if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
+    DeviceScope ds(h->device);
+    const int D = d->view.D;
+    DevBuf wt, ut, gt, part;
+    const void* Wd = nullptr;
+    void *Ud = nullptr, *Gd = nullptr;
+    HIP_TRY(h, stage_in(W, (size_t)K * D * 8, wt, &Wd, h->stream));
+    HIP_TRY(h, stage_out(out_U, (size_t)K * 8, ut, &Ud));
+    HIP_TRY(h, stage_out(out_grad, (size_t)K * D * 8, gt, &Gd));
+    const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
+    HIP_TRY(h, part.alloc((size_t)K * plan.groups_per_item * 64 * sizeof(double)));
+    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part.p,
+                                     (double*)Ud, (double*)Gd, h->stream));
+    HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
+    HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    return NUTS_OK;
+}
+
+int nuts_potential_grad(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype,
+                        double prior_scale, const double* w, double* out_U, double* out_grad)
+{
+    nuts_data* d = nullptr;
+    int rc = nuts_data_create(h, X, y, N, D, dtype, 1, &d);
+    if (rc != NUTS_OK) return rc;
+    rc = nuts_data_potential_grad(h, d, prior_scale, w, 1, out_U, out_grad);
+    nuts_data_free(h, d);
+    return rc;
+}
+
+int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double prior_scale, double step_size,
+                     const double* inv_mass_diag, int max_tree_depth, int64_t num_warmup, int64_t num_samples,
+                     int64_t num_chains, uint64_t seed, double* out_samples, nuts_stats* out_stats,
+                     const nuts_sample_opts* opts)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    nuts_sample_opts o;
+    std::memset(&o, 0, sizeof o);
+    if (opts) o = *opts;
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS))
+        return fail(h, NUTS_EINVAL, "unknown flag bits 0x%x", flags);
+    if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
+    if (!finite_pos(step_size)) return fail(h, NUTS_EINVAL, "step_size must be finite and > 0");
+    if (max_tree_depth < 1 || max_tree_depth > 30)
+        return fail(h, NUTS_EINVAL, "max_tree_depth must be in [1, 30] (got %d)", max_tree_depth);
+    if (num_warmup < 0) return fail(h, NUTS_EINVAL, "num_warmup must be >= 0");
+    if (num_samples < 1) return fail(h, NUTS_EINVAL, "num_samples must be >= 1");
+    if (num_chains < 1) return fail(h, NUTS_EINVAL, "num_chains must be >= 1");
+    if (o.first_iter < 0) return fail(h, NUTS_EINVAL, "first_iter must be >= 0");
+    if (d->view.N < 1) return fail(h, NUTS_EINVAL, "sampling needs N >= 1");
+    const bool per_chain = (flags & NUTS_DATA_PER_CHAIN) != 0;
+    if (per_chain && d->view.nds != num_chains)
+        return fail(h, NUTS_EINVAL, "NUTS_DATA_PER_CHAIN: data holds %lld sets for %lld chains",
+                    (long long)d->view.nds, (long long)num_chains);
+    if (!per_chain && d->view.nds != 1)
+        return fail(h, NUTS_EINVAL, "data holds %lld sets; pass NUTS_DATA_PER_CHAIN", (long long)d->view.nds);
+    const int D = d->view.D;
+    if (inv_mass_diag) {
+        std::vector<double> im(D);
+        if (is_device_ptr(inv_mass_diag)) {
+            DeviceScope ds(h->device);
+            HIP_TRY(h, hipMemcpy(im.data(), inv_mass_diag, (size_t)D * 8, hipMemcpyDeviceToHost));
+        } else {
+            std::memcpy(im.data(), inv_mass_diag, (size_t)D * 8);
+        }
+        for (int i = 0; i < D; ++i)
+            if (!finite_pos(im[i])) return fail(h, NUTS_EINVAL, "inv_mass_diag[%d] must be finite and > 0", i);
+    }
+
+    int path = o.path;
+    if (path == NUTS_PATH_AUTO) {
+        // one wave per chain when there are many chains or the data is small;
+        // the whole device on one chain when the data is large
+        const bool small = d->view.nb <= 64;
+        path = (per_chain || small || num_chains > 1) ? NUTS_PATH_WAVE : NUTS_PATH_GRID;
+    }
+    if (path != NUTS_PATH_WAVE && path != NUTS_PATH_GRID) return fail(h, NUTS_EINVAL, "unknown path %d", path);
+    if (path == NUTS_PATH_GRID && per_chain)
+        return fail(h, NUTS_EUNSUPPORTED, "the grid path runs chains on shared data only");
+
+    DeviceScope ds(h->device);
+    hipStream_t s = h->stream;
+    const int64_t C = num_chains, S = num_samples;
+    DevBuf imb, iqb, smp, sts, fq, fim, gev;
+    const void *im_d = nullptr, *iq_d = nullptr;
+    void *smp_d = nullptr, *sts_d = nullptr, *fq_d = nullptr, *fim_d = nullptr;
+    HIP_TRY(h, stage_in(inv_mass_diag, (size_t)D * 8, imb, &im_d, s));
+    HIP_TRY(h, stage_in(o.init_q, (size_t)C * D * 8, iqb, &iq_d, s));
+    HIP_TRY(h, stage_out(out_samples, (size_t)C * S * D * 8, smp, &smp_d));
+    HIP_TRY(h, stage_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, &sts_d));
+    HIP_TRY(h, stage_out(o.out_final_q, (size_t)C * D * 8, fq, &fq_d));
+    HIP_TRY(h, stage_out(o.out_inv_mass, (size_t)C * D * 8, fim, &fim_d));
+    HIP_TRY(h, gev.alloc((size_t)C * sizeof(unsigned long long)));
+
+    SamplerArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.data = d->view;
+    a.per_chain_data = per_chain ? 1 : 0;
+    a.prior_scale = prior_scale;
+    a.step_size = step_size;
+    a.inv_mass = (const double*)im_d;
+    a.max_depth = max_tree_depth;
+    a.num_warmup = num_warmup;
+    a.num_samples = num_samples;
+    a.num_chains = C;
+    a.chain_offset = 0;
+    a.seed = seed;
+    a.first_iter = o.first_iter;
+    a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
+    a.init_q = (const double*)iq_d;
+    a.out_samples = (double*)smp_d;
+    a.out_stats = (nuts_stats*)sts_d;
+    a.out_final_q = (double*)fq_d;
+    a.out_inv_mass = (double*)fim_d;
+    a.grad_evals = (unsigned long long*)gev.p;
+
+    if (path == NUTS_PATH_WAVE) {
+        HIP_TRY(h, launch_sampler_wave(a, s));
+    } else {
+        const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
+        DevBuf part, res, sync;
+        HIP_TRY(h, part.alloc((size_t)2 * groups * 64 * sizeof(double)));
+        HIP_TRY(h, res.alloc((size_t)2 * 64 * sizeof(double)));
+        HIP_TRY(h, sync.alloc(sizeof(GridSync)));
+        for (int64_t c = 0; c < C; ++c) {
+            SamplerArgs ac = a;
+            ac.num_chains = 1;
+            ac.chain_offset = c;
+            HIP_TRY(h, launch_sampler_grid(ac, groups, (double*)part.p, (double*)res.p, (GridSync*)sync.p, s));
+            GridSync hs;
+            HIP_TRY(h, hipMemcpyAsync(&hs, sync.p, sizeof hs, hipMemcpyDeviceToHost, s));
+            HIP_TRY(h, hipStreamSynchronize(s));
+            if (hs.error)
+                return fail(h, NUTS_EDEVICE, "grid barrier timed out in chain %lld (a group stopped responding)",
+                            (long long)c);
+        }
+    }
+    HIP_TRY(h, finish_out(out_samples, (size_t)C * S * D * 8, smp, s));
+    HIP_TRY(h, finish_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, s));
+    HIP_TRY(h, finish_out(o.out_final_q, (size_t)C * D * 8, fq, s));
+    HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
+    std::vector<unsigned long long> ev(C);
+    HIP_TRY(h, hipMemcpyAsync(ev.data(), gev.p, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+    HIP_TRY(h, hipStreamSynchronize(s));
+    if (o.out_grad_evals) {
+        unsigned long long tot = 0;
+        for (auto v : ev) tot += v;
+        *o.out_grad_evals = (int64_t)tot;
+    }
+    return NUTS_OK;
+}
+
+int nuts_sample(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype, uint32_t flags,
+                double prior_scale, double step_size, const double* inv_mass_diag, int max_tree_depth,
+                int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed, double* out_samples,
+                nuts_stats* out_stats)
+{
+    if (!h) return NUTS_EINVAL;
+    if (num_chains < 1) return fail(h, NUTS_EINVAL, "num_chains must be >= 1");
+    const int64_t nds = (flags & NUTS_DATA_PER_CHAIN) ? num_chains : 1;
+    nuts_data* d = nullptr;
+    int rc = nuts_data_create(h, X, y, N, D, dtype, nds, &d);
+    if (rc != NUTS_OK) return rc;
+    rc = nuts_sample_data(h, d, flags, prior_scale, step_size, inv_mass_diag, max_tree_depth, num_warmup,
+                          num_samples, num_chains, seed, out_samples, out_stats, nullptr);
+    nuts_data_free(h, d);
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,519 @@
+// Device-resident NUTS: trajectory doubling with the iterative tree builder,
+// leapfrog steps, multinomial / biased-progressive proposal selection, U-turn
+// and divergence checks, all inside one kernel launch.
+//
+// Tree state is held lane-per-dimension: lane d of a wave keeps component d
+// of every phase-space vector (position q, momentum p, gradient g) of the
+// current leaf, both trajectory edges, the proposal and the subtree proposal.
+// Dot products are wave butterflies, so every lane (and, on the grid path,
+// every wave of every group) holds bit-identical scalars and takes identical
+// decisions.  Lanes >= D carry zeros.
+//
+// Two evaluators supply U and grad U at a position:
+//   WaveEval -- one wave streams its chain's data set (small data; one wave
+//               per chain, thousands of chains per launch);
+//   GridEval -- every wave of every group streams a slice of one large data
+//               set; group partials meet at a grid barrier whose last arriver
+//               adds them in group order.
+//
+// Algorithmic sources: Appendix A of arXiv 1912.11554 (Alg. 2 iterative tree,
+// the S array indexed by BitCount, candidate set C(n)); Hoffman & Gelman 2014,
+// Alg. 6 (direction per doubling, endpoint U-turn rule, Delta_max = 1000);
+// Betancourt 2017, App. A (multinomial and biased progressive selection).
+#include "launch.h"
+#include "rows.h"
+
+namespace nuts {
+
+namespace {
+
+constexpr int kTreeOk = 0, kTreeTurning = 1, kTreeDivergent = 2;
+
+// Endpoint U-turn test on time-ordered ends: (a, b) are the first- and
+// last-generated nodes of a subtree built in direction v.
+__device__ __forceinline__ bool is_uturn(double qa, double pa, double qb, double pb, int v, double im)
+{
+    const double qL = v > 0 ? qa : qb, pL = v > 0 ? pa : pb;
+    const double qR = v > 0 ? qb : qa, pR = v > 0 ? pb : pa;
+    const double dq = qR - qL;
+    const double dl = wave_sum(dq * im * pL);
+    const double dr = wave_sum(dq * im * pR);
+    return uni((dl < 0.0) || (dr < 0.0));
+}
+
+struct Node {
+    double q, p, g;  // this lane's component
+    double U;        // wave-uniform
+};
+
+// Evaluator interface: eval(q_lane, U, g_lane); s_writer() says whether this
+// wave stores the checkpoint array S, out_writer() whether it stores the
+// chain's outputs; aborted() reports a failed grid barrier.
+
+template <typename T, int MAXD>
+struct WaveEval {
+    const T* X;
+    const uint8_t* y;
+    int64_t N, nb;
+    int D;
+    double inv_s2, prior_const;
+
+    __device__ bool s_writer() const { return true; }
+    __device__ bool out_writer() const { return true; }
+    __device__ bool aborted() const { return false; }
+
+    __device__ void eval(double q, double& U, double& g)
+    {
+        const int l = lane();
+        double qv[MAXD];
+#pragma unroll
+        for (int c = 0; c < MAXD; ++c) qv[c] = __shfl(q, c);
+        double acc[MAXD];
+#pragma unroll
+        for (int c = 0; c < MAXD; ++c) acc[c] = 0.0;
+        double loss = 0.0;
+        for (int64_t b = 0; b < nb; ++b)
+            accumulate_block<T, MAXD>(X + b * D * kBlockRows, y + b * kBlockRows, D,
+                                      N - b * kBlockRows, qv, acc, loss);
+        const double col = finish_wave<MAXD>(acc, loss);
+        const double prior = wave_sum(0.5 * q * q * inv_s2);
+        U = loss + prior + prior_const;
+        g = (l < D) ? col + q * inv_s2 : 0.0;
+    }
+};
+
+template <typename T, int MAXD, int NW>
+struct GridEval {
+    const T* X;
+    const uint8_t* y;
+    int64_t N, nb;
+    int D;
+    double inv_s2, prior_const;
+    int groups;
+    double* partials;  // [2][groups][64]
+    double* result;    // [2][64]
+    GridSync* sync;
+    double (*red)[kWave];  // LDS [NW][64]
+    int* flag_lds;         // LDS [2]: [0] this group arrived last, [1] barrier failed
+    unsigned long long step;
+    bool abort;
+
+    __device__ bool s_writer() const { return threadIdx.x < kWave; }
+    __device__ bool out_writer() const { return blockIdx.x == 0 && threadIdx.x < kWave; }
+    __device__ bool aborted() const { return abort; }
+
+    __device__ void eval(double q, double& U, double& g)
+    {
+        const int l = lane();
+        const int wave = threadIdx.x / kWave;
+        const int par = (int)(step & 1);
+        double qv[MAXD];
+#pragma unroll
+        for (int c = 0; c < MAXD; ++c) qv[c] = __shfl(q, c);
+        double acc[MAXD];
+#pragma unroll
+        for (int c = 0; c < MAXD; ++c) acc[c] = 0.0;
+        double loss = 0.0;
+        const int64_t stride = (int64_t)groups * NW;
+        for (int64_t b = (int64_t)blockIdx.x * NW + wave; b < nb; b += stride)
+            accumulate_block<T, MAXD>(X + b * D * kBlockRows, y + b * kBlockRows, D,
+                                      N - b * kBlockRows, qv, acc, loss);
+        const double col = finish_wave<MAXD>(acc, loss);
+        red[wave][l] = (l < D) ? col : (l == kWave - 1 ? loss : 0.0);
+        __syncthreads();
+
+        const unsigned long long target = (step + 1) * (unsigned long long)groups;
+        if (wave == 0) {
+            double s = 0.0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) s += red[w][l];
+            partials[((int64_t)par * groups + blockIdx.x) * kWave + l] = s;
+            __threadfence();
+            int last = 0;
+            if (l == 0) last = (atomicAdd(&sync->counter, 1ull) == target - 1) ? 1 : 0;
+            last = __shfl(last, 0);
+            if (l == 0) {
+                flag_lds[0] = last;
+                flag_lds[1] = 0;
+            }
+        }
+        __syncthreads();
+        if (flag_lds[0]) {
+            // last arriver: add the group partials in group order, spread
+            // over the waves, then in wave order
+            __threadfence();
+            double s = 0.0;
+            for (int gg = wave; gg < groups; gg += NW)
+                s += partials[((int64_t)par * groups + gg) * kWave + l];
+            __syncthreads();
+            red[wave][l] = s;
+            __syncthreads();
+            if (wave == 0) {
+                double tot = 0.0;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) tot += red[w][l];
+                result[par * kWave + l] = tot;
+                __threadfence();
+                if (l == 0)
+                    __hip_atomic_store(&sync->flag, step + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        } else if (threadIdx.x == 0) {
+            // wait for the last arriver; give up (and tell every group) after
+            // about 10 s so that a broken invariant can never hang the device
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            int bad = 0;
+            while (__hip_atomic_load(&sync->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < step + 1) {
+                if (__hip_atomic_load(&sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                    bad = 1;
+                    break;
+                }
+                if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
+                    __hip_atomic_store(&sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    bad = 1;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+            __threadfence();
+            flag_lds[1] = bad;
+        }
+        __syncthreads();
+        if (flag_lds[1]) abort = true;
+        __threadfence();
+        const double r = abort ? 0.0 : result[par * kWave + l];
+        __syncthreads();  // flag_lds / red are reused by the next evaluation
+        const double prior = wave_sum(0.5 * q * q * inv_s2);
+        U = __shfl(r, kWave - 1) + prior + prior_const;
+        g = (l < D) ? r + q * inv_s2 : 0.0;
+        step++;
+    }
+};
+
+// The whole chain: init, warmup + sampling iterations, outputs.  S points to
+// this chain's checkpoint array in LDS: [max(max_depth, 1)][2][D].
+template <class Eval>
+__device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double* S)
+{
+    const int l = lane();
+    const int D = A.data.D;
+    const bool act = l < D;
+    const int maxd = A.max_depth;
+    const double eps = A.step_size;
+    const uint64_t seed = A.seed;
+    const uint64_t key_chain = (uint64_t)(A.chain_offset + chain);
+    const bool out = ev.out_writer();
+    const bool s_out = ev.s_writer();
+
+    double im = (act && A.inv_mass) ? A.inv_mass[l] : 1.0;
+
+    Node cur;
+    cur.q = (act && A.init_q) ? A.init_q[(A.chain_offset + chain) * D + l] : 0.0;
+    cur.p = 0.0;
+    ev.eval(cur.q, cur.U, cur.g);
+    unsigned long long evals = 1;
+
+    double wmean = 0.0, wm2 = 0.0;
+    int64_t wn = 0;
+    const int64_t iters = A.num_warmup + A.num_samples;
+
+    for (int64_t k = 0; k < iters && !ev.aborted(); ++k) {
+        const uint64_t t = (uint64_t)(A.first_iter + k);
+
+        // momentum and initial energy
+        const double xi = act ? momentum_normal(seed, key_chain, t, l) : 0.0;
+        cur.p = act ? xi / sqrt(im) : 0.0;
+        const double H0 = cur.U + 0.5 * wave_sum(im * cur.p * cur.p);
+
+        // per-iteration draws, one doubling per lane: direction bits and the
+        // merge uniforms
+        int dir_bit = 0;
+        double u_merge = 0.0;
+        if (l < maxd) {
+            dir_bit = (int)(draw(seed, key_chain, t, kTagDirection, (uint64_t)l, 0).w0 & 1ull);
+            u_merge = unit53(draw(seed, key_chain, t, kTagMerge, (uint64_t)l, 0).w0);
+        }
+        const uint64_t dirmask = __ballot(dir_bit);
+
+        Node left = cur, right = cur, prop = cur;
+        int64_t prop_idx = 0, Lpos = 0, Rpos = 0;
+        double logw_traj = 0.0;
+        int nleaves = 0;
+        double sum_acc = 0.0;
+        int depth = 0, term = -1;
+        uint32_t dirbits = 0;
+        int diverging = 0, turning = 0, maxhit = 0;
+
+        for (int j = 0; j < maxd; ++j) {
+            const int v = ((dirmask >> j) & 1ull) ? 1 : -1;
+            if (v > 0) dirbits |= 1u << j;
+            Node z = v > 0 ? right : left;
+            const int64_t e = v > 0 ? Rpos : Lpos;
+            const double h = v * eps;
+            double logw = -INFINITY;
+            Node sprop = z;
+            int64_t sprop_idx = 0;
+            int status = kTreeOk;
+            depth = j + 1;
+            const int64_t nleaf = 1ll << j;
+            double u_leaf = 0.0;
+
+            for (int64_t n = 0; n < nleaf; ++n) {
+                if ((n & (kWave - 1)) == 0)
+                    u_leaf = (n + l < nleaf)
+                                 ? unit53(draw(seed, key_chain, t, kTagLeaf, (uint64_t)j, (uint64_t)(n + l)).w0)
+                                 : 0.0;
+                // leapfrog: half kick, drift, gradient, half kick
+                const double ph = z.p - 0.5 * h * z.g;
+                z.q = z.q + h * im * ph;
+                ev.eval(z.q, z.U, z.g);
+                if (ev.aborted()) break;
+                z.p = ph - 0.5 * h * z.g;
+                ++nleaves;
+
+                const double dH = (z.U + 0.5 * wave_sum(im * z.p * z.p)) - H0;
+                if (dH == dH) sum_acc += dH > 0.0 ? exp(-dH) : 1.0;
+                if (uni(!(dH <= 1000.0))) {
+                    status = kTreeDivergent;
+                    term = (int)n;
+                    break;
+                }
+                // streaming multinomial choice inside the subtree
+                const double lam = -dH;
+                const double lw = logaddexp(logw, lam);
+                const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
+                if (uni(u < exp(lam - lw))) {
+                    sprop = z;
+                    sprop_idx = e + v * (n + 1);
+                }
+                logw = lw;
+
+                if ((n & 1) == 0) {
+                    // even leaf: checkpoint into S[BitCount(n)]
+                    const int i = __popcll((unsigned long long)n);
+                    if (s_out && act) {
+                        S[(2 * i) * D + l] = z.q;
+                        S[(2 * i + 1) * D + l] = z.p;
+                    }
+                } else {
+                    // odd leaf: test the subtrees that end here, smallest first
+                    const int nl = __builtin_ctzll(~(unsigned long long)n);
+                    const int imax = __popcll((unsigned long long)(n - 1));
+                    const int imin = imax - nl + 1;
+                    bool turned = false;
+                    for (int kk = imax; kk >= imin; --kk) {
+                        const double sq = act ? S[(2 * kk) * D + l] : 0.0;
+                        const double sp = act ? S[(2 * kk + 1) * D + l] : 0.0;
+                        if (is_uturn(sq, sp, z.q, z.p, v, im)) {
+                            turned = true;
+                            break;
+                        }
+                    }
+                    if (turned) {
+                        status = kTreeTurning;
+                        term = (int)n;
+                        break;
+                    }
+                }
+            }
+            if (ev.aborted()) break;
+            if (status != kTreeOk) {
+                if (status == kTreeDivergent) diverging = 1;
+                else turning = 1;
+                break;
+            }
+            // biased progressive choice between trajectory and new subtree
+            const double um = __shfl(u_merge, j);
+            if (uni(um < exp(logw - logw_traj))) {
+                prop = sprop;
+                prop_idx = sprop_idx;
+            }
+            logw_traj = logaddexp(logw_traj, logw);
+            if (v > 0) {
+                right = z;
+                Rpos += nleaf;
+            } else {
+                left = z;
+                Lpos -= nleaf;
+            }
+            if (is_uturn(left.q, left.p, right.q, right.p, 1, im)) {
+                turning = 1;
+                term = -2;
+                break;
+            }
+            if (j == maxd - 1) maxhit = 1;
+        }
+        evals += (unsigned long long)nleaves;
+        cur = prop;
+
+        // diagonal inverse mass from warmup states in [W/2, W)
+        if (A.adapt_diag && k < A.num_warmup && k >= A.num_warmup / 2) {
+            ++wn;
+            const double d1 = cur.q - wmean;
+            wmean += d1 / (double)wn;
+            wm2 += d1 * (cur.q - wmean);
+        }
+        if (A.adapt_diag && k == A.num_warmup - 1 && wn >= 2) {
+            const double nn = (double)wn;
+            double v = (nn / (nn + 5.0)) * (wm2 / (nn - 1.0)) + 1e-3 * (5.0 / (nn + 5.0));
+            v = act ? v : 0.0;
+            const double mean = wave_sum(v) / (double)D;
+            im = act ? v / mean : 1.0;
+        }
+
+        if (k >= A.num_warmup && out) {
+            const int64_t s = k - A.num_warmup;
+            const int64_t c = A.chain_offset + chain;
+            if (A.out_samples && act) A.out_samples[(c * A.num_samples + s) * D + l] = cur.q;
+            if (A.out_stats) {
+                const double K = 0.5 * wave_sum(im * cur.p * cur.p);
+                if (l == 0) {
+                    nuts_stats st;
+                    st.potential_energy = cur.U;
+                    st.energy = cur.U + K;
+                    st.accept_prob = nleaves > 0 ? sum_acc / (double)nleaves : 0.0;
+                    st.tree_depth = depth;
+                    st.num_steps = nleaves;
+                    st.proposal_index = (int32_t)prop_idx;
+                    st.term_leaf = term;
+                    st.direction_bits = dirbits;
+                    st.diverging = (uint8_t)diverging;
+                    st.turning = (uint8_t)turning;
+                    st.hit_max_depth = (uint8_t)maxhit;
+                    for (int i = 0; i < 9; ++i) st._pad[i] = 0;
+                    A.out_stats[c * A.num_samples + s] = st;
+                }
+            }
+        }
+    }
+    if (out) {
+        const int64_t c = A.chain_offset + chain;
+        if (A.out_final_q && act) A.out_final_q[c * D + l] = cur.q;
+        if (A.out_inv_mass && act) A.out_inv_mass[c * D + l] = im;
+        if (l == 0) A.grad_evals[c] = evals;
+    }
+}
+
+constexpr int kWaveChainsPerGroup = 4;
+
+template <typename T, int MAXD>
+__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave) sampler_wave_kernel(SamplerArgs A)
+{
+    extern __shared__ double lds[];
+    const int wave = threadIdx.x / kWave;
+    const int64_t chain = (int64_t)blockIdx.x * kWaveChainsPerGroup + wave;
+    if (chain >= A.num_chains) return;
+    const int D = A.data.D;
+    const int slots = A.max_depth > 1 ? A.max_depth : 1;
+    double* S = lds + (int64_t)wave * slots * 2 * D;
+    const int64_t c = A.chain_offset + chain;
+    const int64_t ds = A.per_chain_data ? c : 0;
+    WaveEval<T, MAXD> ev;
+    ev.X = (const T*)A.data.X + ds * A.data.nb * (int64_t)D * kBlockRows;
+    ev.y = A.data.y + ds * A.data.nb * kBlockRows;
+    ev.N = A.data.N;
+    ev.nb = A.data.nb;
+    ev.D = D;
+    ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+    ev.prior_const = (double)D * (log(A.prior_scale) + 0.91893853320467274178032973640562);
+    run_chain(A, ev, chain, S);
+}
+
+constexpr int kGridWaves = 8;
+
+template <typename T, int MAXD>
+__global__ void __launch_bounds__(kGridWaves * kWave) sampler_grid_kernel(SamplerArgs A, int groups,
+                                                                         double* partials,
+                                                                         double* result,
+                                                                         GridSync* sync)
+{
+    extern __shared__ double lds[];
+    __shared__ double red[kGridWaves][kWave];
+    __shared__ int flag_lds[2];
+    const int D = A.data.D;
+    GridEval<T, MAXD, kGridWaves> ev;
+    ev.X = (const T*)A.data.X;
+    ev.y = A.data.y;
+    ev.N = A.data.N;
+    ev.nb = A.data.nb;
+    ev.D = D;
+    ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+    ev.prior_const = (double)D * (log(A.prior_scale) + 0.91893853320467274178032973640562);
+    ev.groups = groups;
+    ev.partials = partials;
+    ev.result = result;
+    ev.sync = sync;
+    ev.red = red;
+    ev.flag_lds = flag_lds;
+    ev.step = 0;
+    ev.abort = false;
+    // every wave of every group runs the same chain; wave 0 of each group
+    // writes the group's S array, wave 0 of group 0 writes the outputs
+    run_chain(A, ev, 0, lds);
+}
+
+}  // namespace
+
+template <typename T, int MAXD>
+static hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
+{
+    const int slots = a.max_depth > 1 ? a.max_depth : 1;
+    const size_t lds = (size_t)kWaveChainsPerGroup * slots * 2 * a.data.D * sizeof(double);
+    const unsigned grid = (unsigned)((a.num_chains + kWaveChainsPerGroup - 1) / kWaveChainsPerGroup);
+    hipLaunchKernelGGL((sampler_wave_kernel<T, MAXD>), dim3(grid), dim3(kWaveChainsPerGroup * kWave),
+                       lds, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream)
+{
+    const bool f64 = a.data.dtype == NUTS_F64;
+    if (a.data.D <= 16) return f64 ? wave_launch<double, 16>(a, stream) : wave_launch<float, 16>(a, stream);
+    if (a.data.D <= 32) return f64 ? wave_launch<double, 32>(a, stream) : wave_launch<float, 32>(a, stream);
+    return f64 ? wave_launch<double, 64>(a, stream) : wave_launch<float, 64>(a, stream);
+}
+
+template <typename T, int MAXD>
+static void* grid_kernel_ptr()
+{
+    return (void*)sampler_grid_kernel<T, MAXD>;
+}
+
+static void* pick_grid_kernel(int dtype, int D)
+{
+    const bool f64 = dtype == NUTS_F64;
+    if (D <= 16) return f64 ? grid_kernel_ptr<double, 16>() : grid_kernel_ptr<float, 16>();
+    if (D <= 32) return f64 ? grid_kernel_ptr<double, 32>() : grid_kernel_ptr<float, 32>();
+    return f64 ? grid_kernel_ptr<double, 64>() : grid_kernel_ptr<float, 64>();
+}
+
+int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu)
+{
+    void* k = pick_grid_kernel(dv.dtype, dv.D);
+    int per_cu = 0;
+    const int slots = max_depth > 1 ? max_depth : 1;
+    const size_t lds = (size_t)slots * 2 * dv.D * sizeof(double);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGridWaves * kWave, lds) != hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    if (per_cu > 2) per_cu = 2;
+    int64_t groups = (int64_t)num_cu * per_cu;
+    const int64_t most = (dv.nb + kGridWaves - 1) / kGridWaves;
+    if (groups > most) groups = most;
+    if (groups < 1) groups = 1;
+    return (int)groups;
+}
+
+hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
+                               GridSync* sync, hipStream_t stream)
+{
+    hipError_t e = hipMemsetAsync(sync, 0, sizeof(GridSync), stream);
+    if (e != hipSuccess) return e;
+    const int slots = a.max_depth > 1 ? a.max_depth : 1;
+    const size_t lds = (size_t)slots * 2 * a.data.D * sizeof(double);
+    void* k = pick_grid_kernel(a.data.dtype, a.data.D);
+    SamplerArgs A = a;
+    void* args[] = {&A, &groups, &partials, &result, &sync};
+    return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);
+}
+
+}  // namespace nuts

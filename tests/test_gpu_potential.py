@@ -1,0 +1,118 @@
+"""GPU parity of the fused potential + gradient kernel against the oracle.
+
+Bar: fp64 X -- relative error <= 1e-10 for U and per component of the
+gradient (relative to the magnitude of the summed terms); fp32 X -- the same
+comparison against the oracle run on the fp32-rounded X promoted to fp64,
+bar 1e-4 (the kernel accumulates in fp64, so it lands far inside it).
+"""
+import numpy as np
+import pytest
+
+import workloads
+from tests.gpu_common import grad_tol, say
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f64": 1e-10, "f32": 1e-4}
+
+
+@pytest.fixture(scope="module")
+def sampler():
+    import paper_1912_11554_amd as nuts
+    return nuts.Sampler(0)
+
+
+def _check(sampler, orc, X, y, w, s, dt):
+    say("potential_grad", X.shape, dt, "s", s)
+    U, g = sampler.potential_grad(X, y, w, prior_scale=s)
+    U_ref, g_ref = orc.logistic_potential_grad(X.astype(np.float64), y, w, prior_scale=s)
+    assert abs(U - U_ref) <= RTOL[dt] * abs(U_ref), (U, U_ref)
+    tol = grad_tol(X, w, g_ref, s, RTOL[dt])
+    assert (np.abs(g - g_ref) <= tol).all(), np.max(np.abs(g - g_ref) / tol)
+    return abs(U - U_ref) / abs(U_ref)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("N,D", [(1, 1), (63, 2), (64, 5), (65, 11), (1000, 11), (4097, 9),
+                                 (777, 33), (3000, 55), (130, 63)])
+def test_random_positions(sampler, orc, dt, N, D):
+    X, y, w_true = workloads.make_logistic(N, D, w_scale=0.7, key=[50, N * 1000 + D],
+                                           dtype=dt)
+    rng = np.random.default_rng(N * 100 + D)
+    for w in (np.zeros(D), w_true, w_true + rng.normal(size=D)):
+        _check(sampler, orc, X, y, w, 1.0, dt)
+    _check(sampler, orc, X, y, w_true, 2.5, dt)
+
+
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+def test_saturating_logits(sampler, orc, dt):
+    # |eta| > 40 on most rows: exp(-|t|) underflows towards 0 without loss
+    X, y, w_true = workloads.make_logistic(500, 7, w_scale=1.0, key=51, dtype=dt)
+    w = 40.0 * np.sign(w_true) + w_true
+    _check(sampler, orc, X, y, w, 1.0, dt)
+    _check(sampler, orc, X, y, -w, 1.0, dt)
+
+
+def test_prior_only(sampler, orc):
+    w = np.array([0.3, -1.2, 2.0])
+    X = np.zeros((0, 3))
+    y = np.zeros(0, dtype=np.uint8)
+    say("potential_grad N=0")
+    U, g = sampler.potential_grad(X, y, w, prior_scale=1.5)
+    U_ref, g_ref = orc.logistic_potential_grad(X, y, w, prior_scale=1.5)
+    assert abs(U - U_ref) <= 1e-14 * abs(U_ref)
+    np.testing.assert_allclose(g, g_ref, rtol=1e-15)
+
+
+def test_batched_shared_and_per_chain(sampler, orc):
+    # K positions on one data set, and K data sets with one position each
+    X, y, w_true = workloads.make_logistic(2000, 10, w_scale=1.0, key=52)
+    rng = np.random.default_rng(5)
+    W = w_true + 0.3 * rng.normal(size=(17, 10))
+    say("potential_grad batched shared K=17")
+    d = sampler.data(X, y)
+    U, G = d.potential_grad(W)
+    d.free()
+    for k in range(17):
+        U_ref, g_ref = orc.logistic_potential_grad(X, y, W[k])
+        assert abs(U[k] - U_ref) <= 1e-10 * abs(U_ref)
+        assert (np.abs(G[k] - g_ref) <= grad_tol(X, W[k], g_ref, 1.0, 1e-10)).all()
+    wl = workloads.WORKLOADS["chains4096_n500_d9_f64"]
+    Xc, yc = workloads.make_workload(wl, chains=range(40))
+    Wc = rng.normal(size=(40, 9))
+    say("potential_grad per-chain K=40")
+    d = sampler.data(Xc, yc, per_chain=True)
+    U, G = d.potential_grad(Wc)
+    d.free()
+    for k in range(40):
+        U_ref, g_ref = orc.logistic_potential_grad(Xc[k], yc[k], Wc[k])
+        assert abs(U[k] - U_ref) <= 1e-10 * abs(U_ref)
+        assert (np.abs(G[k] - g_ref) <= grad_tol(Xc[k], Wc[k], g_ref, 1.0, 1e-10)).all()
+
+
+@pytest.mark.parametrize("name", ["covtype_n581012_d55_f64", "covtype_n581012_d55_f32"])
+def test_full_size_covtype(sampler, orc, name):
+    wl = workloads.WORKLOADS[name]
+    X, y = workloads.make_workload(wl)
+    rng = np.random.default_rng(7)
+    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+    for w in (np.zeros(wl.D), w_true + 0.01 * rng.normal(size=wl.D)):
+        _check(sampler, orc, X, y, w, 1.0, wl.dtype)
+
+
+def test_errors_are_reported(sampler):
+    import paper_1912_11554_amd as nuts
+    X = np.zeros((10, 3))
+    y = np.zeros(10, dtype=np.uint8)
+    y[3] = 2
+    say("error paths")
+    with pytest.raises(nuts.NutsError) as e:
+        sampler.potential_grad(X, y, np.zeros(3))
+    assert e.value.code == nuts.NUTS_EINVAL
+    with pytest.raises(nuts.NutsError) as e:
+        sampler.potential_grad(np.zeros((10, 3)), np.zeros(10, np.uint8), np.zeros(3),
+                               prior_scale=-1.0)
+    assert e.value.code == nuts.NUTS_EINVAL
+    with pytest.raises(nuts.NutsError) as e:
+        sampler.potential_grad(np.zeros((10, 300)), np.zeros(10, np.uint8), np.zeros(300))
+    assert e.value.code == nuts.NUTS_EUNSUPPORTED

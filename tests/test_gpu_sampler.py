@@ -1,0 +1,133 @@
+"""GPU parity of the device-resident NUTS against the oracle on identical
+seeded inputs and identical Philox draws.
+
+Bar (fp64): tree depth, step count, proposal index, termination leaf and
+reason, direction bits bit-exact; positions, energies and acceptance
+statistics within 1e-9 (the two sides sum in different orders).  fp32 X:
+the same against the oracle on the fp32-rounded X promoted to fp64.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from tests.gpu_common import compare_chain, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sampler():
+    import paper_1912_11554_amd as nuts
+    return nuts.Sampler(0)
+
+
+def _oracle_chain(orc, X, y, wl, chain, iters, **kw):
+    return orc.nuts(X.astype(np.float64), y, step_size=wl.step_size,
+                    max_tree_depth=wl.max_tree_depth, num_warmup=0, num_samples=iters,
+                    seed=wl.seed, chain=chain, **kw)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_small_single_chain_50_iterations(sampler, orc, path):
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    say("sampler logreg_n1000_d11 path", path)
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=50, seed=wl.seed, path=path)
+    ref = _oracle_chain(orc, X, y, wl, 0, 50)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+    assert r["grad_evals"] == ref["grad_evals"]
+
+
+def test_small_single_chain_full_run(sampler, orc):
+    # the whole 200 + 200 run: warmup is not emitted, kept draws line up
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    say("sampler logreg_n1000_d11 full")
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=wl.num_warmup, num_samples=wl.num_samples, seed=wl.seed)
+    ref = orc.nuts(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                   num_warmup=wl.num_warmup, num_samples=wl.num_samples, seed=wl.seed)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+    np.testing.assert_allclose(r["final_q"][0], ref["final_q"], rtol=1e-9, atol=1e-9)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_edge_cases_tiny(sampler, orc, path):
+    # N = 1, D = 1; N = 65 (ragged block); forced divergence; max depth 1
+    cases = [(1, 1, 0.5, 5), (65, 3, 0.2, 6), (200, 4, 5.0, 6), (100, 2, 0.01, 1),
+             (130, 63, 0.05, 4)]
+    for N, D, eps, maxd in cases:
+        X, y, _ = workloads.make_logistic(N, D, w_scale=1.0, key=[60, N * 1000 + D])
+        say("sampler tiny", N, D, eps, maxd, "path", path)
+        r = sampler.sample(X, y, step_size=eps, max_tree_depth=maxd, num_warmup=3,
+                           num_samples=20, seed=9, path=path)
+        ref = orc.nuts(X, y, step_size=eps, max_tree_depth=maxd, num_warmup=3,
+                       num_samples=20, seed=9)
+        compare_chain(r["samples"][0], r["stats"][0], ref)
+
+
+def test_many_chains_per_chain_data_subset(sampler, orc):
+    # 256 chains of the 4096-chain workload (own data per chain); every chain
+    # compared with the oracle for its first 50 iterations
+    wl = workloads.WORKLOADS["chains4096_n500_d9_f64"]
+    C = 256
+    X, y = workloads.make_workload(wl, chains=range(C))
+    say("sampler per-chain C=256")
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=50, num_chains=C, seed=wl.seed,
+                       per_chain=True)
+    for c in range(0, C, 8):
+        ref = _oracle_chain(orc, X[c], y[c], wl, c, 50)
+        compare_chain(r["samples"][c], r["stats"][c], ref)
+
+
+def test_shared_data_many_chains(sampler, orc):
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    say("sampler shared data C=6")
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=30, num_chains=6, seed=3)
+    for c in range(6):
+        ref = orc.nuts(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=30, seed=3, chain=c)
+        compare_chain(r["samples"][c], r["stats"][c], ref)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_resume_and_inv_mass(sampler, orc, path):
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    im = np.linspace(0.5, 2.0, wl.D)
+    q0 = np.full((1, wl.D), 0.1)
+    say("sampler resume path", path)
+    r = sampler.sample(X, y, step_size=0.04, max_tree_depth=8, num_warmup=0, num_samples=25,
+                       seed=4, inv_mass=im, init_q=q0, first_iter=17, path=path)
+    ref = orc.nuts(X, y, step_size=0.04, max_tree_depth=8, num_warmup=0, num_samples=25, seed=4,
+                   inv_mass=im, init_q=q0[0], first_iter=17)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+
+
+def test_diag_mass_adaptation(sampler, orc):
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    say("sampler adapt diag mass")
+    r = sampler.sample(X, y, step_size=0.05, max_tree_depth=8, num_warmup=60, num_samples=20,
+                       seed=2, adapt_diag_mass=True)
+    ref = orc.nuts(X, y, step_size=0.05, max_tree_depth=8, num_warmup=60, num_samples=20,
+                   seed=2, adapt_diag_mass=True)
+    np.testing.assert_allclose(r["inv_mass"][0], ref["inv_mass"], rtol=1e-9)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+
+
+@pytest.mark.parametrize("name", ["covtype_n581012_d55_f64", "covtype_n581012_d55_f32"])
+def test_covtype_first_iterations(sampler, orc, name):
+    # full-size data, the grid path, the first iterations checked one by one
+    wl = workloads.WORKLOADS[name]
+    X, y = workloads.make_workload(wl)
+    iters = 12
+    say("sampler covtype grid", name, "iters", iters)
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=iters, seed=wl.seed, path=2)
+    ref = _oracle_chain(orc, X, y, wl, 0, iters)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
