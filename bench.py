@@ -1,0 +1,194 @@
+#!/usr/bin/env python3
+"""Throughput of the device-resident NUTS on the covtype-shaped logistic
+regression (N = 581,012 rows, D = 55 columns with the intercept, synthetic
+iid N(0, 1) features), one chain on one MI355X.
+
+A "step" is one NUTS iteration (one draw): momentum, trajectory doubling
+with the iterative tree builder, every leapfrog step's fused potential and
+gradient over all rows, proposal selection.  --warmup W iterations run
+first (untimed); the timed call resumes the chain from that state for
+exactly --steps K iterations with the data already in HBM.
+
+The JSON line reports leapfrog gradient evaluations per second (`value`),
+ESS/s, the roofline of the sampler kernel (algorithmic bytes = one read of
+X and y per gradient evaluation, over the kernel's time measured with HIP
+events on the launch stream), and the CPU oracle's gradient rate on the
+same data as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def run_workload(name, steps, warmup):
+    import torch
+
+    import paper_1912_11554_amd as nuts
+    import workloads
+    from paper_1912_11554_amd.diagnostics import effective_sample_size
+
+    wl = workloads.WORKLOADS[name]
+    t0 = time.time()
+    X, y = workloads.make_workload(wl)
+    log(f"{name}: generated {X.shape} {X.dtype} in {time.time() - t0:.1f}s")
+    Xd = torch.from_numpy(X).cuda()
+    yd = torch.from_numpy(y).cuda()
+    del X
+    torch.cuda.synchronize()
+    s = nuts.Sampler(0)
+    t0 = time.time()
+    d = s.data(Xd, yd)
+    torch.cuda.synchronize()
+    layout_s = time.time() - t0
+    del Xd
+    kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
+              prior_scale=wl.prior_scale, path=nuts.NUTS_PATH_GRID)
+
+    t0 = time.time()
+    r0 = d.sample(num_warmup=warmup, num_samples=1, **kw)
+    log(f"{name}: warmup {warmup} iterations, {r0['grad_evals']} gradient evaluations, "
+        f"{time.time() - t0:.2f}s")
+    q = r0["final_q"]
+
+    D = wl.D
+    samples = torch.empty((1, steps, D), dtype=torch.float64, device="cuda")
+    stats = torch.empty((1, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(stream)
+    r = d.sample(num_warmup=0, num_samples=steps, init_q=q, first_iter=warmup + 1,
+                 out_samples=samples, out_stats=stats, **kw)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    gpu_s = ev0.elapsed_time(ev1) / 1e3
+    st = stats.cpu().numpy().reshape(-1).view(nuts.STATS_DTYPE)
+    draws = samples.cpu().numpy()[0]
+    evals = r["grad_evals"]
+    assert evals == int(st["num_steps"].sum()) + 1
+    ess = effective_sample_size(draws)
+    es = 8 if wl.dtype == "f64" else 4
+    bytes_per_eval = wl.N * wl.D * es + wl.N
+    achieved = evals * bytes_per_eval / gpu_s / 1e9
+    log(f"{name}: {steps} iterations, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
+        f"({wall * 1e3:.1f} ms wall): {evals / gpu_s:.0f} evals/s, {achieved:.0f} GB/s, "
+        f"min ESS {ess.min():.0f}")
+    d.free()
+    s.close()
+    return dict(
+        workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, step_size=wl.step_size,
+        max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
+        gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
+        evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
+        ess_min=float(ess.min()), ess_median=float(np.median(ess)),
+        ess_per_s=float(ess.min() / wall), bytes_per_eval=bytes_per_eval, achieved_gbs=achieved,
+        mean_tree_depth=float(st["tree_depth"].mean()),
+        mean_steps_per_iter=float(st["num_steps"].mean()),
+        divergences=int(st["diverging"].sum()), accept_prob=float(st["accept_prob"].mean()),
+    )
+
+
+def cpu_baseline(name, seconds):
+    """The oracle's fp64 gradient evaluations on the same data, one core."""
+    import oracle
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    X, y = workloads.make_workload(wl)
+    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+    f = oracle.logistic_potential_grad_f32 if wl.dtype == "f32" else oracle.logistic_potential_grad
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        f(X, y, w_true)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
+    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle",
+                sample=f"{n} full potential+gradient evaluations of {name} at w_true, "
+                       f"single-threaded fp64 C, {el:.1f}s",
+                host_cores_available=len(os.sched_getaffinity(0)))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=1000)
+    ap.add_argument("--workload", default="covtype_n581012_d55_f32")
+    ap.add_argument("--also", default="covtype_n581012_d55_f64",
+                    help="second workload reported beside the first ('' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    main_res = run_workload(args.workload, args.steps, args.warmup)
+    other = run_workload(args.also, args.steps, args.warmup) if args.also else None
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
+
+    achieved = main_res["achieved_gbs"]
+    line = {
+        "metric": "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline",
+        "value": round(main_res["evals_per_s"], 1),
+        "unit": "grad-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": main_res["dtype"],
+        "data": "synthetic",
+        "config": {
+            "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
+            "chains": 1, "step_size": main_res["step_size"],
+            "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
+        },
+        "ess_per_s": round(main_res["ess_per_s"], 2),
+        "ess_min": round(main_res["ess_min"], 1),
+        "ess_median": round(main_res["ess_median"], 1),
+        "grad_evals": main_res["grad_evals"],
+        "mean_steps_per_iter": round(main_res["mean_steps_per_iter"], 2),
+        "layout_seconds": round(main_res["layout_seconds"], 4),
+        "roofline": {
+            "kernel": "sampler_grid_kernel",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "bytes_per_eval": main_res["bytes_per_eval"],
+        },
+        "cpu_baseline": cpu,
+    }
+    if other:
+        line["also"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in other.items()}
+        line["also"]["frac_hbm"] = round(other["achieved_gbs"] / HBM_PEAK_GBS, 4)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

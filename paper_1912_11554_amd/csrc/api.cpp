@@ -12,8 +12,8 @@
 #include <vector>
 
 #include "../../include/nuts.h"
-#include "device.h"
 #include "launch.h"
+#include "rows.h"
 
 using namespace nuts;
 
@@ -216,11 +216,13 @@ int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N,
     d->view.N = N;
     d->view.D = (int)D;
     d->view.dtype = dtype;
-    d->view.nb = (N + kBlockRows - 1) / kBlockRows;
+    d->view.split = lanes_per_row((int)D, kColsPerLane);
+    const int R = rows_per_block(d->view);
+    d->view.nb = (N + R - 1) / R;
     d->view.nds = num_datasets;
     const size_t es = elem_size(dtype);
-    const size_t xblk = (size_t)d->view.nb * D * kBlockRows * num_datasets * es;
-    const size_t yblk = (size_t)d->view.nb * kBlockRows * num_datasets;
+    const size_t xblk = ((size_t)d->view.nb * D * R * num_datasets + (size_t)kTailElems) * es;
+    const size_t yblk = (size_t)d->view.nb * R * num_datasets;
     auto cleanup = [&](int code) {
         if (d->X) (void)hipFree(d->X);
         if (d->y) (void)hipFree(d->y);
@@ -238,6 +240,7 @@ int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N,
         const void* yd = nullptr;
         e = stage_in(X, (size_t)N * D * num_datasets * es, xs, &Xd, h->stream);
         if (e == hipSuccess) e = stage_in(y, (size_t)N * num_datasets, ys, &yd, h->stream);
+        if (e == hipSuccess) e = hipMemsetAsync(d->X, 0, xblk, h->stream);
         if (e == hipSuccess) e = flag.alloc(sizeof(unsigned int));
         if (e == hipSuccess) e = hipMemsetAsync(flag.p, 0, sizeof(unsigned int), h->stream);
         if (e == hipSuccess)

@@ -8,7 +8,6 @@
 namespace nuts {
 
 constexpr int kWave = 64;       // CDNA wavefront width
-constexpr int kBlockRows = 64;  // rows per column block of the device layout (one per lane)
 
 __device__ __forceinline__ int lane() { return __lane_id(); }
 
@@ -54,8 +53,10 @@ __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64
 // Which quantity a block feeds; part of the counter.
 enum : uint64_t { kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4 };
 
-__device__ __forceinline__ Block4 draw(uint64_t seed, uint64_t chain, uint64_t iter, uint64_t tag,
-                                       uint64_t doubling, uint64_t index)
+// Kept out of line: it is called a few times per iteration, and inlining it
+// would keep its temporaries and constants live across the tree loops.
+__device__ __noinline__ Block4 draw(uint64_t seed, uint64_t chain, uint64_t iter, uint64_t tag,
+                                    uint64_t doubling, uint64_t index)
 {
     return philox4x64_10(iter, (tag << 32) | doubling, index, 0, seed, chain);
 }
@@ -69,7 +70,7 @@ __device__ __forceinline__ double unit53(uint64_t w)
 // Standard normal number i of an iteration's momentum: block i/4 holds two
 // Box-Muller pairs (u_a, u_b) giving (r cos th, r sin th), r = sqrt(-2 ln(1 -
 // u_a)), th = 2 pi u_b.
-__device__ __forceinline__ double momentum_normal(uint64_t seed, uint64_t chain, uint64_t iter, int i)
+__device__ __noinline__ double momentum_normal(uint64_t seed, uint64_t chain, uint64_t iter, int i)
 {
     const Block4 b = draw(seed, chain, iter, kTagMomentum, 0, (uint64_t)(i >> 2));
     const bool second_pair = (i & 2) != 0;
@@ -81,41 +82,61 @@ __device__ __forceinline__ double momentum_normal(uint64_t seed, uint64_t chain,
 }
 
 // ---------------------------------------------------------------------------
-// Wave reductions.  Butterflies over xor partners: every lane ends with the
-// same total, summed in the same fixed tree order on every run.
-__device__ __forceinline__ double wave_sum(double v)
+// Cross-lane moves.  DPP (data-parallel primitives) patterns act inside rows
+// of 16 lanes at register-read cost; the rest go through ds_bpermute.
+enum : int {
+    kDppXor1 = 0xB1,        // quad_perm [1, 0, 3, 2]
+    kDppXor2 = 0x4E,        // quad_perm [2, 3, 0, 1]
+    kDppHalfMirror = 0x141, // lane i <-> 7 - i inside each 8 lanes
+    kDppMirror = 0x140,     // lane i <-> 15 - i inside each 16 lanes
+    kDppRor8 = 0x128        // lane i <-  (i + 8) mod 16, i.e. i ^ 8
+};
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v)
 {
-#pragma unroll
-    for (int m = kWave / 2; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return v;
+    const int2 h = __builtin_bit_cast(int2, v);
+    const int lo = __builtin_amdgcn_update_dpp(0, h.x, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, h.y, CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, int2{lo, hi});
 }
 
-// Reduce SLOTS per-lane partial sums over the wave at once.  Each butterfly
-// step halves the number of live slots: the lane whose partner bit is set
-// keeps the upper half, the other the lower half, and each adds what its
-// partner sends for the half it keeps.  After log2(SLOTS) steps lane L holds
-// slot L / (64 / SLOTS); the remaining steps sum the lanes that share a slot.
-// Cost is about SLOTS shuffles instead of 6 * SLOTS for slot-by-slot sums.
-template <int SLOTS>
-__device__ __forceinline__ double transpose_reduce(double (&a)[SLOTS])
+__device__ __forceinline__ double readlane_f64(double v, int src)
 {
-    static_assert(SLOTS >= 1 && SLOTS <= kWave && (SLOTS & (SLOTS - 1)) == 0, "power of two");
-    const int l = lane();
-    int bit = kWave / 2;
-#pragma unroll
-    for (int h = SLOTS / 2; h >= 1; h /= 2) {
-        const bool upper = (l & bit) != 0;
-#pragma unroll
-        for (int i = 0; i < h; ++i) {
-            const double send = upper ? a[i] : a[i + h];
-            const double keep = upper ? a[i + h] : a[i];
-            a[i] = keep + __shfl_xor(send, bit);
-        }
-        bit >>= 1;
-    }
-    double v = a[0];
-    for (; bit >= 1; bit >>= 1) v += __shfl_xor(v, bit);
-    return v;
+    const int2 h = __builtin_bit_cast(int2, v);
+    return __builtin_bit_cast(double, int2{__builtin_amdgcn_readlane(h.x, src),
+                                           __builtin_amdgcn_readlane(h.y, src)});
+}
+
+// The value of lane (this lane ^ M).
+template <int M>
+__device__ __forceinline__ double xor_move(double v)
+{
+    if constexpr (M == 1) return dpp_f64<kDppXor1>(v);
+    else if constexpr (M == 2) return dpp_f64<kDppXor2>(v);
+    else if constexpr (M == 8) return dpp_f64<kDppRor8>(v);
+    else return __shfl_xor(v, M);
+}
+
+// For sums over aligned groups of 2M lanes: the value of a partner lane in
+// the other half of this lane's group (an involution, not always i ^ M).
+template <int M>
+__device__ __forceinline__ double pair_move(double v)
+{
+    if constexpr (M == 4) return dpp_f64<kDppHalfMirror>(v);
+    else if constexpr (M == 8) return dpp_f64<kDppMirror>(v);
+    else return xor_move<M>(v);
+}
+
+// Sum over the whole wave; every lane gets the same bits.  Rows of 16 are
+// summed by pair butterflies, then the four row sums are added in row order.
+__device__ __forceinline__ double wave_sum(double v)
+{
+    v += pair_move<1>(v);
+    v += pair_move<2>(v);
+    v += pair_move<4>(v);
+    v += pair_move<8>(v);
+    return ((readlane_f64(v, 0) + readlane_f64(v, 16)) + readlane_f64(v, 32)) + readlane_f64(v, 48);
 }
 
 // ---------------------------------------------------------------------------
@@ -135,6 +156,39 @@ __device__ __forceinline__ RowTerms logistic_row(double eta, bool y_is_one)
     const double inv = 1.0 / (1.0 + e);
     const double sig = t >= 0.0 ? inv : e * inv;
     return RowTerms{fmax(t, 0.0) + log1p(e), sgn * sig};
+}
+
+// The same terms for fp32 data: eta and t stay fp64; the exponential, log
+// and reciprocal use the fp32 hardware instructions (v_exp_f32, v_log_f32,
+// v_rcp_f32; a few ulp, i.e. ~1e-6 relative per row at worst) and return as
+// fp64 for accumulation.  log1p(e) is formed as log(u) * e / (u - 1) with
+// u = 1 + e, which cancels the rounding of u (Goldberg 1991, Thm. 4).
+__device__ __forceinline__ RowTerms logistic_row_f32(double eta, bool y_is_one)
+{
+    const double sgn = y_is_one ? -1.0 : 1.0;
+    const double t = sgn * eta;
+    const float a = (float)fabs(t);
+    const float e = __builtin_amdgcn_exp2f(-a * 1.4426950408889634f);
+    const float u = 1.0f + e;
+    const float inv = __builtin_amdgcn_rcpf(u);
+    const float um1 = u - 1.0f;
+    const float lg = __builtin_amdgcn_logf(u) * 0.69314718055994531f;
+    const float l1p = um1 == 0.0f ? e : lg * (e * __builtin_amdgcn_rcpf(um1));
+    const float sig = t >= 0.0 ? inv : e * inv;
+    return RowTerms{fmax(t, 0.0) + (double)l1p, sgn * (double)sig};
+}
+
+template <typename T>
+__device__ __forceinline__ RowTerms logistic_row_t(double eta, bool y_is_one);
+template <>
+__device__ __forceinline__ RowTerms logistic_row_t<double>(double eta, bool y_is_one)
+{
+    return logistic_row(eta, y_is_one);
+}
+template <>
+__device__ __forceinline__ RowTerms logistic_row_t<float>(double eta, bool y_is_one)
+{
+    return logistic_row_f32(eta, y_is_one);
 }
 
 __device__ __forceinline__ double logaddexp(double a, double b)

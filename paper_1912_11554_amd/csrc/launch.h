@@ -10,19 +10,30 @@
 
 namespace nuts {
 
-// Device layout of one or more data sets: X as column blocks of 64 rows,
-// block b of data set s at element offset (s * nb + b) * D * 64, column c of
-// the block at + c * 64, row r of the block at + r; rows past N are zero.
-// y as bytes at (s * nb + b) * 64 + r, zero past N.
+// Device layout of one or more data sets: X as column blocks of R = 64 / S
+// rows (S lanes of a wavefront share a row), block b of data set s at element
+// offset (s * nb + b) * D * R, column c of the block at + c * R, row r of the
+// block at + r; rows past N are zero.  y as bytes at (s * nb + b) * R + r,
+// zero past N.
 struct DataView {
     const void* X;
     const uint8_t* y;
     int64_t N;
     int D;
     int dtype;        // NUTS_F64 or NUTS_F32
-    int64_t nb;       // ceil(N / 64)
+    int split;        // S: lanes per row, 64 / rows per block
+    int64_t nb;       // ceil(N / R)
     int64_t nds;      // number of data sets
 };
+
+// Columns one lane holds in registers during the data pass.
+constexpr int kColsPerLane = 8;
+
+// Zeroed elements after the last block of an X allocation: the data pass
+// reads up to kColsPerLane * 64 elements from a block's start.
+constexpr int64_t kTailElems = (int64_t)kColsPerLane * 64;
+
+inline int rows_per_block(const DataView& dv) { return 64 / dv.split; }
 
 // Largest D the lane-per-dimension kernels accept: dimension d lives in lane d
 // and lane 63 carries the potential through the reductions.
@@ -71,10 +82,13 @@ hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream);
 // zeroed by this call; `partials` holds [2][groups][64] doubles, `result`
 // [2][64].  Returns the group count used through *groups_used.
 struct GridSync {
-    unsigned long long counter;
-    unsigned long long flag;
-    unsigned int error;
-    unsigned int pad;
+    unsigned long long counter;          // arrivals of slot leaders, (step + 1) * 8 after step
+    unsigned long long pad0[15];
+    unsigned long long flag;             // step + 1 once the result of step is published
+    unsigned long long pad1[15];
+    unsigned int error;                  // a wait timed out
+    unsigned int pad2[31];
+    unsigned long long slot[8][16];      // arrivals per group slot (group index mod 8)
 };
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream);

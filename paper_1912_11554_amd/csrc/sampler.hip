@@ -6,15 +6,20 @@
 // of every phase-space vector (position q, momentum p, gradient g) of the
 // current leaf, both trajectory edges, the proposal and the subtree proposal.
 // Dot products are wave butterflies, so every lane (and, on the grid path,
-// every wave of every group) holds bit-identical scalars and takes identical
-// decisions.  Lanes >= D carry zeros.
+// the controller wave of every group) holds bit-identical scalars and takes
+// identical decisions.  Lanes >= D carry zeros.
 //
 // Two evaluators supply U and grad U at a position:
 //   WaveEval -- one wave streams its chain's data set (small data; one wave
 //               per chain, thousands of chains per launch);
-//   GridEval -- every wave of every group streams a slice of one large data
-//               set; group partials meet at a grid barrier whose last arriver
-//               adds them in group order.
+//   GridEval -- one chain on the whole device.  In every group, wave 0 is the
+//               controller (it runs the tree logic) and the other waves are
+//               workers (they stream a slice of the rows).  Group partials
+//               meet at a grid barrier whose last arriver adds them in group
+//               order.  Controller and workers run the same collective with
+//               the same workgroup barriers; only the workers' copy contains
+//               the data pass, so tree state and data-pass registers are never
+//               live together.
 //
 // Algorithmic sources: Appendix A of arXiv 1912.11554 (Alg. 2 iterative tree,
 // the S array indexed by BitCount, candidate set C(n)); Hoffman & Gelman 2014,
@@ -28,6 +33,7 @@ namespace nuts {
 namespace {
 
 constexpr int kTreeOk = 0, kTreeTurning = 1, kTreeDivergent = 2;
+constexpr double kHalfLog2Pi = 0.91893853320467274178032973640562;
 
 // Endpoint U-turn test on time-ordered ends: (a, b) are the first- and
 // last-generated nodes of a subtree built in direction v.
@@ -50,7 +56,7 @@ struct Node {
 // wave stores the checkpoint array S, out_writer() whether it stores the
 // chain's outputs; aborted() reports a failed grid barrier.
 
-template <typename T, int MAXD>
+template <typename T, int S>
 struct WaveEval {
     const T* X;
     const uint8_t* y;
@@ -64,128 +70,225 @@ struct WaveEval {
 
     __device__ void eval(double q, double& U, double& g)
     {
-        const int l = lane();
-        double qv[MAXD];
+        constexpr int R = RowSplit<S>::R;
+        constexpr int CPS = kColsPerLane;
+        double qv[CPS];
+        spread_position<CPS, S>(q, qv);
+        double acc[CPS];
 #pragma unroll
-        for (int c = 0; c < MAXD; ++c) qv[c] = __shfl(q, c);
-        double acc[MAXD];
-#pragma unroll
-        for (int c = 0; c < MAXD; ++c) acc[c] = 0.0;
+        for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
         double loss = 0.0;
+#pragma unroll 1
         for (int64_t b = 0; b < nb; ++b)
-            accumulate_block<T, MAXD>(X + b * D * kBlockRows, y + b * kBlockRows, D,
-                                      N - b * kBlockRows, qv, acc, loss);
-        const double col = finish_wave<MAXD>(acc, loss);
+            accumulate_block<T, CPS, S>(X + b * D * R, y + b * R, D, N - b * R, qv, acc, loss);
+        const double col = finish_pass<CPS, S>(acc, loss);
         const double prior = wave_sum(0.5 * q * q * inv_s2);
         U = loss + prior + prior_const;
-        g = (l < D) ? col + q * inv_s2 : 0.0;
+        g = (lane() < D) ? col + q * inv_s2 : 0.0;
     }
 };
 
-template <typename T, int MAXD, int NW>
-struct GridEval {
-    const T* X;
+// ---------------------------------------------------------------------------
+// Grid path.
+
+constexpr int kCmdEval = 1, kCmdExit = 2;
+
+template <int NW>
+struct GridShared {
+    double qbuf[kWave];
+    double red[NW][kWave];
+    int cmd;
+    int last;
+    int abort;
+};
+
+struct GridCtx {
+    const void* X;
     const uint8_t* y;
     int64_t N, nb;
     int D;
-    double inv_s2, prior_const;
     int groups;
     double* partials;  // [2][groups][64]
     double* result;    // [2][64]
     GridSync* sync;
-    double (*red)[kWave];  // LDS [NW][64]
-    int* flag_lds;         // LDS [2]: [0] this group arrived last, [1] barrier failed
+};
+
+// Cross-group exchange.  Everything that one group publishes for another
+// (partials, the result, counters, the flag) is written and read with
+// agent-scope atomic accesses, which the L2 keeps coherent across the XCDs one
+// access at a time.  Ordering between them comes from waiting for the
+// group's outstanding memory operations (s_waitcnt) before the next one is
+// issued.  No whole-cache write-back or invalidate (what a device-scope
+// fence does) is needed: no ordinary store has to become visible to another
+// group, and no ordinary load may observe another group's writes.
+__device__ __forceinline__ void store_shared(double* p, double v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double load_shared(const double* p)
+{
+    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void drain_memory_ops()
+{
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One collective evaluation for the whole group.  Wave 0 passes the position
+// (lane per dimension) and the command; with kCmdEval every worker streams its
+// blocks and the group joins the grid-wide sum.  Returns the command; on
+// return wave 0 finds the full sums (columns, loss in slot 63) in *out_r.
+// Every wave executes the same workgroup barriers.
+template <typename T, int S, int NW, bool WORKER>
+__device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned long long step, double q,
+                               int cmd_in, double* out_r, bool* aborted)
+{
+    constexpr int R = RowSplit<S>::R;
+    constexpr int CPS = kColsPerLane;
+    const int l = lane();
+    const int wave = threadIdx.x / kWave;
+    const int par = (int)(step & 1);
+    if (wave == 0) {
+        sh.qbuf[l] = q;
+        if (l == 0) sh.cmd = cmd_in;
+    }
+    __syncthreads();  // position and command published
+    const int cmd = sh.cmd;
+    if (cmd == kCmdExit) return cmd;
+
+    double mine = 0.0;
+    if (WORKER) {
+        double qv[CPS];
+        const int p = l & (S - 1);
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) qv[k] = sh.qbuf[(k * S + p) & (kWave - 1)];
+        double acc[CPS];
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
+        double loss = 0.0;
+        const T* X = (const T*)c.X;
+        const int workers = NW - 1;
+        const int64_t stride = (int64_t)c.groups * workers;
+#pragma unroll 1
+        for (int64_t b = (int64_t)blockIdx.x * workers + (wave - 1); b < c.nb; b += stride)
+            accumulate_block<T, CPS, S>(X + b * c.D * R, c.y + b * R, c.D, c.N - b * R, qv, acc, loss);
+        const double col = finish_pass<CPS, S>(acc, loss);
+        mine = (l < c.D) ? col : (l == kWave - 1 ? loss : 0.0);
+    }
+    sh.red[wave][l] = mine;
+    __syncthreads();  // group partials in LDS
+
+    if (wave == 0) {
+        double s = 0.0;
+#pragma unroll
+        for (int w = 1; w < NW; ++w) s += sh.red[w][l];
+        store_shared(&c.partials[((int64_t)par * c.groups + blockIdx.x) * kWave + l], s);
+        drain_memory_ops();
+        // arrival: per slot (group index mod 8) first; the last group of a
+        // slot then arrives at the top counter; the last of those reduces
+        int last = 0;
+        if (l == 0) {
+            const int slot = blockIdx.x & 7;
+            const unsigned long long per = (unsigned long long)((c.groups - slot + 7) / 8);
+            const unsigned long long o =
+                __hip_atomic_fetch_add(&c.sync->slot[slot][0], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (o + 1 == (step + 1) * per) {
+                const unsigned long long slots = c.groups < 8 ? (unsigned long long)c.groups : 8ull;
+                const unsigned long long t =
+                    __hip_atomic_fetch_add(&c.sync->counter, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                last = (t + 1 == (step + 1) * slots) ? 1 : 0;
+            }
+        }
+        last = __shfl(last, 0);
+        if (l == 0) {
+            sh.last = last;
+            sh.abort = 0;
+        }
+    }
+    __syncthreads();  // arrival recorded
+    if (sh.last) {
+        // last arriver: add the group partials in group order, spread over
+        // the waves, then in wave order
+        double s = 0.0;
+        const double* src = c.partials + (int64_t)par * c.groups * kWave + l;
+        int gg = wave;
+        // loads in batches of 8 independent requests, added in group order
+        for (; gg + 7 * NW < c.groups; gg += 8 * NW) {
+            double v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = load_shared(src + (int64_t)(gg + i * NW) * kWave);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s += v[i];
+        }
+        for (; gg < c.groups; gg += NW) s += load_shared(src + (int64_t)gg * kWave);
+        sh.red[wave][l] = s;
+        __syncthreads();  // per-wave sums in LDS
+        if (wave == 0) {
+            double tot = 0.0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += sh.red[w][l];
+            store_shared(&c.result[par * kWave + l], tot);
+            drain_memory_ops();
+            if (l == 0) __hip_atomic_store(&c.sync->flag, step + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else if (threadIdx.x == 0) {
+        // wait for the last arriver; give up (and tell every group) after
+        // about 10 s so that a broken invariant can never hang the device
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        int bad = 0;
+        while (__hip_atomic_load(&c.sync->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < step + 1) {
+            if (__hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                bad = 1;
+                break;
+            }
+            if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
+                __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                bad = 1;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        drain_memory_ops();
+        sh.abort = bad;
+    }
+    __syncthreads();  // result published (or the barrier failed)
+    const bool ab = sh.abort != 0;
+    *aborted = ab;
+    if (wave == 0) *out_r = ab ? 0.0 : load_shared(&c.result[par * kWave + l]);
+    return cmd;
+}
+
+template <typename T, int S, int NW>
+struct GridEval {
+    GridCtx c;
+    GridShared<NW>* sh;
+    double inv_s2, prior_const;
     unsigned long long step;
     bool abort;
 
-    __device__ bool s_writer() const { return threadIdx.x < kWave; }
-    __device__ bool out_writer() const { return blockIdx.x == 0 && threadIdx.x < kWave; }
+    __device__ bool s_writer() const { return true; }  // only the controller runs the chain
+    __device__ bool out_writer() const { return blockIdx.x == 0; }
     __device__ bool aborted() const { return abort; }
 
     __device__ void eval(double q, double& U, double& g)
     {
-        const int l = lane();
-        const int wave = threadIdx.x / kWave;
-        const int par = (int)(step & 1);
-        double qv[MAXD];
-#pragma unroll
-        for (int c = 0; c < MAXD; ++c) qv[c] = __shfl(q, c);
-        double acc[MAXD];
-#pragma unroll
-        for (int c = 0; c < MAXD; ++c) acc[c] = 0.0;
-        double loss = 0.0;
-        const int64_t stride = (int64_t)groups * NW;
-        for (int64_t b = (int64_t)blockIdx.x * NW + wave; b < nb; b += stride)
-            accumulate_block<T, MAXD>(X + b * D * kBlockRows, y + b * kBlockRows, D,
-                                      N - b * kBlockRows, qv, acc, loss);
-        const double col = finish_wave<MAXD>(acc, loss);
-        red[wave][l] = (l < D) ? col : (l == kWave - 1 ? loss : 0.0);
-        __syncthreads();
-
-        const unsigned long long target = (step + 1) * (unsigned long long)groups;
-        if (wave == 0) {
-            double s = 0.0;
-#pragma unroll
-            for (int w = 0; w < NW; ++w) s += red[w][l];
-            partials[((int64_t)par * groups + blockIdx.x) * kWave + l] = s;
-            __threadfence();
-            int last = 0;
-            if (l == 0) last = (atomicAdd(&sync->counter, 1ull) == target - 1) ? 1 : 0;
-            last = __shfl(last, 0);
-            if (l == 0) {
-                flag_lds[0] = last;
-                flag_lds[1] = 0;
-            }
-        }
-        __syncthreads();
-        if (flag_lds[0]) {
-            // last arriver: add the group partials in group order, spread
-            // over the waves, then in wave order
-            __threadfence();
-            double s = 0.0;
-            for (int gg = wave; gg < groups; gg += NW)
-                s += partials[((int64_t)par * groups + gg) * kWave + l];
-            __syncthreads();
-            red[wave][l] = s;
-            __syncthreads();
-            if (wave == 0) {
-                double tot = 0.0;
-#pragma unroll
-                for (int w = 0; w < NW; ++w) tot += red[w][l];
-                result[par * kWave + l] = tot;
-                __threadfence();
-                if (l == 0)
-                    __hip_atomic_store(&sync->flag, step + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        } else if (threadIdx.x == 0) {
-            // wait for the last arriver; give up (and tell every group) after
-            // about 10 s so that a broken invariant can never hang the device
-            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-            int bad = 0;
-            while (__hip_atomic_load(&sync->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < step + 1) {
-                if (__hip_atomic_load(&sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
-                    bad = 1;
-                    break;
-                }
-                if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
-                    __hip_atomic_store(&sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    bad = 1;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(2);
-            }
-            __threadfence();
-            flag_lds[1] = bad;
-        }
-        __syncthreads();
-        if (flag_lds[1]) abort = true;
-        __threadfence();
-        const double r = abort ? 0.0 : result[par * kWave + l];
-        __syncthreads();  // flag_lds / red are reused by the next evaluation
+        double r = 0.0;
+        bool ab = false;
+        grid_collective<T, S, NW, false>(c, *sh, step, q, kCmdEval, &r, &ab);
+        abort = ab;
+        step++;
         const double prior = wave_sum(0.5 * q * q * inv_s2);
         U = __shfl(r, kWave - 1) + prior + prior_const;
-        g = (l < D) ? r + q * inv_s2 : 0.0;
-        step++;
+        g = (lane() < c.D) ? r + q * inv_s2 : 0.0;
+    }
+
+    __device__ void finish()
+    {
+        double r;
+        bool ab;
+        grid_collective<T, S, NW, false>(c, *sh, step, 0.0, kCmdExit, &r, &ab);
     }
 };
 
@@ -200,14 +303,15 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     const int maxd = A.max_depth;
     const double eps = A.step_size;
     const uint64_t seed = A.seed;
-    const uint64_t key_chain = (uint64_t)(A.chain_offset + chain);
+    const int64_t cidx = A.chain_offset + chain;
+    const uint64_t key_chain = (uint64_t)cidx;
     const bool out = ev.out_writer();
     const bool s_out = ev.s_writer();
 
     double im = (act && A.inv_mass) ? A.inv_mass[l] : 1.0;
 
     Node cur;
-    cur.q = (act && A.init_q) ? A.init_q[(A.chain_offset + chain) * D + l] : 0.0;
+    cur.q = (act && A.init_q) ? A.init_q[cidx * D + l] : 0.0;
     cur.p = 0.0;
     ev.eval(cur.q, cur.U, cur.g);
     unsigned long long evals = 1;
@@ -354,16 +458,15 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         }
         if (A.adapt_diag && k == A.num_warmup - 1 && wn >= 2) {
             const double nn = (double)wn;
-            double v = (nn / (nn + 5.0)) * (wm2 / (nn - 1.0)) + 1e-3 * (5.0 / (nn + 5.0));
-            v = act ? v : 0.0;
-            const double mean = wave_sum(v) / (double)D;
-            im = act ? v / mean : 1.0;
+            double var = (nn / (nn + 5.0)) * (wm2 / (nn - 1.0)) + 1e-3 * (5.0 / (nn + 5.0));
+            var = act ? var : 0.0;
+            const double mean = wave_sum(var) / (double)D;
+            im = act ? var / mean : 1.0;
         }
 
         if (k >= A.num_warmup && out) {
             const int64_t s = k - A.num_warmup;
-            const int64_t c = A.chain_offset + chain;
-            if (A.out_samples && act) A.out_samples[(c * A.num_samples + s) * D + l] = cur.q;
+            if (A.out_samples && act) A.out_samples[(cidx * A.num_samples + s) * D + l] = cur.q;
             if (A.out_stats) {
                 const double K = 0.5 * wave_sum(im * cur.p * cur.p);
                 if (l == 0) {
@@ -380,124 +483,139 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     st.turning = (uint8_t)turning;
                     st.hit_max_depth = (uint8_t)maxhit;
                     for (int i = 0; i < 9; ++i) st._pad[i] = 0;
-                    A.out_stats[c * A.num_samples + s] = st;
+                    A.out_stats[cidx * A.num_samples + s] = st;
                 }
             }
         }
     }
     if (out) {
-        const int64_t c = A.chain_offset + chain;
-        if (A.out_final_q && act) A.out_final_q[c * D + l] = cur.q;
-        if (A.out_inv_mass && act) A.out_inv_mass[c * D + l] = im;
-        if (l == 0) A.grad_evals[c] = evals;
+        if (A.out_final_q && act) A.out_final_q[cidx * D + l] = cur.q;
+        if (A.out_inv_mass && act) A.out_inv_mass[cidx * D + l] = im;
+        if (l == 0) A.grad_evals[cidx] = evals;
     }
 }
 
 constexpr int kWaveChainsPerGroup = 4;
 
-template <typename T, int MAXD>
-__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave) sampler_wave_kernel(SamplerArgs A)
+template <typename T, int S>
+__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, 3) sampler_wave_kernel(SamplerArgs A)
 {
+    constexpr int R = RowSplit<S>::R;
     extern __shared__ double lds[];
     const int wave = threadIdx.x / kWave;
     const int64_t chain = (int64_t)blockIdx.x * kWaveChainsPerGroup + wave;
     if (chain >= A.num_chains) return;
     const int D = A.data.D;
     const int slots = A.max_depth > 1 ? A.max_depth : 1;
-    double* S = lds + (int64_t)wave * slots * 2 * D;
+    double* S_arr = lds + (int64_t)wave * slots * 2 * D;
     const int64_t c = A.chain_offset + chain;
     const int64_t ds = A.per_chain_data ? c : 0;
-    WaveEval<T, MAXD> ev;
-    ev.X = (const T*)A.data.X + ds * A.data.nb * (int64_t)D * kBlockRows;
-    ev.y = A.data.y + ds * A.data.nb * kBlockRows;
+    WaveEval<T, S> ev;
+    ev.X = (const T*)A.data.X + ds * A.data.nb * (int64_t)D * R;
+    ev.y = A.data.y + ds * A.data.nb * R;
     ev.N = A.data.N;
     ev.nb = A.data.nb;
     ev.D = D;
     ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
-    ev.prior_const = (double)D * (log(A.prior_scale) + 0.91893853320467274178032973640562);
-    run_chain(A, ev, chain, S);
+    ev.prior_const = (double)D * (log(A.prior_scale) + kHalfLog2Pi);
+    run_chain(A, ev, chain, S_arr);
 }
 
-constexpr int kGridWaves = 8;
+constexpr int kGridWaves = 16;  // 1 controller + 15 workers
 
-template <typename T, int MAXD>
-__global__ void __launch_bounds__(kGridWaves * kWave) sampler_grid_kernel(SamplerArgs A, int groups,
+template <typename T, int S>
+__global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(SamplerArgs A, int groups,
                                                                          double* partials,
                                                                          double* result,
                                                                          GridSync* sync)
 {
     extern __shared__ double lds[];
-    __shared__ double red[kGridWaves][kWave];
-    __shared__ int flag_lds[2];
-    const int D = A.data.D;
-    GridEval<T, MAXD, kGridWaves> ev;
-    ev.X = (const T*)A.data.X;
-    ev.y = A.data.y;
-    ev.N = A.data.N;
-    ev.nb = A.data.nb;
-    ev.D = D;
-    ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
-    ev.prior_const = (double)D * (log(A.prior_scale) + 0.91893853320467274178032973640562);
-    ev.groups = groups;
-    ev.partials = partials;
-    ev.result = result;
-    ev.sync = sync;
-    ev.red = red;
-    ev.flag_lds = flag_lds;
-    ev.step = 0;
-    ev.abort = false;
-    // every wave of every group runs the same chain; wave 0 of each group
-    // writes the group's S array, wave 0 of group 0 writes the outputs
-    run_chain(A, ev, 0, lds);
+    __shared__ GridShared<kGridWaves> sh;
+    GridCtx c;
+    c.X = A.data.X;
+    c.y = A.data.y;
+    c.N = A.data.N;
+    c.nb = A.data.nb;
+    c.D = A.data.D;
+    c.groups = groups;
+    c.partials = partials;
+    c.result = result;
+    c.sync = sync;
+    const int wave = threadIdx.x / kWave;
+    if (wave == 0) {
+        GridEval<T, S, kGridWaves> ev;
+        ev.c = c;
+        ev.sh = &sh;
+        ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+        ev.prior_const = (double)A.data.D * (log(A.prior_scale) + kHalfLog2Pi);
+        ev.step = 0;
+        ev.abort = false;
+        run_chain(A, ev, 0, lds);
+        ev.finish();
+    } else {
+        unsigned long long step = 0;
+        for (;;) {
+            double r;
+            bool ab;
+            if (grid_collective<T, S, kGridWaves, true>(c, sh, step, 0.0, 0, &r, &ab) == kCmdExit) break;
+            step++;
+        }
+    }
 }
 
 }  // namespace
 
-template <typename T, int MAXD>
+template <typename T, int S>
 static hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
 {
     const int slots = a.max_depth > 1 ? a.max_depth : 1;
     const size_t lds = (size_t)kWaveChainsPerGroup * slots * 2 * a.data.D * sizeof(double);
     const unsigned grid = (unsigned)((a.num_chains + kWaveChainsPerGroup - 1) / kWaveChainsPerGroup);
-    hipLaunchKernelGGL((sampler_wave_kernel<T, MAXD>), dim3(grid), dim3(kWaveChainsPerGroup * kWave),
-                       lds, stream, a);
+    hipLaunchKernelGGL((sampler_wave_kernel<T, S>), dim3(grid), dim3(kWaveChainsPerGroup * kWave), lds,
+                       stream, a);
     return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t wave_launch_split(const SamplerArgs& a, hipStream_t stream)
+{
+    if (a.data.split == 1) return wave_launch<T, 1>(a, stream);
+    if (a.data.split == 2) return wave_launch<T, 2>(a, stream);
+    if (a.data.split == 4) return wave_launch<T, 4>(a, stream);
+    return wave_launch<T, 8>(a, stream);
 }
 
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream)
 {
-    const bool f64 = a.data.dtype == NUTS_F64;
-    if (a.data.D <= 16) return f64 ? wave_launch<double, 16>(a, stream) : wave_launch<float, 16>(a, stream);
-    if (a.data.D <= 32) return f64 ? wave_launch<double, 32>(a, stream) : wave_launch<float, 32>(a, stream);
-    return f64 ? wave_launch<double, 64>(a, stream) : wave_launch<float, 64>(a, stream);
+    return a.data.dtype == NUTS_F64 ? wave_launch_split<double>(a, stream) : wave_launch_split<float>(a, stream);
 }
 
-template <typename T, int MAXD>
-static void* grid_kernel_ptr()
+static void* pick_grid_kernel(int dtype, int split)
 {
-    return (void*)sampler_grid_kernel<T, MAXD>;
-}
-
-static void* pick_grid_kernel(int dtype, int D)
-{
-    const bool f64 = dtype == NUTS_F64;
-    if (D <= 16) return f64 ? grid_kernel_ptr<double, 16>() : grid_kernel_ptr<float, 16>();
-    if (D <= 32) return f64 ? grid_kernel_ptr<double, 32>() : grid_kernel_ptr<float, 32>();
-    return f64 ? grid_kernel_ptr<double, 64>() : grid_kernel_ptr<float, 64>();
+    if (dtype == NUTS_F64) {
+        if (split == 1) return (void*)sampler_grid_kernel<double, 1>;
+        if (split == 2) return (void*)sampler_grid_kernel<double, 2>;
+        if (split == 4) return (void*)sampler_grid_kernel<double, 4>;
+        return (void*)sampler_grid_kernel<double, 8>;
+    }
+    if (split == 1) return (void*)sampler_grid_kernel<float, 1>;
+    if (split == 2) return (void*)sampler_grid_kernel<float, 2>;
+    if (split == 4) return (void*)sampler_grid_kernel<float, 4>;
+    return (void*)sampler_grid_kernel<float, 8>;
 }
 
 int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu)
 {
-    void* k = pick_grid_kernel(dv.dtype, dv.D);
+    void* k = pick_grid_kernel(dv.dtype, dv.split);
     int per_cu = 0;
     const int slots = max_depth > 1 ? max_depth : 1;
     const size_t lds = (size_t)slots * 2 * dv.D * sizeof(double);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGridWaves * kWave, lds) != hipSuccess ||
         per_cu < 1)
         per_cu = 1;
-    if (per_cu > 2) per_cu = 2;
+    if (per_cu > 1) per_cu = 1;
     int64_t groups = (int64_t)num_cu * per_cu;
-    const int64_t most = (dv.nb + kGridWaves - 1) / kGridWaves;
+    const int64_t most = (dv.nb + kGridWaves - 2) / (kGridWaves - 1);
     if (groups > most) groups = most;
     if (groups < 1) groups = 1;
     return (int)groups;
@@ -510,7 +628,7 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
     if (e != hipSuccess) return e;
     const int slots = a.max_depth > 1 ? a.max_depth : 1;
     const size_t lds = (size_t)slots * 2 * a.data.D * sizeof(double);
-    void* k = pick_grid_kernel(a.data.dtype, a.data.D);
+    void* k = pick_grid_kernel(a.data.dtype, a.data.split);
     SamplerArgs A = a;
     void* args[] = {&A, &groups, &partials, &result, &sync};
     return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);

@@ -130,4 +130,6 @@ def test_covtype_first_iterations(sampler, orc, name):
     r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
                        num_warmup=0, num_samples=iters, seed=wl.seed, path=2)
     ref = _oracle_chain(orc, X, y, wl, 0, iters)
-    compare_chain(r["samples"][0], r["stats"][0], ref)
+    # fp32 data: the per-row exp/log/reciprocal run in fp32 (~1e-6 relative
+    # per row), so positions drift apart at the 1e-8 level over the run
+    compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-9 if wl.dtype == "f64" else 1e-6)
