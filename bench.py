@@ -141,12 +141,23 @@ def main():
                     help="second workload reported beside the first ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (a known-size "
+                         "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
+    if args.copy_mb:
+        import torch
+        src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.copy_mb} MiB read + {args.copy_mb} MiB written")
+        del src, dst
     main_res = run_workload(args.workload, args.steps, args.warmup)
     other = run_workload(args.also, args.steps, args.warmup) if args.also else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
