@@ -10,8 +10,9 @@
 
 namespace nuts {
 
-// Device layout of one or more data sets: X as column blocks of R = 64 / S
-// rows (S lanes of a wavefront share a row), block b of data set s at element
+// Device layout of one or more data sets: X as column blocks of R rows
+// (R = 64 / S for fp64, 128 / S for fp32; S lanes of a wavefront share a row,
+// each lane takes one fp64 or two fp32 rows), block b of data set s at element
 // offset (s * nb + b) * D * R, column c of the block at + c * R, row r of the
 // block at + r; rows past N are zero.  y as bytes at (s * nb + b) * R + r,
 // zero past N.
@@ -30,10 +31,10 @@ struct DataView {
 constexpr int kColsPerLane = 8;
 
 // Zeroed elements after the last block of an X allocation: the data pass
-// reads up to kColsPerLane * 64 elements from a block's start.
-constexpr int64_t kTailElems = (int64_t)kColsPerLane * 64;
+// reads up to kColsPerLane * 128 elements from a block's start.
+constexpr int64_t kTailElems = (int64_t)kColsPerLane * 128;
 
-inline int rows_per_block(const DataView& dv) { return 64 / dv.split; }
+inline int rows_per_block(const DataView& dv) { return (dv.dtype == NUTS_F32 ? 128 : 64) / dv.split; }
 
 // Largest D the lane-per-dimension kernels accept: dimension d lives in lane d
 // and lane 63 carries the potential through the reductions.
@@ -78,17 +79,15 @@ struct SamplerArgs {
 // One wavefront per chain: launches ceil(C / 4) groups of four waves.
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream);
 
-// One chain over the whole device.  `sync` holds the grid-barrier counters,
-// zeroed by this call; `partials` holds [2][groups][64] doubles, `result`
-// [2][64].  Returns the group count used through *groups_used.
+// One chain over the whole device.  `sync` holds the arrival counter and the
+// error flag, zeroed by this call; `partials` holds [2][groups][64] doubles,
+// `result` [2][64] (marked empty by this call).
 struct GridSync {
-    unsigned long long counter;          // arrivals of slot leaders, (step + 1) * 8 after step
+    unsigned long long counter;          // completed group slots, (step + 1) * min(groups, 8) after step
     unsigned long long pad0[15];
-    unsigned long long flag;             // step + 1 once the result of step is published
-    unsigned long long pad1[15];
     unsigned int error;                  // a wait timed out
-    unsigned int pad2[31];
-    unsigned long long slot[8][16];      // arrivals per group slot (group index mod 8)
+    unsigned int pad1[31];
+    unsigned long long slot[8][16];      // group arrivals per slot (group index mod 8)
 };
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream);

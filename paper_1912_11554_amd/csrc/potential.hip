@@ -19,7 +19,7 @@ __global__ void __launch_bounds__(kPotWaves * kWave, 4) potential_pass_kernel(Da
                                                                            int G,
                                                                            double* __restrict__ partials)
 {
-    constexpr int R = RowSplit<S>::R;
+    constexpr int R = BlockShape<T, S>::R;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
     const int64_t k = blockIdx.y;
@@ -37,10 +37,8 @@ __global__ void __launch_bounds__(kPotWaves * kWave, 4) potential_pass_kernel(Da
     for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
     double loss = 0.0;
 
-    const int64_t stride = (int64_t)G * kPotWaves;
-#pragma unroll 1
-    for (int64_t b = (int64_t)g * kPotWaves + wave; b < dv.nb; b += stride)
-        accumulate_block<T, CPS, S>(X + b * D * R, y + b * R, D, dv.N - b * R, qv, acc, loss);
+    stream_blocks<T, CPS, S>(X, y, D, dv.N, dv.nb, (int64_t)g * kPotWaves + wave, (int64_t)G * kPotWaves, qv,
+                             acc, loss);
 
     const double col = finish_pass<CPS, S>(acc, loss);
     __shared__ double part[kPotWaves][kWave];

@@ -1,11 +1,12 @@
 // The data pass of the logistic potential on gfx950.
 //
-// Layout: X is stored in blocks of R = 64 / S rows; inside a block, column c
-// is R consecutive elements (one per row).  A wavefront processes one block
-// per step: lane L works on row L / S and on the columns c = k * S + L % S,
-// k < CPS, so that S lanes share a row and each holds at most CPS columns in
-// registers.  For a fixed k the 64 lanes read columns k*S .. k*S + S - 1 of
-// all R rows: one contiguous 64-element segment per load instruction.
+// Layout: X is stored in blocks of R = RPL * 64 / S rows; inside a block,
+// column c is R consecutive elements (one per row).  A wavefront processes one
+// block per step: lane L works on rows RPL * (L / S) .. + RPL - 1 (RPL = 2 for
+// fp32, 1 for fp64) and on the columns c = k * S + L % S, k < CPS, so that S
+// lanes share a row and each holds at most CPS columns in registers.  For a
+// fixed k the 64 lanes read columns k*S .. k*S + S - 1 of all R rows: one
+// contiguous 512-byte segment per load instruction.
 //
 // Per row: the S partial dot products are combined with xor shuffles (every
 // lane of the row ends with the same eta), the loss and residual follow from
@@ -26,57 +27,138 @@ __host__ __device__ constexpr int lanes_per_row(int D, int CPS)
     return D <= CPS ? 1 : D <= 2 * CPS ? 2 : D <= 4 * CPS ? 4 : D <= 8 * CPS ? 8 : D <= 16 * CPS ? 16 : 32;
 }
 
-template <int S>
-struct RowSplit {
-    static_assert(S >= 1 && S <= 32 && (S & (S - 1)) == 0, "S is a power of two");
-    static constexpr int R = kWave / S;  // rows per block
-    static constexpr int LOG_S = S == 1 ? 0 : S == 2 ? 1 : S == 4 ? 2 : S == 8 ? 3 : S == 16 ? 4 : 5;
+// Rows per lane: fp32 blocks give each lane two consecutive rows so that a
+// load instruction moves 512 bytes, as for fp64.
+template <typename T>
+struct RowsPerLane {
+    static constexpr int value = sizeof(T) == 4 ? 2 : 1;
 };
 
-// qv[k] must hold q[k * S + L % S], which is zero for columns c >= D.  The
-// loads are unconditional: a slot past column D - 1 reads the next block's
-// memory (or the zeroed tail of the allocation, at least kTailElems long), a
-// finite value that meets a zero position in eta and only feeds an
-// accumulator slot that is never output.
+template <typename T, int N>
+struct VecOf;
+template <>
+struct VecOf<float, 2> {
+    using type = float2;
+};
+template <>
+struct VecOf<double, 1> {
+    using type = double;
+};
+
+template <typename T, int S>
+struct BlockShape {
+    static constexpr int RPL = RowsPerLane<T>::value;
+    static constexpr int R = RPL * kWave / S;  // rows per block
+};
+
+// Raw registers of one block for one lane: CPS column slots of RPL rows,
+// and the RPL labels.
 template <typename T, int CPS, int S>
-__device__ __forceinline__ void accumulate_block(const T* __restrict__ blk,
-                                                 const uint8_t* __restrict__ yb, int D,
-                                                 int64_t rows_left, const double (&qv)[CPS],
-                                                 double (&acc)[CPS], double& loss)
+struct BlockRegs {
+    using V = typename VecOf<T, BlockShape<T, S>::RPL>::type;
+    V x[CPS];
+    uint8_t y[BlockShape<T, S>::RPL];
+};
+
+// Issue the loads of one block.  The loads are unconditional: a slot past
+// column D - 1 reads the next block's memory (or the zeroed tail of the
+// allocation, at least kTailElems long), a finite value that meets a zero
+// position component in eta and only feeds an accumulator slot that is
+// never output.
+template <typename T, int CPS, int S>
+__device__ __forceinline__ BlockRegs<T, CPS, S> load_block(const T* __restrict__ blk,
+                                                           const uint8_t* __restrict__ yb)
 {
-    constexpr int R = RowSplit<S>::R;
+    using B = BlockRegs<T, CPS, S>;
+    constexpr int RPL = BlockShape<T, S>::RPL;
+    constexpr int R = BlockShape<T, S>::R;
     const int L = lane();
     const int p = L & (S - 1);
-    const int row = L / S;
-    const T* base = blk + p * R + row;
-    (void)D;
-    double x[CPS];
+    const int row0 = (L / S) * RPL;
+    const T* base = blk + p * R + row0;
+    B out;
 #pragma unroll
-    for (int k = 0; k < CPS; ++k) x[k] = (double)base[k * S * R];
-    double eta = 0.0;
+    for (int k = 0; k < CPS; ++k) out.x[k] = *reinterpret_cast<const typename B::V*>(base + k * S * R);
 #pragma unroll
-    for (int k = 0; k < CPS; ++k) eta = fma(x[k], qv[k], eta);
-    if constexpr (S >= 2) eta += pair_move<1>(eta);
-    if constexpr (S >= 4) eta += pair_move<2>(eta);
-    if constexpr (S >= 8) eta += pair_move<4>(eta);
-    if constexpr (S >= 16) eta += pair_move<8>(eta);
-    if constexpr (S >= 32) eta += pair_move<16>(eta);
-    const RowTerms rt = logistic_row_t<T>(eta, yb[row] != 0);
-    const bool valid = row < rows_left;
-    const double r = valid ? rt.resid : 0.0;
-    loss += (valid && p == 0) ? rt.loss : 0.0;
+    for (int i = 0; i < RPL; ++i) out.y[i] = yb[row0 + i];
+    return out;
+}
+
+// Rows of one loaded block.  qv[k] must hold q[k * S + L % S] (zero for
+// columns c >= D).
+template <typename T, int CPS, int S>
+__device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, int64_t rows_left,
+                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss)
+{
+    constexpr int RPL = BlockShape<T, S>::RPL;
+    const int L = lane();
+    const int p = L & (S - 1);
+    const int row0 = (L / S) * RPL;
+    double x[RPL][CPS];
 #pragma unroll
-    for (int k = 0; k < CPS; ++k) acc[k] = fma(r, x[k], acc[k]);
+    for (int k = 0; k < CPS; ++k) {
+        if constexpr (RPL == 2) {
+            x[0][k] = (double)in.x[k].x;
+            x[1][k] = (double)in.x[k].y;
+        } else {
+            x[0][k] = (double)in.x[k];
+        }
+    }
+    double r[RPL];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+        double eta = 0.0;
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) eta = fma(x[i][k], qv[k], eta);
+        if constexpr (S >= 2) eta += pair_move<1>(eta);
+        if constexpr (S >= 4) eta += pair_move<2>(eta);
+        if constexpr (S >= 8) eta += pair_move<4>(eta);
+        if constexpr (S >= 16) eta += pair_move<8>(eta);
+        if constexpr (S >= 32) eta += pair_move<16>(eta);
+        const RowTerms rt = logistic_row_t<T>(eta, in.y[i] != 0);
+        const bool valid = row0 + i < rows_left;
+        r[i] = valid ? rt.resid : 0.0;
+        loss += (valid && p == 0) ? rt.loss : 0.0;
+    }
+#pragma unroll
+    for (int k = 0; k < CPS; ++k) {
+#pragma unroll
+        for (int i = 0; i < RPL; ++i) acc[k] = fma(r[i], x[i][k], acc[k]);
+    }
+}
+
+// The blocks first, first + stride, ... < nb of one data set, with the next
+// block's loads in flight while the current block is computed.
+template <typename T, int CPS, int S>
+__device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
+                                              int64_t N, int64_t nb, int64_t first, int64_t stride,
+                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss)
+{
+    constexpr int R = BlockShape<T, S>::R;
+    int64_t b = first;
+    if (b >= nb) return;
+    BlockRegs<T, CPS, S> cur = load_block<T, CPS, S>(X + b * D * R, y + b * R);
+#pragma unroll 1
+    for (;;) {
+        const int64_t nx = b + stride;
+        const bool more = nx < nb;
+        const int64_t lb = more ? nx : b;  // a valid block either way
+        const BlockRegs<T, CPS, S> nxt = load_block<T, CPS, S>(X + lb * D * R, y + lb * R);
+        compute_block<T, CPS, S>(cur, N - b * R, qv, acc, loss);
+        if (!more) break;
+        cur = nxt;
+        b = nx;
+    }
 }
 
 // Lane that holds column c after reduce_rows<CPS, S>.
 template <int CPS, int S>
 __device__ __forceinline__ int column_source_lane(int c)
 {
-    constexpr int R = RowSplit<S>::R;
-    static_assert(CPS <= R, "one slot per row lane at least");
+    constexpr int LANES_PER_PART = kWave / S;
+    static_assert(CPS <= LANES_PER_PART, "one slot per row lane at least");
     const int sigma = c / S, p = c & (S - 1);
-    const int rho = sigma * (R / CPS);
+    const int rho = sigma * (LANES_PER_PART / CPS);
     return (rho * S) | p;
 }
 

@@ -70,7 +70,6 @@ struct WaveEval {
 
     __device__ void eval(double q, double& U, double& g)
     {
-        constexpr int R = RowSplit<S>::R;
         constexpr int CPS = kColsPerLane;
         double qv[CPS];
         spread_position<CPS, S>(q, qv);
@@ -78,9 +77,7 @@ struct WaveEval {
 #pragma unroll
         for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
         double loss = 0.0;
-#pragma unroll 1
-        for (int64_t b = 0; b < nb; ++b)
-            accumulate_block<T, CPS, S>(X + b * D * R, y + b * R, D, N - b * R, qv, acc, loss);
+        stream_blocks<T, CPS, S>(X, y, D, N, nb, 0, 1, qv, acc, loss);
         const double col = finish_pass<CPS, S>(acc, loss);
         const double prior = wave_sum(0.5 * q * q * inv_s2);
         U = loss + prior + prior_const;
@@ -99,7 +96,6 @@ struct GridShared {
     double red[NW][kWave];
     int cmd;
     int last;
-    int abort;
 };
 
 struct GridCtx {
@@ -136,16 +132,32 @@ __device__ __forceinline__ void drain_memory_ops()
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// The result slots hold this bit pattern (a signalling NaN, which no
+// arithmetic produces) until the step's result is written.
+constexpr unsigned long long kEmptySlot = 0x7FF4DEADBEEF0001ull;
+
+__device__ __forceinline__ unsigned long long slot_bits(const double* p)
+{
+    return __hip_atomic_load(reinterpret_cast<unsigned long long*>(const_cast<double*>(p)), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // One collective evaluation for the whole group.  Wave 0 passes the position
 // (lane per dimension) and the command; with kCmdEval every worker streams its
 // blocks and the group joins the grid-wide sum.  Returns the command; on
 // return wave 0 finds the full sums (columns, loss in slot 63) in *out_r.
-// Every wave executes the same workgroup barriers.
+// Controller and workers execute the same workgroup barriers; the workers
+// return as soon as their part is handed over.
+//
+// Step s uses parity buffer s & 1.  Each group stores its partial and counts
+// itself in; the group that completes the count adds all partials in group
+// order, re-arms the other parity's result slots (every controller has read
+// them: it arrived at this step after reading them) and stores the result.
+// Controllers poll their own lane's result slot until it is no longer empty.
 template <typename T, int S, int NW, bool WORKER>
 __device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned long long step, double q,
                                int cmd_in, double* out_r, bool* aborted)
 {
-    constexpr int R = RowSplit<S>::R;
     constexpr int CPS = kColsPerLane;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
@@ -168,12 +180,9 @@ __device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned lo
 #pragma unroll
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
-        const T* X = (const T*)c.X;
         const int workers = NW - 1;
-        const int64_t stride = (int64_t)c.groups * workers;
-#pragma unroll 1
-        for (int64_t b = (int64_t)blockIdx.x * workers + (wave - 1); b < c.nb; b += stride)
-            accumulate_block<T, CPS, S>(X + b * c.D * R, c.y + b * R, c.D, c.N - b * R, qv, acc, loss);
+        stream_blocks<T, CPS, S>((const T*)c.X, c.y, c.D, c.N, c.nb, (int64_t)blockIdx.x * workers + (wave - 1),
+                                 (int64_t)c.groups * workers, qv, acc, loss);
         const double col = finish_pass<CPS, S>(acc, loss);
         mine = (l < c.D) ? col : (l == kWave - 1 ? loss : 0.0);
     }
@@ -186,8 +195,10 @@ __device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned lo
         for (int w = 1; w < NW; ++w) s += sh.red[w][l];
         store_shared(&c.partials[((int64_t)par * c.groups + blockIdx.x) * kWave + l], s);
         drain_memory_ops();
-        // arrival: per slot (group index mod 8) first; the last group of a
-        // slot then arrives at the top counter; the last of those reduces
+        // arrival: per group slot (group index mod 8) first, so that the
+        // atomics spread over eight addresses; the group completing its slot
+        // counts the slot in at the top counter; the group completing the top
+        // count reduces
         int last = 0;
         if (l == 0) {
             const int slot = blockIdx.x & 7;
@@ -202,19 +213,20 @@ __device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned lo
             }
         }
         last = __shfl(last, 0);
-        if (l == 0) {
-            sh.last = last;
-            sh.abort = 0;
-        }
+        if (l == 0) sh.last = last;
     }
     __syncthreads();  // arrival recorded
     if (sh.last) {
-        // last arriver: add the group partials in group order, spread over
-        // the waves, then in wave order
+        // every controller has read the other parity's result by now: re-arm
+        // those slots while the partials load
+        if (wave == 0)
+            __hip_atomic_store(reinterpret_cast<unsigned long long*>(&c.result[(par ^ 1) * kWave + l]), kEmptySlot,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // add the group partials in group order, spread over the waves, then
+        // in wave order
         double s = 0.0;
         const double* src = c.partials + (int64_t)par * c.groups * kWave + l;
         int gg = wave;
-        // loads in batches of 8 independent requests, added in group order
         for (; gg + 7 * NW < c.groups; gg += 8 * NW) {
             double v[8];
 #pragma unroll
@@ -229,34 +241,35 @@ __device__ int grid_collective(const GridCtx& c, GridShared<NW>& sh, unsigned lo
             double tot = 0.0;
 #pragma unroll
             for (int w = 0; w < NW; ++w) tot += sh.red[w][l];
+            drain_memory_ops();  // the re-arm above lands before this result
             store_shared(&c.result[par * kWave + l], tot);
-            drain_memory_ops();
-            if (l == 0) __hip_atomic_store(&c.sync->flag, step + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-    } else if (threadIdx.x == 0) {
-        // wait for the last arriver; give up (and tell every group) after
-        // about 10 s so that a broken invariant can never hang the device
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        int bad = 0;
-        while (__hip_atomic_load(&c.sync->flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < step + 1) {
-            if (__hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
-                bad = 1;
-                break;
-            }
-            if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
-                __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                bad = 1;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-        drain_memory_ops();
-        sh.abort = bad;
     }
-    __syncthreads();  // result published (or the barrier failed)
-    const bool ab = sh.abort != 0;
-    *aborted = ab;
-    if (wave == 0) *out_r = ab ? 0.0 : load_shared(&c.result[par * kWave + l]);
+    if (WORKER) return cmd;
+
+    // controller: wait for this lane's result slot; give up (and tell every
+    // group) after about 10 s so that a broken invariant can never hang the
+    // device
+    const double* slot = &c.result[par * kWave + l];
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool bad = false;
+    unsigned long long bits = kEmptySlot;
+    for (;;) {
+        if (bits == kEmptySlot) bits = slot_bits(slot);
+        if (__all(bits != kEmptySlot)) break;
+        if (__hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+            bad = true;
+            break;
+        }
+        if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
+            if (l == 0) __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            bad = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    *aborted = bad;
+    *out_r = bad ? 0.0 : __builtin_bit_cast(double, bits);
     return cmd;
 }
 
@@ -500,7 +513,7 @@ constexpr int kWaveChainsPerGroup = 4;
 template <typename T, int S>
 __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, 3) sampler_wave_kernel(SamplerArgs A)
 {
-    constexpr int R = RowSplit<S>::R;
+    constexpr int R = BlockShape<T, S>::R;
     extern __shared__ double lds[];
     const int wave = threadIdx.x / kWave;
     const int64_t chain = (int64_t)blockIdx.x * kWaveChainsPerGroup + wave;
@@ -565,6 +578,11 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
 
 }  // namespace
 
+__global__ void fill_empty_slots(double* result)
+{
+    reinterpret_cast<unsigned long long*>(result)[threadIdx.x] = kEmptySlot;
+}
+
 template <typename T, int S>
 static hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
 {
@@ -625,6 +643,9 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
                                GridSync* sync, hipStream_t stream)
 {
     hipError_t e = hipMemsetAsync(sync, 0, sizeof(GridSync), stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fill_empty_slots, dim3(1), dim3(2 * kWave), 0, stream, result);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int slots = a.max_depth > 1 ? a.max_depth : 1;
     const size_t lds = (size_t)slots * 2 * a.data.D * sizeof(double);
