@@ -216,7 +216,9 @@ int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N,
     d->view.N = N;
     d->view.D = (int)D;
     d->view.dtype = dtype;
-    d->view.split = lanes_per_row((int)D, kColsPerLane);
+    const PassShape shape = pass_shape((int)D);
+    d->view.split = shape.split;
+    d->view.cols = shape.cols;
     const int R = rows_per_block(d->view);
     d->view.nb = (N + R - 1) / R;
     d->view.nds = num_datasets;
@@ -295,7 +297,7 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     HIP_TRY(h, stage_out(out_U, (size_t)K * 8, ut, &Ud));
     HIP_TRY(h, stage_out(out_grad, (size_t)K * D * 8, gt, &Gd));
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
-    HIP_TRY(h, part.alloc((size_t)K * plan.groups_per_item * 64 * sizeof(double)));
+    HIP_TRY(h, part.alloc((size_t)K * plan.groups_per_item * plan.width * sizeof(double)));
     HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part.p,
                                      (double*)Ud, (double*)Gd, h->stream));
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
@@ -360,12 +362,15 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     if (path == NUTS_PATH_AUTO) {
         // one wave per chain when there are many chains or the data is small;
         // the whole device on one chain when the data is large
-        const bool small = d->view.nb <= 64;
-        path = (per_chain || small || num_chains > 1) ? NUTS_PATH_WAVE : NUTS_PATH_GRID;
+        const bool small = d->view.N <= 4096;
+        path = ((per_chain || small || num_chains > 1) && wave_path_supports(d->view)) ? NUTS_PATH_WAVE
+                                                                                       : NUTS_PATH_GRID;
     }
     if (path != NUTS_PATH_WAVE && path != NUTS_PATH_GRID) return fail(h, NUTS_EINVAL, "unknown path %d", path);
     if (path == NUTS_PATH_GRID && per_chain)
         return fail(h, NUTS_EUNSUPPORTED, "the grid path runs chains on shared data only");
+    if (path == NUTS_PATH_WAVE && !wave_path_supports(d->view))
+        return fail(h, NUTS_EUNSUPPORTED, "the one-wave-per-chain path takes D <= 64 (got %d)", d->view.D);
 
     DeviceScope ds(h->device);
     hipStream_t s = h->stream;
@@ -408,8 +413,9 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     } else {
         const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
         DevBuf part, res, sync;
-        HIP_TRY(h, part.alloc((size_t)2 * groups * 64 * sizeof(double)));
-        HIP_TRY(h, res.alloc((size_t)2 * 64 * sizeof(double)));
+        const int W = partial_width(D);
+        HIP_TRY(h, part.alloc((size_t)2 * groups * W * sizeof(double)));
+        HIP_TRY(h, res.alloc((size_t)2 * W * sizeof(double)));
         HIP_TRY(h, sync.alloc(sizeof(GridSync)));
         for (int64_t c = 0; c < C; ++c) {
             SamplerArgs ac = a;

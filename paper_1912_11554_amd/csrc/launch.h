@@ -10,44 +10,66 @@
 
 namespace nuts {
 
+// Largest D the kernels accept: lanes hold up to 5 dimensions each.
+constexpr int kMaxDim = 320;
+
+// Shape of the data pass for D columns: S lanes of a wavefront share a row
+// and each lane holds `cols` column slots of it (slot k of lane part p is
+// column k * S + p); `dims` = ceil(D / 64) dimensions per lane in the tree
+// state (dimension d in lane d % 64, component d / 64).
+struct PassShape {
+    int split;  // S
+    int cols;   // CPS
+    int dims;   // DPL
+};
+
+inline PassShape pass_shape(int D)
+{
+    const int dims = (D + 63) / 64;
+    if (D <= 8) return {1, 8, dims};
+    if (D <= 16) return {2, 8, dims};
+    if (D <= 32) return {4, 8, dims};
+    if (D <= 64) return {8, 8, dims};
+    if (D <= 128) return {16, 8, dims};
+    if (D <= 256) return {32, 8, dims};
+    return {32, 10, dims};
+}
+
 // Device layout of one or more data sets: X as column blocks of R rows
-// (R = 64 / S for fp64, 128 / S for fp32; S lanes of a wavefront share a row,
-// each lane takes one fp64 or two fp32 rows), block b of data set s at element
-// offset (s * nb + b) * D * R, column c of the block at + c * R, row r of the
-// block at + r; rows past N are zero.  y as bytes at (s * nb + b) * R + r,
-// zero past N.
+// (R = 64 / S for fp64, 128 / S for fp32; each lane takes one fp64 or two
+// fp32 rows), block b of data set s at element offset (s * nb + b) * D * R,
+// column c of the block at + c * R, row r of the block at + r; rows past N
+// are zero.  y as bytes at (s * nb + b) * R + r, zero past N.
 struct DataView {
     const void* X;
     const uint8_t* y;
     int64_t N;
     int D;
     int dtype;        // NUTS_F64 or NUTS_F32
-    int split;        // S: lanes per row, 64 / rows per block
+    int split;        // S
+    int cols;         // CPS
     int64_t nb;       // ceil(N / R)
     int64_t nds;      // number of data sets
 };
 
-// Columns one lane holds in registers during the data pass.
-constexpr int kColsPerLane = 8;
-
 // Zeroed elements after the last block of an X allocation: the data pass
-// reads up to kColsPerLane * 128 elements from a block's start.
-constexpr int64_t kTailElems = (int64_t)kColsPerLane * 128;
+// reads up to cols * S * R <= 10 * 128 elements from a block's start.
+constexpr int64_t kTailElems = 2048;
 
 inline int rows_per_block(const DataView& dv) { return (dv.dtype == NUTS_F32 ? 128 : 64) / dv.split; }
 
-// Largest D the lane-per-dimension kernels accept: dimension d lives in lane d
-// and lane 63 carries the potential through the reductions.
-constexpr int kMaxDim = 63;
+// Width of one partial-sum row: the D columns padded to whole lanes, then
+// one more lane-row whose slot 0 is the loss sum.
+inline int partial_width(int D) { return 64 * ((D + 63) / 64 + 1); }
 
 hipError_t launch_to_blocks(const void* X_rowmajor, const uint8_t* y_in, DataView dst,
                             void* X_out, uint8_t* y_out, unsigned int* bad_label,
                             hipStream_t stream);
 
-// Workspace of the batched potential/gradient: partial sums [K][G][64].
+// Workspace of the batched potential/gradient: partial sums [K][G][width].
 struct PotentialPlan {
     int groups_per_item;  // G
-    int waves_per_group;
+    int width;            // partial_width(D)
 };
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu);
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
@@ -76,12 +98,14 @@ struct SamplerArgs {
     unsigned long long* grad_evals;  // [C]
 };
 
-// One wavefront per chain: launches ceil(C / 4) groups of four waves.
+// One wavefront per chain (D <= 64): ceil(C / 4) groups of four waves.
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream);
+bool wave_path_supports(const DataView& dv);
 
-// One chain over the whole device.  `sync` holds the arrival counter and the
-// error flag, zeroed by this call; `partials` holds [2][groups][64] doubles,
-// `result` [2][64] (marked empty by this call).
+// One chain over the whole device.  `sync` holds the arrival counters and
+// the error flag, zeroed by this call; `partials` holds
+// [2][groups][partial_width(D)] doubles, `result` [2][partial_width(D)]
+// (marked empty by this call).
 struct GridSync {
     unsigned long long counter;          // completed group slots, (step + 1) * min(groups, 8) after step
     unsigned long long pad0[15];
@@ -92,5 +116,12 @@ struct GridSync {
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream);
 int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu);
+
+// Per-dtype kernel entry points (sampler_f32.hip, sampler_f64.hip).
+hipError_t launch_sampler_wave_f32(const SamplerArgs& a, hipStream_t stream);
+hipError_t launch_sampler_wave_f64(const SamplerArgs& a, hipStream_t stream);
+const void* grid_kernel_f32(const DataView& dv);
+const void* grid_kernel_f64(const DataView& dv);
+constexpr int kGridWaves = 16;  // per group: 1 controller + 15 workers
 
 }  // namespace nuts

@@ -200,6 +200,38 @@ __device__ __forceinline__ double reduce_rows(double (&a)[CPS])
     return v;
 }
 
+// Sum the per-lane accumulators over the rows of the wave (lane bits from 32
+// down to S) with plain xor butterflies, then store column k * S + p's
+// total from the lanes of row 0 into row[] (columns < D only) and the loss
+// total into row[loss_slot].  For wide rows, where the transposing
+// reduction has too few row lanes per slot.
+template <int BIT, int S, int CPS>
+__device__ __forceinline__ void add_over_rows(double (&a)[CPS])
+{
+    if constexpr (BIT >= S) {
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) a[k] += xor_move<BIT>(a[k]);
+        add_over_rows<BIT / 2, S>(a);
+    }
+}
+
+template <int CPS, int S>
+__device__ __forceinline__ void finish_pass_to_row(double (&acc)[CPS], double loss, double* row, int D,
+                                                   int loss_slot)
+{
+    add_over_rows<kWave / 2, S>(acc);
+    loss = wave_sum(loss);
+    const int L = lane();
+    if (L < S) {
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) {
+            const int c = k * S + L;
+            if (c < D) row[c] = acc[k];
+        }
+    }
+    if (L == 0) row[loss_slot] = loss;
+}
+
 // Finish a wave's pass: column c's wave total in lane c (c < CPS * S, zero
 // elsewhere), and the wave's total loss in every lane.
 template <int CPS, int S>
@@ -219,6 +251,18 @@ __device__ __forceinline__ void spread_position(double q, double (&qv)[CPS])
     const int p = lane() & (S - 1);
 #pragma unroll
     for (int k = 0; k < CPS; ++k) qv[k] = __shfl(q, (k * S + p) & (kWave - 1));
+}
+
+// The same from a position vector in LDS (zero past D).
+template <int CPS, int S>
+__device__ __forceinline__ void spread_position_lds(const double* q, int D, double (&qv)[CPS])
+{
+    const int p = lane() & (S - 1);
+#pragma unroll
+    for (int k = 0; k < CPS; ++k) {
+        const int c = k * S + p;
+        qv[k] = c < D ? q[c] : 0.0;
+    }
 }
 
 }  // namespace nuts

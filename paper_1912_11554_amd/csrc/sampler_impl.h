@@ -1,0 +1,737 @@
+// Device-resident NUTS: trajectory doubling with the iterative tree builder,
+// leapfrog steps, multinomial / biased-progressive proposal selection, U-turn
+// and divergence checks, all inside one kernel launch.
+//
+// Tree state is held lane-per-dimension: dimension d lives in lane d % 64,
+// component d / 64 (DPL = ceil(D / 64) components per lane).  Every lane
+// keeps its components of the phase-space vectors (position q, momentum p,
+// gradient g) of the current leaf, both trajectory edges, the proposal and
+// the subtree proposal.  Dot products are DPP wave sums, so every lane (and,
+// on the grid path, the controller wave of every group) holds bit-identical
+// scalars and takes identical decisions.  Dimensions >= D carry zeros.
+//
+// Two evaluators supply U and grad U at a position:
+//   WaveEval -- one wave streams its chain's data set (small data; one wave
+//               per chain, thousands of chains per launch; D <= 64);
+//   GridEval -- one chain on the whole device.  In every group, wave 0 is the
+//               controller (it runs the tree logic) and the other waves are
+//               workers (they stream a slice of the rows).  Group partials
+//               meet in a grid-wide exchange whose last arriver adds them in
+//               group order.  Controller and workers run the same collective
+//               with the same workgroup barriers; only the workers' copy
+//               contains the data pass, so tree state and data-pass
+//               registers are never live together.
+//
+// Algorithmic sources: Appendix A of arXiv 1912.11554 (Alg. 2 iterative tree,
+// the S array indexed by BitCount, candidate set C(n)); Hoffman & Gelman 2014,
+// Alg. 6 (direction per doubling, endpoint U-turn rule, Delta_max = 1000);
+// Betancourt 2017, App. A (multinomial and biased progressive selection).
+#pragma once
+
+#include "launch.h"
+#include "rows.h"
+
+namespace nuts {
+namespace sampler {
+
+constexpr int kTreeOk = 0, kTreeTurning = 1, kTreeDivergent = 2;
+constexpr double kHalfLog2Pi = 0.91893853320467274178032973640562;
+
+template <int DPL>
+struct Node {
+    double q[DPL], p[DPL], g[DPL];  // this lane's components
+    double U;                       // wave-uniform
+};
+
+template <int DPL>
+__device__ __forceinline__ double dot3(const double (&a)[DPL], const double (&b)[DPL], const double (&c)[DPL])
+{
+    double s = 0.0;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) s += a[m] * b[m] * c[m];
+    return wave_sum(s);
+}
+
+// Endpoint U-turn test on time-ordered ends: (a, b) are the first- and
+// last-generated nodes of a subtree built in direction v.
+template <int DPL>
+__device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (&pa)[DPL], const double (&qb)[DPL],
+                                         const double (&pb)[DPL], int v, const double (&im)[DPL])
+{
+    double sl = 0.0, sr = 0.0;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        const double qL = v > 0 ? qa[m] : qb[m], pL = v > 0 ? pa[m] : pb[m];
+        const double qR = v > 0 ? qb[m] : qa[m], pR = v > 0 ? pb[m] : pa[m];
+        const double dq = qR - qL;
+        sl += dq * im[m] * pL;
+        sr += dq * im[m] * pR;
+    }
+    const double dl = wave_sum(sl);
+    const double dr = wave_sum(sr);
+    return uni((dl < 0.0) || (dr < 0.0));
+}
+
+// Evaluator interface: eval(q, U, g) with q, g lane-per-dimension arrays;
+// s_writer() says whether this wave stores the checkpoint array S,
+// out_writer() whether it stores the chain's outputs; aborted() reports a
+// failed grid exchange.
+
+template <typename T, int S>
+struct WaveEval {
+    const T* X;
+    const uint8_t* y;
+    int64_t N, nb;
+    int D;
+    double inv_s2, prior_const;
+
+    __device__ bool s_writer() const { return true; }
+    __device__ bool out_writer() const { return true; }
+    __device__ bool aborted() const { return false; }
+
+    __device__ void eval(const double (&q)[1], double& U, double (&g)[1])
+    {
+        constexpr int CPS = 8;
+        double qv[CPS];
+        spread_position<CPS, S>(q[0], qv);
+        double acc[CPS];
+#pragma unroll
+        for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
+        double loss = 0.0;
+        stream_blocks<T, CPS, S>(X, y, D, N, nb, 0, 1, qv, acc, loss);
+        const double col = finish_pass<CPS, S>(acc, loss);
+        const double prior = wave_sum(0.5 * q[0] * q[0] * inv_s2);
+        U = loss + prior + prior_const;
+        g[0] = (lane() < D) ? col + q[0] * inv_s2 : 0.0;
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Grid path.
+
+constexpr int kCmdEval = 1, kCmdExit = 2;
+
+template <int DPL, int NW>
+struct GridShared {
+    static constexpr int W = 64 * (DPL + 1);  // partial_width(D)
+    double qbuf[64 * DPL];
+    double red[NW][W];
+    int cmd;
+    int last;
+};
+
+struct GridCtx {
+    const void* X;
+    const uint8_t* y;
+    int64_t N, nb;
+    int D;
+    int groups;
+    double* partials;  // [2][groups][W]
+    double* result;    // [2][W]
+    GridSync* sync;
+};
+
+// Cross-group exchange.  Everything that one group publishes for another
+// (partials, the result, counters) is written and read with agent-scope
+// atomic accesses, which the L2 keeps coherent across the XCDs one access at
+// a time.  Ordering between them comes from waiting for the wave's
+// outstanding memory operations (s_waitcnt) before the next one is issued.
+// No whole-cache write-back or invalidate (what a device-scope fence does) is
+// needed: no ordinary store has to become visible to another group, and no
+// ordinary load may observe another group's writes.
+__device__ __forceinline__ void store_shared(double* p, double v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double load_shared(const double* p)
+{
+    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void drain_memory_ops()
+{
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// The result slots hold this bit pattern (a signalling NaN, which no
+// arithmetic produces) until the step's result is written.
+constexpr unsigned long long kEmptySlot = 0x7FF4DEADBEEF0001ull;
+
+__device__ __forceinline__ unsigned long long slot_bits(const double* p)
+{
+    return __hip_atomic_load(reinterpret_cast<unsigned long long*>(const_cast<double*>(p)), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One collective evaluation for the whole group.  Wave 0 passes the position
+// and the command; with kCmdEval every worker streams its blocks and the
+// group joins the grid-wide sum.  Returns the command; on return wave 0 finds
+// the full sums in out_r: component m of lane l is column l + 64 m, and
+// component DPL of lane 0 is the loss.  Controller and workers execute the
+// same workgroup barriers; the workers return as soon as their part is
+// handed over.
+//
+// Step s uses parity buffer s & 1.  Each group stores its partial and counts
+// itself in; the group that completes the count adds all partials in group
+// order, re-arms the other parity's result slots (every controller has read
+// them: it arrived at this step after reading them) and stores the result.
+// Controllers poll their own lane's result slots until none is empty.
+template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
+__device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step,
+                               const double (&q)[DPL], int cmd_in, double (&out_r)[DPL + 1], bool* aborted)
+{
+    constexpr int W = GridShared<DPL, NW>::W;
+    const int l = lane();
+    const int wave = threadIdx.x / kWave;
+    const int par = (int)(step & 1);
+    if (wave == 0) {
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) sh.qbuf[l + 64 * m] = q[m];
+        if (l == 0) sh.cmd = cmd_in;
+    }
+    __syncthreads();  // position and command published
+    const int cmd = sh.cmd;
+    if (cmd == kCmdExit) return cmd;
+
+    if (WORKER) {
+        double qv[CPS];
+        spread_position_lds<CPS, S>(sh.qbuf, c.D, qv);
+        double acc[CPS];
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
+        double loss = 0.0;
+        const int workers = NW - 1;
+        stream_blocks<T, CPS, S>((const T*)c.X, c.y, c.D, c.N, c.nb, (int64_t)blockIdx.x * workers + (wave - 1),
+                                 (int64_t)c.groups * workers, qv, acc, loss);
+        if constexpr (S <= 8 && CPS == 8) {
+            const double col = finish_pass<CPS, S>(acc, loss);
+            if (l < c.D) sh.red[wave][l] = col;
+            if (l == 0) sh.red[wave][64 * DPL] = loss;
+        } else {
+            finish_pass_to_row<CPS, S>(acc, loss, sh.red[wave], c.D, 64 * DPL);
+        }
+    }
+    __syncthreads();  // group partials in LDS
+
+    if (wave == 0) {
+#pragma unroll
+        for (int m = 0; m <= DPL; ++m) {
+            const int col = l + 64 * m;
+            const bool used = (m < DPL) ? (col < c.D) : (l == 0);
+            double s = 0.0;
+            if (used) {
+#pragma unroll
+                for (int w = 1; w < NW; ++w) s += sh.red[w][col];
+            }
+            store_shared(&c.partials[((int64_t)par * c.groups + blockIdx.x) * W + col], s);
+        }
+        drain_memory_ops();
+        // arrival: per group slot (group index mod 8) first, so that the
+        // atomics spread over eight addresses; the group completing its slot
+        // counts the slot in at the top counter; the group completing the top
+        // count reduces
+        int last = 0;
+        if (l == 0) {
+            const int slot = blockIdx.x & 7;
+            const unsigned long long per = (unsigned long long)((c.groups - slot + 7) / 8);
+            const unsigned long long o =
+                __hip_atomic_fetch_add(&c.sync->slot[slot][0], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (o + 1 == (step + 1) * per) {
+                const unsigned long long slots = c.groups < 8 ? (unsigned long long)c.groups : 8ull;
+                const unsigned long long t =
+                    __hip_atomic_fetch_add(&c.sync->counter, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                last = (t + 1 == (step + 1) * slots) ? 1 : 0;
+            }
+        }
+        last = __shfl(last, 0);
+        if (l == 0) sh.last = last;
+    }
+    __syncthreads();  // arrival recorded
+    if (sh.last) {
+        // every controller has read the other parity's result by now: re-arm
+        // those slots while the partials load
+        if (wave == 0) {
+#pragma unroll
+            for (int m = 0; m <= DPL; ++m)
+                __hip_atomic_store(reinterpret_cast<unsigned long long*>(&c.result[(par ^ 1) * W + l + 64 * m]),
+                                   kEmptySlot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // add the group partials in group order, spread over the waves, then
+        // in wave order
+        double s[DPL + 1];
+#pragma unroll
+        for (int m = 0; m <= DPL; ++m) s[m] = 0.0;
+        const double* src = c.partials + (int64_t)par * c.groups * W + l;
+        constexpr int B = DPL <= 1 ? 8 : 4;
+        int gg = wave;
+        for (; gg + (B - 1) * NW < c.groups; gg += B * NW) {
+            double v[B][DPL + 1];
+#pragma unroll
+            for (int i = 0; i < B; ++i)
+#pragma unroll
+                for (int m = 0; m <= DPL; ++m) v[i][m] = load_shared(src + (int64_t)(gg + i * NW) * W + 64 * m);
+#pragma unroll
+            for (int i = 0; i < B; ++i)
+#pragma unroll
+                for (int m = 0; m <= DPL; ++m) s[m] += v[i][m];
+        }
+        for (; gg < c.groups; gg += NW)
+#pragma unroll
+            for (int m = 0; m <= DPL; ++m) s[m] += load_shared(src + (int64_t)gg * W + 64 * m);
+#pragma unroll
+        for (int m = 0; m <= DPL; ++m) sh.red[wave][l + 64 * m] = s[m];
+        __syncthreads();  // per-wave sums in LDS
+        if (wave == 0) {
+            double tot[DPL + 1];
+#pragma unroll
+            for (int m = 0; m <= DPL; ++m) {
+                tot[m] = 0.0;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) tot[m] += sh.red[w][l + 64 * m];
+            }
+            drain_memory_ops();  // the re-arm above lands before this result
+#pragma unroll
+            for (int m = 0; m <= DPL; ++m) store_shared(&c.result[par * W + l + 64 * m], tot[m]);
+        }
+    }
+    if (WORKER) return cmd;
+
+    // controller: wait for this lane's result slots; give up (and tell every
+    // group) after about 10 s so that a broken invariant can never hang the
+    // device
+    const double* slot = &c.result[par * W + l];
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool bad = false;
+    unsigned long long bits[DPL + 1];
+#pragma unroll
+    for (int m = 0; m <= DPL; ++m) bits[m] = kEmptySlot;
+    for (;;) {
+        bool ready = true;
+#pragma unroll
+        for (int m = 0; m <= DPL; ++m) {
+            if (bits[m] == kEmptySlot) bits[m] = slot_bits(slot + 64 * m);
+            ready = ready && bits[m] != kEmptySlot;
+        }
+        if (__all(ready)) break;
+        if (__hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+            bad = true;
+            break;
+        }
+        if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
+            if (l == 0) __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            bad = true;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    *aborted = bad;
+#pragma unroll
+    for (int m = 0; m <= DPL; ++m) out_r[m] = bad ? 0.0 : __builtin_bit_cast(double, bits[m]);
+    return cmd;
+}
+
+template <typename T, int S, int CPS, int DPL, int NW>
+struct GridEval {
+    GridCtx c;
+    GridShared<DPL, NW>* sh;
+    double inv_s2, prior_const;
+    unsigned long long step;
+    bool abort;
+
+    __device__ bool s_writer() const { return true; }  // only the controller runs the chain
+    __device__ bool out_writer() const { return blockIdx.x == 0; }
+    __device__ bool aborted() const { return abort; }
+
+    __device__ void eval(const double (&q)[DPL], double& U, double (&g)[DPL])
+    {
+        double r[DPL + 1];
+        bool ab = false;
+        grid_collective<T, S, CPS, DPL, NW, false>(c, *sh, step, q, kCmdEval, r, &ab);
+        abort = ab;
+        step++;
+        double pr = 0.0;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) pr += 0.5 * q[m] * q[m] * inv_s2;
+        const double prior = wave_sum(pr);
+        U = readlane_f64(r[DPL], 0) + prior + prior_const;
+        const int l = lane();
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) g[m] = (l + 64 * m < c.D) ? r[m] + q[m] * inv_s2 : 0.0;
+    }
+
+    __device__ void finish()
+    {
+        double r[DPL + 1];
+        bool ab;
+        double q[DPL];
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) q[m] = 0.0;
+        grid_collective<T, S, CPS, DPL, NW, false>(c, *sh, step, q, kCmdExit, r, &ab);
+    }
+};
+
+template <int DPL>
+__device__ __forceinline__ void copy_node(Node<DPL>& dst, const Node<DPL>& src)
+{
+    dst = src;
+}
+
+// The whole chain: init, warmup + sampling iterations, outputs.  S_arr points
+// to this chain's checkpoint array in LDS: [max(max_depth, 1)][2][D].
+template <int DPL, class Eval>
+__device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double* S_arr)
+{
+    const int l = lane();
+    const int D = A.data.D;
+    bool act[DPL];
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) act[m] = l + 64 * m < D;
+    const int maxd = A.max_depth;
+    const double eps = A.step_size;
+    const uint64_t seed = A.seed;
+    const int64_t cidx = A.chain_offset + chain;
+    const uint64_t key_chain = (uint64_t)cidx;
+    const bool out = ev.out_writer();
+    const bool s_out = ev.s_writer();
+
+    double im[DPL];
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) im[m] = (act[m] && A.inv_mass) ? A.inv_mass[l + 64 * m] : 1.0;
+
+    Node<DPL> cur;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        cur.q[m] = (act[m] && A.init_q) ? A.init_q[cidx * D + l + 64 * m] : 0.0;
+        cur.p[m] = 0.0;
+    }
+    ev.eval(cur.q, cur.U, cur.g);
+    unsigned long long evals = 1;
+
+    double wmean[DPL], wm2[DPL];
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) wmean[m] = wm2[m] = 0.0;
+    int64_t wn = 0;
+    const int64_t iters = A.num_warmup + A.num_samples;
+
+    for (int64_t k = 0; k < iters && !ev.aborted(); ++k) {
+        const uint64_t t = (uint64_t)(A.first_iter + k);
+
+        // momentum and initial energy
+        double kin = 0.0;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) {
+            const double xi = act[m] ? momentum_normal(seed, key_chain, t, l + 64 * m) : 0.0;
+            cur.p[m] = act[m] ? xi / sqrt(im[m]) : 0.0;
+            kin += im[m] * cur.p[m] * cur.p[m];
+        }
+        const double H0 = cur.U + 0.5 * wave_sum(kin);
+
+        // per-iteration draws, one doubling per lane: direction bits and the
+        // merge uniforms
+        int dir_bit = 0;
+        double u_merge = 0.0;
+        if (l < maxd) {
+            dir_bit = (int)(draw(seed, key_chain, t, kTagDirection, (uint64_t)l, 0).w0 & 1ull);
+            u_merge = unit53(draw(seed, key_chain, t, kTagMerge, (uint64_t)l, 0).w0);
+        }
+        const uint64_t dirmask = __ballot(dir_bit);
+
+        Node<DPL> left = cur, right = cur, prop = cur;
+        int64_t prop_idx = 0, Lpos = 0, Rpos = 0;
+        double logw_traj = 0.0;
+        int nleaves = 0;
+        double sum_acc = 0.0;
+        int depth = 0, term = -1;
+        uint32_t dirbits = 0;
+        int diverging = 0, turning = 0, maxhit = 0;
+
+        for (int j = 0; j < maxd; ++j) {
+            const int v = ((dirmask >> j) & 1ull) ? 1 : -1;
+            if (v > 0) dirbits |= 1u << j;
+            Node<DPL> z = v > 0 ? right : left;
+            const int64_t e = v > 0 ? Rpos : Lpos;
+            const double h = v * eps;
+            double logw = -INFINITY;
+            Node<DPL> sprop = z;
+            int64_t sprop_idx = 0;
+            int status = kTreeOk;
+            depth = j + 1;
+            const int64_t nleaf = 1ll << j;
+            double u_leaf = 0.0;
+
+            for (int64_t n = 0; n < nleaf; ++n) {
+                if ((n & (kWave - 1)) == 0)
+                    u_leaf = (n + l < nleaf)
+                                 ? unit53(draw(seed, key_chain, t, kTagLeaf, (uint64_t)j, (uint64_t)(n + l)).w0)
+                                 : 0.0;
+                // leapfrog: half kick, drift, gradient, half kick
+                double ph[DPL];
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) {
+                    ph[m] = z.p[m] - 0.5 * h * z.g[m];
+                    z.q[m] = z.q[m] + h * im[m] * ph[m];
+                }
+                ev.eval(z.q, z.U, z.g);
+                if (ev.aborted()) break;
+                double k2 = 0.0;
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) {
+                    z.p[m] = ph[m] - 0.5 * h * z.g[m];
+                    k2 += im[m] * z.p[m] * z.p[m];
+                }
+                ++nleaves;
+
+                const double dH = (z.U + 0.5 * wave_sum(k2)) - H0;
+                if (dH == dH) sum_acc += dH > 0.0 ? exp(-dH) : 1.0;
+                if (uni(!(dH <= 1000.0))) {
+                    status = kTreeDivergent;
+                    term = (int)n;
+                    break;
+                }
+                // streaming multinomial choice inside the subtree
+                const double lam = -dH;
+                const double lw = logaddexp(logw, lam);
+                const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
+                if (uni(u < exp(lam - lw))) {
+                    sprop = z;
+                    sprop_idx = e + v * (n + 1);
+                }
+                logw = lw;
+
+                if ((n & 1) == 0) {
+                    // even leaf: checkpoint into S[BitCount(n)]
+                    const int i = __popcll((unsigned long long)n);
+                    if (s_out) {
+#pragma unroll
+                        for (int m = 0; m < DPL; ++m) {
+                            if (act[m]) {
+                                S_arr[(2 * i) * D + l + 64 * m] = z.q[m];
+                                S_arr[(2 * i + 1) * D + l + 64 * m] = z.p[m];
+                            }
+                        }
+                    }
+                } else {
+                    // odd leaf: test the subtrees that end here, smallest first
+                    const int nl = __builtin_ctzll(~(unsigned long long)n);
+                    const int imax = __popcll((unsigned long long)(n - 1));
+                    const int imin = imax - nl + 1;
+                    bool turned = false;
+                    for (int kk = imax; kk >= imin; --kk) {
+                        double sq[DPL], sp[DPL];
+#pragma unroll
+                        for (int m = 0; m < DPL; ++m) {
+                            sq[m] = act[m] ? S_arr[(2 * kk) * D + l + 64 * m] : 0.0;
+                            sp[m] = act[m] ? S_arr[(2 * kk + 1) * D + l + 64 * m] : 0.0;
+                        }
+                        if (is_uturn<DPL>(sq, sp, z.q, z.p, v, im)) {
+                            turned = true;
+                            break;
+                        }
+                    }
+                    if (turned) {
+                        status = kTreeTurning;
+                        term = (int)n;
+                        break;
+                    }
+                }
+            }
+            if (ev.aborted()) break;
+            if (status != kTreeOk) {
+                if (status == kTreeDivergent) diverging = 1;
+                else turning = 1;
+                break;
+            }
+            // biased progressive choice between trajectory and new subtree
+            const double um = __shfl(u_merge, j);
+            if (uni(um < exp(logw - logw_traj))) {
+                prop = sprop;
+                prop_idx = sprop_idx;
+            }
+            logw_traj = logaddexp(logw_traj, logw);
+            if (v > 0) {
+                right = z;
+                Rpos += nleaf;
+            } else {
+                left = z;
+                Lpos -= nleaf;
+            }
+            if (is_uturn<DPL>(left.q, left.p, right.q, right.p, 1, im)) {
+                turning = 1;
+                term = -2;
+                break;
+            }
+            if (j == maxd - 1) maxhit = 1;
+        }
+        evals += (unsigned long long)nleaves;
+        cur = prop;
+
+        // diagonal inverse mass from warmup states in [W/2, W)
+        if (A.adapt_diag && k < A.num_warmup && k >= A.num_warmup / 2) {
+            ++wn;
+#pragma unroll
+            for (int m = 0; m < DPL; ++m) {
+                const double d1 = cur.q[m] - wmean[m];
+                wmean[m] += d1 / (double)wn;
+                wm2[m] += d1 * (cur.q[m] - wmean[m]);
+            }
+        }
+        if (A.adapt_diag && k == A.num_warmup - 1 && wn >= 2) {
+            const double nn = (double)wn;
+            double var[DPL], tot = 0.0;
+#pragma unroll
+            for (int m = 0; m < DPL; ++m) {
+                var[m] = (nn / (nn + 5.0)) * (wm2[m] / (nn - 1.0)) + 1e-3 * (5.0 / (nn + 5.0));
+                var[m] = act[m] ? var[m] : 0.0;
+                tot += var[m];
+            }
+            const double mean = wave_sum(tot) / (double)D;
+#pragma unroll
+            for (int m = 0; m < DPL; ++m) im[m] = act[m] ? var[m] / mean : 1.0;
+        }
+
+        if (k >= A.num_warmup && out) {
+            const int64_t s = k - A.num_warmup;
+            if (A.out_samples) {
+#pragma unroll
+                for (int m = 0; m < DPL; ++m)
+                    if (act[m]) A.out_samples[(cidx * A.num_samples + s) * D + l + 64 * m] = cur.q[m];
+            }
+            if (A.out_stats) {
+                double kk2 = 0.0;
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) kk2 += im[m] * cur.p[m] * cur.p[m];
+                const double K = 0.5 * wave_sum(kk2);
+                if (l == 0) {
+                    nuts_stats st;
+                    st.potential_energy = cur.U;
+                    st.energy = cur.U + K;
+                    st.accept_prob = nleaves > 0 ? sum_acc / (double)nleaves : 0.0;
+                    st.tree_depth = depth;
+                    st.num_steps = nleaves;
+                    st.proposal_index = (int32_t)prop_idx;
+                    st.term_leaf = term;
+                    st.direction_bits = dirbits;
+                    st.diverging = (uint8_t)diverging;
+                    st.turning = (uint8_t)turning;
+                    st.hit_max_depth = (uint8_t)maxhit;
+                    for (int i = 0; i < 9; ++i) st._pad[i] = 0;
+                    A.out_stats[cidx * A.num_samples + s] = st;
+                }
+            }
+        }
+    }
+    if (out) {
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) {
+            if (act[m] && A.out_final_q) A.out_final_q[cidx * D + l + 64 * m] = cur.q[m];
+            if (act[m] && A.out_inv_mass) A.out_inv_mass[cidx * D + l + 64 * m] = im[m];
+        }
+        if (l == 0) A.grad_evals[cidx] = evals;
+    }
+}
+
+constexpr int kWaveChainsPerGroup = 4;
+
+template <typename T, int S>
+__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, 3) sampler_wave_kernel(SamplerArgs A)
+{
+    constexpr int R = BlockShape<T, S>::R;
+    extern __shared__ double lds[];
+    const int wave = threadIdx.x / kWave;
+    const int64_t chain = (int64_t)blockIdx.x * kWaveChainsPerGroup + wave;
+    if (chain >= A.num_chains) return;
+    const int D = A.data.D;
+    const int slots = A.max_depth > 1 ? A.max_depth : 1;
+    double* S_arr = lds + (int64_t)wave * slots * 2 * D;
+    const int64_t c = A.chain_offset + chain;
+    const int64_t ds = A.per_chain_data ? c : 0;
+    WaveEval<T, S> ev;
+    ev.X = (const T*)A.data.X + ds * A.data.nb * (int64_t)D * R;
+    ev.y = A.data.y + ds * A.data.nb * R;
+    ev.N = A.data.N;
+    ev.nb = A.data.nb;
+    ev.D = D;
+    ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+    ev.prior_const = (double)D * (log(A.prior_scale) + kHalfLog2Pi);
+    run_chain<1>(A, ev, chain, S_arr);
+}
+
+template <typename T, int S, int CPS, int DPL>
+__global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(SamplerArgs A, int groups,
+                                                                            double* partials, double* result,
+                                                                            GridSync* sync)
+{
+    extern __shared__ double lds[];
+    __shared__ GridShared<DPL, kGridWaves> sh;
+    GridCtx c;
+    c.X = A.data.X;
+    c.y = A.data.y;
+    c.N = A.data.N;
+    c.nb = A.data.nb;
+    c.D = A.data.D;
+    c.groups = groups;
+    c.partials = partials;
+    c.result = result;
+    c.sync = sync;
+    const int wave = threadIdx.x / kWave;
+    if (wave == 0) {
+        GridEval<T, S, CPS, DPL, kGridWaves> ev;
+        ev.c = c;
+        ev.sh = &sh;
+        ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+        ev.prior_const = (double)A.data.D * (log(A.prior_scale) + kHalfLog2Pi);
+        ev.step = 0;
+        ev.abort = false;
+        run_chain<DPL>(A, ev, 0, lds);
+        ev.finish();
+    } else {
+        unsigned long long step = 0;
+        double q[DPL], r[DPL + 1];
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) q[m] = 0.0;
+        for (;;) {
+            bool ab;
+            if (grid_collective<T, S, CPS, DPL, kGridWaves, true>(c, sh, step, q, 0, r, &ab) == kCmdExit) break;
+            step++;
+        }
+    }
+}
+
+// Kernel for a data shape (S, CPS, DPL as pass_shape gives them).
+template <typename T>
+const void* grid_kernel_for(const DataView& dv)
+{
+    const int D = dv.D;
+    if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1>;
+    if (D <= 16) return (const void*)sampler_grid_kernel<T, 2, 8, 1>;
+    if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1>;
+    if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1>;
+    if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2>;
+    if (D <= 192) return (const void*)sampler_grid_kernel<T, 32, 8, 3>;
+    if (D <= 256) return (const void*)sampler_grid_kernel<T, 32, 8, 4>;
+    return (const void*)sampler_grid_kernel<T, 32, 10, 5>;
+}
+
+template <typename T, int S>
+hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
+{
+    const int slots = a.max_depth > 1 ? a.max_depth : 1;
+    const size_t lds = (size_t)kWaveChainsPerGroup * slots * 2 * a.data.D * sizeof(double);
+    const unsigned grid = (unsigned)((a.num_chains + kWaveChainsPerGroup - 1) / kWaveChainsPerGroup);
+    hipLaunchKernelGGL((sampler_wave_kernel<T, S>), dim3(grid), dim3(kWaveChainsPerGroup * kWave), lds, stream,
+                       a);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t wave_launch_split(const SamplerArgs& a, hipStream_t stream)
+{
+    if (a.data.split == 1) return wave_launch<T, 1>(a, stream);
+    if (a.data.split == 2) return wave_launch<T, 2>(a, stream);
+    if (a.data.split == 4) return wave_launch<T, 4>(a, stream);
+    return wave_launch<T, 8>(a, stream);
+}
+
+}  // namespace sampler
+}  // namespace nuts

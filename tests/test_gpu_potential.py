@@ -34,7 +34,8 @@ def _check(sampler, orc, X, y, w, s, dt):
 
 @pytest.mark.parametrize("dt", ["f64", "f32"])
 @pytest.mark.parametrize("N,D", [(1, 1), (63, 2), (64, 5), (65, 11), (1000, 11), (4097, 9),
-                                 (777, 33), (3000, 55), (130, 63)])
+                                 (777, 33), (3000, 55), (130, 63), (500, 64), (301, 65),
+                                 (1000, 129), (777, 200), (513, 257), (200, 320)])
 def test_random_positions(sampler, orc, dt, N, D):
     X, y, w_true = workloads.make_logistic(N, D, w_scale=0.7, key=[50, N * 1000 + D],
                                            dtype=dt)
@@ -114,5 +115,5 @@ def test_errors_are_reported(sampler):
                                prior_scale=-1.0)
     assert e.value.code == nuts.NUTS_EINVAL
     with pytest.raises(nuts.NutsError) as e:
-        sampler.potential_grad(np.zeros((10, 300)), np.zeros(10, np.uint8), np.zeros(300))
+        sampler.potential_grad(np.zeros((10, 400)), np.zeros(10, np.uint8), np.zeros(400))
     assert e.value.code == nuts.NUTS_EUNSUPPORTED

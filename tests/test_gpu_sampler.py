@@ -67,6 +67,18 @@ def test_edge_cases_tiny(sampler, orc, path):
         compare_chain(r["samples"][0], r["stats"][0], ref)
 
 
+@pytest.mark.parametrize("D,path", [(64, 1), (64, 2), (129, 2), (257, 2)])
+def test_wide_models(sampler, orc, D, path):
+    # several lanes per row and several dimensions per lane
+    N = 3000
+    X, y, _ = workloads.make_logistic(N, D, w_scale=0.1, key=[61, D])
+    say("sampler wide", N, D, "path", path)
+    r = sampler.sample(X, y, step_size=0.02, max_tree_depth=6, num_warmup=2, num_samples=8, seed=5,
+                       path=path)
+    ref = orc.nuts(X, y, step_size=0.02, max_tree_depth=6, num_warmup=2, num_samples=8, seed=5)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+
+
 def test_many_chains_per_chain_data_subset(sampler, orc):
     # 256 chains of the 4096-chain workload (own data per chain); every chain
     # compared with the oracle for its first 50 iterations
