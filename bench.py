@@ -1,19 +1,25 @@
 #!/usr/bin/env python3
-"""Throughput of the device-resident NUTS on the covtype-shaped logistic
-regression (N = 581,012 rows, D = 55 columns with the intercept, synthetic
-iid N(0, 1) features), one chain on one MI355X.
+"""Throughput of the device-resident NUTS on one MI355X.
 
-A "step" is one NUTS iteration (one draw): momentum, trajectory doubling
-with the iterative tree builder, every leapfrog step's fused potential and
-gradient over all rows, proposal selection.  --warmup W iterations run
-first (untimed); the timed call resumes the chain from that state for
-exactly --steps K iterations with the data already in HBM.
+Default workload: the covtype-shaped logistic regression (N = 581,012 rows,
+D = 55 columns with the intercept, synthetic iid N(0, 1) features, fp32),
+one chain.  `--workload` selects another configured workload (see
+workloads.py), e.g. the 4,096 small per-chain models or the 4,000,000 x 257
+streaming model.
 
-The JSON line reports leapfrog gradient evaluations per second (`value`),
-ESS/s, the roofline of the sampler kernel (algorithmic bytes = one read of
-X and y per gradient evaluation, over the kernel's time measured with HIP
-events on the launch stream), and the CPU oracle's gradient rate on the
-same data as a baseline.
+A "step" is one NUTS iteration of every chain: momentum, trajectory
+doubling with the iterative tree builder, every leapfrog step's fused
+potential and gradient over all rows, proposal selection.  --warmup W
+iterations run first (untimed, NUTS warmup with the workload's settings);
+the timed call resumes each chain from that state for exactly --steps K
+iterations with the data already in HBM.  Defaults: the workload's own
+warmup / sample counts.
+
+The JSON line reports leapfrog gradient evaluations per second (`value`,
+summed over chains), ESS/s, the roofline of the sampler kernel
+(algorithmic bytes = one read of X and y per gradient evaluation, over the
+kernel's time measured with HIP events on the launch stream) and the CPU
+oracle's gradient rate on the same data as a baseline.
 """
 from __future__ import annotations
 
@@ -30,13 +36,14 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+METRIC = "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline"
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_workload(name, steps, warmup):
+def run_workload(name, steps=None, warmup=None):
     import torch
 
     import paper_1912_11554_amd as nuts
@@ -44,31 +51,35 @@ def run_workload(name, steps, warmup):
     from paper_1912_11554_amd.diagnostics import effective_sample_size
 
     wl = workloads.WORKLOADS[name]
+    steps = wl.num_samples if steps is None else steps
+    warmup = wl.num_warmup if warmup is None else warmup
+    C = wl.num_chains
     t0 = time.time()
     X, y = workloads.make_workload(wl)
-    log(f"{name}: generated {X.shape} {X.dtype} in {time.time() - t0:.1f}s")
+    log(f"{name}: generated X {X.shape} {X.dtype} in {time.time() - t0:.1f}s")
     Xd = torch.from_numpy(X).cuda()
     yd = torch.from_numpy(y).cuda()
     del X
     torch.cuda.synchronize()
     s = nuts.Sampler(0)
     t0 = time.time()
-    d = s.data(Xd, yd)
+    d = s.data(Xd, yd, per_chain=wl.per_chain_data)
     torch.cuda.synchronize()
     layout_s = time.time() - t0
     del Xd
     kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
-              prior_scale=wl.prior_scale, path=nuts.NUTS_PATH_GRID)
+              prior_scale=wl.prior_scale, num_chains=C)
 
     t0 = time.time()
-    r0 = d.sample(num_warmup=warmup, num_samples=1, **kw)
-    log(f"{name}: warmup {warmup} iterations, {r0['grad_evals']} gradient evaluations, "
-        f"{time.time() - t0:.2f}s")
+    r0 = d.sample(num_warmup=warmup, num_samples=1, adapt_diag_mass=wl.adapt_diag_mass, **kw)
+    log(f"{name}: warmup {warmup} iterations x {C} chains, {r0['grad_evals']} gradient "
+        f"evaluations, {time.time() - t0:.2f}s")
     q = r0["final_q"]
+    inv_mass = r0["inv_mass"][0] if wl.adapt_diag_mass else None
 
     D = wl.D
-    samples = torch.empty((1, steps, D), dtype=torch.float64, device="cuda")
-    stats = torch.empty((1, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
+    samples = torch.empty((C, steps, D), dtype=torch.float64, device="cuda")
+    stats = torch.empty((C, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -76,26 +87,26 @@ def run_workload(name, steps, warmup):
     w0 = time.perf_counter()
     ev0.record(stream)
     r = d.sample(num_warmup=0, num_samples=steps, init_q=q, first_iter=warmup + 1,
-                 out_samples=samples, out_stats=stats, **kw)
+                 inv_mass=inv_mass, out_samples=samples, out_stats=stats, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     gpu_s = ev0.elapsed_time(ev1) / 1e3
-    st = stats.cpu().numpy().reshape(-1).view(nuts.STATS_DTYPE)
-    draws = samples.cpu().numpy()[0]
+    st = stats.cpu().numpy().reshape(C, steps, -1).view(nuts.STATS_DTYPE)[..., 0]
+    draws = samples.cpu().numpy()
     evals = r["grad_evals"]
-    assert evals == int(st["num_steps"].sum()) + 1
-    ess = effective_sample_size(draws)
+    assert evals == int(st["num_steps"].sum()) + C
+    ess = effective_sample_size(draws)   # multi-chain ESS per coordinate
     es = 8 if wl.dtype == "f64" else 4
     bytes_per_eval = wl.N * wl.D * es + wl.N
     achieved = evals * bytes_per_eval / gpu_s / 1e9
-    log(f"{name}: {steps} iterations, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
+    log(f"{name}: {steps} iterations x {C} chains, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
         f"({wall * 1e3:.1f} ms wall): {evals / gpu_s:.0f} evals/s, {achieved:.0f} GB/s, "
         f"min ESS {ess.min():.0f}")
     d.free()
     s.close()
     return dict(
-        workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, step_size=wl.step_size,
+        workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=wl.step_size,
         max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
         gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
         evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
@@ -113,7 +124,9 @@ def cpu_baseline(name, seconds):
     import workloads
 
     wl = workloads.WORKLOADS[name]
-    X, y = workloads.make_workload(wl)
+    X, y = workloads.make_workload(wl, chains=[0] if wl.per_chain_data else None)
+    if wl.per_chain_data:
+        X, y = X[0], y[0]
     _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
     f = oracle.logistic_potential_grad_f32 if wl.dtype == "f32" else oracle.logistic_potential_grad
     n = 0
@@ -126,7 +139,8 @@ def cpu_baseline(name, seconds):
             break
     log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
     return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle",
-                sample=f"{n} full potential+gradient evaluations of {name} at w_true, "
+                sample=f"{n} full potential+gradient evaluations of {name}"
+                       f"{' (one chain data set)' if wl.per_chain_data else ''} at w_true, "
                        f"single-threaded fp64 C, {el:.1f}s",
                 host_cores_available=len(os.sched_getaffinity(0)))
 
@@ -134,8 +148,8 @@ def cpu_baseline(name, seconds):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=1000)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="covtype_n581012_d55_f32")
     ap.add_argument("--also", default="covtype_n581012_d55_f64",
                     help="second workload reported beside the first ('' for none)")
@@ -163,13 +177,14 @@ def main():
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
 
     achieved = main_res["achieved_gbs"]
+    kernel = "sampler_grid_kernel" if main_res["chains"] == 1 else "sampler_wave_kernel"
     line = {
-        "metric": "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline",
+        "metric": METRIC,
         "value": round(main_res["evals_per_s"], 1),
         "unit": "grad-evals/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": main_res["steps"],
+        "warmup": main_res["warmup"],
         "ms_per_step": round(main_res["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -178,7 +193,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
-            "chains": 1, "step_size": main_res["step_size"],
+            "chains": main_res["chains"], "step_size": main_res["step_size"],
             "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
         },
         "ess_per_s": round(main_res["ess_per_s"], 2),
@@ -186,9 +201,10 @@ def main():
         "ess_median": round(main_res["ess_median"], 1),
         "grad_evals": main_res["grad_evals"],
         "mean_steps_per_iter": round(main_res["mean_steps_per_iter"], 2),
+        "divergences": main_res["divergences"],
         "layout_seconds": round(main_res["layout_seconds"], 4),
         "roofline": {
-            "kernel": "sampler_grid_kernel",
+            "kernel": kernel,
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
             "bytes_per_eval": main_res["bytes_per_eval"],

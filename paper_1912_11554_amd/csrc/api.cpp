@@ -29,7 +29,32 @@ struct nuts_handle {
     bool own_stream = false;
     int num_cu = 0;
     std::string err;
+    // grow-only device scratch for partial sums and exchange buffers; a call
+    // uses it between its launches and its final stream synchronisation
+    void* scratch = nullptr;
+    size_t scratch_bytes = 0;
 };
+
+// Scratch of at least `bytes`, 256-byte aligned, owned by the handle.
+static hipError_t handle_scratch(nuts_handle* h, size_t bytes, void** out)
+{
+    if (bytes > h->scratch_bytes) {
+        if (h->scratch) {
+            hipError_t e = hipStreamSynchronize(h->stream);
+            if (e != hipSuccess) return e;
+            (void)hipFree(h->scratch);
+            h->scratch = nullptr;
+            h->scratch_bytes = 0;
+        }
+        hipError_t e = hipMalloc(&h->scratch, bytes);
+        if (e != hipSuccess) return e;
+        h->scratch_bytes = bytes;
+    }
+    *out = h->scratch;
+    return hipSuccess;
+}
+
+static size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
 static thread_local std::string g_init_error;
 
@@ -186,6 +211,8 @@ void nuts_free(nuts_handle* h)
 {
     if (!h) return;
     DeviceScope ds(h->device);
+    (void)hipStreamSynchronize(h->stream);
+    if (h->scratch) (void)hipFree(h->scratch);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
 }
@@ -290,15 +317,16 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
     DeviceScope ds(h->device);
     const int D = d->view.D;
-    DevBuf wt, ut, gt, part;
+    DevBuf wt, ut, gt;
     const void* Wd = nullptr;
     void *Ud = nullptr, *Gd = nullptr;
     HIP_TRY(h, stage_in(W, (size_t)K * D * 8, wt, &Wd, h->stream));
     HIP_TRY(h, stage_out(out_U, (size_t)K * 8, ut, &Ud));
     HIP_TRY(h, stage_out(out_grad, (size_t)K * D * 8, gt, &Gd));
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
-    HIP_TRY(h, part.alloc((size_t)K * plan.groups_per_item * plan.width * sizeof(double)));
-    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part.p,
+    void* part = nullptr;
+    HIP_TRY(h, handle_scratch(h, (size_t)K * plan.groups_per_item * plan.width * sizeof(double), &part));
+    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part,
                                      (double*)Ud, (double*)Gd, h->stream));
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
     HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
@@ -412,18 +440,21 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
         HIP_TRY(h, launch_sampler_wave(a, s));
     } else {
         const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
-        DevBuf part, res, sync;
         const int W = partial_width(D);
-        HIP_TRY(h, part.alloc((size_t)2 * groups * W * sizeof(double)));
-        HIP_TRY(h, res.alloc((size_t)2 * W * sizeof(double)));
-        HIP_TRY(h, sync.alloc(sizeof(GridSync)));
+        const size_t part_bytes = align256((size_t)2 * groups * W * sizeof(double));
+        const size_t res_bytes = align256((size_t)2 * W * sizeof(double));
+        void* scratch = nullptr;
+        HIP_TRY(h, handle_scratch(h, part_bytes + res_bytes + sizeof(GridSync), &scratch));
+        double* part = (double*)scratch;
+        double* res = (double*)((char*)scratch + part_bytes);
+        GridSync* sync = (GridSync*)((char*)scratch + part_bytes + res_bytes);
         for (int64_t c = 0; c < C; ++c) {
             SamplerArgs ac = a;
             ac.num_chains = 1;
             ac.chain_offset = c;
-            HIP_TRY(h, launch_sampler_grid(ac, groups, (double*)part.p, (double*)res.p, (GridSync*)sync.p, s));
+            HIP_TRY(h, launch_sampler_grid(ac, groups, part, res, sync, s));
             GridSync hs;
-            HIP_TRY(h, hipMemcpyAsync(&hs, sync.p, sizeof hs, hipMemcpyDeviceToHost, s));
+            HIP_TRY(h, hipMemcpyAsync(&hs, sync, sizeof hs, hipMemcpyDeviceToHost, s));
             HIP_TRY(h, hipStreamSynchronize(s));
             if (hs.error)
                 return fail(h, NUTS_EDEVICE, "grid barrier timed out in chain %lld (a group stopped responding)",
