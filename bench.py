@@ -48,7 +48,8 @@ def run_workload(name, steps=None, warmup=None):
 
     import paper_1912_11554_amd as nuts
     import workloads
-    from paper_1912_11554_amd.diagnostics import effective_sample_size
+    from paper_1912_11554_amd.diagnostics import (effective_sample_size,
+                                                  effective_sample_size_per_chain)
 
     wl = workloads.WORKLOADS[name]
     steps = wl.num_samples if steps is None else steps
@@ -96,7 +97,10 @@ def run_workload(name, steps=None, warmup=None):
     draws = samples.cpu().numpy()
     evals = r["grad_evals"]
     assert evals == int(st["num_steps"].sum()) + C
-    ess = effective_sample_size(draws)   # multi-chain ESS per coordinate
+    # per-coordinate ESS: pooled over chains that share one target, per chain
+    # (then the minimum over chains) when every chain has its own data
+    ess = (effective_sample_size_per_chain(draws).min(axis=0) if wl.per_chain_data
+           else effective_sample_size(draws))
     es = 8 if wl.dtype == "f64" else 4
     bytes_per_eval = wl.N * wl.D * es + wl.N
     achieved = evals * bytes_per_eval / gpu_s / 1e9

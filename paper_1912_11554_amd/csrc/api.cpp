@@ -390,7 +390,7 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     if (path == NUTS_PATH_AUTO) {
         // one wave per chain when there are many chains or the data is small;
         // the whole device on one chain when the data is large
-        const bool small = d->view.N <= 4096;
+        const bool small = d->view.nb <= 6;  // a few blocks: one wave beats a grid-wide exchange
         path = ((per_chain || small || num_chains > 1) && wave_path_supports(d->view)) ? NUTS_PATH_WAVE
                                                                                        : NUTS_PATH_GRID;
     }

@@ -38,3 +38,12 @@ def effective_sample_size(draws) -> np.ndarray:
     tau = np.maximum(tau, 1.0 / np.log10(C * n))
     ess = C * n / tau
     return np.where(var_hat > 0, ess, float(C * n))
+
+
+def effective_sample_size_per_chain(draws) -> np.ndarray:
+    """draws: [C, n, D] from C chains with different targets.  Returns the
+    single-chain ESS of every (chain, coordinate), shape [C, D]."""
+    x = np.asarray(draws, dtype=np.float64)
+    C, n, D = x.shape
+    flat = np.transpose(x, (1, 0, 2)).reshape(n, C * D)
+    return effective_sample_size(flat).reshape(C, D)

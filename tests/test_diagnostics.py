@@ -25,3 +25,14 @@ def test_matches_oracle_and_closed_form(phi, C):
         assert got[d] == pytest.approx(ess(x[:, :, d]), rel=1e-9)
     want = C * 20000 * (1 - phi) / (1 + phi)
     assert np.all(np.abs(got / want - 1) < 0.2)
+
+
+def test_per_chain_ess_matches_single_chain_calls():
+    from paper_1912_11554_amd.diagnostics import effective_sample_size_per_chain
+    rng = np.random.default_rng(9)
+    x = np.stack([_ar1(phi, 4000, rng)[0] for phi in (0.1, 0.5, 0.8)])   # [3, n]
+    draws = np.stack([x, -x], axis=2)                                       # [3, n, 2]
+    got = effective_sample_size_per_chain(draws)
+    for c in range(3):
+        assert got[c, 0] == pytest.approx(effective_sample_size(draws[c])[0], rel=1e-12)
+    assert got[0, 0] > got[2, 0]
