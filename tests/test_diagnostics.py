@@ -30,7 +30,7 @@ def test_matches_oracle_and_closed_form(phi, C):
 def test_per_chain_ess_matches_single_chain_calls():
     from paper_1912_11554_amd.diagnostics import effective_sample_size_per_chain
     rng = np.random.default_rng(9)
-    x = np.stack([_ar1(phi, 4000, rng)[0] for phi in (0.1, 0.5, 0.8)])   # [3, n]
+    x = np.stack([_ar1(phi, 4000, rng, D=1)[0, :, 0] for phi in (0.1, 0.5, 0.8)])   # [3, n]
     draws = np.stack([x, -x], axis=2)                                       # [3, n, 2]
     got = effective_sample_size_per_chain(draws)
     for c in range(3):
