@@ -63,7 +63,9 @@ enum {
 enum {
     NUTS_PATH_AUTO = 0,
     NUTS_PATH_WAVE = 1,  /* one wavefront per chain, whole tree on device */
-    NUTS_PATH_GRID = 2   /* one chain over the whole GPU, grid barrier per leapfrog step */
+    NUTS_PATH_GRID = 2,  /* one chain over the whole GPU, grid barrier per leapfrog step */
+    NUTS_PATH_BATCH = 3  /* many chains on shared fp32 data: one leapfrog step of every chain
+                            per pass, the gradients as a matrix product on the matrix cores */
 };
 
 /* One record per (chain, kept sample).  56 bytes, no implicit padding. */
@@ -108,6 +110,20 @@ void nuts_data_free(nuts_handle* h, nuts_data* d);
  * for fp32 X. */
 int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_scale,
                              const double* W, int64_t K, double* out_U, double* out_grad);
+
+/* The same quantities for K positions on shared fp32 data, computed as one
+ * contraction: E = X W^T (N x D by D x K) and G = X^T R (D x N by N x K) on
+ * the fp32 matrix cores, with R = sigmoid(E) - y elementwise (the batched
+ * form of the gradient in Section 3.1's vectorized setting).  X and W enter
+ * the products as fp32 (W is rounded to fp32 for the likelihood terms; the
+ * prior uses W in fp64), products accumulate in fp32 per row range, and the
+ * per-position sums of the loss and of the partial rows are fp64.  Relative
+ * error versus fp64 arithmetic on the same fp32 X is ~1e-6.  NUTS_EUNSUPPORTED
+ * for fp64 data, per-chain data or D > 132.  The first call on a data set
+ * builds a second device copy of X in the row-stage layout this path reads
+ * (kept until nuts_data_free). */
+int nuts_data_potential_grad_batched(nuts_handle* h, const nuts_data* d, double prior_scale,
+                                     const double* W, int64_t K, double* out_U, double* out_grad);
 
 /* One-shot form of the above for a single position w [D]: lays out X and y,
  * evaluates, releases.  N = 0 is allowed (the prior alone). */

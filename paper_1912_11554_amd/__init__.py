@@ -19,11 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libnuts.so")
 NUTS_OK, NUTS_EINVAL, NUTS_ENOMEM, NUTS_EDEVICE, NUTS_EUNSUPPORTED = 0, -1, -2, -3, -4
 NUTS_F64, NUTS_F32 = 0, 1
 NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS = 1, 2
-NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID = 0, 1, 2
+NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID, NUTS_PATH_BATCH = 0, 1, 2, 3
 
 EXPORTED = [
     "nuts_init", "nuts_free", "nuts_last_error", "nuts_data_create", "nuts_data_free",
-    "nuts_data_potential_grad", "nuts_potential_grad", "nuts_sample_data", "nuts_sample",
+    "nuts_data_potential_grad", "nuts_data_potential_grad_batched", "nuts_potential_grad",
+    "nuts_sample_data", "nuts_sample",
 ]
 
 STATS_DTYPE = np.dtype([
@@ -56,6 +57,19 @@ class _Opts(ctypes.Structure):
 _lib = None
 
 
+def _torch_runtime_first():
+    """With torch in the process there are two HIP runtimes (torch's bundled
+    one and the one libnuts.so links).  They coexist when torch's is brought
+    up on the device before libnuts.so is loaded; loaded the other way round,
+    the second one to initialise has been seen to find no device."""
+    try:
+        import torch
+        if torch.cuda.is_available():
+            torch.empty(1, device="cuda")
+    except Exception:
+        pass
+
+
 def load_library():
     """Load libnuts.so (raises if it has not been built)."""
     global _lib
@@ -64,6 +78,7 @@ def load_library():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing; build it with "
                            "`python -m paper_1912_11554_amd.build`")
+    _torch_runtime_first()
     L = ctypes.CDLL(LIB_PATH)
     P, i64, u64, i32, u32, dbl = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                   ctypes.c_int, ctypes.c_uint32, ctypes.c_double)
@@ -79,6 +94,8 @@ def load_library():
     L.nuts_data_free.restype = None
     L.nuts_data_potential_grad.argtypes = [P, P, dbl, P, i64, P, P]
     L.nuts_data_potential_grad.restype = i32
+    L.nuts_data_potential_grad_batched.argtypes = [P, P, dbl, P, i64, P, P]
+    L.nuts_data_potential_grad_batched.restype = i32
     L.nuts_potential_grad.argtypes = [P, P, P, i64, i64, i32, dbl, P, P, P]
     L.nuts_potential_grad.restype = i32
     L.nuts_sample_data.argtypes = [P, P, u32, dbl, dbl, P, i32, i64, i64, i64, u64, P, P,
@@ -111,11 +128,12 @@ def _dtype_code(X):
     raise TypeError(f"X must be float64 or float32, got {X.dtype}")
 
 
-def _current_stream():
+def _current_stream(device: int = 0):
+    """torch's current HIP stream on ``device`` (None without torch or GPU)."""
     try:
         import torch
         if torch.cuda.is_available():
-            return torch.cuda.current_stream().cuda_stream
+            return torch.cuda.current_stream(device).cuda_stream
     except Exception:
         pass
     return None
@@ -128,7 +146,7 @@ class Sampler:
         L = load_library()
         h = ctypes.c_void_p()
         if stream is None:
-            stream = _current_stream()
+            stream = _current_stream(device)
         rc = L.nuts_init(ctypes.byref(h), device, stream)
         if rc != NUTS_OK:
             raise NutsError(rc, L.nuts_last_error(None).decode())
@@ -203,8 +221,9 @@ class Data:
         except Exception:
             pass
 
-    def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None):
-        """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor)."""
+    def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None, batched=False):
+        """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor).
+        batched=True uses nuts_data_potential_grad_batched (fp32 matrix cores)."""
         if isinstance(W, np.ndarray):
             W = np.ascontiguousarray(W, dtype=np.float64).reshape(-1, self.D)
         K = W.shape[0]
@@ -212,9 +231,10 @@ class Data:
             out_U = np.zeros(K)
         if out_grad is None:
             out_grad = np.zeros((K, self.D))
-        self.s._check(self.s._L.nuts_data_potential_grad(self.s._h, self._d, prior_scale,
-                                                          _ptr(W), K, _ptr(out_U),
-                                                          _ptr(out_grad)))
+        fn = (self.s._L.nuts_data_potential_grad_batched if batched
+              else self.s._L.nuts_data_potential_grad)
+        self.s._check(fn(self.s._h, self._d, prior_scale, _ptr(W), K, _ptr(out_U),
+                         _ptr(out_grad)))
         return out_U, out_grad
 
     def sample(self, *, step_size, max_tree_depth, num_warmup, num_samples, num_chains=1,

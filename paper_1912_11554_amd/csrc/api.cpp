@@ -4,6 +4,7 @@
 // plus a message kept on the handle.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -21,7 +22,19 @@ struct nuts_data {
     DataView view;
     void* X = nullptr;
     uint8_t* y = nullptr;
+    // row-stage copy for the batched (matrix-core) path, built on first use
+    BatchView batch{};
+    float* bX = nullptr;
+    uint8_t* by = nullptr;
 };
+
+static void free_data_buffers(nuts_data* d)
+{
+    if (d->X) (void)hipFree(d->X);
+    if (d->y) (void)hipFree(d->y);
+    if (d->bX) (void)hipFree(d->bX);
+    if (d->by) (void)hipFree(d->by);
+}
 
 struct nuts_handle {
     int device = 0;
@@ -253,8 +266,7 @@ int nuts_data_create(nuts_handle* h, const void* X, const uint8_t* y, int64_t N,
     const size_t xblk = ((size_t)d->view.nb * D * R * num_datasets + (size_t)kTailElems) * es;
     const size_t yblk = (size_t)d->view.nb * R * num_datasets;
     auto cleanup = [&](int code) {
-        if (d->X) (void)hipFree(d->X);
-        if (d->y) (void)hipFree(d->y);
+        free_data_buffers(d);
         delete d;
         return code;
     };
@@ -294,11 +306,9 @@ void nuts_data_free(nuts_handle* h, nuts_data* d)
     if (h) {
         DeviceScope ds(h->device);
         (void)hipStreamSynchronize(h->stream);
-        if (d->X) (void)hipFree(d->X);
-        if (d->y) (void)hipFree(d->y);
+        free_data_buffers(d);
     } else {
-        if (d->X) (void)hipFree(d->X);
-        if (d->y) (void)hipFree(d->y);
+        free_data_buffers(d);
     }
     delete d;
 }
@@ -328,6 +338,82 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     HIP_TRY(h, handle_scratch(h, (size_t)K * plan.groups_per_item * plan.width * sizeof(double), &part));
     HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part,
                                      (double*)Ud, (double*)Gd, h->stream));
+    HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
+    HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    return NUTS_OK;
+}
+
+// The row-stage layout of a shared fp32 data set (built on first use).
+static int ensure_batch_layout(nuts_handle* h, const nuts_data* dc)
+{
+    nuts_data* d = const_cast<nuts_data*>(dc);
+    if (d->bX) return NUTS_OK;
+    if (d->view.dtype != NUTS_F32)
+        return fail(h, NUTS_EUNSUPPORTED, "the batched path takes fp32 data");
+    if (d->view.nds != 1) return fail(h, NUTS_EUNSUPPORTED, "the batched path takes one shared data set");
+    int kt = 0, tc = 0;
+    if (!batch_shape(d->view.D, &kt, &tc))
+        return fail(h, NUTS_EUNSUPPORTED, "the batched path takes D <= %d (got %d)", 16 * kBatchMaxKT + 4,
+                    d->view.D);
+    BatchView b;
+    b.N = d->view.N;
+    b.D = d->view.D;
+    b.kt = kt;
+    b.tc = tc;
+    b.stride = 16 * kt + 4;
+    b.ns = (b.N + kBatchStageRows - 1) / kBatchStageRows;
+    const size_t xb = (size_t)b.ns * kBatchStageRows * b.stride * sizeof(float);
+    const size_t yb = (size_t)b.ns * kBatchStageRows;
+    float* X = nullptr;
+    uint8_t* y = nullptr;
+    if (xb) {
+        hipError_t e = hipMalloc(&X, xb);
+        if (e == hipSuccess) e = hipMalloc(&y, yb);
+        if (e == hipSuccess) e = launch_to_batch_layout(d->view, b, X, y, h->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+        if (e != hipSuccess) {
+            if (X) (void)hipFree(X);
+            if (y) (void)hipFree(y);
+            return fail(h, e == hipErrorOutOfMemory ? NUTS_ENOMEM : NUTS_EDEVICE, "batched layout: %s",
+                        hipGetErrorString(e));
+        }
+    }
+    b.X = X;
+    b.y = y;
+    d->batch = b;
+    d->bX = X;
+    d->by = y;
+    return NUTS_OK;
+}
+
+int nuts_data_potential_grad_batched(nuts_handle* h, const nuts_data* d, double prior_scale, const double* W,
+                                     int64_t K, double* out_U, double* out_grad)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (!W || !out_U || !out_grad) return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be non-NULL");
+    if (K < 1 || K > 65535) return fail(h, NUTS_EINVAL, "K must be in [1, 65535] (got %lld)", (long long)K);
+    if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
+    if (d->view.N < 1) return fail(h, NUTS_EINVAL, "the batched path needs N >= 1");
+    DeviceScope ds(h->device);
+    const int rc = ensure_batch_layout(h, d);
+    if (rc != NUTS_OK) return rc;
+    const int D = d->view.D;
+    DevBuf wt, ut, gt;
+    const void* Wd = nullptr;
+    void *Ud = nullptr, *Gd = nullptr;
+    HIP_TRY(h, stage_in(W, (size_t)K * D * 8, wt, &Wd, h->stream));
+    HIP_TRY(h, stage_out(out_U, (size_t)K * 8, ut, &Ud));
+    HIP_TRY(h, stage_out(out_grad, (size_t)K * D * 8, gt, &Gd));
+    const BatchPlan plan = plan_batch_potential(d->batch, K, h->num_cu);
+    const size_t rows = (size_t)plan.tiles * plan.groups * kBatchTileChains;
+    const size_t pbytes = align256(rows * plan.pw * sizeof(float));
+    void* scratch = nullptr;
+    HIP_TRY(h, handle_scratch(h, pbytes + rows * sizeof(double), &scratch));
+    HIP_TRY(h, launch_batch_potential(d->batch, prior_scale, (const double*)Wd, K, plan, (float*)scratch,
+                                      (double*)((char*)scratch + pbytes), (double*)Ud, (double*)Gd, h->stream));
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
     HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
     HIP_TRY(h, hipStreamSynchronize(h->stream));
@@ -386,21 +472,38 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
             if (!finite_pos(im[i])) return fail(h, NUTS_EINVAL, "inv_mass_diag[%d] must be finite and > 0", i);
     }
 
+    DeviceScope ds(h->device);
     int path = o.path;
     if (path == NUTS_PATH_AUTO) {
+        // many chains on a large shared fp32 data set: the matrix-core batch;
         // one wave per chain when there are many chains or the data is small;
         // the whole device on one chain when the data is large
+        int kt = 0, tc = 0;
+        const bool batchable = !per_chain && d->view.dtype == NUTS_F32 && num_chains >= 16 &&
+                               (double)d->view.N * d->view.D >= 262144.0 && batch_shape(d->view.D, &kt, &tc);
         const bool small = d->view.nb <= 6;  // a few blocks: one wave beats a grid-wide exchange
-        path = ((per_chain || small || num_chains > 1) && wave_path_supports(d->view)) ? NUTS_PATH_WAVE
-                                                                                       : NUTS_PATH_GRID;
+        if (batchable && ensure_batch_layout(h, d) == NUTS_OK &&
+            batch_sampler_supported(d->batch, max_tree_depth, h->num_cu))
+            path = NUTS_PATH_BATCH;
+        else
+            path = ((per_chain || small || num_chains > 1) && wave_path_supports(d->view)) ? NUTS_PATH_WAVE
+                                                                                           : NUTS_PATH_GRID;
+        h->err.clear();
     }
-    if (path != NUTS_PATH_WAVE && path != NUTS_PATH_GRID) return fail(h, NUTS_EINVAL, "unknown path %d", path);
-    if (path == NUTS_PATH_GRID && per_chain)
-        return fail(h, NUTS_EUNSUPPORTED, "the grid path runs chains on shared data only");
+    if (path != NUTS_PATH_WAVE && path != NUTS_PATH_GRID && path != NUTS_PATH_BATCH)
+        return fail(h, NUTS_EINVAL, "unknown path %d", path);
+    if ((path == NUTS_PATH_GRID || path == NUTS_PATH_BATCH) && per_chain)
+        return fail(h, NUTS_EUNSUPPORTED, "the grid and batch paths run chains on shared data only");
     if (path == NUTS_PATH_WAVE && !wave_path_supports(d->view))
         return fail(h, NUTS_EUNSUPPORTED, "the one-wave-per-chain path takes D <= 64 (got %d)", d->view.D);
+    if (path == NUTS_PATH_BATCH) {
+        const int rc = ensure_batch_layout(h, d);
+        if (rc != NUTS_OK) return rc;
+        if (!batch_sampler_supported(d->batch, max_tree_depth, h->num_cu))
+            return fail(h, NUTS_EUNSUPPORTED, "the batch path needs >= %d compute units and D <= 132",
+                        kBatchTileChains);
+    }
 
-    DeviceScope ds(h->device);
     hipStream_t s = h->stream;
     const int64_t C = num_chains, S = num_samples;
     DevBuf imb, iqb, smp, sts, fq, fim, gev;
@@ -438,6 +541,37 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
 
     if (path == NUTS_PATH_WAVE) {
         HIP_TRY(h, launch_sampler_wave(a, s));
+    } else if (path == NUTS_PATH_BATCH) {
+        // launches of up to kBatchMaxTiles tiles of 128 chains, the groups of
+        // the device split evenly between the tiles of a launch
+        const int max_tiles = std::min(kBatchMaxTiles, h->num_cu / kBatchTileChains);
+        const int64_t per_launch = (int64_t)max_tiles * kBatchTileChains;
+        const int pw = 64 * ((D + 63) / 64);
+        const int max_groups = h->num_cu;  // one tile: every group
+        const size_t qbytes = align256((size_t)2 * max_tiles * kBatchTileChains * kBatchQWidth * sizeof(float));
+        const size_t rows = (size_t)2 * max_groups * kBatchTileChains;  // [2][tiles][groups][128]
+        const size_t pbytes = align256(rows * pw * sizeof(float));
+        const size_t lbytes = align256(rows * sizeof(double));
+        void* scratch = nullptr;
+        HIP_TRY(h, handle_scratch(h, qbytes + pbytes + lbytes + sizeof(BatchSync), &scratch));
+        float* qbuf = (float*)scratch;
+        float* P = (float*)((char*)scratch + qbytes);
+        double* L = (double*)((char*)scratch + qbytes + pbytes);
+        BatchSync* sync = (BatchSync*)((char*)scratch + qbytes + pbytes + lbytes);
+        for (int64_t c0 = 0; c0 < C; c0 += per_launch) {
+            SamplerArgs ac = a;
+            ac.num_chains = std::min(per_launch, C - c0);
+            ac.chain_offset = c0;
+            const int tiles = (int)((ac.num_chains + kBatchTileChains - 1) / kBatchTileChains);
+            const int groups = h->num_cu / tiles;
+            HIP_TRY(h, launch_sampler_batch(ac, d->batch, tiles, groups, qbuf, P, L, sync, s));
+            unsigned int err = 0;
+            HIP_TRY(h, hipMemcpyAsync(&err, &sync->error, sizeof err, hipMemcpyDeviceToHost, s));
+            HIP_TRY(h, hipStreamSynchronize(s));
+            if (err)
+                return fail(h, NUTS_EDEVICE, "batch exchange timed out in chains %lld.. (a group stopped responding)",
+                            (long long)c0);
+        }
     } else {
         const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
         const int W = partial_width(D);

@@ -1,0 +1,627 @@
+// Batched chains on shared fp32 data (the many-chain case): the potential
+// and gradient of up to 128 positions per tile as one fused pass of matrix
+// products over X, and the persistent sampler that drives 128 chains per tile
+// with it, one leapfrog step of every chain per pass.
+#include "batch.h"
+#include "sampler_impl.h"
+
+namespace nuts {
+
+// ---------------------------------------------------------------------------
+// Layout conversion: column blocks (fp32, one data set) -> 64-row stages.
+
+__global__ void __launch_bounds__(256) to_batch_kernel(const float* __restrict__ Xb, const uint8_t* __restrict__ yb,
+                                                       int R, int64_t N, int D, float* __restrict__ X,
+                                                       uint8_t* __restrict__ y, int stride, int64_t ns)
+{
+    const int64_t per_stage = (int64_t)kBatchStageRows * stride;
+    const int64_t total = ns * per_stage;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t st = o / per_stage;
+        const int64_t rem = o - st * per_stage;
+        const int r = (int)(rem / stride);
+        const int c = (int)(rem - (int64_t)r * stride);
+        const int64_t i = st * kBatchStageRows + r;
+        float v = 0.0f;
+        if (i < N && c < D) v = Xb[((i / R) * D + c) * R + (i % R)];
+        X[o] = v;
+        if (c == 0) y[i] = i < N ? yb[i] : (uint8_t)0xFF;
+    }
+}
+
+hipError_t launch_to_batch_layout(const DataView& src, const BatchView& dst, float* X, uint8_t* y,
+                                  hipStream_t stream)
+{
+    const int64_t total = dst.ns * kBatchStageRows * dst.stride;
+    if (total == 0) return hipSuccess;
+    const int64_t want = (total + 255) / 256;
+    const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+    hipLaunchKernelGGL(to_batch_kernel, dim3(grid), dim3(256), 0, stream, (const float*)src.X, src.y,
+                       rows_per_block(src), src.N, src.D, X, y, dst.stride, dst.ns);
+    return hipGetLastError();
+}
+
+namespace {
+
+using batch::WaveAcc;
+using batch::WaveQ;
+
+// Store a wave's partial row for its 16 positions: G columns from the
+// matrix-core accumulators, the tail columns and the loss from the lanes of
+// the first row group.  ATOMIC selects agent-scope stores (read by other
+// groups of the same launch).
+template <bool ATOMIC>
+__device__ __forceinline__ void put_f(float* p, float v)
+{
+    if constexpr (ATOMIC) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
+template <bool ATOMIC>
+__device__ __forceinline__ void put_d(double* p, double v)
+{
+    if constexpr (ATOMIC) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
+
+template <int KT, bool ATOMIC>
+__device__ __forceinline__ void store_partials(const BatchView& bv, WaveAcc& acc, int widx, int pw, float* P,
+                                               double* L)
+{
+    const int l = lane();
+    const int m = l & 15;
+    const int jj = l >> 4;
+    batch::reduce_position(acc);
+    const int slot = widx * 16 + m;
+    float* row = P + (int64_t)slot * pw;
+#pragma unroll
+    for (int mt = 0; mt < KT; ++mt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) put_f<ATOMIC>(row + 16 * mt + 4 * jj + r, acc.g[mt][r]);
+    }
+    if (jj == 0) {
+#pragma unroll
+        for (int k = 0; k < batch::kTail; ++k)
+            if (k < bv.tc) put_f<ATOMIC>(row + 16 * KT + k, acc.gt[k]);
+        put_d<ATOMIC>(L + slot, acc.loss);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Stand-alone batched potential: pass 1 on a grid of (groups, tiles), pass 2
+// adds the partial rows of each position in group order and the prior.
+
+template <int KT>
+__global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_pass_kernel(BatchView bv, const double* __restrict__ W,
+                                                                              int64_t K, int groups, int pw,
+                                                                              float* __restrict__ P,
+                                                                              double* __restrict__ L)
+{
+    __shared__ __align__(16) float xs[2 * batch::kStageBuf];
+    __shared__ uint32_t ys[2 * kBatchStageRows / 4];
+    const int l = lane();
+    const int m = l & 15;
+    const int jj = l >> 4;
+    const int widx = threadIdx.x / kWave;
+    const int g = blockIdx.x;
+    const int t = blockIdx.y;
+    const int D = bv.D;
+    const int64_t pos = (int64_t)t * kBatchTileChains + widx * 16 + m;
+    const bool live = pos < K;
+
+    WaveQ Q;
+#pragma unroll
+    for (int c = 0; c < KT; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int col = 16 * c + 4 * jj + i;
+            Q.q[4 * c + i] = (live && col < D) ? (float)W[pos * D + col] : 0.0f;
+        }
+#pragma unroll
+    for (int k = 0; k < batch::kTail; ++k)
+        Q.qt[k] = (live && k < bv.tc) ? (float)W[pos * D + 16 * KT + k] : 0.0f;
+
+    WaveAcc acc;
+    batch::zero(acc);
+    const int64_t st0 = (int64_t)g * bv.ns / groups;
+    const int64_t st1 = (int64_t)(g + 1) * bv.ns / groups;
+    batch::stage_loop<KT, true>(bv, st0, st1, (int)threadIdx.x, xs, ys, Q, acc);
+    const int64_t base = (int64_t)t * groups + g;
+    store_partials<KT, false>(bv, acc, widx, pw, P + base * kBatchTileChains * pw, L + base * kBatchTileChains);
+}
+
+constexpr int kFinishWaves = 4;
+
+__global__ void __launch_bounds__(kFinishWaves * kWave) batch_finish_kernel(int D, int groups, int pw,
+                                                                           const double* __restrict__ W,
+                                                                           const float* __restrict__ P,
+                                                                           const double* __restrict__ L,
+                                                                           double prior_scale,
+                                                                           double* __restrict__ out_U,
+                                                                           double* __restrict__ out_grad)
+{
+    extern __shared__ double red[];  // [kFinishWaves][pw + 64]
+    const int l = lane();
+    const int wave = threadIdx.x / kWave;
+    const int64_t k = blockIdx.x;
+    const int64_t t = k / kBatchTileChains;
+    const int slot = (int)(k % kBatchTileChains);
+    const int rw = pw + 64;
+    const int64_t rstride = (int64_t)kBatchTileChains * pw;
+    const float* src = P + t * groups * rstride + (int64_t)slot * pw;
+    const double* lsrc = L + t * groups * kBatchTileChains + slot;
+    for (int col = l; col < pw; col += 64) {
+        double s = 0.0;
+        if (col < D)
+            for (int g = wave; g < groups; g += kFinishWaves) s += (double)src[g * rstride + col];
+        red[wave * rw + col] = s;
+    }
+    // loss partials: lane l of wave w takes groups w + 4 l, w + 4 (l + 64), ...
+    double ls = 0.0;
+    for (int g = wave + kFinishWaves * l; g < groups; g += kFinishWaves * 64) ls += lsrc[(int64_t)g * kBatchTileChains];
+    ls = wave_sum(ls);
+    if (l == 0) red[wave * rw + pw] = ls;
+    __syncthreads();
+    if (wave != 0) return;
+    const double inv_s2 = 1.0 / (prior_scale * prior_scale);
+    double pr = 0.0;
+    for (int col = l; col < D; col += 64) {
+        double tot = 0.0;
+#pragma unroll
+        for (int w = 0; w < kFinishWaves; ++w) tot += red[w * rw + col];
+        const double w = W[k * D + col];
+        pr += 0.5 * w * w * inv_s2;
+        out_grad[k * D + col] = tot + w * inv_s2;
+    }
+    const double prior = wave_sum(pr);
+    if (l == 0) {
+        double loss = 0.0;
+        for (int w = 0; w < kFinishWaves; ++w) loss += red[w * rw + pw];
+        out_U[k] = loss + prior + (double)D * (log(prior_scale) + sampler::kHalfLog2Pi);
+    }
+}
+
+}  // namespace
+
+BatchPlan plan_batch_potential(const BatchView& bv, int64_t K, int num_cu)
+{
+    BatchPlan p;
+    p.tiles = (int)((K + kBatchTileChains - 1) / kBatchTileChains);
+    int64_t g = (int64_t)num_cu * 2 / p.tiles;
+    if (g > bv.ns) g = bv.ns;
+    if (g < 1) g = 1;
+    p.groups = (int)g;
+    p.pw = 64 * ((bv.D + 63) / 64);
+    return p;
+}
+
+namespace {
+
+template <int KT>
+void enqueue_batch_pass(const BatchView& bv, const double* W, int64_t K, const BatchPlan& plan, float* P, double* L,
+                        hipStream_t stream)
+{
+    hipLaunchKernelGGL(batch_pass_kernel<KT>, dim3(plan.groups, plan.tiles), dim3(batch::kWaves * kWave), 0, stream,
+                       bv, W, K, plan.groups, plan.pw, P, L);
+}
+
+}  // namespace
+
+hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const double* W, int64_t K,
+                                  const BatchPlan& plan, float* P, double* L, double* out_U, double* out_grad,
+                                  hipStream_t stream)
+{
+    switch (bv.kt) {
+    case 0: enqueue_batch_pass<0>(bv, W, K, plan, P, L, stream); break;
+    case 1: enqueue_batch_pass<1>(bv, W, K, plan, P, L, stream); break;
+    case 2: enqueue_batch_pass<2>(bv, W, K, plan, P, L, stream); break;
+    case 3: enqueue_batch_pass<3>(bv, W, K, plan, P, L, stream); break;
+    case 4: enqueue_batch_pass<4>(bv, W, K, plan, P, L, stream); break;
+    case 5: enqueue_batch_pass<5>(bv, W, K, plan, P, L, stream); break;
+    case 6: enqueue_batch_pass<6>(bv, W, K, plan, P, L, stream); break;
+    case 7: enqueue_batch_pass<7>(bv, W, K, plan, P, L, stream); break;
+    case 8: enqueue_batch_pass<8>(bv, W, K, plan, P, L, stream); break;
+    default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(batch_finish_kernel, dim3((unsigned)K), dim3(kFinishWaves * kWave),
+                       (size_t)kFinishWaves * (plan.pw + 64) * sizeof(double), stream, bv.D, plan.groups, plan.pw,
+                       W, P, L, prior_scale, out_U, out_grad);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Persistent batched sampler.
+//
+// Tile t holds chain slots 0..127 and `groups` workgroups; group i of the
+// tile runs the tree logic of slot i (if i < 128) in its wave 0 and the
+// matrix-core pass over its stage range in waves 1..8.  A step s of the tile:
+//   1. every slot's controller publishes its next position Q(s) (fp32) and
+//      then stamp[slot] = s + 1; a slot with no iterations left first sets
+//      done_at[slot] = s (once) and publishes zeros;
+//   2. each group's wave 0 waits until all 128 stamps of the tile are > s;
+//      if every done_at of the tile is <= s, the tile stops;
+//   3. the workers compute the group's partial rows for all 128 positions
+//      and store them; the group counts itself in at tile_count[t];
+//   4. once the count reaches (s + 1) * groups, the group hosting slot i adds
+//      the groups' partial rows of slot i in group order (all nine waves,
+//      then in wave order) and hands U and grad U to its controller.
+// Tiles never wait for each other.  Buffers alternate with the parity of s;
+// a buffer of parity s & 1 is rewritten only at step s + 2, after every
+// controller of the tile has consumed step s + 1 (stamps of s + 2 are out),
+// hence after every reader of step s is done.  stamp only grows and done_at
+// is written once, so every group reads the same stop decision at every step.
+
+namespace {
+
+constexpr int kGroupWaves = 1 + batch::kWaves;
+constexpr int kCmdEval = 1, kCmdStop = 2, kCmdError = 3;
+
+template <int DPL>
+struct BatchShared {
+    __align__(16) float xs[2 * batch::kStageBuf];
+    uint32_t ys[2 * kBatchStageRows / 4];
+    double red[kGroupWaves][(DPL + 1) * 64];
+    int cmd;
+};
+
+struct BatchCtx {
+    BatchView bv;
+    int tiles, groups;
+    int t, i;  // this group's tile and index in the tile
+    int64_t st0, st1;
+    int pw;
+    float* qbuf;
+    float* P;
+    double* L;
+    BatchSync* sync;
+};
+
+__device__ __forceinline__ unsigned long long load_u64(const unsigned long long* p)
+{
+    return __hip_atomic_load(const_cast<unsigned long long*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_u64(unsigned long long* p, unsigned long long v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_f(const float* p)
+{
+    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+constexpr uint64_t kWaitTicks = 1000000000ull;  // ~10 s of the 100 MHz real-time counter
+
+__device__ __forceinline__ bool error_set(const BatchCtx& c)
+{
+    return __hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+}
+__device__ __forceinline__ void raise_error(const BatchCtx& c)
+{
+    if (lane() == 0) __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int DPL>
+__device__ void publish(const BatchCtx& c, unsigned long long step, const double (&q)[DPL], bool mark_done)
+{
+    const int l = lane();
+    const int par = (int)(step & 1);
+    const int64_t slot = (int64_t)c.t * kBatchTileChains + c.i;
+    float* dst = c.qbuf + ((int64_t)par * c.tiles * kBatchTileChains + slot) * kBatchQWidth;
+#pragma unroll
+    for (int m = 0; m < kBatchQWidth / 64; ++m) {
+        const int col = l + 64 * m;
+        float v = 0.0f;
+        if (m < DPL && col < c.bv.D) v = (float)q[m < DPL ? m : 0];
+        __hip_atomic_store(dst + col, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    sampler::drain_memory_ops();
+    if (mark_done) {
+        if (l == 0) store_u64(&c.sync->done_at[slot], step);
+        sampler::drain_memory_ops();
+    }
+    if (l == 0) store_u64(&c.sync->stamp[slot], step + 1);
+}
+
+// Wave 0: wait for the tile's positions of step s; returns the command.
+__device__ int wait_positions(const BatchCtx& c, unsigned long long step)
+{
+    const int l = lane();
+    const unsigned long long* st = c.sync->stamp + (int64_t)c.t * kBatchTileChains;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool a = false, b = false;
+    for (;;) {
+        if (!a) a = load_u64(st + l) > step;
+        if (!b) b = load_u64(st + 64 + l) > step;
+        if (__all(a && b)) break;
+        if (error_set(c)) return kCmdError;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
+            raise_error(c);
+            return kCmdError;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    const unsigned long long* da = c.sync->done_at + (int64_t)c.t * kBatchTileChains;
+    const bool done = load_u64(da + l) <= step && load_u64(da + 64 + l) <= step;
+    return __all(done) ? kCmdStop : kCmdEval;
+}
+
+// Wave 0: count the group in for step s and wait for the rest of the tile.
+__device__ bool arrive_and_wait(const BatchCtx& c, unsigned long long step)
+{
+    unsigned long long* cnt = &c.sync->tile_count[c.t][0];
+    if (lane() == 0) __hip_atomic_fetch_add(cnt, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long target = (step + 1) * (unsigned long long)c.groups;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    for (;;) {
+        if (load_u64(cnt) >= target) return true;
+        if (error_set(c)) return false;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
+            raise_error(c);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// One step of the tile for this group, executed by all nine waves with the
+// same workgroup barriers.  LEADER is wave 0.  Returns the command; for the
+// leader of a hosting group, `out` receives the sums for its slot: component
+// m of lane l is column l + 64 m of X^T r, component DPL of lane 0 the loss.
+template <int KT, int DPL, bool LEADER>
+__device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigned long long step,
+                                const double (&q)[DPL], bool publish_q, bool mark_done, double (&out)[DPL + 1])
+{
+    const int l = lane();
+    const int wave = threadIdx.x / kWave;
+    const int par = (int)(step & 1);
+    const bool host = c.i < kBatchTileChains;
+    if (LEADER) {
+        if (publish_q && host) publish<DPL>(c, step, q, mark_done);
+        const int cmd = wait_positions(c, step);
+        if (l == 0) sh.cmd = cmd;
+    }
+    __syncthreads();  // command out
+    const int cmd = sh.cmd;
+    if (cmd != kCmdEval) return cmd;
+
+    const int64_t tile_base = ((int64_t)par * c.tiles + c.t) * c.groups;
+    const int64_t rstride = (int64_t)kBatchTileChains * c.pw;
+    if (LEADER) {
+        WaveQ Q;
+        WaveAcc acc;
+        batch::stage_loop<KT, false>(c.bv, c.st0, c.st1, 0, sh.xs, sh.ys, Q, acc);
+    } else {
+        const int widx = wave - 1;
+        const int m = l & 15;
+        const int jj = l >> 4;
+        const float* qsrc = c.qbuf + ((int64_t)par * c.tiles * kBatchTileChains +
+                                      (int64_t)c.t * kBatchTileChains + widx * 16 + m) * kBatchQWidth;
+        WaveQ Q;
+#pragma unroll
+        for (int ch = 0; ch < KT; ++ch)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Q.q[4 * ch + i] = load_f(qsrc + 16 * ch + 4 * jj + i);
+#pragma unroll
+        for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = load_f(qsrc + 16 * KT + k);
+        WaveAcc acc;
+        batch::zero(acc);
+        batch::stage_loop<KT, true>(c.bv, c.st0, c.st1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
+        store_partials<KT, true>(c.bv, acc, widx, c.pw, c.P + (tile_base + c.i) * rstride,
+                                 c.L + (tile_base + c.i) * kBatchTileChains);
+        sampler::drain_memory_ops();
+    }
+    __syncthreads();  // the group's partial rows are out
+    if (LEADER) {
+        const bool ok = arrive_and_wait(c, step);
+        if (l == 0) sh.cmd = ok ? kCmdEval : kCmdError;
+    }
+    __syncthreads();  // every group of the tile is in
+    const int status = sh.cmd;
+    if (host) {
+        // this wave's share of the groups, in group order
+        const float* src = c.P + tile_base * rstride + (int64_t)c.i * c.pw;
+        const double* lsrc = c.L + tile_base * kBatchTileChains + c.i;
+        double s[DPL + 1];
+#pragma unroll
+        for (int mm = 0; mm <= DPL; ++mm) s[mm] = 0.0;
+        constexpr int B = 4;
+        int g = wave;
+        for (; g + (B - 1) * kGroupWaves < c.groups; g += B * kGroupWaves) {
+            float v[B][DPL];
+            double lv[B];
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const int64_t gg = g + b * kGroupWaves;
+#pragma unroll
+                for (int mm = 0; mm < DPL; ++mm) {
+                    const int col = l + 64 * mm;
+                    v[b][mm] = col < c.bv.D ? load_f(src + gg * rstride + col) : 0.0f;
+                }
+                lv[b] = l == 0 ? sampler::load_shared(lsrc + gg * kBatchTileChains) : 0.0;
+            }
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+#pragma unroll
+                for (int mm = 0; mm < DPL; ++mm) s[mm] += (double)v[b][mm];
+                s[DPL] += lv[b];
+            }
+        }
+        for (; g < c.groups; g += kGroupWaves) {
+#pragma unroll
+            for (int mm = 0; mm < DPL; ++mm) {
+                const int col = l + 64 * mm;
+                s[mm] += col < c.bv.D ? (double)load_f(src + (int64_t)g * rstride + col) : 0.0;
+            }
+            s[DPL] += l == 0 ? sampler::load_shared(lsrc + (int64_t)g * kBatchTileChains) : 0.0;
+        }
+#pragma unroll
+        for (int mm = 0; mm <= DPL; ++mm) sh.red[wave][mm * 64 + l] = s[mm];
+    }
+    __syncthreads();  // per-wave sums in LDS
+    if (LEADER && host) {
+#pragma unroll
+        for (int mm = 0; mm <= DPL; ++mm) {
+            double tot = 0.0;
+#pragma unroll
+            for (int w = 0; w < kGroupWaves; ++w) tot += sh.red[w][mm * 64 + l];
+            out[mm] = tot;
+        }
+    }
+    // a failed exchange ends the chain; the workers stay in step until the
+    // leader's next call hands them the stop at the first barrier
+    return LEADER ? status : kCmdEval;
+}
+
+template <int KT, int DPL>
+struct BatchEval {
+    BatchCtx c;
+    BatchShared<DPL>* sh;
+    double inv_s2, prior_const;
+    unsigned long long step;
+    bool abort;
+
+    __device__ bool s_writer() const { return true; }
+    __device__ bool out_writer() const { return true; }
+    __device__ bool aborted() const { return abort; }
+
+    __device__ void eval(const double (&q)[DPL], double& U, double (&g)[DPL])
+    {
+        double r[DPL + 1];
+        const int cmd = batch_collective<KT, DPL, true>(c, *sh, step, q, true, false, r);
+        step++;
+        const int l = lane();
+        if (cmd != kCmdEval) {
+            abort = true;
+            U = 0.0;
+#pragma unroll
+            for (int m = 0; m < DPL; ++m) g[m] = 0.0;
+            return;
+        }
+        double pr = 0.0;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) pr += 0.5 * q[m] * q[m] * inv_s2;
+        const double prior = wave_sum(pr);
+        U = readlane_f64(r[DPL], 0) + prior + prior_const;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) g[m] = (l + 64 * m < c.bv.D) ? r[m] + q[m] * inv_s2 : 0.0;
+    }
+
+    // Keep the tile's steps going with zero positions until every slot of the
+    // tile is finished (or an exchange failed).
+    __device__ void finish(bool publish_q)
+    {
+        double q[DPL], r[DPL + 1];
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) q[m] = 0.0;
+        bool first = true;
+        for (;;) {
+            const int cmd = batch_collective<KT, DPL, true>(c, *sh, step, q, publish_q, first, r);
+            first = false;
+            step++;
+            if (cmd != kCmdEval) break;
+        }
+    }
+};
+
+template <int KT, int DPL>
+__global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(SamplerArgs A, BatchView bv,
+                                                                              int tiles, int groups, float* qbuf,
+                                                                              float* P, double* L,
+                                                                              BatchSync* sync)
+{
+    extern __shared__ double lds[];  // the controller's checkpoint array
+    __shared__ BatchShared<DPL> sh;
+    BatchCtx c;
+    c.bv = bv;
+    c.tiles = tiles;
+    c.groups = groups;
+    c.t = (int)(blockIdx.x / groups);
+    c.i = (int)(blockIdx.x % groups);
+    c.st0 = (int64_t)c.i * bv.ns / groups;
+    c.st1 = (int64_t)(c.i + 1) * bv.ns / groups;
+    c.pw = 64 * DPL;
+    c.qbuf = qbuf;
+    c.P = P;
+    c.L = L;
+    c.sync = sync;
+    const int wave = threadIdx.x / kWave;
+    if (wave == 0) {
+        BatchEval<KT, DPL> ev;
+        ev.c = c;
+        ev.sh = &sh;
+        ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
+        ev.prior_const = (double)bv.D * (log(A.prior_scale) + sampler::kHalfLog2Pi);
+        ev.step = 0;
+        ev.abort = false;
+        const int64_t chain = (int64_t)c.t * kBatchTileChains + c.i;
+        const bool host = c.i < kBatchTileChains;
+        if (host && chain < A.num_chains) sampler::run_chain<DPL>(A, ev, chain, lds);
+        ev.finish(host);
+    } else {
+        double q[DPL], r[DPL + 1];
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) q[m] = 0.0;
+        for (unsigned long long step = 0;; ++step)
+            if (batch_collective<KT, DPL, false>(c, sh, step, q, false, false, r) != kCmdEval) break;
+    }
+}
+
+// Kernel for a shape: KT chunks (0..8) and DPL = ceil(D / 64) (1..3); the
+// pairs that occur for D <= 132.
+const void* batch_kernel_for(const BatchView& bv)
+{
+    const int dpl = (bv.D + 63) / 64;
+    switch (bv.kt * 4 + dpl) {
+    case 0 * 4 + 1: return (const void*)sampler_batch_kernel<0, 1>;
+    case 1 * 4 + 1: return (const void*)sampler_batch_kernel<1, 1>;
+    case 2 * 4 + 1: return (const void*)sampler_batch_kernel<2, 1>;
+    case 3 * 4 + 1: return (const void*)sampler_batch_kernel<3, 1>;
+    case 4 * 4 + 1: return (const void*)sampler_batch_kernel<4, 1>;
+    case 4 * 4 + 2: return (const void*)sampler_batch_kernel<4, 2>;
+    case 5 * 4 + 2: return (const void*)sampler_batch_kernel<5, 2>;
+    case 6 * 4 + 2: return (const void*)sampler_batch_kernel<6, 2>;
+    case 7 * 4 + 2: return (const void*)sampler_batch_kernel<7, 2>;
+    case 8 * 4 + 2: return (const void*)sampler_batch_kernel<8, 2>;
+    case 8 * 4 + 3: return (const void*)sampler_batch_kernel<8, 3>;
+    default: return nullptr;
+    }
+}
+
+size_t batch_sampler_lds(const SamplerArgs& a)
+{
+    const int slots = a.max_depth > 1 ? a.max_depth : 1;
+    return (size_t)slots * 2 * a.data.D * sizeof(double);
+}
+
+}  // namespace
+
+bool batch_sampler_supported(const BatchView& bv, int max_depth, int num_cu)
+{
+    if (bv.D > 64 * 3 || num_cu < kBatchTileChains) return false;
+    int per_cu = 0;
+    const size_t lds = (size_t)(max_depth > 1 ? max_depth : 1) * 2 * bv.D * sizeof(double);
+    const void* k = batch_kernel_for(bv);
+    if (!k) return false;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGroupWaves * kWave, lds) != hipSuccess) return false;
+    return per_cu >= 1;
+}
+
+hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int tiles, int groups, float* qbuf,
+                                float* P, double* L, BatchSync* sync, hipStream_t stream)
+{
+    hipError_t e = hipMemsetAsync(sync, 0, sizeof(BatchSync), stream);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(sync->done_at, 0xFF, sizeof(sync->done_at), stream);
+    if (e != hipSuccess) return e;
+    SamplerArgs A = a;
+    BatchView B = bv;
+    void* args[] = {&A, &B, &tiles, &groups, &qbuf, &P, &L, &sync};
+    const void* k = batch_kernel_for(bv);
+    if (!k) return hipErrorInvalidValue;
+    return hipLaunchCooperativeKernel(k, dim3((unsigned)(tiles * groups)),
+                                      dim3(kGroupWaves * kWave), args, (unsigned)batch_sampler_lds(a), stream);
+}
+
+}  // namespace nuts

@@ -117,6 +117,81 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
                                GridSync* sync, hipStream_t stream);
 int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu);
 
+// ---------------------------------------------------------------------------
+// Batched chains on shared fp32 data: the potential and gradient of K
+// positions as one contraction E = X Q (N x D by D x K) on the matrix cores,
+// the row terms on E, then G = X^T R (D x N by N x K).
+//
+// Layout: stages of 64 rows; a stage is 64 rows of `stride` floats, row r of
+// stage s at (s * 64 + r) * stride.  Columns 0 .. 16 kt - 1 feed the matrix
+// cores in 16-column chunks; a tail of up to four more columns (16 kt ..
+// 16 kt + 3) is handled on the vector ALUs.  Entries past N or past D are
+// zero.  y is one byte per row, 0xFF past N.
+struct BatchView {
+    const float* X;
+    const uint8_t* y;
+    int64_t N;
+    int D;
+    int kt;          // 16-column chunks on the matrix cores
+    int tc;          // tail columns on the vector ALUs (0..4)
+    int stride;      // 16 kt + 4 floats
+    int64_t ns;      // stages: ceil(N / 64)
+};
+constexpr int kBatchStageRows = 64;
+constexpr int kBatchMaxKT = 8;          // D <= 132
+constexpr int kBatchTileChains = 128;   // chains (positions) per tile: 8 waves x 16
+constexpr int kBatchMaxTiles = 2;       // tiles per sampler launch
+
+// Chunk and tail counts for D columns; false if D is too wide.
+inline bool batch_shape(int D, int* kt, int* tc)
+{
+    const int rem = D % 16;
+    int k = D / 16, t = rem;
+    if (rem > 4) {
+        k += 1;
+        t = 0;
+    }
+    if (k > kBatchMaxKT) return false;
+    *kt = k;
+    *tc = t;
+    return true;
+}
+
+// Fill X/y of the batch layout from the column-block layout of `src` (fp32,
+// one data set).
+hipError_t launch_to_batch_layout(const DataView& src, const BatchView& dst, float* X, uint8_t* y,
+                                  hipStream_t stream);
+
+// Workspace of the batched potential: fp32 partial rows P[T][G][128][pw]
+// and fp64 loss partials L[T][G][128], T = ceil(K / 128) tiles of G groups.
+struct BatchPlan {
+    int tiles;
+    int groups;   // per tile
+    int pw;       // 64 * ceil(D / 64)
+};
+BatchPlan plan_batch_potential(const BatchView& bv, int64_t K, int num_cu);
+hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const double* W, int64_t K,
+                                  const BatchPlan& plan, float* P, double* L, double* out_U, double* out_grad,
+                                  hipStream_t stream);
+
+// Batched sampler exchange state.  Zeroed per launch except done_at, which
+// starts at all ones ("not finished").
+struct BatchSync {
+    unsigned int error;                                       // a wait timed out
+    unsigned int pad0[31];
+    unsigned long long tile_count[kBatchMaxTiles][16];        // groups done with step s: (s + 1) * G
+    unsigned long long stamp[kBatchMaxTiles * kBatchTileChains];    // s + 1 once Q(s) of the chain is out
+    unsigned long long done_at[kBatchMaxTiles * kBatchTileChains];  // first step with no iteration left
+};
+// Sampler on `tiles` tiles of `groups` groups (groups >= 128): chain slot i
+// of tile t is run by group t * groups + i.  qbuf holds [2][tiles * 128][192]
+// floats, P [2][tiles][groups][128][pw] floats, L [2][tiles][groups][128]
+// doubles.
+hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int tiles, int groups, float* qbuf,
+                                float* P, double* L, BatchSync* sync, hipStream_t stream);
+bool batch_sampler_supported(const BatchView& bv, int max_depth, int num_cu);
+constexpr int kBatchQWidth = 192;
+
 // Per-dtype kernel entry points (sampler_f32.hip, sampler_f64.hip).
 hipError_t launch_sampler_wave_f32(const SamplerArgs& a, hipStream_t stream);
 hipError_t launch_sampler_wave_f64(const SamplerArgs& a, hipStream_t stream);
