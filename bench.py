@@ -36,6 +36,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
 METRIC = "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline"
 
 
@@ -68,8 +69,15 @@ def run_workload(name, steps=None, warmup=None):
     torch.cuda.synchronize()
     layout_s = time.time() - t0
     del Xd
+    # the path the library's AUTO rule takes for this shape, named explicitly
+    if C == 1:
+        path, kernel = nuts.NUTS_PATH_GRID, "sampler_grid_kernel"
+    elif wl.per_chain_data or wl.dtype != "f32":
+        path, kernel = nuts.NUTS_PATH_WAVE, "sampler_wave_kernel"
+    else:
+        path, kernel = nuts.NUTS_PATH_BATCH, "sampler_batch_kernel"
     kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
-              prior_scale=wl.prior_scale, num_chains=C)
+              prior_scale=wl.prior_scale, num_chains=C, path=path)
 
     t0 = time.time()
     r0 = d.sample(num_warmup=warmup, num_samples=1, adapt_diag_mass=wl.adapt_diag_mass, **kw)
@@ -104,9 +112,16 @@ def run_workload(name, steps=None, warmup=None):
     es = 8 if wl.dtype == "f64" else 4
     bytes_per_eval = wl.N * wl.D * es + wl.N
     achieved = evals * bytes_per_eval / gpu_s / 1e9
+    # batched path: every chain of a 128-chain tile takes one leapfrog step
+    # per pass until the tile's last chain is done; passes = the most
+    # evaluations of any chain of the tile
+    per_chain = 1 + st["num_steps"].sum(axis=1)
+    passes = max(int(per_chain[t:t + 128].max()) for t in range(0, C, 128))
+    flops_per_eval = 4.0 * wl.N * wl.D       # E = X q and G = X^T r, 2 flops per multiply-add
+    tflops = evals * flops_per_eval / gpu_s / 1e12
     log(f"{name}: {steps} iterations x {C} chains, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
         f"({wall * 1e3:.1f} ms wall): {evals / gpu_s:.0f} evals/s, {achieved:.0f} GB/s, "
-        f"min ESS {ess.min():.0f}")
+        f"{tflops:.1f} TFLOP/s, min ESS {ess.min():.0f}")
     d.free()
     s.close()
     return dict(
@@ -119,6 +134,8 @@ def run_workload(name, steps=None, warmup=None):
         mean_tree_depth=float(st["tree_depth"].mean()),
         mean_steps_per_iter=float(st["num_steps"].mean()),
         divergences=int(st["diverging"].sum()), accept_prob=float(st["accept_prob"].mean()),
+        path=path, kernel=kernel, flops_per_eval=flops_per_eval, achieved_tflops=tflops,
+        passes=passes, pass_fill=evals / (passes * C), ms_per_pass=1e3 * gpu_s / passes,
     )
 
 
@@ -181,7 +198,18 @@ def main():
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
 
     achieved = main_res["achieved_gbs"]
-    kernel = "sampler_grid_kernel" if main_res["chains"] == 1 else "sampler_wave_kernel"
+    kernel = main_res["kernel"]
+    if kernel == "sampler_batch_kernel":
+        roof = {"kernel": kernel, "bound": "mfma", "achieved": round(main_res["achieved_tflops"], 2),
+                "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(main_res["achieved_tflops"] / MFMA_F32_PEAK_TFLOPS, 4), "traffic": None,
+                "flops_per_eval": main_res["flops_per_eval"], "passes": main_res["passes"],
+                "pass_fill": round(main_res["pass_fill"], 4),
+                "ms_per_pass": round(main_res["ms_per_pass"], 4)}
+    else:
+        roof = {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "bytes_per_eval": main_res["bytes_per_eval"]}
     line = {
         "metric": METRIC,
         "value": round(main_res["evals_per_s"], 1),
@@ -199,6 +227,7 @@ def main():
             "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
             "chains": main_res["chains"], "step_size": main_res["step_size"],
             "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
+            "path": main_res["kernel"],
         },
         "ess_per_s": round(main_res["ess_per_s"], 2),
         "ess_min": round(main_res["ess_min"], 1),
@@ -207,12 +236,7 @@ def main():
         "mean_steps_per_iter": round(main_res["mean_steps_per_iter"], 2),
         "divergences": main_res["divergences"],
         "layout_seconds": round(main_res["layout_seconds"], 4),
-        "roofline": {
-            "kernel": kernel,
-            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-            "bytes_per_eval": main_res["bytes_per_eval"],
-        },
+        "roofline": roof,
         "cpu_baseline": cpu,
     }
     if other:

@@ -361,7 +361,7 @@ static int ensure_batch_layout(nuts_handle* h, const nuts_data* dc)
     b.D = d->view.D;
     b.kt = kt;
     b.tc = tc;
-    b.stride = 16 * kt + 4;
+    b.stride = 16 * batch_kp(kt) + 4;
     b.ns = (b.N + kBatchStageRows - 1) / kBatchStageRows;
     const size_t xb = (size_t)b.ns * kBatchStageRows * b.stride * sizeof(float);
     const size_t yb = (size_t)b.ns * kBatchStageRows;

@@ -36,10 +36,38 @@ constexpr int kWaves = 8;                                   // matrix-core waves
 constexpr int kTileRows = 16;
 constexpr int kTiles = kBatchStageRows / kTileRows;         // MFMA tiles per stage
 constexpr int kTail = 4;
-constexpr int kMaxStride = 16 * kBatchMaxKT + kTail;        // 132 floats
-constexpr int kStageFloats = kBatchStageRows * kMaxStride;  // one LDS stage buffer
-constexpr int kStageBuf = kStageFloats + 4;                 // plus one junk 16-byte slot
-constexpr int kStageVecs = (kStageFloats / 4 + kWaves * kWave - 1) / (kWaves * kWave);
+constexpr int kMaxStride = 16 * kBatchMaxKT + kTail;        // 132 floats per row in HBM
+
+// LDS geometry of a stage for KT chunks.  The HBM row (16 KP permuted
+// matrix-core slots, then the tail) is spread out so that column residue g
+// starts at g * GS: GS = 12 for KP = 8 (two 16-byte pieces per residue) and
+// 4 for KP = 4, and the row stride RS = 16 GS + 4 is 4 mod 64 floats.  With
+// these, a 16-lane phase of every 16-byte LDS read below (16 rows at one
+// residue, or 16 residues of one row) touches 64 distinct banks.
+template <int KT>
+struct Geo {
+    static constexpr int KP = (KT + 3) / 4 * 4;
+    static constexpr int GS = KP == 8 ? 12 : 4;
+    static constexpr int RS = 16 * GS + 4;
+    static constexpr int HS = 16 * KP + 4;          // HBM row: floats
+    static constexpr int HV = HS / 4;               // HBM row: 16-byte pieces
+};
+constexpr int kStageFloats = kBatchStageRows * Geo<kBatchMaxKT>::RS;  // largest LDS stage
+constexpr int kStageBuf = kStageFloats + 4;                          // plus one junk 16-byte slot
+constexpr int kStageVecs = (kBatchStageRows * kMaxStride / 4 + kWaves * kWave - 1) / (kWaves * kWave);
+
+// Column of the matrix-core operand that lane group jj reads as component i
+// of its 16-byte piece in chunk t of the column contraction (E = X Q):
+// piece f = 4 t + jj of the row is residue g, half h of the permuted slots.
+template <int KT>
+__host__ __device__ constexpr int e_column(int t, int jj, int i)
+{
+    constexpr int KP = Geo<KT>::KP;
+    const int f = 4 * t + jj;
+    const int g = KP == 8 ? f >> 1 : f;
+    const int h = KP == 8 ? f & 1 : 0;
+    return 16 * (4 * h + i) + g;   // chunk 4 h + i (valid if < KT), residue g
+}
 
 __device__ __forceinline__ v4f mfma(float a, float b, v4f c)
 {
@@ -47,29 +75,28 @@ __device__ __forceinline__ v4f mfma(float a, float b, v4f c)
 }
 
 // Negative log-likelihood and residual of one (row, position) from eta in
-// fp32: with s = 1 - 2y and t = s eta, loss = softplus(t), residual =
-// s sigmoid(t), both from one exp(-|t|); log1p(e) as log(u) e / (u - 1),
-// u = 1 + e (Goldberg 1991, Thm. 4).  A label byte > 1 marks a padding row,
-// which contributes nothing.
-__device__ __forceinline__ void row_terms(float eta, uint32_t ybyte, float& loss, float& resid)
+// fp32, with sgn = 1 - 2y: t = sgn eta, loss = softplus(t) = max(t, 0) +
+// ln 2 log2(1 + e), residual = sgn sigmoid(t), e = exp(-|t|); three
+// transcendentals (exp2, log2, reciprocal) on the fp32 hardware units.  The
+// rounding of 1 + e costs at most 2^-24 absolute per term (log1p accuracy is
+// not needed for a sum of softplus values that are O(1) each).  Padding rows
+// (zero X, y = 0) have eta = 0 exactly and add exactly ln 2 (in fp32) to the
+// loss and nothing to the gradient; the caller subtracts them.
+constexpr float kLn2f = 0.69314718055994531f;
+
+__device__ __forceinline__ void row_terms(float eta, float sgn, float& loss, float& resid)
 {
-    const bool one = ybyte == 1u;
-    const float t = one ? -eta : eta;
-    const float a = fabsf(t);
-    const float e = __builtin_amdgcn_exp2f(-a * 1.4426950408889634f);
+    const float t = sgn * eta;
+    const float e = __builtin_amdgcn_exp2f(-fabsf(t) * 1.4426950408889634f);
     const float u = 1.0f + e;
     const float inv = __builtin_amdgcn_rcpf(u);
-    const float um1 = u - 1.0f;
-    const float lg = __builtin_amdgcn_logf(u) * 0.69314718055994531f;
-    const float l1p = um1 == 0.0f ? e : lg * (e * __builtin_amdgcn_rcpf(um1));
-    const float sig = t >= 0.0f ? inv : e * inv;
-    const bool pad = ybyte > 1u;
-    loss = pad ? 0.0f : fmaxf(t, 0.0f) + l1p;
-    resid = pad ? 0.0f : (one ? -sig : sig);
+    loss = __builtin_fmaf(kLn2f, __builtin_amdgcn_logf(u), fmaxf(t, 0.0f));
+    resid = sgn * ((t >= 0.0f ? 1.0f : e) * inv);
 }
 
 // A wave's share of the positions: Q in the B-operand order of the column
-// contraction (q[4 t + i] = Q[16 t + 4 (l / 16) + i][l % 16]) and the tail.
+// contraction (q[4 t + i] = Q[e_column(t, l / 16, i)][l % 16], zero where
+// that chunk is >= KT) and the tail.
 struct WaveQ {
     float q[4 * kBatchMaxKT];
     float qt[kTail];
@@ -108,65 +135,119 @@ __device__ __forceinline__ void load_stage(const BatchView& bv, int64_t st, int 
     if (tid < kBatchStageRows / 4) r.y = reinterpret_cast<const uint32_t*>(bv.y + st * kBatchStageRows)[tid];
 }
 
-__device__ __forceinline__ void store_stage(const BatchView& bv, const StageRegs& r, int tid, float* xs,
-                                            uint32_t* ys)
+// Scatter a stage into the LDS geometry: HBM piece q of a row goes to
+// residue q / (KP / 4), half q % (KP / 4); the last piece is the tail.
+template <int KT>
+__device__ __forceinline__ void store_stage(const StageRegs& r, int tid, float* xs, float* ys)
 {
-    // pieces past the stage go to a junk slot after the buffer (never read)
-    const int last = kBatchStageRows * bv.stride / 4 - 1;
+    using G = Geo<KT>;
+    constexpr int last = kBatchStageRows * G::HV - 1;
 #pragma unroll
     for (int i = 0; i < kStageVecs; ++i) {
         const int idx = tid + i * kWaves * kWave;
-        reinterpret_cast<v4f*>(xs)[idx <= last ? idx : kStageFloats / 4] = r.v[i];
+        const int row = idx / G::HV;
+        const int q = idx - row * G::HV;
+        int dst;
+        if constexpr (G::KP == 8) dst = q < 32 ? (q >> 1) * 3 + (q & 1) : 4 * G::GS;
+        else dst = q < 4 * G::KP ? q : 4 * G::GS;  // KP = 4: one piece per residue
+        dst += row * (G::RS / 4);
+        // pieces past the stage go to a junk slot after the buffer (never read)
+        reinterpret_cast<v4f*>(xs)[idx <= last ? dst : kStageFloats / 4] = r.v[i];
     }
-    if (tid < kBatchStageRows / 4) ys[tid] = r.y;
+    if (tid < kBatchStageRows / 4) {
+        // labels as signs 1 - 2y
+        v4f sg;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) sg[k] = ((r.y >> (8 * k)) & 1u) ? -1.0f : 1.0f;
+        reinterpret_cast<v4f*>(ys)[tid] = sg;
+    }
 }
 
-// All four 16-row tiles of one LDS stage for this wave's 16 positions.  KT
-// is the chunk count; the four tail slots are always processed (slots past
-// the tail hold zero columns and zero positions, so they add nothing).
+// All four 16-row tiles of one LDS stage for this wave's 16 positions, two
+// tiles at a time so that two independent accumulation chains alternate on
+// the matrix core.  KT is the chunk count; the four tail slots are always
+// processed (slots past the tail hold zero columns and zero positions, so
+// they add nothing).
+//
+// `flip` reverses the pair order: the two waves that share a SIMD (loader
+// index w and w + 4) take the pairs in opposite orders, so that one is on
+// the matrix core while the other evaluates its row terms.
 template <int KT>
-__device__ __forceinline__ void compute_stage(const float* __restrict__ xs, const uint32_t* __restrict__ ys,
-                                              int stride, const WaveQ& Q, WaveAcc& acc)
+__device__ __forceinline__ void compute_stage(const float* __restrict__ xs, const float* __restrict__ ys,
+                                              const WaveQ& Q, WaveAcc& acc, bool flip)
 {
+    using G = Geo<KT>;
     const int l = lane();
     const int m = l & 15;
     const int jj = l >> 4;
+    // this lane's piece of chunk 0 in its E row, and its G residue
+    const int e_off = m * G::RS + (G::KP == 8 ? 12 * (jj >> 1) + 4 * (jj & 1) : 4 * jj);
+    constexpr int e_step = G::KP == 8 ? 24 : 16;
+    const int g_off = 4 * jj * G::RS + m * G::GS;
 #pragma unroll 1
-    for (int ti = 0; ti < kTiles; ++ti) {
-        const float* xt = xs + ti * kTileRows * stride;
-        v4f e = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int step = 0; step < kTiles; step += 2) {
+        const int tp = flip ? kTiles - 2 - step : step;
+        const float* x0 = xs + tp * kTileRows * G::RS;
+        const float* x1 = x0 + kTileRows * G::RS;
+        v4f e0 = {0.0f, 0.0f, 0.0f, 0.0f};
+        v4f e1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int t = 0; t < KT; ++t) {
-            const v4f a = *reinterpret_cast<const v4f*>(xt + m * stride + 16 * t + 4 * jj);
-            e = mfma(a[0], Q.q[4 * t + 0], e);
-            e = mfma(a[1], Q.q[4 * t + 1], e);
-            e = mfma(a[2], Q.q[4 * t + 2], e);
-            e = mfma(a[3], Q.q[4 * t + 3], e);
+        for (int t = 0; t < G::KP; ++t) {
+            const v4f a0 = *reinterpret_cast<const v4f*>(x0 + e_off + e_step * t);
+            const v4f a1 = *reinterpret_cast<const v4f*>(x1 + e_off + e_step * t);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                e0 = mfma(a0[i], Q.q[4 * t + i], e0);
+                e1 = mfma(a1[i], Q.q[4 * t + i], e1);
+            }
         }
-        // tail slots of this lane's four rows 4 jj + r
-        v4f xr[4];
+        // tail slots of this lane's four rows 4 jj + r of both tiles
+        v4f xr0[4], xr1[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            xr[r] = *reinterpret_cast<const v4f*>(xt + (4 * jj + r) * stride + 16 * KT);
-            e[r] += ((xr[r][0] * Q.qt[0] + xr[r][1] * Q.qt[1]) + xr[r][2] * Q.qt[2]) + xr[r][3] * Q.qt[3];
+            xr0[r] = *reinterpret_cast<const v4f*>(x0 + (4 * jj + r) * G::RS + 16 * G::GS);
+            xr1[r] = *reinterpret_cast<const v4f*>(x1 + (4 * jj + r) * G::RS + 16 * G::GS);
+            e0[r] += ((xr0[r][0] * Q.qt[0] + xr0[r][1] * Q.qt[1]) + xr0[r][2] * Q.qt[2]) + xr0[r][3] * Q.qt[3];
+            e1[r] += ((xr1[r][0] * Q.qt[0] + xr1[r][1] * Q.qt[1]) + xr1[r][2] * Q.qt[2]) + xr1[r][3] * Q.qt[3];
         }
-        const uint32_t yw = ys[ti * 4 + jj];
-        float rr[4];
+        const v4f s0 = *reinterpret_cast<const v4f*>(ys + tp * kTileRows + 4 * jj);
+        const v4f s1 = *reinterpret_cast<const v4f*>(ys + (tp + 1) * kTileRows + 4 * jj);
+        float r0[4], r1[4];
+        float lsum = 0.0f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            float ls;
-            row_terms(e[r], (yw >> (8 * r)) & 0xFFu, ls, rr[r]);
-            acc.loss += (double)ls;
+            float l0, l1;
+            row_terms(e0[r], s0[r], l0, r0[r]);
+            row_terms(e1[r], s1[r], l1, r1[r]);
+            lsum += l0 + l1;
+        }
+        acc.loss += (double)lsum;
+        // G: residue m of row 4 jj + r holds chunks 4 h .. 4 h + 3 in piece h
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+            for (int h = 0; h < G::KP / 4; ++h) {
+                const v4f b0 = *reinterpret_cast<const v4f*>(x0 + g_off + r * G::RS + 4 * h);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * h + i < KT) acc.g[4 * h + i] = mfma(b0[i], r0[r], acc.g[4 * h + i]);
+            }
         }
 #pragma unroll
-        for (int mt = 0; mt < KT; ++mt) {
+        for (int r = 0; r < 4; ++r) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                acc.g[mt] = mfma(xt[(4 * jj + r) * stride + 16 * mt + m], rr[r], acc.g[mt]);
+            for (int h = 0; h < G::KP / 4; ++h) {
+                const v4f b1 = *reinterpret_cast<const v4f*>(x1 + g_off + r * G::RS + 4 * h);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * h + i < KT) acc.g[4 * h + i] = mfma(b1[i], r1[r], acc.g[4 * h + i]);
+            }
         }
 #pragma unroll
-        for (int k = 0; k < kTail; ++k)
-            acc.gt[k] += ((xr[0][k] * rr[0] + xr[1][k] * rr[1]) + xr[2][k] * rr[2]) + xr[3][k] * rr[3];
+        for (int k = 0; k < kTail; ++k) {
+            acc.gt[k] += ((xr0[0][k] * r0[0] + xr0[1][k] * r0[1]) + xr0[2][k] * r0[2]) + xr0[3][k] * r0[3];
+            acc.gt[k] += ((xr1[0][k] * r1[0] + xr1[1][k] * r1[1]) + xr1[2][k] * r1[2]) + xr1[3][k] * r1[3];
+        }
     }
 }
 
@@ -176,7 +257,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
 // does nothing else.
 template <int KT, bool WORKER>
 __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int64_t st1, int tid, float* xs,
-                                           uint32_t* ys, const WaveQ& Q, WaveAcc& acc)
+                                           float* ys, const WaveQ& Q, WaveAcc& acc)
 {
     if constexpr (!WORKER) {
         for (int64_t st = st0; st <= st1; ++st) __syncthreads();
@@ -184,7 +265,7 @@ __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int
         if (st0 < st1) {
             StageRegs r;
             load_stage(bv, st0, tid, r);
-            store_stage(bv, r, tid, xs, ys);
+            store_stage<KT>(r, tid, xs, ys);
         }
         __syncthreads();
         for (int64_t st = st0; st < st1; ++st) {
@@ -192,8 +273,8 @@ __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int
             const bool more = st + 1 < st1;
             StageRegs r;
             if (more) load_stage(bv, st + 1, tid, r);
-            compute_stage<KT>(xs + b * kStageBuf, ys + b * (kBatchStageRows / 4), bv.stride, Q, acc);
-            if (more) store_stage(bv, r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * (kBatchStageRows / 4));
+            compute_stage<KT>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, acc, tid >= 4 * kWave);
+            if (more) store_stage<KT>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
             __syncthreads();
         }
     }

@@ -11,9 +11,10 @@ namespace nuts {
 // Layout conversion: column blocks (fp32, one data set) -> 64-row stages.
 
 __global__ void __launch_bounds__(256) to_batch_kernel(const float* __restrict__ Xb, const uint8_t* __restrict__ yb,
-                                                       int R, int64_t N, int D, float* __restrict__ X,
+                                                       int R, int64_t N, int D, int kt, float* __restrict__ X,
                                                        uint8_t* __restrict__ y, int stride, int64_t ns)
 {
+    const int kp = batch_kp(kt);
     const int64_t per_stage = (int64_t)kBatchStageRows * stride;
     const int64_t total = ns * per_stage;
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
@@ -23,10 +24,18 @@ __global__ void __launch_bounds__(256) to_batch_kernel(const float* __restrict__
         const int r = (int)(rem / stride);
         const int c = (int)(rem - (int64_t)r * stride);
         const int64_t i = st * kBatchStageRows + r;
+        // slot c: permuted matrix-core columns, then the tail
+        int col;
+        if (c < 16 * kp) {
+            const int t = c % kp;
+            col = t < kt ? 16 * t + c / kp : D;
+        } else {
+            col = 16 * kt + (c - 16 * kp);
+        }
         float v = 0.0f;
-        if (i < N && c < D) v = Xb[((i / R) * D + c) * R + (i % R)];
+        if (i < N && col < D) v = Xb[((i / R) * D + col) * R + (i % R)];
         X[o] = v;
-        if (c == 0) y[i] = i < N ? yb[i] : (uint8_t)0xFF;
+        if (c == 0) y[i] = i < N ? yb[i] : (uint8_t)0;
     }
 }
 
@@ -38,7 +47,7 @@ hipError_t launch_to_batch_layout(const DataView& src, const BatchView& dst, flo
     const int64_t want = (total + 255) / 256;
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
     hipLaunchKernelGGL(to_batch_kernel, dim3(grid), dim3(256), 0, stream, (const float*)src.X, src.y,
-                       rows_per_block(src), src.N, src.D, X, y, dst.stride, dst.ns);
+                       rows_per_block(src), src.N, src.D, dst.kt, X, y, dst.stride, dst.ns);
     return hipGetLastError();
 }
 
@@ -98,7 +107,7 @@ __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_pass_kernel(Ba
                                                                               double* __restrict__ L)
 {
     __shared__ __align__(16) float xs[2 * batch::kStageBuf];
-    __shared__ uint32_t ys[2 * kBatchStageRows / 4];
+    __shared__ __align__(16) float ys[2 * kBatchStageRows];
     const int l = lane();
     const int m = l & 15;
     const int jj = l >> 4;
@@ -110,12 +119,14 @@ __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_pass_kernel(Ba
     const bool live = pos < K;
 
     WaveQ Q;
+    constexpr int KP = batch::Geo<KT>::KP;
 #pragma unroll
-    for (int c = 0; c < KT; ++c)
+    for (int t = 0; t < KP; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int col = 16 * c + 4 * jj + i;
-            Q.q[4 * c + i] = (live && col < D) ? (float)W[pos * D + col] : 0.0f;
+            const int col = batch::e_column<KT>(t, jj, i);
+            const bool used = (col / 16) < KT && col < D;
+            Q.q[4 * t + i] = (live && used) ? (float)W[pos * D + col] : 0.0f;
         }
 #pragma unroll
     for (int k = 0; k < batch::kTail; ++k)
@@ -132,7 +143,7 @@ __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_pass_kernel(Ba
 
 constexpr int kFinishWaves = 4;
 
-__global__ void __launch_bounds__(kFinishWaves * kWave) batch_finish_kernel(int D, int groups, int pw,
+__global__ void __launch_bounds__(kFinishWaves * kWave) batch_finish_kernel(int D, int groups, int pw, int npad,
                                                                            const double* __restrict__ W,
                                                                            const float* __restrict__ P,
                                                                            const double* __restrict__ L,
@@ -177,6 +188,7 @@ __global__ void __launch_bounds__(kFinishWaves * kWave) batch_finish_kernel(int 
     if (l == 0) {
         double loss = 0.0;
         for (int w = 0; w < kFinishWaves; ++w) loss += red[w * rw + pw];
+        loss -= (double)npad * (double)batch::kLn2f;  // padding rows of the last stage
         out_U[k] = loss + prior + (double)D * (log(prior_scale) + sampler::kHalfLog2Pi);
     }
 }
@@ -227,7 +239,7 @@ hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(batch_finish_kernel, dim3((unsigned)K), dim3(kFinishWaves * kWave),
                        (size_t)kFinishWaves * (plan.pw + 64) * sizeof(double), stream, bv.D, plan.groups, plan.pw,
-                       W, P, L, prior_scale, out_U, out_grad);
+                       (int)(bv.ns * kBatchStageRows - bv.N), W, P, L, prior_scale, out_U, out_grad);
     return hipGetLastError();
 }
 
@@ -261,7 +273,7 @@ constexpr int kCmdEval = 1, kCmdStop = 2, kCmdError = 3;
 template <int DPL>
 struct BatchShared {
     __align__(16) float xs[2 * batch::kStageBuf];
-    uint32_t ys[2 * kBatchStageRows / 4];
+    __align__(16) float ys[2 * kBatchStageRows];
     double red[kGroupWaves][(DPL + 1) * 64];
     int cmd;
 };
@@ -399,10 +411,14 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         const float* qsrc = c.qbuf + ((int64_t)par * c.tiles * kBatchTileChains +
                                       (int64_t)c.t * kBatchTileChains + widx * 16 + m) * kBatchQWidth;
         WaveQ Q;
+        constexpr int KP = batch::Geo<KT>::KP;
 #pragma unroll
-        for (int ch = 0; ch < KT; ++ch)
+        for (int t = 0; t < KP; ++t)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) Q.q[4 * ch + i] = load_f(qsrc + 16 * ch + 4 * jj + i);
+            for (int i = 0; i < 4; ++i) {
+                const int col = batch::e_column<KT>(t, jj, i);
+                Q.q[4 * t + i] = (col / 16) < KT ? load_f(qsrc + col) : 0.0f;
+            }
 #pragma unroll
         for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = load_f(qsrc + 16 * KT + k);
         WaveAcc acc;
@@ -468,6 +484,8 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
             for (int w = 0; w < kGroupWaves; ++w) tot += sh.red[w][mm * 64 + l];
             out[mm] = tot;
         }
+        // padding rows of the last stage
+        out[DPL] -= (double)(c.bv.ns * kBatchStageRows - c.bv.N) * (double)batch::kLn2f;
     }
     // a failed exchange ends the chain; the workers stay in step until the
     // leader's next call hands them the stop at the first barrier

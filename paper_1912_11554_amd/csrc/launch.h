@@ -123,10 +123,14 @@ int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu);
 // the row terms on E, then G = X^T R (D x N by N x K).
 //
 // Layout: stages of 64 rows; a stage is 64 rows of `stride` floats, row r of
-// stage s at (s * 64 + r) * stride.  Columns 0 .. 16 kt - 1 feed the matrix
-// cores in 16-column chunks; a tail of up to four more columns (16 kt ..
-// 16 kt + 3) is handled on the vector ALUs.  Entries past N or past D are
-// zero.  y is one byte per row, 0xFF past N.
+// stage s at (s * 64 + r) * stride.  The first 16 kp floats of a row
+// (kp = kt rounded up to a multiple of 4) hold the columns that feed the
+// matrix cores, permuted: slot g * kp + t holds column 16 t + g (g < 16,
+// t < kp; zero for t >= kt), so that the 16-column chunks t of one column
+// residue g are contiguous.  The last 4 floats hold the tail: up to four more
+// columns (16 kt .. 16 kt + 3) handled on the vector ALUs.  Entries past N
+// or past D are zero.  y is one byte per row, 0 past N (padding rows: zero X,
+// label 0).
 struct BatchView {
     const float* X;
     const uint8_t* y;
@@ -134,9 +138,10 @@ struct BatchView {
     int D;
     int kt;          // 16-column chunks on the matrix cores
     int tc;          // tail columns on the vector ALUs (0..4)
-    int stride;      // 16 kt + 4 floats
+    int stride;      // 16 kp + 4 floats
     int64_t ns;      // stages: ceil(N / 64)
 };
+__host__ __device__ inline int batch_kp(int kt) { return (kt + 3) / 4 * 4; }
 constexpr int kBatchStageRows = 64;
 constexpr int kBatchMaxKT = 8;          // D <= 132
 constexpr int kBatchTileChains = 128;   // chains (positions) per tile: 8 waves x 16

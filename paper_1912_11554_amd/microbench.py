@@ -1,0 +1,86 @@
+"""Time the fused potential+gradient kernels alone on a configured workload.
+
+    python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 1
+    python -m paper_1912_11554_amd.microbench --workload shared256_n200000_d129_f32 --positions 256 --batched
+
+Each call evaluates U and grad U at K positions (around the data's generating
+weights) with the data already in device memory; the outputs stay on the
+device.  Prints one JSON line: microseconds per call (HIP events on the
+stream the kernels run on), the algorithmic rate (bytes of X and y per
+position for the streaming kernel, 4 N D flops per position for the batched
+matrix-core kernel) and its fraction of the MI355X peak.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--workload", default="covtype_n581012_d55_f32")
+    ap.add_argument("--positions", type=int, default=1)
+    ap.add_argument("--batched", action="store_true",
+                    help="nuts_data_potential_grad_batched (fp32 matrix cores)")
+    ap.add_argument("--reps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    args = ap.parse_args()
+
+    import torch
+
+    import paper_1912_11554_amd as nuts
+    import workloads
+
+    wl = workloads.WORKLOADS[args.workload]
+    if wl.per_chain_data:
+        sys.exit("microbench takes shared-data workloads")
+    X, y, w_true = workloads.make_logistic(wl.N, wl.D, w_scale=wl.w_scale, key=wl.data_seed,
+                                           dtype=wl.dtype, zero_frac=wl.zero_frac)
+    K = args.positions
+    rng = np.random.default_rng(0)
+    W = torch.from_numpy(w_true[None, :] + rng.normal(0.0, 0.01, size=(K, wl.D))).cuda()
+    s = nuts.Sampler(0)
+    d = s.data(torch.from_numpy(X).cuda(), torch.from_numpy(y).cuda())
+    U = torch.empty(K, dtype=torch.float64, device="cuda")
+    G = torch.empty((K, wl.D), dtype=torch.float64, device="cuda")
+    for _ in range(args.warmup):
+        d.potential_grad(W, out_U=U, out_grad=G, batched=args.batched)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.reps):
+        d.potential_grad(W, out_U=U, out_grad=G, batched=args.batched)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / args.reps
+    es = 8 if wl.dtype == "f64" else 4
+    out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K,
+               kernel="batch_pass_kernel" if args.batched else "potential_pass_kernel",
+               reps=args.reps, us_per_call=round(us, 2))
+    if args.batched:
+        tflops = 4.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12
+        out.update(bound="mfma", achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
+                   frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4))
+    else:
+        gbs = (wl.N * wl.D * es + wl.N) * K / (us * 1e-6) / 1e9
+        out.update(bound="hbm", achieved_gbs=round(gbs, 1), peak=HBM_PEAK_GBS,
+                   frac=round(gbs / HBM_PEAK_GBS, 4))
+    print(json.dumps(out), flush=True)
+    d.free()
+    s.close()
+
+
+if __name__ == "__main__":
+    main()
