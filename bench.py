@@ -139,6 +139,29 @@ def run_workload(name, steps=None, warmup=None):
     )
 
 
+def recorded_traffic(kernel, workload, evals):
+    """HBM bytes of the timed launch from the PMC record in
+    profiles/traffic.json (FETCH_SIZE + WRITE_SIZE per gradient evaluation,
+    each scaled by the same counter's reading on a copy of known size), or
+    None when there is no record for this kernel and workload or the kernel
+    sources have changed since it was taken."""
+    from paper_1912_11554_amd.profiling import source_fingerprint
+
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("fingerprint") != source_fingerprint():
+        return None
+    e = rec.get("kernels", {}).get(f"{kernel}/{workload}")
+    if not e:
+        return None
+    return dict(bytes=round((e["fetch_bytes_per_eval"] + e["write_bytes_per_eval"]) * evals),
+                fetch_bytes_per_eval=e["fetch_bytes_per_eval"],
+                write_bytes_per_eval=e["write_bytes_per_eval"], source="profiles/traffic.json")
+
+
 def cpu_baseline(name, seconds):
     """The oracle's fp64 gradient evaluations on the same data, one core."""
     import oracle
@@ -199,16 +222,19 @@ def main():
 
     achieved = main_res["achieved_gbs"]
     kernel = main_res["kernel"]
+    traffic = recorded_traffic(kernel, main_res["workload"], main_res["grad_evals"])
     if kernel == "sampler_batch_kernel":
         roof = {"kernel": kernel, "bound": "mfma", "achieved": round(main_res["achieved_tflops"], 2),
                 "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(main_res["achieved_tflops"] / MFMA_F32_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(main_res["achieved_tflops"] / MFMA_F32_PEAK_TFLOPS, 4),
+                "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
                 "flops_per_eval": main_res["flops_per_eval"], "passes": main_res["passes"],
                 "pass_fill": round(main_res["pass_fill"], 4),
                 "ms_per_pass": round(main_res["ms_per_pass"], 4)}
     else:
         roof = {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
                 "bytes_per_eval": main_res["bytes_per_eval"]}
     line = {
         "metric": METRIC,

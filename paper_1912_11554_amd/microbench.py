@@ -6,9 +6,12 @@
 Each call evaluates U and grad U at K positions (around the data's generating
 weights) with the data already in device memory; the outputs stay on the
 device.  Prints one JSON line: microseconds per call (HIP events on the
-stream the kernels run on), the algorithmic rate (bytes of X and y per
-position for the streaming kernel, 4 N D flops per position for the batched
-matrix-core kernel) and its fraction of the MI355X peak.
+stream the kernels run on; the C-ABI call is synchronous, so this includes
+its host side: pointer checks, launches, the final synchronisation), the
+algorithmic rate at that time (bytes of X and y per position for the
+streaming kernel, 4 N D flops per position for the batched matrix-core
+kernel) and its fraction of the MI355X peak.  Run it under
+`rocprofv3 --kernel-trace --stats` for the kernels' own durations.
 """
 from __future__ import annotations
 
@@ -68,7 +71,7 @@ def main():
     es = 8 if wl.dtype == "f64" else 4
     out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K,
                kernel="batch_pass_kernel" if args.batched else "potential_pass_kernel",
-               reps=args.reps, us_per_call=round(us, 2))
+               reps=args.reps, us_per_call_with_host=round(us, 2))
     if args.batched:
         tflops = 4.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12
         out.update(bound="mfma", achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
