@@ -70,8 +70,12 @@ def run_workload(name, steps=None, warmup=None):
     layout_s = time.time() - t0
     del Xd
     # the path the library's AUTO rule takes for this shape, named explicitly
-    if C == 1:
+    es = 8 if wl.dtype == "f64" else 4
+    if C == 1 and wl.N * wl.D * es > 120 * 1024:
         path, kernel = nuts.NUTS_PATH_GRID, "sampler_grid_kernel"
+    elif C == 1:
+        # a data set that fits one group's LDS: one wavefront, data resident
+        path, kernel = nuts.NUTS_PATH_WAVE, "sampler_wave_kernel"
     elif wl.per_chain_data or wl.dtype != "f32":
         path, kernel = nuts.NUTS_PATH_WAVE, "sampler_wave_kernel"
     else:

@@ -482,12 +482,21 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
         const bool batchable = !per_chain && d->view.dtype == NUTS_F32 && num_chains >= 16 &&
                                (double)d->view.N * d->view.D >= 262144.0 && batch_shape(d->view.D, &kt, &tc);
         const bool small = d->view.nb <= 6;  // a few blocks: one wave beats a grid-wide exchange
+        // a lone chain whose data set fits in one group's LDS is faster on
+        // one wave than on a grid-wide exchange per step
+        SamplerArgs probe;
+        std::memset(&probe, 0, sizeof probe);
+        probe.data = d->view;
+        probe.max_depth = max_tree_depth;
+        probe.num_chains = num_chains;
+        const bool resident = wave_path_supports(d->view) && wave_path_resident(probe);
         if (batchable && ensure_batch_layout(h, d) == NUTS_OK &&
             batch_sampler_supported(d->batch, max_tree_depth, h->num_cu))
             path = NUTS_PATH_BATCH;
         else
-            path = ((per_chain || small || num_chains > 1) && wave_path_supports(d->view)) ? NUTS_PATH_WAVE
-                                                                                           : NUTS_PATH_GRID;
+            path = ((per_chain || small || resident || num_chains > 1) && wave_path_supports(d->view))
+                       ? NUTS_PATH_WAVE
+                       : NUTS_PATH_GRID;
         h->err.clear();
     }
     if (path != NUTS_PATH_WAVE && path != NUTS_PATH_GRID && path != NUTS_PATH_BATCH)

@@ -142,20 +142,95 @@ __device__ __forceinline__ double wave_sum(double v)
 // ---------------------------------------------------------------------------
 // Logistic row terms.  With s = 1 - 2y and t = s * eta, the row's negative
 // log-likelihood is softplus(t) >= 0 and d/d eta of it is s * sigmoid(t); both
-// come from one exp(-|t|).
+// come from one exp(-|t|).  The fp64 versions below are written out (range
+// reduction and series) for the arguments that occur here, at a few ulp,
+// instead of the general library routines.
 struct RowTerms {
     double loss;
     double resid;
 };
 
+// 1 / d to full fp64 precision: the hardware reciprocal refined by two
+// Newton steps (each doubles the correct bits).
+__device__ __forceinline__ double recip(double d)
+{
+    double r = __builtin_amdgcn_rcp(d);
+    double err = fma(-d, r, 1.0);
+    r = fma(r, err, r);
+    err = fma(-d, r, 1.0);
+    return fma(r, err, r);
+}
+
+// e^x for x <= 0: x = k ln 2 + r with |r| <= ln 2 / 2 (Cody-Waite: ln 2 split
+// into its float rounding and the remainder, so k * hi is exact), e^r from
+// its Taylor series to degree 13 (truncation below 5e-18 relative), scaled by
+// 2^k (which underflows to 0 for very negative x).  NaN propagates.
+__device__ __forceinline__ double exp_nonpos(double x)
+{
+    constexpr double kLog2e = 1.4426950408889634;
+    constexpr double kLn2Hi = 0.693147182464599609375;  // ln 2 rounded to a float
+    constexpr double kLn2Lo = -1.904654299957768e-09;   // ln 2 - kLn2Hi
+    x = x < -1100.0 ? -1100.0 : x;                      // keeps NaN
+    double k = rint(x * kLog2e);
+    double r = fma(-k, kLn2Hi, x);
+    r = fma(-k, kLn2Lo, r);
+    // Horner over 1/n!, n = 13 .. 0
+    double p = 1.6059043836821613e-10;
+    p = fma(p, r, 2.08767569878681e-09);
+    p = fma(p, r, 2.505210838544172e-08);
+    p = fma(p, r, 2.755731922398589e-07);
+    p = fma(p, r, 2.7557319223985893e-06);
+    p = fma(p, r, 2.48015873015873e-05);
+    p = fma(p, r, 0.0001984126984126984);
+    p = fma(p, r, 0.001388888888888889);
+    p = fma(p, r, 0.008333333333333333);
+    p = fma(p, r, 0.041666666666666664);
+    p = fma(p, r, 0.16666666666666666);
+    p = fma(p, r, 0.5);
+    p = fma(p, r, 1.0);
+    p = fma(p, r, 1.0);
+    k = k == k ? k : 0.0;
+    return ldexp(p, (int)k);
+}
+
+// log(1 + e) for 0 <= e <= 1, given u = 1 + e rounded and inv = 1 / u.
+// log u: m = u (or u / 2, adding ln 2) in [0.707, 1.415], s = (m - 1) /
+// (m + 1) with |s| <= 3 - 2 sqrt 2, log m = 2 atanh s = 2 s sum_k s^2k /
+// (2k + 1) to k = 11 (remainder below 2e-20); then the rounding of u is
+// put back: log(1 + e) = log u + (e - (u - 1)) / u to first order.
+__device__ __forceinline__ double log1p_unit(double e, double u, double inv)
+{
+    constexpr double kLn2 = 0.6931471805599453;
+    const bool big = u > 1.4142135623730951;
+    const double m = big ? 0.5 * u : u;
+    const double s = (m - 1.0) * recip(m + 1.0);  // m - 1 is exact here
+    const double w = s * s;
+    double p = 0.043478260869565216;               // 1/23
+    p = fma(p, w, 0.047619047619047616);           // 1/21
+    p = fma(p, w, 0.05263157894736842);            // 1/19
+    p = fma(p, w, 0.058823529411764705);           // 1/17
+    p = fma(p, w, 0.06666666666666667);            // 1/15
+    p = fma(p, w, 0.07692307692307693);            // 1/13
+    p = fma(p, w, 0.09090909090909091);            // 1/11
+    p = fma(p, w, 0.1111111111111111);             // 1/9
+    p = fma(p, w, 0.14285714285714285);            // 1/7
+    p = fma(p, w, 0.2);                            // 1/5
+    p = fma(p, w, 0.3333333333333333);             // 1/3
+    p = fma(p, w, 1.0);
+    double lg = 2.0 * s * p;
+    lg = big ? lg + kLn2 : lg;
+    return lg + (e - (u - 1.0)) * inv;  // u - 1 is exact for u in [1, 2]
+}
+
 __device__ __forceinline__ RowTerms logistic_row(double eta, bool y_is_one)
 {
     const double sgn = y_is_one ? -1.0 : 1.0;
     const double t = sgn * eta;
-    const double e = exp(-fabs(t));
-    const double inv = 1.0 / (1.0 + e);
+    const double e = exp_nonpos(-fabs(t));
+    const double u = 1.0 + e;
+    const double inv = recip(u);
     const double sig = t >= 0.0 ? inv : e * inv;
-    return RowTerms{fmax(t, 0.0) + log1p(e), sgn * sig};
+    return RowTerms{fmax(t, 0.0) + log1p_unit(e, u, inv), sgn * sig};
 }
 
 // The same terms for fp32 data: eta and t stay fp64; the exponential, log
@@ -195,7 +270,9 @@ __device__ __forceinline__ double logaddexp(double a, double b)
 {
     if (a == -INFINITY) return b;
     if (b == -INFINITY) return a;
-    return fmax(a, b) + log1p(exp(-fabs(a - b)));
+    const double e = exp_nonpos(-fabs(a - b));
+    const double u = 1.0 + e;
+    return fmax(a, b) + log1p_unit(e, u, recip(u));
 }
 
 }  // namespace nuts

@@ -27,7 +27,7 @@ inline PassShape pass_shape(int D)
 {
     const int dims = (D + 63) / 64;
     if (D <= 8) return {1, 8, dims};
-    if (D <= 16) return {2, 8, dims};
+    if (D <= 16) return {1, 16, dims};
     if (D <= 32) return {4, 8, dims};
     if (D <= 64) return {8, 8, dims};
     if (D <= 128) return {16, 8, dims};
@@ -36,8 +36,8 @@ inline PassShape pass_shape(int D)
 }
 
 // Device layout of one or more data sets: X as column blocks of R rows
-// (R = 64 / S for fp64, 128 / S for fp32; each lane takes one fp64 or two
-// fp32 rows), block b of data set s at element offset (s * nb + b) * D * R,
+// (R = RPL * 64 / S; each lane takes RPL rows: two for fp32 or S = 1, one
+// otherwise), block b of data set s at element offset (s * nb + b) * D * R,
 // column c of the block at + c * R, row r of the block at + r; rows past N
 // are zero.  y as bytes at (s * nb + b) * R + r, zero past N.
 struct DataView {
@@ -53,10 +53,14 @@ struct DataView {
 };
 
 // Zeroed elements after the last block of an X allocation: the data pass
-// reads up to cols * S * R <= 10 * 128 elements from a block's start.
+// reads up to cols * S * R <= 16 * 128 elements from a block's start.
 constexpr int64_t kTailElems = 2048;
 
-inline int rows_per_block(const DataView& dv) { return (dv.dtype == NUTS_F32 ? 128 : 64) / dv.split; }
+inline int rows_per_block(const DataView& dv)
+{
+    const int rpl = (dv.dtype == NUTS_F32 || dv.split == 1) ? 2 : 1;
+    return rpl * 64 / dv.split;
+}
 
 // Width of one partial-sum row: the D columns padded to whole lanes, then
 // one more lane-row whose slot 0 is the loss sum.
@@ -101,6 +105,8 @@ struct SamplerArgs {
 // One wavefront per chain (D <= 64): ceil(C / 4) groups of four waves.
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream);
 bool wave_path_supports(const DataView& dv);
+// The chains' data sets fit in LDS (the resident variant of the wave path).
+bool wave_path_resident(const SamplerArgs& a);
 
 // One chain over the whole device.  `sync` holds the arrival counters and
 // the error flag, zeroed by this call; `partials` holds
@@ -200,6 +206,8 @@ constexpr int kBatchQWidth = 192;
 // Per-dtype kernel entry points (sampler_f32.hip, sampler_f64.hip).
 hipError_t launch_sampler_wave_f32(const SamplerArgs& a, hipStream_t stream);
 hipError_t launch_sampler_wave_f64(const SamplerArgs& a, hipStream_t stream);
+bool wave_resident_f32(const SamplerArgs& a);
+bool wave_resident_f64(const SamplerArgs& a);
 const void* grid_kernel_f32(const DataView& dv);
 const void* grid_kernel_f64(const DataView& dv);
 constexpr int kGridWaves = 16;  // per group: 1 controller + 15 workers

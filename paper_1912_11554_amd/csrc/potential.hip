@@ -115,7 +115,7 @@ void enqueue_pass_shape(const DataView& dv, const double* W, int64_t K, int G, i
 {
     const int D = dv.D;
     if (D <= 8) enqueue_pass<T, 1, 8>(dv, W, K, G, width, partials, stream);
-    else if (D <= 16) enqueue_pass<T, 2, 8>(dv, W, K, G, width, partials, stream);
+    else if (D <= 16) enqueue_pass<T, 1, 16>(dv, W, K, G, width, partials, stream);
     else if (D <= 32) enqueue_pass<T, 4, 8>(dv, W, K, G, width, partials, stream);
     else if (D <= 64) enqueue_pass<T, 8, 8>(dv, W, K, G, width, partials, stream);
     else if (D <= 128) enqueue_pass<T, 16, 8>(dv, W, K, G, width, partials, stream);

@@ -28,10 +28,12 @@ __host__ __device__ constexpr int lanes_per_row(int D, int CPS)
 }
 
 // Rows per lane: fp32 blocks give each lane two consecutive rows so that a
-// load instruction moves 512 bytes, as for fp64.
-template <typename T>
+// load instruction moves 512 bytes, as for fp64; with one lane per row (S =
+// 1) fp64 lanes take two rows as well (16-byte loads, and two independent
+// rows of per-row arithmetic per lane).
+template <typename T, int S>
 struct RowsPerLane {
-    static constexpr int value = sizeof(T) == 4 ? 2 : 1;
+    static constexpr int value = (sizeof(T) == 4 || S == 1) ? 2 : 1;
 };
 
 template <typename T, int N>
@@ -44,10 +46,14 @@ template <>
 struct VecOf<double, 1> {
     using type = double;
 };
+template <>
+struct VecOf<double, 2> {
+    using type = double2;
+};
 
 template <typename T, int S>
 struct BlockShape {
-    static constexpr int RPL = RowsPerLane<T>::value;
+    static constexpr int RPL = RowsPerLane<T, S>::value;
     static constexpr int R = RPL * kWave / S;  // rows per block
 };
 

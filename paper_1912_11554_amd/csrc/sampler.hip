@@ -21,6 +21,11 @@ const void* pick_grid_kernel(const DataView& dv)
 
 bool wave_path_supports(const DataView& dv) { return dv.D <= 64; }
 
+bool wave_path_resident(const SamplerArgs& a)
+{
+    return a.data.dtype == NUTS_F64 ? wave_resident_f64(a) : wave_resident_f32(a);
+}
+
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream)
 {
     return a.data.dtype == NUTS_F64 ? launch_sampler_wave_f64(a, stream) : launch_sampler_wave_f32(a, stream);

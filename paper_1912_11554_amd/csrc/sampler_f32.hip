@@ -9,6 +9,11 @@ hipError_t launch_sampler_wave_f32(const SamplerArgs& a, hipStream_t stream)
     return sampler::wave_launch_split<float>(a, stream);
 }
 
+bool wave_resident_f32(const SamplerArgs& a)
+{
+    return sampler::wave_resident_split<float>(a);
+}
+
 const void* grid_kernel_f32(const DataView& dv)
 {
     return sampler::grid_kernel_for<float>(dv);

@@ -77,7 +77,7 @@ __device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (
 // out_writer() whether it stores the chain's outputs; aborted() reports a
 // failed grid exchange.
 
-template <typename T, int S>
+template <typename T, int S, int CPS>
 struct WaveEval {
     const T* X;
     const uint8_t* y;
@@ -91,7 +91,6 @@ struct WaveEval {
 
     __device__ void eval(const double (&q)[1], double& U, double (&g)[1])
     {
-        constexpr int CPS = 8;
         double qv[CPS];
         spread_position<CPS, S>(q[0], qv);
         double acc[CPS];
@@ -483,7 +482,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 ++nleaves;
 
                 const double dH = (z.U + 0.5 * wave_sum(k2)) - H0;
-                if (dH == dH) sum_acc += dH > 0.0 ? exp(-dH) : 1.0;
+                if (dH == dH) sum_acc += dH > 0.0 ? exp_nonpos(-dH) : 1.0;
                 if (uni(!(dH <= 1000.0))) {
                     status = kTreeDivergent;
                     term = (int)n;
@@ -493,7 +492,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 const double lam = -dH;
                 const double lw = logaddexp(logw, lam);
                 const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
-                if (uni(u < exp(lam - lw))) {
+                if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
                     sprop = z;
                     sprop_idx = e + v * (n + 1);
                 }
@@ -544,7 +543,8 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             }
             // biased progressive choice between trajectory and new subtree
             const double um = __shfl(u_merge, j);
-            if (uni(um < exp(logw - logw_traj))) {
+            const double dw = logw - logw_traj;
+            if (uni(um < (dw >= 0.0 ? 1.0 : exp_nonpos(dw)))) {
                 prop = sprop;
                 prop_idx = sprop_idx;
             }
@@ -632,25 +632,90 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
 }
 
 constexpr int kWaveChainsPerGroup = 4;
+// LDS a workgroup may use on gfx950.
+constexpr size_t kMaxGroupLds = 160 * 1024;
 
-template <typename T, int S>
-__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, 3) sampler_wave_kernel(SamplerArgs A)
+// LDS bytes of one group of the wave path with `cpg` chains: their
+// checkpoint arrays and, when RESIDENT, their data sets (column blocks back
+// to back, then a zero pad for the last chain's over-read, then the labels).
+template <typename T, int S, int CPS>
+struct WaveLds {
+    static constexpr int R = BlockShape<T, S>::R;
+    __host__ __device__ static size_t s_bytes(int D, int max_depth, int cpg)
+    {
+        const int slots = max_depth > 1 ? max_depth : 1;
+        return (size_t)cpg * slots * 2 * D * sizeof(double);
+    }
+    __host__ __device__ static int64_t x_elems(int D, int64_t nb) { return nb * D * R; }
+    __host__ __device__ static int64_t pad_elems(int D) { return (int64_t)(CPS * S - D) * R; }
+    static size_t bytes(int D, int64_t nb, int max_depth, bool resident, int cpg)
+    {
+        size_t b = s_bytes(D, max_depth, cpg);
+        if (resident)
+            b += (size_t)(cpg * x_elems(D, nb) + pad_elems(D)) * sizeof(T) + (size_t)cpg * nb * R;
+        return b;
+    }
+};
+
+// One wavefront per chain, `cpg` chains (waves) per group.  RESIDENT: the
+// group first copies its chains' data sets into LDS (one barrier) and every
+// gradient evaluation then streams from LDS; a group is then one per CU, so
+// the register budget is the whole wave's share of the SIMD.
+template <typename T, int S, int CPS, bool RESIDENT>
+__global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3) sampler_wave_kernel(SamplerArgs A,
+                                                                                                   int cpg)
 {
-    constexpr int R = BlockShape<T, S>::R;
+    using G = WaveLds<T, S, CPS>;
+    constexpr int R = G::R;
     extern __shared__ double lds[];
     const int wave = threadIdx.x / kWave;
-    const int64_t chain = (int64_t)blockIdx.x * kWaveChainsPerGroup + wave;
-    if (chain >= A.num_chains) return;
+    if (wave >= cpg) return;
+    const int l = lane();
+    const int64_t chain = (int64_t)blockIdx.x * cpg + wave;
     const int D = A.data.D;
+    const int64_t nb = A.data.nb;
     const int slots = A.max_depth > 1 ? A.max_depth : 1;
     double* S_arr = lds + (int64_t)wave * slots * 2 * D;
     const int64_t c = A.chain_offset + chain;
     const int64_t ds = A.per_chain_data ? c : 0;
-    WaveEval<T, S> ev;
-    ev.X = (const T*)A.data.X + ds * A.data.nb * (int64_t)D * R;
-    ev.y = A.data.y + ds * A.data.nb * R;
+    const T* Xg = (const T*)A.data.X + ds * nb * (int64_t)D * R;
+    const uint8_t* yg = A.data.y + ds * nb * R;
+    WaveEval<T, S, CPS> ev;
+    if constexpr (RESIDENT) {
+        const int64_t xe = G::x_elems(D, nb);
+        T* Xl = reinterpret_cast<T*>(reinterpret_cast<char*>(lds) + G::s_bytes(D, A.max_depth, cpg));
+        T* Xw = Xl + wave * xe;
+        uint8_t* yl = reinterpret_cast<uint8_t*>(Xl + cpg * xe + G::pad_elems(D));
+        uint8_t* yw = yl + wave * nb * R;
+        // 16-byte pieces: a chain's X is nb * D * R * sizeof(T) bytes, a
+        // multiple of 16 since R * sizeof(T) is 512 / S or 1024 and S <= 8
+        const int64_t n16 = xe * (int64_t)sizeof(T) / 16;
+        uint4* dst = reinterpret_cast<uint4*>(Xw);
+        if (chain < A.num_chains) {
+            const uint4* src = reinterpret_cast<const uint4*>(Xg);
+            for (int64_t i = l; i < n16; i += kWave) dst[i] = src[i];
+            const int64_t n8 = nb * R / 8;
+            for (int64_t i = l; i < n8; i += kWave)
+                reinterpret_cast<uint2*>(yw)[i] = reinterpret_cast<const uint2*>(yg)[i];
+        } else {
+            // a neighbour's last block over-reads into this region: zeros
+            for (int64_t i = l; i < n16; i += kWave) dst[i] = uint4{0u, 0u, 0u, 0u};
+        }
+        if (wave == cpg - 1) {
+            T* pad = Xl + cpg * xe;
+            for (int64_t i = l; i < G::pad_elems(D); i += kWave) pad[i] = T(0);
+        }
+        __syncthreads();
+        if (chain >= A.num_chains) return;
+        ev.X = Xw;
+        ev.y = yw;
+    } else {
+        if (chain >= A.num_chains) return;
+        ev.X = Xg;
+        ev.y = yg;
+    }
     ev.N = A.data.N;
-    ev.nb = A.data.nb;
+    ev.nb = nb;
     ev.D = D;
     ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
     ev.prior_const = (double)D * (log(A.prior_scale) + kHalfLog2Pi);
@@ -704,7 +769,7 @@ const void* grid_kernel_for(const DataView& dv)
 {
     const int D = dv.D;
     if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1>;
-    if (D <= 16) return (const void*)sampler_grid_kernel<T, 2, 8, 1>;
+    if (D <= 16) return (const void*)sampler_grid_kernel<T, 1, 16, 1>;
     if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1>;
     if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1>;
     if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2>;
@@ -713,24 +778,62 @@ const void* grid_kernel_for(const DataView& dv)
     return (const void*)sampler_grid_kernel<T, 32, 10, 5>;
 }
 
-template <typename T, int S>
+// Chains per group of the LDS-resident variant (the most of 4, 2, 1 whose
+// data sets fit), or 0 if not even one chain's data fits.
+template <typename T, int S, int CPS>
+int resident_chains_per_group(const SamplerArgs& a)
+{
+    using G = WaveLds<T, S, CPS>;
+    for (int cpg = kWaveChainsPerGroup; cpg >= 1; cpg /= 2) {
+        if (cpg > a.num_chains && cpg > 1) continue;
+        if (G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg) <= kMaxGroupLds) return cpg;
+    }
+    return 0;
+}
+
+template <typename T, int S, int CPS>
 hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
 {
-    const int slots = a.max_depth > 1 ? a.max_depth : 1;
-    const size_t lds = (size_t)kWaveChainsPerGroup * slots * 2 * a.data.D * sizeof(double);
-    const unsigned grid = (unsigned)((a.num_chains + kWaveChainsPerGroup - 1) / kWaveChainsPerGroup);
-    hipLaunchKernelGGL((sampler_wave_kernel<T, S>), dim3(grid), dim3(kWaveChainsPerGroup * kWave), lds, stream,
-                       a);
+    using G = WaveLds<T, S, CPS>;
+    const int cpg = resident_chains_per_group<T, S, CPS>(a);
+    if (cpg > 0) {
+        const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg);
+        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true>;
+        hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        const unsigned grid = (unsigned)((a.num_chains + cpg - 1) / cpg);
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true>), dim3(grid), dim3(kWaveChainsPerGroup * kWave), lds,
+                           stream, a, cpg);
+    } else {
+        const int c4 = kWaveChainsPerGroup;
+        const unsigned grid = (unsigned)((a.num_chains + c4 - 1) / c4);
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false>), dim3(grid), dim3(kWaveChainsPerGroup * kWave),
+                           G::bytes(a.data.D, a.data.nb, a.max_depth, false, c4), stream, a, c4);
+    }
     return hipGetLastError();
+}
+
+// Whether the resident variant takes this shape.
+template <typename T>
+bool wave_resident_split(const SamplerArgs& a)
+{
+    if (a.data.split == 1) {
+        if (a.data.cols == 16) return resident_chains_per_group<T, 1, 16>(a) > 0;
+        return resident_chains_per_group<T, 1, 8>(a) > 0;
+    }
+    if (a.data.split == 4) return resident_chains_per_group<T, 4, 8>(a) > 0;
+    return resident_chains_per_group<T, 8, 8>(a) > 0;
 }
 
 template <typename T>
 hipError_t wave_launch_split(const SamplerArgs& a, hipStream_t stream)
 {
-    if (a.data.split == 1) return wave_launch<T, 1>(a, stream);
-    if (a.data.split == 2) return wave_launch<T, 2>(a, stream);
-    if (a.data.split == 4) return wave_launch<T, 4>(a, stream);
-    return wave_launch<T, 8>(a, stream);
+    if (a.data.split == 1) {
+        if (a.data.cols == 16) return wave_launch<T, 1, 16>(a, stream);
+        return wave_launch<T, 1, 8>(a, stream);
+    }
+    if (a.data.split == 4) return wave_launch<T, 4, 8>(a, stream);
+    return wave_launch<T, 8, 8>(a, stream);
 }
 
 }  // namespace sampler
