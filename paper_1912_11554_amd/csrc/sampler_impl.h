@@ -114,7 +114,10 @@ template <int DPL, int NW>
 struct GridShared {
     static constexpr int W = 64 * (DPL + 1);  // partial_width(D)
     double qbuf[64 * DPL];
-    double red[NW][W];
+    union {
+        double red[NW][W];                  // per-wave column sums of the group
+        double red_flat[(NW - 1) * kWave];  // per-set sums of the last arriver
+    };
     int cmd;
     int last;
 };
@@ -172,9 +175,11 @@ __device__ __forceinline__ unsigned long long slot_bits(const double* p)
 // handed over.
 //
 // Step s uses parity buffer s & 1.  Each group stores its partial and counts
-// itself in; the group that completes the count adds all partials in group
-// order, re-arms the other parity's result slots (every controller has read
-// them: it arrived at this step after reading them) and stores the result.
+// itself in; the workers of the group that completes the count add all
+// partials (each worker lane one used column of a fixed subset of groups,
+// in increasing group order, then the subsets in order), re-arm the other
+// parity's result slots (every controller has read them: it arrived at this
+// step after reading them) and store the result.
 // Controllers poll their own lane's result slots until none is empty.
 template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
 __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step,
@@ -248,46 +253,58 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
     }
     __syncthreads();  // arrival recorded
     if (sh.last) {
-        // every controller has read the other parity's result by now: re-arm
-        // those slots while the partials load
-        if (wave == 0) {
+        // The workers of the last arriving group add the group partials, in
+        // one round of loads: worker k takes groups k, k + (NW - 1), ..., in
+        // increasing order, then worker 0 adds the per-worker sums in worker
+        // order and publishes.  The controller only passes the barrier, so
+        // none of this is live beside its tree state.
+        if (WORKER) {
+            // worker lane t takes used column c = t % (D + 1) (column c < D,
+            // or the loss for c = D) of groups j, j + J, ... (j = t / (D + 1),
+            // J lane sets), in increasing group order
+            const int k = wave - 1;
+            if (k == 0) {
+                // every controller has read the other parity's result by
+                // now: re-arm those slots while the partials load
 #pragma unroll
-            for (int m = 0; m <= DPL; ++m)
-                __hip_atomic_store(reinterpret_cast<unsigned long long*>(&c.result[(par ^ 1) * W + l + 64 * m]),
-                                   kEmptySlot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                for (int m = 0; m <= DPL; ++m)
+                    __hip_atomic_store(reinterpret_cast<unsigned long long*>(&c.result[(par ^ 1) * W + l + 64 * m]),
+                                       kEmptySlot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            const int used = c.D + 1;
+            const int sets = ((NW - 1) * kWave) / used;  // J >= 1 since D + 1 <= 321 < 960
+            const int t = k * kWave + l;
+            const int j = t / used;
+            const int col = t - j * used;
+            if (j < sets) {
+                const double* src = c.partials + (int64_t)par * c.groups * W + (col < c.D ? col : 64 * DPL);
+                double s_ = 0.0;
+                constexpr int B = 16;
+                for (int g0 = j; g0 < c.groups; g0 += B * sets) {
+                    double v[B];
+#pragma unroll
+                    for (int i = 0; i < B; ++i) {
+                        const int g = g0 + i * sets;
+                        v[i] = g < c.groups ? load_shared(src + (int64_t)g * W) : 0.0;
+                    }
+#pragma unroll
+                    for (int i = 0; i < B; ++i) s_ += v[i];
+                }
+                sh.red_flat[j * used + col] = s_;
+            }
         }
-        // add the group partials in group order, spread over the waves, then
-        // in wave order
-        double s[DPL + 1];
-#pragma unroll
-        for (int m = 0; m <= DPL; ++m) s[m] = 0.0;
-        const double* src = c.partials + (int64_t)par * c.groups * W + l;
-        constexpr int B = DPL <= 1 ? 8 : 4;
-        int gg = wave;
-        for (; gg + (B - 1) * NW < c.groups; gg += B * NW) {
-            double v[B][DPL + 1];
-#pragma unroll
-            for (int i = 0; i < B; ++i)
-#pragma unroll
-                for (int m = 0; m <= DPL; ++m) v[i][m] = load_shared(src + (int64_t)(gg + i * NW) * W + 64 * m);
-#pragma unroll
-            for (int i = 0; i < B; ++i)
-#pragma unroll
-                for (int m = 0; m <= DPL; ++m) s[m] += v[i][m];
-        }
-        for (; gg < c.groups; gg += NW)
-#pragma unroll
-            for (int m = 0; m <= DPL; ++m) s[m] += load_shared(src + (int64_t)gg * W + 64 * m);
-#pragma unroll
-        for (int m = 0; m <= DPL; ++m) sh.red[wave][l + 64 * m] = s[m];
-        __syncthreads();  // per-wave sums in LDS
-        if (wave == 0) {
+        __syncthreads();  // per-set sums in LDS
+        if (WORKER && wave == 1) {
+            const int used = c.D + 1;
+            const int sets = ((NW - 1) * kWave) / used;
             double tot[DPL + 1];
 #pragma unroll
             for (int m = 0; m <= DPL; ++m) {
+                const int colw = l + 64 * m;  // column of the result row
+                const int ci = m < DPL ? colw : (l == 0 ? c.D : -1);
                 tot[m] = 0.0;
-#pragma unroll
-                for (int w = 0; w < NW; ++w) tot[m] += sh.red[w][l + 64 * m];
+                if (ci >= 0 && (m == DPL || colw < c.D))
+                    for (int jj = 0; jj < sets; ++jj) tot[m] += sh.red_flat[jj * used + ci];
             }
             drain_memory_ops();  // the re-arm above lands before this result
 #pragma unroll
