@@ -46,7 +46,30 @@ struct nuts_handle {
     // uses it between its launches and its final stream synchronisation
     void* scratch = nullptr;
     size_t scratch_bytes = 0;
+    // arrival counts of the potential kernel, one per item; zeroed once, the
+    // kernel leaves them zero
+    unsigned int* pot_counts = nullptr;
 };
+
+static hipError_t potential_counts(nuts_handle* h, unsigned int** out)
+{
+    if (!h->pot_counts) {
+        const size_t bytes = (size_t)kMaxPotentialItems * sizeof(unsigned int);
+        hipError_t e = hipMalloc(&h->pot_counts, bytes);
+        if (e != hipSuccess) {
+            h->pot_counts = nullptr;
+            return e;
+        }
+        e = hipMemsetAsync(h->pot_counts, 0, bytes, h->stream);
+        if (e != hipSuccess) {
+            (void)hipFree(h->pot_counts);
+            h->pot_counts = nullptr;
+            return e;
+        }
+    }
+    *out = h->pot_counts;
+    return hipSuccess;
+}
 
 // Scratch of at least `bytes`, 256-byte aligned, owned by the handle.
 static hipError_t handle_scratch(nuts_handle* h, size_t bytes, void** out)
@@ -226,6 +249,7 @@ void nuts_free(nuts_handle* h)
     DeviceScope ds(h->device);
     (void)hipStreamSynchronize(h->stream);
     if (h->scratch) (void)hipFree(h->scratch);
+    if (h->pot_counts) (void)hipFree(h->pot_counts);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
 }
@@ -320,7 +344,8 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     h->err.clear();
     if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
     if (!W || !out_U || !out_grad) return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be non-NULL");
-    if (K < 1 || K > 65535) return fail(h, NUTS_EINVAL, "K must be in [1, 65535] (got %lld)", (long long)K);
+    if (K < 1 || K > kMaxPotentialItems)
+        return fail(h, NUTS_EINVAL, "K must be in [1, %d] (got %lld)", kMaxPotentialItems, (long long)K);
     if (d->view.nds > 1 && K != d->view.nds)
         return fail(h, NUTS_EINVAL, "per-chain data: K (%lld) must equal the number of data sets (%lld)",
                     (long long)K, (long long)d->view.nds);
@@ -336,7 +361,9 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
     void* part = nullptr;
     HIP_TRY(h, handle_scratch(h, (size_t)K * plan.groups_per_item * plan.width * sizeof(double), &part));
-    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part,
+    unsigned int* counts = nullptr;
+    HIP_TRY(h, potential_counts(h, &counts));
+    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part, counts,
                                      (double*)Ud, (double*)Gd, h->stream));
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
     HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
@@ -583,9 +610,8 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
         }
     } else {
         const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
-        const int W = partial_width(D);
-        const size_t part_bytes = align256((size_t)2 * groups * W * sizeof(double));
-        const size_t res_bytes = align256((size_t)2 * W * sizeof(double));
+        const size_t part_bytes = align256((size_t)grid_partial_elems(D, groups) * sizeof(double));
+        const size_t res_bytes = align256((size_t)grid_result_elems(D) * sizeof(double));
         void* scratch = nullptr;
         HIP_TRY(h, handle_scratch(h, part_bytes + res_bytes + sizeof(GridSync), &scratch));
         double* part = (double*)scratch;

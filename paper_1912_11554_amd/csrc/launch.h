@@ -70,15 +70,18 @@ hipError_t launch_to_blocks(const void* X_rowmajor, const uint8_t* y_in, DataVie
                             void* X_out, uint8_t* y_out, unsigned int* bad_label,
                             hipStream_t stream);
 
-// Workspace of the batched potential/gradient: partial sums [K][G][width].
+// Workspace of the batched potential/gradient: partial sums [K][G][width]
+// and one arrival count per item, [K] unsigned ints that must be zero before
+// the launch and are zero again after it (the kernel re-arms them).
 struct PotentialPlan {
     int groups_per_item;  // G
     int width;            // partial_width(D)
 };
+constexpr int kMaxPotentialItems = 65535;
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu);
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
-                                 const PotentialPlan& plan, double* partials, double* out_U,
-                                 double* out_grad, hipStream_t stream);
+                                 const PotentialPlan& plan, double* partials, unsigned int* counters,
+                                 double* out_U, double* out_grad, hipStream_t stream);
 
 // Sampler arguments common to both paths (device pointers).
 struct SamplerArgs {
@@ -108,16 +111,15 @@ bool wave_path_supports(const DataView& dv);
 // The chains' data sets fit in LDS (the resident variant of the wave path).
 bool wave_path_resident(const SamplerArgs& a);
 
-// One chain over the whole device.  `sync` holds the arrival counters and
-// the error flag, zeroed by this call; `partials` holds
-// [2][groups][partial_width(D)] doubles, `result` [2][partial_width(D)]
-// (marked empty by this call).
+// One chain over the whole device.  `sync` holds the error flag, zeroed by
+// this call; `partials` holds grid_partial_elems(D, groups) doubles and
+// `result` grid_result_elems(D) doubles, both marked empty by this call.
+constexpr int kGridPhases = 3;
+inline int64_t grid_partial_elems(int D, int groups) { return (int64_t)kGridPhases * (D + 1) * groups; }
+inline int64_t grid_result_elems(int D) { return (int64_t)kGridPhases * partial_width(D); }
 struct GridSync {
-    unsigned long long counter;          // completed group slots, (step + 1) * min(groups, 8) after step
-    unsigned long long pad0[15];
-    unsigned int error;                  // a wait timed out
-    unsigned int pad1[31];
-    unsigned long long slot[8][16];      // group arrivals per slot (group index mod 8)
+    unsigned int error;  // a wait timed out
+    unsigned int pad[63];
 };
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream);

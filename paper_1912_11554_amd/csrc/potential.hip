@@ -1,10 +1,13 @@
-// Batched potential and gradient of the logistic log-joint at K positions.
-// Pass 1: a grid of (G groups) x (K items); each wave streams the blocks
-// b = g * waves + w, g * waves + w + G * waves, ... of its item's data set and
-// each group writes one fp64 partial row of width partial_width(D) (columns
-// 0..D-1, the loss sum at 64 * ceil(D / 64)).  Pass 2: four waves per item
-// add the G partials in a fixed order, then the Gaussian prior terms.  No
-// floating-point atomics anywhere, so results are bitwise reproducible.
+// Batched potential and gradient of the logistic log-joint at K positions,
+// in one launch.  A grid of (G groups) x (K items); the NW waves of a group
+// (16, or 8 where a lane holds many columns and needs the registers) stream
+// the blocks b = g * NW + w, g * NW + w + G * NW, ... of their item's
+// data set, the group adds its waves' column sums in wave order and stores
+// one fp64 partial row of width partial_width(D) (columns 0..D-1, the loss at
+// 64 * ceil(D / 64)), then counts itself in for its item.  The group that
+// completes an item's count adds the item's G partial rows in a fixed order
+// and the Gaussian prior terms, writes U and grad U, and re-zeroes the count.
+// No floating-point atomics anywhere, so results are bitwise reproducible.
 #include "launch.h"
 #include "rows.h"
 
@@ -12,18 +15,39 @@ namespace nuts {
 
 namespace {
 
-constexpr int kPotWaves = 8;
-constexpr int kFinishWaves = 4;
 constexpr double kHalfLog2Pi = 0.91893853320467274178032973640562;
 
+// waves per group: 16 (4 per SIMD, 128 registers a lane) unless the shape's
+// per-lane state needs more registers than that
+template <int S, int CPS>
+constexpr int pot_waves() { return (S == 1 && CPS == 16) || CPS > 8 ? 8 : 16; }
+static_assert(kMaxDim + 1 <= 8 * kWave, "one thread per used column in the final sum");
+
+__device__ __forceinline__ void store_agent(double* p, double v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double load_agent(const double* p)
+{
+    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void drain()
+{
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 template <typename T, int S, int CPS>
-__global__ void __launch_bounds__(kPotWaves * kWave, 4) potential_pass_kernel(DataView dv,
-                                                                              const double* __restrict__ W,
-                                                                              int G, int width,
-                                                                              double* __restrict__ partials)
+__global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_kernel(
+    DataView dv, const double* __restrict__ W, int G, int width, double* __restrict__ partials,
+    unsigned int* __restrict__ counters, double prior_scale, double* __restrict__ out_U,
+    double* __restrict__ out_grad)
 {
     constexpr int R = BlockShape<T, S>::R;
-    extern __shared__ double part[];  // [kPotWaves][width]
+    constexpr int NW = pot_waves<S, CPS>();
+    extern __shared__ double part[];  // [NW][width], later the per-set sums
+    __shared__ int last;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
     const int64_t k = blockIdx.y;
@@ -40,7 +64,7 @@ __global__ void __launch_bounds__(kPotWaves * kWave, 4) potential_pass_kernel(Da
 #pragma unroll
     for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
     double loss = 0.0;
-    stream_blocks<T, CPS, S>(X, y, D, dv.N, dv.nb, (int64_t)g * kPotWaves + wave, (int64_t)G * kPotWaves, qv,
+    stream_blocks<T, CPS, S>(X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv,
                              acc, loss);
 
     double* row = part + wave * width;
@@ -51,103 +75,130 @@ __global__ void __launch_bounds__(kPotWaves * kWave, 4) potential_pass_kernel(Da
     } else {
         finish_pass_to_row<CPS, S>(acc, loss, row, D, loss_slot);
     }
-    __syncthreads();
+    __syncthreads();  // per-wave sums in LDS
     if (wave == 0) {
+        double* mine = partials + (k * G + g) * width;
         for (int col = l; col < width; col += 64) {
-            const bool used = col < D || col == loss_slot;
-            double s = 0.0;
-            if (used) {
+            if (col < D || col == loss_slot) {
+                double s = 0.0;
 #pragma unroll
-                for (int w = 0; w < kPotWaves; ++w) s += part[w * width + col];
+                for (int w = 0; w < NW; ++w) s += part[w * width + col];
+                store_agent(mine + col, s);
             }
-            partials[(k * G + g) * width + col] = s;
+        }
+        drain();  // the partial row is out before the count
+        int is_last = 0;
+        if (l == 0) {
+            const unsigned int o =
+                __hip_atomic_fetch_add(&counters[k], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            is_last = o + 1 == (unsigned int)G ? 1 : 0;
+        }
+        is_last = __shfl(is_last, 0);
+        if (l == 0) last = is_last;
+    }
+    __syncthreads();  // the count is taken
+    if (!last) return;
+
+    // Every group of item k is in.  Thread t takes used column c = t mod
+    // (D + 1) (column c < D, or the loss for c = D) of the groups j, j + J,
+    // j + 2 J, ... (j = t div (D + 1), J sets) in increasing order.
+    const int used = D + 1;
+    const int t = threadIdx.x;
+    const int sets = (NW * kWave) / used;
+    const int j = t / used;
+    const int c = t - j * used;
+    double s = 0.0;
+    if (j < sets) {
+        const double* src = partials + k * G * width + (c < D ? c : loss_slot);
+        constexpr int B = 16;
+        for (int g0 = j; g0 < G; g0 += B * sets) {
+            double v[B];
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                const int gg = g0 + i * sets;
+                v[i] = gg < G ? load_agent(src + (int64_t)gg * width) : 0.0;
+            }
+#pragma unroll
+            for (int i = 0; i < B; ++i) s += v[i];
         }
     }
-}
-
-__global__ void __launch_bounds__(kFinishWaves * kWave) potential_finish_kernel(
-    int D, int width, const double* __restrict__ W, int G, const double* __restrict__ partials,
-    double prior_scale, double* __restrict__ out_U, double* __restrict__ out_grad)
-{
-    extern __shared__ double red[];  // [kFinishWaves][width]
-    const int l = lane();
-    const int wave = threadIdx.x / kWave;
-    const int64_t k = blockIdx.x;
-    // wave w adds groups w, w + 4, ... ; then wave order
-    for (int col = l; col < width; col += 64) {
-        double s = 0.0;
-#pragma unroll 8
-        for (int g = wave; g < G; g += kFinishWaves) s += partials[(k * G + g) * width + col];
-        red[wave * width + col] = s;
-    }
-    __syncthreads();
+    __syncthreads();  // no wave reads its LDS row any more
+    if (j < sets) part[j * used + c] = s;
+    __syncthreads();  // per-set sums in LDS
     if (wave != 0) return;
     const double inv_s2 = 1.0 / (prior_scale * prior_scale);
     double pr = 0.0;
-    double loss = 0.0;
-    for (int col = l; col < width; col += 64) {
+    double lossv = 0.0;
+    for (int col = l; col < used; col += 64) {
         double tot = 0.0;
-#pragma unroll
-        for (int w = 0; w < kFinishWaves; ++w) tot += red[w * width + col];
+        for (int jj = 0; jj < sets; ++jj) tot += part[jj * used + col];
         if (col < D) {
             const double w = W[k * D + col];
             pr += 0.5 * w * w * inv_s2;
             out_grad[k * D + col] = tot + w * inv_s2;
+        } else {
+            lossv = tot;
         }
-        if (col == width - 64) loss = tot;
     }
     const double prior = wave_sum(pr);
-    loss = readlane_f64(loss, 0);  // the loss slot is column 64 * m of lane 0
-    if (l == 0) out_U[k] = loss + prior + (double)D * (log(prior_scale) + kHalfLog2Pi);
+    lossv = readlane_f64(lossv, D & 63);  // column D sits in lane D mod 64
+    if (l == 0) {
+        out_U[k] = lossv + prior + (double)D * (log(prior_scale) + kHalfLog2Pi);
+        // re-arm the count for the next call (kernels on one stream are ordered)
+        __hip_atomic_store(&counters[k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 template <typename T, int S, int CPS>
-void enqueue_pass(const DataView& dv, const double* W, int64_t K, int G, int width, double* partials,
-                  hipStream_t stream)
+void enqueue(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
+             double* partials, unsigned int* counters, double* out_U, double* out_grad, hipStream_t stream)
 {
-    hipLaunchKernelGGL((potential_pass_kernel<T, S, CPS>), dim3(G, (unsigned)K), dim3(kPotWaves * kWave),
-                       (size_t)kPotWaves * width * sizeof(double), stream, dv, W, G, width, partials);
+    constexpr int NW = pot_waves<S, CPS>();
+    hipLaunchKernelGGL((potential_grad_kernel<T, S, CPS>), dim3(G, (unsigned)K), dim3(NW * kWave),
+                       (size_t)NW * width * sizeof(double), stream, dv, W, G, width, partials, counters,
+                       prior_scale, out_U, out_grad);
 }
 
 template <typename T>
-void enqueue_pass_shape(const DataView& dv, const double* W, int64_t K, int G, int width, double* partials,
-                        hipStream_t stream)
+void enqueue_shape(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
+                   double* partials, unsigned int* counters, double* out_U, double* out_grad, hipStream_t stream)
 {
     const int D = dv.D;
-    if (D <= 8) enqueue_pass<T, 1, 8>(dv, W, K, G, width, partials, stream);
-    else if (D <= 16) enqueue_pass<T, 1, 16>(dv, W, K, G, width, partials, stream);
-    else if (D <= 32) enqueue_pass<T, 4, 8>(dv, W, K, G, width, partials, stream);
-    else if (D <= 64) enqueue_pass<T, 8, 8>(dv, W, K, G, width, partials, stream);
-    else if (D <= 128) enqueue_pass<T, 16, 8>(dv, W, K, G, width, partials, stream);
-    else if (D <= 256) enqueue_pass<T, 32, 8>(dv, W, K, G, width, partials, stream);
-    else enqueue_pass<T, 32, 10>(dv, W, K, G, width, partials, stream);
+#define NUTS_POT(S_, C_) \
+    enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, counters, out_U, out_grad, stream)
+    if (D <= 8) NUTS_POT(1, 8);
+    else if (D <= 16) NUTS_POT(1, 16);
+    else if (D <= 32) NUTS_POT(4, 8);
+    else if (D <= 64) NUTS_POT(8, 8);
+    else if (D <= 128) NUTS_POT(16, 8);
+    else if (D <= 256) NUTS_POT(32, 8);
+    else NUTS_POT(32, 10);
+#undef NUTS_POT
 }
 
 }  // namespace
 
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
 {
-    // about two groups per CU over all items, never more than the blocks
-    // give their waves work
-    int64_t want = ((int64_t)num_cu * 2 + K - 1) / K;
-    int64_t most = (dv.nb + kPotWaves - 1) / kPotWaves;
+    // one group per CU over all items, never more groups than the blocks give
+    // their waves work
+    int64_t want = ((int64_t)num_cu + K - 1) / K;
+    int64_t most = (dv.nb + 15) / 16;
     if (want > most) want = most;
     if (want < 1) want = 1;
     return PotentialPlan{(int)want, partial_width(dv.D)};
 }
 
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
-                                 const PotentialPlan& plan, double* partials, double* out_U,
-                                 double* out_grad, hipStream_t stream)
+                                 const PotentialPlan& plan, double* partials, unsigned int* counters,
+                                 double* out_U, double* out_grad, hipStream_t stream)
 {
-    const int G = plan.groups_per_item;
-    if (dv.dtype == NUTS_F64) enqueue_pass_shape<double>(dv, W, K, G, plan.width, partials, stream);
-    else enqueue_pass_shape<float>(dv, W, K, G, plan.width, partials, stream);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(potential_finish_kernel, dim3((unsigned)K), dim3(kFinishWaves * kWave),
-                       (size_t)kFinishWaves * plan.width * sizeof(double), stream, dv.D, plan.width, W, G,
-                       partials, prior_scale, out_U, out_grad);
+    if (dv.dtype == NUTS_F64)
+        enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, counters, out_U,
+                              out_grad, stream);
+    else
+        enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, counters,
+                             out_U, out_grad, stream);
     return hipGetLastError();
 }
 

@@ -6,10 +6,13 @@ namespace nuts {
 
 namespace {
 
-__global__ void fill_empty_slots(double* result, int n)
+__global__ void fill_empty_slots(double* a, int64_t na, double* b, int64_t nb)
 {
-    for (int i = threadIdx.x; i < n; i += blockDim.x)
-        reinterpret_cast<unsigned long long*>(result)[i] = sampler::kEmptySlot;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < na + nb; i += stride) {
+        unsigned long long* p = reinterpret_cast<unsigned long long*>(i < na ? a + i : b + (i - na));
+        *p = sampler::kEmptySlot;
+    }
 }
 
 const void* pick_grid_kernel(const DataView& dv)
@@ -44,6 +47,10 @@ int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu)
     int64_t groups = (int64_t)num_cu * per_cu;
     const int64_t most = (dv.nb + kGridWaves - 2) / (kGridWaves - 1);
     if (groups > most) groups = most;
+    // a group gathers the partials of its used columns in one pass of its
+    // worker lanes: ceil((D + 1) / groups) * groups <= D + groups slots
+    const int64_t gather = (int64_t)(kGridWaves - 1) * kWave - dv.D;
+    if (groups > gather) groups = gather;
     if (groups < 1) groups = 1;
     return (int)groups;
 }
@@ -53,8 +60,8 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
 {
     hipError_t e = hipMemsetAsync(sync, 0, sizeof(GridSync), stream);
     if (e != hipSuccess) return e;
-    const int W = partial_width(a.data.D);
-    hipLaunchKernelGGL(fill_empty_slots, dim3(1), dim3(256), 0, stream, result, 2 * W);
+    hipLaunchKernelGGL(fill_empty_slots, dim3(64), dim3(256), 0, stream, partials,
+                       grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int slots = a.max_depth > 1 ? a.max_depth : 1;

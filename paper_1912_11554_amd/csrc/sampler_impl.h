@@ -16,8 +16,8 @@
 //   GridEval -- one chain on the whole device.  In every group, wave 0 is the
 //               controller (it runs the tree logic) and the other waves are
 //               workers (they stream a slice of the rows).  Group partials
-//               meet in a grid-wide exchange whose last arriver adds them in
-//               group order.  Controller and workers run the same collective
+//               meet in a grid-wide exchange where each column has an owner
+//               group that adds its partials in a fixed order.  Controller and workers run the same collective
 //               with the same workgroup barriers; only the workers' copy
 //               contains the data pass, so tree state and data-pass
 //               registers are never live together.
@@ -116,10 +116,9 @@ struct GridShared {
     double qbuf[64 * DPL];
     union {
         double red[NW][W];                  // per-wave column sums of the group
-        double red_flat[(NW - 1) * kWave];  // per-set sums of the last arriver
+        double red_flat[(NW - 1) * kWave];  // the gathered partials of the group's columns
     };
     int cmd;
-    int last;
 };
 
 struct GridCtx {
@@ -128,17 +127,19 @@ struct GridCtx {
     int64_t N, nb;
     int D;
     int groups;
-    double* partials;  // [2][groups][W]
-    double* result;    // [2][W]
+    double* partials;  // [kGridPhases][D + 1][groups]
+    double* result;    // [kGridPhases][W]
     GridSync* sync;
 };
 
 // Cross-group exchange.  Everything that one group publishes for another
-// (partials, the result, counters) is written and read with agent-scope
+// (partials, results, the error flag) is written and read with agent-scope
 // atomic accesses, which the L2 keeps coherent across the XCDs one access at
-// a time.  Ordering between them comes from waiting for the wave's
-// outstanding memory operations (s_waitcnt) before the next one is issued.
-// No whole-cache write-back or invalidate (what a device-scope fence does) is
+// a time.  A slot that carries a value holds kEmptySlot until the value is
+// written, so a reader needs no separate flag: it waits for the slot itself.
+// Ordering between accesses comes from waiting for the wave's outstanding
+// memory operations (s_waitcnt) before the next one is issued.  No
+// whole-cache write-back or invalidate (what a device-scope fence does) is
 // needed: no ordinary store has to become visible to another group, and no
 // ordinary load may observe another group's writes.
 __device__ __forceinline__ void store_shared(double* p, double v)
@@ -156,8 +157,8 @@ __device__ __forceinline__ void drain_memory_ops()
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// The result slots hold this bit pattern (a signalling NaN, which no
-// arithmetic produces) until the step's result is written.
+// The slot bit pattern meaning "not written yet" (a signalling NaN, which no
+// arithmetic produces).
 constexpr unsigned long long kEmptySlot = 0x7FF4DEADBEEF0001ull;
 
 __device__ __forceinline__ unsigned long long slot_bits(const double* p)
@@ -165,22 +166,66 @@ __device__ __forceinline__ unsigned long long slot_bits(const double* p)
     return __hip_atomic_load(reinterpret_cast<unsigned long long*>(const_cast<double*>(p)), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void empty_slot(double* p)
+{
+    __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), kEmptySlot, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool grid_error(const GridCtx& c)
+{
+    return __hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+}
+__device__ __forceinline__ void raise_grid_error(const GridCtx& c)
+{
+    __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// about 10 s of the 100 MHz constant clock: a wait that long means a broken
+// invariant, and every group then gives up instead of hanging the device
+constexpr uint64_t kGridWaitTicks = 1000000000ull;
+
+// Wait until *p holds a value; false if the exchange failed meanwhile.
+__device__ __forceinline__ bool wait_slot(const GridCtx& c, const double* p, double& v)
+{
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    for (;;) {
+        // both loads in flight together: one round trip per poll
+        const unsigned long long b = slot_bits(p);
+        const bool err = grid_error(c);
+        if (b != kEmptySlot) {
+            v = __builtin_bit_cast(double, b);
+            return true;
+        }
+        if (err) return false;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kGridWaitTicks) {
+            raise_grid_error(c);
+            return false;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// Position in a result row of used column ci (0..D-1, or D for the loss).
+__device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < D ? ci : 64 * DPL; }
 
 // One collective evaluation for the whole group.  Wave 0 passes the position
 // and the command; with kCmdEval every worker streams its blocks and the
 // group joins the grid-wide sum.  Returns the command; on return wave 0 finds
 // the full sums in out_r: component m of lane l is column l + 64 m, and
 // component DPL of lane 0 is the loss.  Controller and workers execute the
-// same workgroup barriers; the workers return as soon as their part is
-// handed over.
+// same workgroup barriers; the workers return as soon as their part is done.
 //
-// Step s uses parity buffer s & 1.  Each group stores its partial and counts
-// itself in; the workers of the group that completes the count add all
-// partials (each worker lane one used column of a fixed subset of groups,
-// in increasing group order, then the subsets in order), re-arm the other
-// parity's result slots (every controller has read them: it arrived at this
-// step after reading them) and store the result.
-// Controllers poll their own lane's result slots until none is empty.
+// Step s uses phase s mod 3 of the buffers.  Each group stores its partial of
+// every used column (the D gradient columns and the loss) into that column's
+// row of group slots.  Group g owns the used columns g, g + G, ...: its
+// workers wait for the G slots of each, empty them again, add them in a fixed
+// order (lane l takes groups l, l + 64, ... in increasing order, then the
+// lanes in butterfly order), store the column's result slot and empty the
+// same slot of the previous phase.  Controllers wait for the result slots of
+// their lanes.  Emptying is safe: a group's partial of step s is written
+// after its controller read all of step s - 1's results, and the next write
+// of an emptied slot comes only after the worker that emptied it has waited
+// for its own stores (s_waitcnt at its next step, before it stores the next
+// result that every writer must first read).
 template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
 __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step,
                                const double (&q)[DPL], int cmd_in, double (&out_r)[DPL + 1], bool* aborted)
@@ -188,7 +233,7 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
     constexpr int W = GridShared<DPL, NW>::W;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
-    const int par = (int)(step & 1);
+    const int ph = (int)(step % kGridPhases);
     if (wave == 0) {
 #pragma unroll
         for (int m = 0; m < DPL; ++m) sh.qbuf[l + 64 * m] = q[m];
@@ -198,144 +243,104 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
     const int cmd = sh.cmd;
     if (cmd == kCmdExit) return cmd;
 
+    const int D = c.D;
+    const int used = D + 1;
+    const int G = c.groups;
+    const int g = blockIdx.x;
+    double* part = c.partials + (int64_t)ph * used * G;
     if (WORKER) {
         double qv[CPS];
-        spread_position_lds<CPS, S>(sh.qbuf, c.D, qv);
+        spread_position_lds<CPS, S>(sh.qbuf, D, qv);
         double acc[CPS];
 #pragma unroll
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
         const int workers = NW - 1;
-        stream_blocks<T, CPS, S>((const T*)c.X, c.y, c.D, c.N, c.nb, (int64_t)blockIdx.x * workers + (wave - 1),
-                                 (int64_t)c.groups * workers, qv, acc, loss);
+        stream_blocks<T, CPS, S>((const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
+                                 (int64_t)G * workers, qv, acc, loss);
         if constexpr (S <= 8 && CPS == 8) {
             const double col = finish_pass<CPS, S>(acc, loss);
-            if (l < c.D) sh.red[wave][l] = col;
+            if (l < D) sh.red[wave][l] = col;
             if (l == 0) sh.red[wave][64 * DPL] = loss;
         } else {
-            finish_pass_to_row<CPS, S>(acc, loss, sh.red[wave], c.D, 64 * DPL);
+            finish_pass_to_row<CPS, S>(acc, loss, sh.red[wave], D, 64 * DPL);
         }
     }
-    __syncthreads();  // group partials in LDS
+    __syncthreads();  // per-worker sums in LDS
 
-    if (wave == 0) {
+    if (WORKER && wave == 1) {
+        // the group's partial of each used column, workers in wave order
 #pragma unroll
         for (int m = 0; m <= DPL; ++m) {
-            const int col = l + 64 * m;
-            const bool used = (m < DPL) ? (col < c.D) : (l == 0);
-            double s = 0.0;
-            if (used) {
+            const int colw = l + 64 * m;
+            const int ci = m < DPL ? colw : (l == 0 ? D : -1);
+            if (ci >= 0 && (m == DPL || colw < D)) {
+                double s = 0.0;
 #pragma unroll
-                for (int w = 1; w < NW; ++w) s += sh.red[w][col];
-            }
-            store_shared(&c.partials[((int64_t)par * c.groups + blockIdx.x) * W + col], s);
-        }
-        drain_memory_ops();
-        // arrival: per group slot (group index mod 8) first, so that the
-        // atomics spread over eight addresses; the group completing its slot
-        // counts the slot in at the top counter; the group completing the top
-        // count reduces
-        int last = 0;
-        if (l == 0) {
-            const int slot = blockIdx.x & 7;
-            const unsigned long long per = (unsigned long long)((c.groups - slot + 7) / 8);
-            const unsigned long long o =
-                __hip_atomic_fetch_add(&c.sync->slot[slot][0], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (o + 1 == (step + 1) * per) {
-                const unsigned long long slots = c.groups < 8 ? (unsigned long long)c.groups : 8ull;
-                const unsigned long long t =
-                    __hip_atomic_fetch_add(&c.sync->counter, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                last = (t + 1 == (step + 1) * slots) ? 1 : 0;
+                for (int w = 1; w < NW; ++w) s += sh.red[w][colw];
+                store_shared(&part[(int64_t)ci * G + g], s);
             }
         }
-        last = __shfl(last, 0);
-        if (l == 0) sh.last = last;
     }
-    __syncthreads();  // arrival recorded
-    if (sh.last) {
-        // The workers of the last arriving group add the group partials, in
-        // one round of loads: worker k takes groups k, k + (NW - 1), ..., in
-        // increasing order, then worker 0 adds the per-worker sums in worker
-        // order and publishes.  The controller only passes the barrier, so
-        // none of this is live beside its tree state.
+
+    const int mine = g < used ? (used - 1 - g) / G + 1 : 0;  // used columns this group owns
+    if (mine > 0) {                                           // uniform over the group
+        __syncthreads();  // the per-worker sums are consumed
         if (WORKER) {
-            // worker lane t takes used column c = t % (D + 1) (column c < D,
-            // or the loss for c = D) of groups j, j + J, ... (j = t / (D + 1),
-            // J lane sets), in increasing group order
-            const int k = wave - 1;
-            if (k == 0) {
-                // every controller has read the other parity's result by
-                // now: re-arm those slots while the partials load
-#pragma unroll
-                for (int m = 0; m <= DPL; ++m)
-                    __hip_atomic_store(reinterpret_cast<unsigned long long*>(&c.result[(par ^ 1) * W + l + 64 * m]),
-                                       kEmptySlot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            const int used = c.D + 1;
-            const int sets = ((NW - 1) * kWave) / used;  // J >= 1 since D + 1 <= 321 < 960
-            const int t = k * kWave + l;
-            const int j = t / used;
-            const int col = t - j * used;
-            if (j < sets) {
-                const double* src = c.partials + (int64_t)par * c.groups * W + (col < c.D ? col : 64 * DPL);
-                double s_ = 0.0;
-                constexpr int B = 16;
-                for (int g0 = j; g0 < c.groups; g0 += B * sets) {
-                    double v[B];
-#pragma unroll
-                    for (int i = 0; i < B; ++i) {
-                        const int g = g0 + i * sets;
-                        v[i] = g < c.groups ? load_shared(src + (int64_t)g * W) : 0.0;
-                    }
-#pragma unroll
-                    for (int i = 0; i < B; ++i) s_ += v[i];
-                }
-                sh.red_flat[j * used + col] = s_;
+            drain_memory_ops();  // this lane's emptying stores of earlier steps have landed
+            bool ok = true;
+            for (int i = (wave - 1) * kWave + l; i < mine * G; i += (NW - 1) * kWave) {
+                const int jc = i / G;
+                const int src = i - jc * G;
+                double* slot = &part[(int64_t)(g + jc * G) * G + src];
+                double v = 0.0;
+                if (ok) ok = wait_slot(c, slot, v);
+                sh.red_flat[i] = v;
+                empty_slot(slot);
             }
         }
-        __syncthreads();  // per-set sums in LDS
-        if (WORKER && wave == 1) {
-            const int used = c.D + 1;
-            const int sets = ((NW - 1) * kWave) / used;
-            double tot[DPL + 1];
-#pragma unroll
-            for (int m = 0; m <= DPL; ++m) {
-                const int colw = l + 64 * m;  // column of the result row
-                const int ci = m < DPL ? colw : (l == 0 ? c.D : -1);
-                tot[m] = 0.0;
-                if (ci >= 0 && (m == DPL || colw < c.D))
-                    for (int jj = 0; jj < sets; ++jj) tot[m] += sh.red_flat[jj * used + ci];
+        __syncthreads();  // the group's columns gathered
+        if (WORKER) {
+            for (int jc = wave - 1; jc < mine; jc += NW - 1) {
+                const int ci = g + jc * G;
+                double s = 0.0;
+                for (int t = l; t < G; t += kWave) s += sh.red_flat[jc * G + t];
+                s = wave_sum(s);
+                if (l == 0) {
+                    const int pos = result_pos(ci, D, DPL);
+                    store_shared(&c.result[ph * W + pos], s);
+                    empty_slot(&c.result[((ph + kGridPhases - 1) % kGridPhases) * W + pos]);
+                }
             }
-            drain_memory_ops();  // the re-arm above lands before this result
-#pragma unroll
-            for (int m = 0; m <= DPL; ++m) store_shared(&c.result[par * W + l + 64 * m], tot[m]);
         }
     }
     if (WORKER) return cmd;
 
-    // controller: wait for this lane's result slots; give up (and tell every
-    // group) after about 10 s so that a broken invariant can never hang the
-    // device
-    const double* slot = &c.result[par * W + l];
-    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    bool bad = false;
+    // controller: wait for this lane's result slots, all at once
+    const double* row = &c.result[ph * W];
     unsigned long long bits[DPL + 1];
 #pragma unroll
-    for (int m = 0; m <= DPL; ++m) bits[m] = kEmptySlot;
+    for (int m = 0; m <= DPL; ++m) {
+        const bool used_slot = m < DPL ? l + 64 * m < D : l == 0;
+        bits[m] = used_slot ? kEmptySlot : 0ull;  // 0ull: +0.0, nothing to wait for
+    }
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool bad = false;
     for (;;) {
+#pragma unroll
+        for (int m = 0; m <= DPL; ++m)
+            if (bits[m] == kEmptySlot) bits[m] = slot_bits(row + l + 64 * m);
+        const bool err = grid_error(c);  // in flight with the slot loads
         bool ready = true;
 #pragma unroll
-        for (int m = 0; m <= DPL; ++m) {
-            if (bits[m] == kEmptySlot) bits[m] = slot_bits(slot + 64 * m);
-            ready = ready && bits[m] != kEmptySlot;
-        }
+        for (int m = 0; m <= DPL; ++m) ready = ready && bits[m] != kEmptySlot;
         if (__all(ready)) break;
-        if (__hip_atomic_load(&c.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+        if (err) {
             bad = true;
             break;
         }
-        if (__builtin_amdgcn_s_memrealtime() - t0 > 1000000000ull) {
-            if (l == 0) __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kGridWaitTicks) {
+            if (l == 0) raise_grid_error(c);
             bad = true;
             break;
         }
