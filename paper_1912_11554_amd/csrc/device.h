@@ -96,8 +96,10 @@ template <int CTRL>
 __device__ __forceinline__ double dpp_f64(double v)
 {
     const int2 h = __builtin_bit_cast(int2, v);
-    const int lo = __builtin_amdgcn_update_dpp(0, h.x, CTRL, 0xF, 0xF, false);
-    const int hi = __builtin_amdgcn_update_dpp(0, h.y, CTRL, 0xF, 0xF, false);
+    // every pattern here reads a lane of the same row with all rows and banks
+    // enabled, so no lane keeps an old value and none needs setting up
+    const int lo = __builtin_amdgcn_mov_dpp(h.x, CTRL, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp(h.y, CTRL, 0xF, 0xF, true);
     return __builtin_bit_cast(double, int2{lo, hi});
 }
 

@@ -91,7 +91,7 @@ __device__ __forceinline__ BlockRegs<T, CPS, S> load_block(const T* __restrict__
 }
 
 // Rows of one loaded block.  qv[k] must hold q[k * S + L % S] (zero for
-// columns c >= D).
+// columns c >= D).  Rows at or past rows_left add nothing.
 template <typename T, int CPS, int S>
 __device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, int64_t rows_left,
                                               const double (&qv)[CPS], double (&acc)[CPS], double& loss)
