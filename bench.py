@@ -37,6 +37,10 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
+# vector ALU issue peak: 256 CUs x 4 SIMDs, one 64-lane instruction per SIMD
+# every 4 clocks, 2.4 GHz -> 614.4 G wave-instructions/s (with one FMA per
+# lane that is the 78.6 TFLOP/s fp64 vector peak)
+VALU_PEAK_GIPS = 614.4
 METRIC = "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline"
 
 
@@ -161,9 +165,12 @@ def recorded_traffic(kernel, workload, evals):
     e = rec.get("kernels", {}).get(f"{kernel}/{workload}")
     if not e:
         return None
-    return dict(bytes=round((e["fetch_bytes_per_eval"] + e["write_bytes_per_eval"]) * evals),
-                fetch_bytes_per_eval=e["fetch_bytes_per_eval"],
-                write_bytes_per_eval=e["write_bytes_per_eval"], source="profiles/traffic.json")
+    out = dict(bytes=round((e["fetch_bytes_per_eval"] + e["write_bytes_per_eval"]) * evals),
+               fetch_bytes_per_eval=e["fetch_bytes_per_eval"],
+               write_bytes_per_eval=e["write_bytes_per_eval"], source="profiles/traffic.json")
+    if "valu_instructions_per_eval" in e:
+        out["valu_instructions_per_eval"] = e["valu_instructions_per_eval"]
+    return out
 
 
 def cpu_baseline(name, seconds):
@@ -235,6 +242,14 @@ def main():
                 "flops_per_eval": main_res["flops_per_eval"], "passes": main_res["passes"],
                 "pass_fill": round(main_res["pass_fill"], 4),
                 "ms_per_pass": round(main_res["ms_per_pass"], 4)}
+    elif kernel == "sampler_wave_kernel" and traffic and "valu_instructions_per_eval" in traffic:
+        # data sets resident in LDS: the vector ALU issue rate bounds the kernel
+        rate = traffic["valu_instructions_per_eval"] * main_res["evals_per_s"] / 1e9
+        roof = {"kernel": kernel, "bound": "alu", "achieved": round(rate, 1), "peak": VALU_PEAK_GIPS,
+                "unit": "G VALU wave-instructions/s", "frac": round(rate / VALU_PEAK_GIPS, 4),
+                "traffic": traffic["bytes"], "traffic_detail": traffic,
+                "valu_instructions_per_eval": traffic["valu_instructions_per_eval"],
+                "bytes_per_eval": main_res["bytes_per_eval"], "algorithmic_gbs": round(achieved, 1)}
     else:
         roof = {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

@@ -38,9 +38,19 @@ def main():
                     help="nuts_data_potential_grad_batched (fp32 matrix cores)")
     ap.add_argument("--reps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="also run a plain device copy of this many MiB first (a known-size "
+                         "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     import torch
+
+    if args.copy_mb:
+        src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     import paper_1912_11554_amd as nuts
     import workloads
@@ -70,7 +80,7 @@ def main():
     us = e0.elapsed_time(e1) * 1e3 / args.reps
     es = 8 if wl.dtype == "f64" else 4
     out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K,
-               kernel="batch_pass_kernel" if args.batched else "potential_pass_kernel",
+               kernel="batch_pass_kernel" if args.batched else "potential_grad_kernel",
                reps=args.reps, us_per_call_with_host=round(us, 2))
     if args.batched:
         tflops = 4.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12
