@@ -95,13 +95,20 @@ def lib():
         L.orc_check_range.argtypes = [u64, P, P]
         L.orc_nuts_chain.argtypes = [
             i32, P, P, P, i64, i64, dbl, dbl, dbl, P, i32, i64, i64, u64, u64, i32, i32, P,
-            i64, P, P, P, P, P, i64, P, P, i64, P, u64,
+            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P,
         ]
         L.orc_nuts_chain.restype = i64
         L.orc_leapfrog_steps.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, dbl, i64, P, P]
         L.orc_leapfrog_steps.restype = dbl
         L.orc_is_uturn_exported.argtypes = [P, P, P, P, i32, P, i64]
         L.orc_is_uturn_exported.restype = i32
+        L.orc_normals_tagged.argtypes = [u64, u64, u64, u64, i64, P]
+        L.orc_dual_avg_run.argtypes = [dbl, dbl, i64, P, P, P]
+        L.orc_mass_windows.argtypes = [i64, P, i32]
+        L.orc_mass_windows.restype = i32
+        L.orc_find_step_size_at.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, P, dbl, u64, u64,
+                                            u64, P]
+        L.orc_find_step_size_at.restype = dbl
         _lib = L
     return _lib
 
@@ -131,9 +138,11 @@ def u53(word: int) -> float:
     return lib().orc_u53(int(word))
 
 
-def normals(seed, chain, t, D):
+def normals(seed, chain, t, D, tag=1):
+    """D standard normals from the Philox stream (tag 1: the momentum of
+    iteration t; tag 5: the step-size heuristic's momentum)."""
     out = np.zeros(D, dtype=np.float64)
-    lib().orc_normals(seed, chain, t, D, _p(out))
+    lib().orc_normals_tagged(seed, chain, t, tag, D, _p(out))
     return out
 
 
@@ -214,9 +223,10 @@ def leapfrog(X, y, q, p, h, nsteps, inv_mass=None, prior_scale=1.0, target=TARGE
 def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chain=0,
          prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
          init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
-         trace_cap=0, leaves_cap=0, sel_salt=0):
+         trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8):
     """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
-    final_q [D], inv_mass [D], grad_evals; with trace_cap the U-turn check
+    final_q [D], inv_mass [D], step_size (the one in use at the end: the
+    adapted one with adapt_step_size), grad_evals; with trace_cap the U-turn check
     trace as (first_leaf, last_leaf) pairs; with leaves_cap the generated
     leaves as records (j, n, position, H - H0).  ``sel_salt`` (test only)
     re-keys the proposal-selection draws and nothing else."""
@@ -230,15 +240,18 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
     trlen = ctypes.c_int64(0)
     lv = np.zeros(max(4 * leaves_cap, 1), dtype=np.int64)
     lvlen = ctypes.c_int64(0)
+    eps_out = ctypes.c_double(0.0)
     nev = lib().orc_nuts_chain(
         target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale, noise_scale, step_size,
         _p(_f64(inv_mass)), max_tree_depth, num_warmup, num_samples, seed, chain, builder,
         1 if adapt_diag_mass else 0, _p(_f64(init_q)), first_iter, _p(samples), _p(stats),
         _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
         ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
-        ctypes.byref(lvlen), sel_salt,
+        ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
+        ctypes.byref(eps_out),
     )
-    out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im, grad_evals=nev)
+    out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im,
+               step_size=eps_out.value, grad_evals=nev)
     if trace_cap:
         out["trace"] = tr[: trlen.value].reshape(-1, 2)
     if leaves_cap:
@@ -253,3 +266,37 @@ def is_uturn(qa, pa, qb, pb, v, inv_mass=None):
     D = qa.shape[0]
     im = _f64(np.ones(D) if inv_mass is None else inv_mass)
     return bool(lib().orc_is_uturn_exported(_p(qa), _p(pa), _p(qb), _p(pb), v, _p(im), D))
+
+
+# --------------------------------------------------- warmup adaptation -----
+def dual_averaging(eps0, delta, alphas):
+    """The dual-averaging recursion (Hoffman & Gelman 2014, Section 3.2)
+    driven by a given sequence of accept statistics; returns (log eps,
+    log eps_bar) after each update."""
+    a = _f64(alphas)
+    n = a.shape[0]
+    le = np.zeros(n)
+    lb = np.zeros(n)
+    lib().orc_dual_avg_run(eps0, delta, n, _p(a), _p(le), _p(lb))
+    return le, lb
+
+
+def mass_windows(num_warmup):
+    """Slow windows [start, end) of the windowed diagonal-mass adaptation."""
+    out = np.zeros(128, dtype=np.int64)
+    n = lib().orc_mass_windows(num_warmup, _p(out), 64)
+    return [(int(out[2 * i]), int(out[2 * i + 1])) for i in range(n)]
+
+
+def find_step_size(X, y, q, eps, *, seed, chain=0, t=0, inv_mass=None, prior_scale=1.0,
+                   target=TARGET_LOGISTIC, yv=None, noise_scale=1.0):
+    """Hoffman & Gelman (2014) Alg. 4 from eps at q; returns (eps, gradient
+    evaluations)."""
+    X = _f64(X)
+    N, D = X.shape
+    im = _f64(np.ones(D) if inv_mass is None else inv_mass)
+    ev = ctypes.c_int64(0)
+    e = lib().orc_find_step_size_at(target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale,
+                                    noise_scale, _p(im), _p(_f64(q)), eps, seed, chain, t,
+                                    ctypes.byref(ev))
+    return e, ev.value

@@ -43,6 +43,19 @@
  *   R8  Philox4x64-10, key (seed, chain), counter (t, tag<<32 | j, n, 0).
  *   R13 optional diagonal inverse mass from warmup variance, normalised to
  *       mean one.
+ *   R19 warmup adaptation (optional): the step-size heuristic of Hoffman &
+ *       Gelman (2014) Alg. 4 from the given step size, then their dual
+ *       averaging (Section 3.2, Alg. 5) with target acceptance delta,
+ *       gamma = 0.05, t0 = 10, kappa = 0.75, mu = log(10 eps); the accept
+ *       statistic of an iteration is the mean over its leaves of
+ *       min(1, exp(H0 - H)); after warmup eps = exp(log eps_bar).  Together
+ *       with the diagonal mass: the windowed scheme of the Stan reference
+ *       manual (initial buffer 75, slow windows of 25, 50, 100, ...
+ *       iterations with the last one stretched to the terminal buffer of
+ *       50; 15 % / 75 % / 10 % when warmup is shorter than 150; no windows
+ *       below 20); at each window end the inverse mass is the regularised
+ *       variance of the window's states (weight 5/(n+5) towards 1e-3, not
+ *       normalised) and the heuristic and dual averaging restart.
  */
 #include <math.h>
 #include <stdint.h>
@@ -89,7 +102,7 @@ void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint6
 }
 
 /* Draw tags: which random quantity a Philox block feeds (reading R8). */
-enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4 };
+enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4, ORC_TAG_STEP = 5 };
 
 static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, uint64_t j,
                       uint64_t n, uint64_t out[4])
@@ -102,14 +115,16 @@ static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, u
 /* 53 high bits of a word -> uniform on [0, 1). */
 double orc_u53(uint64_t w) { return (double)(w >> 11) * (1.0 / 9007199254740992.0); }
 
-/* D standard normals for the momentum of iteration t: block b gives four
- * uniforms, i.e. two Box-Muller pairs, i.e. normals 4b .. 4b+3. */
-void orc_normals(uint64_t seed, uint64_t chain, uint64_t t, int64_t D, double *out)
+/* D standard normals under a tag (the momentum of iteration t with
+ * ORC_TAG_MOMENTUM): block b gives four uniforms, i.e. two Box-Muller pairs,
+ * i.e. normals 4b .. 4b+3. */
+void orc_normals_tagged(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, int64_t D,
+                        double *out)
 {
     const double two_pi = 6.283185307179586476925286766559;
     for (int64_t b = 0; 4 * b < D; ++b) {
         uint64_t w[4];
-        orc_block(seed, chain, t, ORC_TAG_MOMENTUM, 0, (uint64_t)b, w);
+        orc_block(seed, chain, t, tag, 0, (uint64_t)b, w);
         for (int pair = 0; pair < 2; ++pair) {
             double ua = orc_u53(w[2 * pair]);
             double ub = orc_u53(w[2 * pair + 1]);
@@ -120,6 +135,11 @@ void orc_normals(uint64_t seed, uint64_t chain, uint64_t t, int64_t D, double *o
             if (i0 + 1 < D) out[i0 + 1] = r * sin(th);
         }
     }
+}
+
+void orc_normals(uint64_t seed, uint64_t chain, uint64_t t, int64_t D, double *out)
+{
+    orc_normals_tagged(seed, chain, t, ORC_TAG_MOMENTUM, D, out);
 }
 
 /* +1 or -1 for doubling j of iteration t. */
@@ -595,6 +615,142 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
     orc_node_free(&prop); orc_node_free(&z);
 }
 
+/* ------------------------------------------------------------------------- */
+/* Warmup adaptation (reading R19).                                           */
+
+#define ORC_LN2 0.69314718055994530942
+#define ORC_STEP_TRIALS 100
+
+/* Hoffman & Gelman (2014) Alg. 4: from eps, one leapfrog step with a fresh
+ * momentum r ~ N(0, M) (drawn under ORC_TAG_STEP at counter t); a = +1 if
+ * the step keeps more than half the density (H0 - H > -ln 2), else -1; then
+ * eps is doubled (a = +1) or halved (a = -1) until that comparison flips.
+ * A non-finite energy counts as density zero.  At most ORC_STEP_TRIALS
+ * changes of eps. */
+static double orc_log_ratio(orc_target *tg, const orc_node *cur, const double *r, double eps,
+                            const double *im, double H0, orc_node *z)
+{
+    int64_t D = tg->D;
+    orc_node_copy(z, cur, D);
+    memcpy(z->p, r, (size_t)D * sizeof(double));
+    orc_leapfrog(tg, z, eps, im);
+    double d = H0 - (z->U + orc_kinetic(z->p, im, D));
+    return d == d ? d : -INFINITY;
+}
+
+static double orc_find_step_size(orc_target *tg, const orc_node *cur, double eps,
+                                 const double *im, uint64_t seed, uint64_t chain, uint64_t t)
+{
+    int64_t D = tg->D;
+    double *r = (double *)malloc((size_t)D * sizeof(double));
+    orc_normals_tagged(seed, chain, t, ORC_TAG_STEP, D, r);
+    for (int64_t j = 0; j < D; ++j) r[j] = r[j] / sqrt(im[j]);
+    double H0 = cur->U + orc_kinetic(r, im, D);
+    orc_node z;
+    orc_node_alloc(&z, D);
+    double d = orc_log_ratio(tg, cur, r, eps, im, H0, &z);
+    double a = d > -ORC_LN2 ? 1.0 : -1.0;
+    for (int k = 0; k < ORC_STEP_TRIALS && a * (d + ORC_LN2) > 0.0; ++k) {
+        eps = a > 0.0 ? eps * 2.0 : eps * 0.5;
+        d = orc_log_ratio(tg, cur, r, eps, im, H0, &z);
+    }
+    orc_node_free(&z);
+    free(r);
+    return eps;
+}
+
+/* Dual averaging of log eps (Hoffman & Gelman 2014, Section 3.2). */
+typedef struct {
+    double mu, hbar, log_eps, log_eps_bar;
+    int64_t m;
+} orc_dual_avg;
+
+#define ORC_DA_GAMMA 0.05
+#define ORC_DA_T0 10.0
+#define ORC_DA_KAPPA 0.75
+
+static void orc_da_start(orc_dual_avg *da, double eps)
+{
+    da->mu = log(10.0 * eps);
+    da->hbar = 0.0;
+    da->log_eps = log(eps);
+    da->log_eps_bar = 0.0;
+    da->m = 0;
+}
+
+/* One update with the accept statistic alpha; returns the next eps. */
+static double orc_da_update(orc_dual_avg *da, double alpha, double delta)
+{
+    da->m += 1;
+    double m = (double)da->m;
+    double w = 1.0 / (m + ORC_DA_T0);
+    da->hbar = (1.0 - w) * da->hbar + w * (delta - alpha);
+    da->log_eps = da->mu - (sqrt(m) / ORC_DA_GAMMA) * da->hbar;
+    double eta = pow(m, -ORC_DA_KAPPA);
+    da->log_eps_bar = eta * da->log_eps + (1.0 - eta) * da->log_eps_bar;
+    return exp(da->log_eps);
+}
+
+/* Exposed for the tests: the recursion driven by a given accept sequence;
+ * writes log eps and log eps_bar after each update. */
+void orc_dual_avg_run(double eps0, double delta, int64_t n, const double *alpha,
+                      double *out_log_eps, double *out_log_eps_bar)
+{
+    orc_dual_avg da = { 0.0, 0.0, 0.0, 0.0, 0 };
+    orc_da_start(&da, eps0);
+    for (int64_t i = 0; i < n; ++i) {
+        orc_da_update(&da, alpha[i], delta);
+        out_log_eps[i] = da.log_eps;
+        out_log_eps_bar[i] = da.log_eps_bar;
+    }
+}
+
+/* The slow windows of the windowed mass adaptation for W warmup
+ * iterations: pairs [start, end) of iteration indices (0-based), at most
+ * cap pairs; returns their number. */
+int orc_mass_windows(int64_t W, int64_t *out, int cap)
+{
+    if (W < 20) return 0;
+    int64_t init = 75, term = 50, base = 25;
+    if (init + term + base > W) {
+        init = (int64_t)(0.15 * (double)W);
+        term = (int64_t)(0.10 * (double)W);
+        base = W - (init + term);
+    }
+    int64_t slow_end = W - term;
+    int n = 0;
+    int64_t start = init, size = base;
+    while (start < slow_end && n < cap) {
+        int64_t end = start + size;
+        /* stretch this window to the terminal buffer when the one after it
+         * would not fit */
+        if (end + 2 * size > slow_end) end = slow_end;
+        out[2 * n] = start;
+        out[2 * n + 1] = end;
+        ++n;
+        start = end;
+        size *= 2;
+    }
+    return n;
+}
+
+/* Exposed for the tests: the step-size heuristic at q for one target. */
+double orc_find_step_size_at(int kind, const double *X, const uint8_t *y, const double *yv,
+                             int64_t N, int64_t D, double s, double sn, const double *inv_mass,
+                             const double *q, double eps, uint64_t seed, uint64_t chain,
+                             uint64_t t, int64_t *evals)
+{
+    orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
+    orc_node cur;
+    orc_node_alloc(&cur, D);
+    memcpy(cur.q, q, (size_t)D * sizeof(double));
+    cur.U = orc_eval(&tg, cur.q, cur.g);
+    double out = orc_find_step_size(&tg, &cur, eps, inv_mass, seed, chain, t);
+    orc_node_free(&cur);
+    if (evals) *evals = tg.nevals;
+    return out;
+}
+
 /* Diagonal inverse mass from warmup draws (reading R13): Welford mean and
  * variance of the states after warmup iterations [W/2, W), shrunk towards
  * 1e-3 with weight 5/(n+5), then scaled to mean one. */
@@ -615,7 +771,8 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
                        int64_t first_iter, double *out_samples, orc_stats *out_stats,
                        double *out_q, double *out_inv_mass, int64_t *trace,
                        int64_t trace_cap, int64_t *trace_len, int64_t *leaves,
-                       int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt)
+                       int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt,
+                       int adapt_step, double target_accept, double *out_step_size)
 {
     orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
     double *im = (double *)malloc((size_t)D * sizeof(double));
@@ -642,11 +799,49 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
     orc_welford wf = { 0, (double *)calloc((size_t)D, sizeof(double)),
                        (double *)calloc((size_t)D, sizeof(double)) };
 
+    /* reading R19: step size by dual averaging, windowed mass with it */
+    int adapt = adapt_step && num_warmup > 0;
+    orc_dual_avg da = { 0.0, 0.0, 0.0, 0.0, 0 };
+    int64_t win[128];
+    int nwin = 0, wi = 0;
+    if (adapt) {
+        it.eps = orc_find_step_size(&tg, &cur, it.eps, im, seed, chain, (uint64_t)first_iter);
+        orc_da_start(&da, it.eps);
+        if (adapt_diag) nwin = orc_mass_windows(num_warmup, win, 64);
+    }
+
     orc_stats st;
     for (int64_t k = 0; k < num_warmup + num_samples; ++k) {
         it.t = (uint64_t)(first_iter + k);
         orc_iteration(&it, &cur, max_depth, builder, &st);
-        if (adapt_diag && k < num_warmup && k >= num_warmup / 2) {
+        if (adapt && k < num_warmup) {
+            it.eps = orc_da_update(&da, st.accept_prob, target_accept);
+            if (wi < nwin && k >= win[2 * wi] && k < win[2 * wi + 1]) {
+                wf.n++;
+                for (int64_t j = 0; j < D; ++j) {
+                    double d1 = cur.q[j] - wf.mean[j];
+                    wf.mean[j] += d1 / (double)wf.n;
+                    wf.m2[j] += d1 * (cur.q[j] - wf.mean[j]);
+                }
+            }
+            if (wi < nwin && k == win[2 * wi + 1] - 1) {
+                if (wf.n >= 2) {
+                    double nn = (double)wf.n;
+                    for (int64_t j = 0; j < D; ++j) {
+                        double var = wf.m2[j] / (nn - 1.0);
+                        im[j] = (nn / (nn + 5.0)) * var + 1e-3 * (5.0 / (nn + 5.0));
+                    }
+                }
+                wf.n = 0;
+                for (int64_t j = 0; j < D; ++j) wf.mean[j] = wf.m2[j] = 0.0;
+                ++wi;
+                it.eps = orc_find_step_size(&tg, &cur, it.eps, im, seed, chain,
+                                            (uint64_t)(first_iter + k + 1));
+                orc_da_start(&da, it.eps);
+            }
+            if (k == num_warmup - 1) it.eps = exp(da.log_eps_bar);
+        }
+        if (!adapt && adapt_diag && k < num_warmup && k >= num_warmup / 2) {
             wf.n++;
             for (int64_t j = 0; j < D; ++j) {
                 double d1 = cur.q[j] - wf.mean[j];
@@ -654,7 +849,7 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
                 wf.m2[j] += d1 * (cur.q[j] - wf.mean[j]);
             }
         }
-        if (adapt_diag && k == num_warmup - 1 && wf.n >= 2) {
+        if (!adapt && adapt_diag && k == num_warmup - 1 && wf.n >= 2) {
             double nn = (double)wf.n, tot = 0.0;
             for (int64_t j = 0; j < D; ++j) {
                 double var = wf.m2[j] / (nn - 1.0);
@@ -672,6 +867,7 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
     }
     if (out_q) memcpy(out_q, cur.q, (size_t)D * sizeof(double));
     if (out_inv_mass) memcpy(out_inv_mass, im, (size_t)D * sizeof(double));
+    if (out_step_size) *out_step_size = it.eps;
     if (trace_len) *trace_len = it.trace_len;
     if (leaves_len) *leaves_len = it.leaves_len;
     free(wf.mean); free(wf.m2);
