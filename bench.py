@@ -48,7 +48,7 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_workload(name, steps=None, warmup=None):
+def run_workload(name, steps=None, warmup=None, adapt=False):
     import torch
 
     import paper_1912_11554_amd as nuts
@@ -88,11 +88,18 @@ def run_workload(name, steps=None, warmup=None):
               prior_scale=wl.prior_scale, num_chains=C, path=path)
 
     t0 = time.time()
-    r0 = d.sample(num_warmup=warmup, num_samples=1, adapt_diag_mass=wl.adapt_diag_mass, **kw)
+    if adapt and C != 1:
+        sys.exit("--adapt takes single-chain workloads (the timed call shares one step size)")
+    r0 = d.sample(num_warmup=warmup, num_samples=1, adapt_diag_mass=wl.adapt_diag_mass,
+                  adapt_step_size=adapt, **kw)
     log(f"{name}: warmup {warmup} iterations x {C} chains, {r0['grad_evals']} gradient "
         f"evaluations, {time.time() - t0:.2f}s")
     q = r0["final_q"]
     inv_mass = r0["inv_mass"][0] if wl.adapt_diag_mass else None
+    if adapt:
+        # the paper's covtype protocol: the step size from warmup adaptation
+        kw["step_size"] = float(r0["step_size"][0])
+        log(f"{name}: step size adapted over {warmup} warmup iterations: {kw['step_size']:.6g}")
 
     D = wl.D
     samples = torch.empty((C, steps, D), dtype=torch.float64, device="cuda")
@@ -133,7 +140,8 @@ def run_workload(name, steps=None, warmup=None):
     d.free()
     s.close()
     return dict(
-        workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=wl.step_size,
+        workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=kw["step_size"],
+        step_size_adapted=bool(adapt),
         max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
         gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
         evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
@@ -210,6 +218,10 @@ def main():
                     help="second workload reported beside the first ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--adapt", action="store_true",
+                    help="adapt the step size during warmup (dual averaging, target acceptance "
+                         "0.8) and time the sampling at the adapted step size (the paper's covtype "
+                         "protocol: 150 adaptation steps); single-chain workloads")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run a plain device copy of this many MiB (a known-size "
                          "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -227,8 +239,8 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy: {args.copy_mb} MiB read + {args.copy_mb} MiB written")
         del src, dst
-    main_res = run_workload(args.workload, args.steps, args.warmup)
-    other = run_workload(args.also, args.steps, args.warmup) if args.also else None
+    main_res = run_workload(args.workload, args.steps, args.warmup, args.adapt)
+    other = run_workload(args.also, args.steps, args.warmup, args.adapt) if args.also else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
 
     achieved = main_res["achieved_gbs"]
@@ -271,6 +283,7 @@ def main():
         "config": {
             "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
             "chains": main_res["chains"], "step_size": main_res["step_size"],
+            "step_size_adapted": main_res["step_size_adapted"],
             "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
             "path": main_res["kernel"],
         },

@@ -56,7 +56,8 @@ enum { NUTS_F64 = 0, NUTS_F32 = 1 };
 
 enum {
     NUTS_DATA_PER_CHAIN = 1u << 0,  /* X is [C][N][D] and y is [C][N]; else one shared data set */
-    NUTS_ADAPT_DIAG_MASS = 1u << 1  /* set the diagonal inverse mass from warmup draws */
+    NUTS_ADAPT_DIAG_MASS = 1u << 1,  /* set the diagonal inverse mass from warmup draws */
+    NUTS_ADAPT_STEP_SIZE = 1u << 3   /* adapt the step size during warmup (dual averaging) */
 };
 
 /* Kernel path selection for nuts_sample_data (opts->path). */
@@ -140,6 +141,8 @@ typedef struct {
     int64_t* out_grad_evals;   /* [1] gradient evaluations of the whole call, or NULL */
     int32_t path;              /* NUTS_PATH_* */
     int32_t _reserved;
+    double target_accept;      /* NUTS_ADAPT_STEP_SIZE: target acceptance in (0, 1); 0 = 0.8 */
+    double* out_step_size;     /* [C] step size in use at the end (the adapted one), or NULL */
 } nuts_sample_opts;
 
 /* Run num_chains chains for num_warmup + num_samples iterations on prepared
@@ -147,11 +150,32 @@ typedef struct {
  * chain starts at init_q (zeros by default) with the gradient evaluated
  * there.  Iteration k of the call has global index first_iter + k; the first
  * num_warmup iterations are not emitted.  inv_mass_diag is [D] (shared by
- * all chains) or NULL for the identity; with NUTS_ADAPT_DIAG_MASS the
- * inverse mass is re-set at the end of warmup from the variance of the
- * warmup states in [num_warmup/2, num_warmup), shrunk towards 1e-3 with
- * weight 5/(n+5) and scaled to mean one.  Writes out_samples [C][S][D] fp64
- * and out_stats [C][S] (either may be NULL).  Divergences are not errors. */
+ * all chains) or NULL for the identity.
+ *
+ * Warmup adaptation (the paper adapts step size and mass during warmup,
+ * Section 2; its covtype step size came from 150 adaptation steps):
+ *   - NUTS_ADAPT_DIAG_MASS alone: the inverse mass is re-set at the end of
+ *     warmup from the variance of the warmup states in [num_warmup/2,
+ *     num_warmup), shrunk towards 1e-3 with weight 5/(n+5) and scaled to
+ *     mean one (the step size stays fixed).
+ *   - NUTS_ADAPT_STEP_SIZE: before the first iteration the step size moves
+ *     from step_size by Hoffman & Gelman's (2014) Alg. 4 heuristic (doubling
+ *     or halving until one leapfrog step from a fresh momentum crosses half
+ *     the density); every warmup iteration then updates it by their dual
+ *     averaging (Section 3.2: gamma 0.05, t0 10, kappa 0.75, mu = log(10
+ *     eps), target acceptance opts->target_accept, the accept statistic
+ *     being the iteration's mean of min(1, exp(H0 - H)) over its leaves);
+ *     sampling uses the averaged step size.  With NUTS_ADAPT_DIAG_MASS as
+ *     well, the inverse mass comes from windowed warmup: slow windows of
+ *     25, 50, 100, ... iterations after an initial buffer of 75 (the last
+ *     stretched to a terminal buffer of 50; 15 % / 75 % / 10 % of warmup
+ *     below 150 iterations; none below 20), each ending with the inverse mass
+ *     set to the window's variance shrunk as above (not normalised) and the
+ *     heuristic and dual averaging restarted.
+ *   The step size in use at the end goes to opts->out_step_size.
+ * Writes out_samples [C][S][D] fp64 and out_stats [C][S] (either may be
+ * NULL).  Divergences are not errors.  NUTS_EINVAL for target_accept outside
+ * (0, 1). */
 int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double prior_scale,
                      double step_size, const double* inv_mass_diag, int max_tree_depth,
                      int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libnuts.so")
 
 NUTS_OK, NUTS_EINVAL, NUTS_ENOMEM, NUTS_EDEVICE, NUTS_EUNSUPPORTED = 0, -1, -2, -3, -4
 NUTS_F64, NUTS_F32 = 0, 1
-NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS = 1, 2
+NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS, NUTS_ADAPT_STEP_SIZE = 1, 2, 8
 NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID, NUTS_PATH_BATCH = 0, 1, 2, 3
 
 EXPORTED = [
@@ -51,6 +51,8 @@ class _Opts(ctypes.Structure):
         ("out_grad_evals", ctypes.c_void_p),
         ("path", ctypes.c_int32),
         ("_reserved", ctypes.c_int32),
+        ("target_accept", ctypes.c_double),
+        ("out_step_size", ctypes.c_void_p),
     ]
 
 
@@ -239,27 +241,32 @@ class Data:
 
     def sample(self, *, step_size, max_tree_depth, num_warmup, num_samples, num_chains=1,
                seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
-               first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None):
+               first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None,
+               adapt_step_size=False, target_accept=0.8):
         """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
-        (STATS_DTYPE), final_q [C, D], inv_mass [C, D], grad_evals.  Outputs
+        (STATS_DTYPE), final_q [C, D], inv_mass [C, D], step_size [C] (in use
+        at the end: the adapted one with adapt_step_size), grad_evals.  Outputs
         are numpy unless device tensors are passed in out_samples /
         out_stats (then those are filled and returned)."""
         C, D = num_chains, self.D
         flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
-            NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0)
+            NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
+            NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0)
         if out_samples is None:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:
             out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
         final_q = np.zeros((C, D))
         out_im = np.zeros((C, D))
+        out_eps = np.zeros(C)
         gev = np.zeros(1, dtype=np.int64)
         im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)
         iq = None if init_q is None else np.ascontiguousarray(init_q, dtype=np.float64)
-        opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), path, 0)
+        opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), path, 0,
+                     target_accept, _ptr(out_eps))
         self.s._check(self.s._L.nuts_sample_data(
             self.s._h, self._d, flags, prior_scale, step_size, _ptr(im), max_tree_depth,
             num_warmup, num_samples, C, seed, _ptr(out_samples), _ptr(out_stats),
             ctypes.byref(opts)))
         return dict(samples=out_samples, stats=out_stats, final_q=final_q, inv_mass=out_im,
-                    grad_evals=int(gev[0]))
+                    step_size=out_eps, grad_evals=int(gev[0]))

@@ -469,8 +469,11 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     std::memset(&o, 0, sizeof o);
     if (opts) o = *opts;
     if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
-    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS))
+    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE))
         return fail(h, NUTS_EINVAL, "unknown flag bits 0x%x", flags);
+    const double target_accept = o.target_accept == 0.0 ? 0.8 : o.target_accept;
+    if (!(target_accept > 0.0 && target_accept < 1.0))
+        return fail(h, NUTS_EINVAL, "target_accept must be in (0, 1) (got %g)", o.target_accept);
     if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
     if (!finite_pos(step_size)) return fail(h, NUTS_EINVAL, "step_size must be finite and > 0");
     if (max_tree_depth < 1 || max_tree_depth > 30)
@@ -542,15 +545,16 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
 
     hipStream_t s = h->stream;
     const int64_t C = num_chains, S = num_samples;
-    DevBuf imb, iqb, smp, sts, fq, fim, gev;
+    DevBuf imb, iqb, smp, sts, fq, fim, fep, gev;
     const void *im_d = nullptr, *iq_d = nullptr;
-    void *smp_d = nullptr, *sts_d = nullptr, *fq_d = nullptr, *fim_d = nullptr;
+    void *smp_d = nullptr, *sts_d = nullptr, *fq_d = nullptr, *fim_d = nullptr, *fep_d = nullptr;
     HIP_TRY(h, stage_in(inv_mass_diag, (size_t)D * 8, imb, &im_d, s));
     HIP_TRY(h, stage_in(o.init_q, (size_t)C * D * 8, iqb, &iq_d, s));
     HIP_TRY(h, stage_out(out_samples, (size_t)C * S * D * 8, smp, &smp_d));
     HIP_TRY(h, stage_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, &sts_d));
     HIP_TRY(h, stage_out(o.out_final_q, (size_t)C * D * 8, fq, &fq_d));
     HIP_TRY(h, stage_out(o.out_inv_mass, (size_t)C * D * 8, fim, &fim_d));
+    HIP_TRY(h, stage_out(o.out_step_size, (size_t)C * 8, fep, &fep_d));
     HIP_TRY(h, gev.alloc((size_t)C * sizeof(unsigned long long)));
 
     SamplerArgs a;
@@ -568,11 +572,14 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     a.seed = seed;
     a.first_iter = o.first_iter;
     a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
+    a.adapt_step = (flags & NUTS_ADAPT_STEP_SIZE) ? 1 : 0;
+    a.target_accept = target_accept;
     a.init_q = (const double*)iq_d;
     a.out_samples = (double*)smp_d;
     a.out_stats = (nuts_stats*)sts_d;
     a.out_final_q = (double*)fq_d;
     a.out_inv_mass = (double*)fim_d;
+    a.out_step_size = (double*)fep_d;
     a.grad_evals = (unsigned long long*)gev.p;
 
     if (path == NUTS_PATH_WAVE) {
@@ -634,6 +641,7 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     HIP_TRY(h, finish_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, s));
     HIP_TRY(h, finish_out(o.out_final_q, (size_t)C * D * 8, fq, s));
     HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
+    HIP_TRY(h, finish_out(o.out_step_size, (size_t)C * 8, fep, s));
     std::vector<unsigned long long> ev(C);
     HIP_TRY(h, hipMemcpyAsync(ev.data(), gev.p, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
     HIP_TRY(h, hipStreamSynchronize(s));

@@ -51,7 +51,7 @@ __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64
 }
 
 // Which quantity a block feeds; part of the counter.
-enum : uint64_t { kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4 };
+enum : uint64_t { kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4, kTagStepSize = 5 };
 
 // Kept out of line: it is called a few times per iteration, and inlining it
 // would keep its temporaries and constants live across the tree loops.
@@ -70,9 +70,10 @@ __device__ __forceinline__ double unit53(uint64_t w)
 // Standard normal number i of an iteration's momentum: block i/4 holds two
 // Box-Muller pairs (u_a, u_b) giving (r cos th, r sin th), r = sqrt(-2 ln(1 -
 // u_a)), th = 2 pi u_b.
-__device__ __noinline__ double momentum_normal(uint64_t seed, uint64_t chain, uint64_t iter, int i)
+__device__ __noinline__ double momentum_normal(uint64_t seed, uint64_t chain, uint64_t iter, int i,
+                                               uint64_t tag = kTagMomentum)
 {
-    const Block4 b = draw(seed, chain, iter, kTagMomentum, 0, (uint64_t)(i >> 2));
+    const Block4 b = draw(seed, chain, iter, tag, 0, (uint64_t)(i >> 2));
     const bool second_pair = (i & 2) != 0;
     const double ua = unit53(second_pair ? b.w2 : b.w0);
     const double ub = unit53(second_pair ? b.w3 : b.w1);

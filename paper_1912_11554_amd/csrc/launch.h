@@ -97,11 +97,14 @@ struct SamplerArgs {
     uint64_t seed;
     int64_t first_iter;
     int adapt_diag;
+    int adapt_step;           // dual-averaging step size during warmup
+    double target_accept;     // its target acceptance
     const double* init_q;     // [C][D] or null
     double* out_samples;      // [C][S][D] or null
     nuts_stats* out_stats;    // [C][S] or null
     double* out_final_q;      // [C][D] or null
     double* out_inv_mass;     // [C][D] or null
+    double* out_step_size;    // [C] or null
     unsigned long long* grad_evals;  // [C]
 };
 
@@ -212,6 +215,13 @@ bool wave_resident_f32(const SamplerArgs& a);
 bool wave_resident_f64(const SamplerArgs& a);
 const void* grid_kernel_f32(const DataView& dv);
 const void* grid_kernel_f64(const DataView& dv);
+// The same with warmup step-size adaptation compiled in (sampler_adapt_*.hip).
+hipError_t launch_sampler_wave_adapt_f32(const SamplerArgs& a, hipStream_t stream);
+hipError_t launch_sampler_wave_adapt_f64(const SamplerArgs& a, hipStream_t stream);
+const void* grid_kernel_adapt_f32(const DataView& dv);
+const void* grid_kernel_adapt_f64(const DataView& dv);
+// Whether a launch needs the kernels with the adaptation.
+inline bool sampler_adapts(const SamplerArgs& a) { return a.adapt_step && a.num_warmup > 0; }
 constexpr int kGridWaves = 16;  // per group: 1 controller + 15 workers
 
 }  // namespace nuts

@@ -6,7 +6,7 @@ namespace nuts {
 
 hipError_t launch_sampler_wave_f32(const SamplerArgs& a, hipStream_t stream)
 {
-    return sampler::wave_launch_split<float>(a, stream);
+    return sampler::wave_launch_split<float, false>(a, stream);
 }
 
 bool wave_resident_f32(const SamplerArgs& a)
@@ -16,7 +16,7 @@ bool wave_resident_f32(const SamplerArgs& a)
 
 const void* grid_kernel_f32(const DataView& dv)
 {
-    return sampler::grid_kernel_for<float>(dv);
+    return sampler::grid_kernel_for<float, false>(dv);
 }
 
 }  // namespace nuts

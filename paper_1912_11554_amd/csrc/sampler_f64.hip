@@ -6,7 +6,7 @@ namespace nuts {
 
 hipError_t launch_sampler_wave_f64(const SamplerArgs& a, hipStream_t stream)
 {
-    return sampler::wave_launch_split<double>(a, stream);
+    return sampler::wave_launch_split<double, false>(a, stream);
 }
 
 bool wave_resident_f64(const SamplerArgs& a)
@@ -16,7 +16,7 @@ bool wave_resident_f64(const SamplerArgs& a)
 
 const void* grid_kernel_f64(const DataView& dv)
 {
-    return sampler::grid_kernel_for<double>(dv);
+    return sampler::grid_kernel_for<double, false>(dv);
 }
 
 }  // namespace nuts

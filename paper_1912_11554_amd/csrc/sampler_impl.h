@@ -398,9 +398,132 @@ __device__ __forceinline__ void copy_node(Node<DPL>& dst, const Node<DPL>& src)
     dst = src;
 }
 
+// ---------------------------------------------------------------------------
+// Warmup adaptation of the step size (Hoffman & Gelman 2014: Alg. 4 to start,
+// dual averaging of Section 3.2 per warmup iteration) and the windowed
+// diagonal mass that goes with it.  Scalars are wave-uniform; every lane (and
+// every controller of the grid path) computes the same bits.
+
+constexpr double kLn2 = 0.69314718055994530942;
+constexpr int kStepTrials = 100;
+constexpr double kDaGamma = 0.05, kDaT0 = 10.0, kDaKappa = 0.75;
+
+struct DualAvg {
+    double mu, hbar, log_eps, log_eps_bar;
+    int64_t m;
+
+    __device__ void start(double eps)
+    {
+        mu = log(10.0 * eps);
+        hbar = 0.0;
+        log_eps = log(eps);
+        log_eps_bar = 0.0;
+        m = 0;
+    }
+    // One update with accept statistic alpha; returns the next step size.
+    __device__ double update(double alpha, double delta)
+    {
+#pragma clang fp contract(off)
+        m += 1;
+        const double mm = (double)m;
+        const double w = 1.0 / (mm + kDaT0);
+        hbar = (1.0 - w) * hbar + w * (delta - alpha);
+        log_eps = mu - (sqrt(mm) / kDaGamma) * hbar;
+        const double eta = pow(mm, -kDaKappa);
+        log_eps_bar = eta * log_eps + (1.0 - eta) * log_eps_bar;
+        return exp(log_eps);
+    }
+};
+
+// log of the density kept by one leapfrog step of size e from (cur.q, r):
+// H0 - H', or -inf when H' is not a number.
+template <int DPL, class Eval>
+__device__ double step_log_ratio(Eval& ev, const Node<DPL>& cur, const double (&r)[DPL], double e,
+                                 const double (&im)[DPL], double H0)
+{
+    Node<DPL> z = cur;
+    double ph[DPL];
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        ph[m] = r[m] - 0.5 * e * z.g[m];
+        z.q[m] = z.q[m] + e * im[m] * ph[m];
+    }
+    ev.eval(z.q, z.U, z.g);
+    double k2 = 0.0;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        z.p[m] = ph[m] - 0.5 * e * z.g[m];
+        k2 += im[m] * z.p[m] * z.p[m];
+    }
+    const double d = H0 - (z.U + 0.5 * wave_sum(k2));
+    return d == d ? d : -INFINITY;
+}
+
+// Alg. 4: from eps, double (the step keeps more than half the density) or
+// halve (it does not) until that flips; the momentum is drawn under
+// kTagStepSize at counter t.  Adds the gradient evaluations to *evals.
+template <int DPL, class Eval>
+__device__ double find_step_size(Eval& ev, const Node<DPL>& cur, double eps, const double (&im)[DPL],
+                                 const bool (&act)[DPL], uint64_t seed, uint64_t chain, uint64_t t,
+                                 unsigned long long* evals)
+{
+    const int l = lane();
+    double r[DPL], kin = 0.0;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        const double xi = act[m] ? momentum_normal(seed, chain, t, l + 64 * m, kTagStepSize) : 0.0;
+        r[m] = act[m] ? xi / sqrt(im[m]) : 0.0;
+        kin += im[m] * r[m] * r[m];
+    }
+    const double H0 = cur.U + 0.5 * wave_sum(kin);
+    double d = step_log_ratio<DPL>(ev, cur, r, eps, im, H0);
+    *evals += 1;
+    const double a = d > -kLn2 ? 1.0 : -1.0;
+    for (int k = 0; k < kStepTrials && a * (d + kLn2) > 0.0 && !ev.aborted(); ++k) {
+        eps = a > 0.0 ? eps * 2.0 : eps * 0.5;
+        d = step_log_ratio<DPL>(ev, cur, r, eps, im, H0);
+        *evals += 1;
+    }
+    return eps;
+}
+
+// The slow windows of the windowed mass adaptation for W warmup iterations:
+// an initial buffer, windows of base, 2 base, ... iterations, the last one
+// stretched to the terminal buffer when a doubled window after it would not
+// fit.  next() moves to the following window.
+struct MassWindows {
+    int64_t start, end, size, slow_end;
+    bool any;
+
+    __device__ void init(int64_t W)
+    {
+        int64_t init = 75, term = 50, base = 25;
+        if (init + term + base > W) {
+            init = (int64_t)(0.15 * (double)W);
+            term = (int64_t)(0.10 * (double)W);
+            base = W - (init + term);
+        }
+        any = W >= 20;
+        slow_end = W - term;
+        start = init;
+        size = base;
+        end = stretch(start + size);
+    }
+    __device__ int64_t stretch(int64_t e) const { return e + 2 * size > slow_end ? slow_end : e; }
+    __device__ void next()
+    {
+        start = end;
+        size *= 2;
+        end = stretch(start + size);
+        any = start < slow_end;
+    }
+};
+
 // The whole chain: init, warmup + sampling iterations, outputs.  S_arr points
 // to this chain's checkpoint array in LDS: [max(max_depth, 1)][2][D].
-template <int DPL, class Eval>
+// ADAPT = false compiles the warmup adaptation of the step size out (the
+// kernels without it keep their registers for the tree and the data pass).
+template <int DPL, bool ADAPT, class Eval>
 __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double* S_arr)
 {
     const int l = lane();
@@ -409,7 +532,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
 #pragma unroll
     for (int m = 0; m < DPL; ++m) act[m] = l + 64 * m < D;
     const int maxd = A.max_depth;
-    const double eps = A.step_size;
+    double eps = A.step_size;
     const uint64_t seed = A.seed;
     const int64_t cidx = A.chain_offset + chain;
     const uint64_t key_chain = (uint64_t)cidx;
@@ -434,6 +557,17 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     for (int m = 0; m < DPL; ++m) wmean[m] = wm2[m] = 0.0;
     int64_t wn = 0;
     const int64_t iters = A.num_warmup + A.num_samples;
+
+    // warmup adaptation of the step size, with windowed mass if asked
+    const bool adapt = ADAPT && A.adapt_step && A.num_warmup > 0;
+    DualAvg da;
+    MassWindows win;
+    win.any = false;
+    if (adapt) {
+        eps = find_step_size<DPL>(ev, cur, eps, im, act, seed, key_chain, (uint64_t)A.first_iter, &evals);
+        da.start(eps);
+        if (A.adapt_diag) win.init(A.num_warmup);
+    }
 
     for (int64_t k = 0; k < iters && !ev.aborted(); ++k) {
         const uint64_t t = (uint64_t)(A.first_iter + k);
@@ -588,8 +722,39 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         evals += (unsigned long long)nleaves;
         cur = prop;
 
+        if (adapt && k < A.num_warmup) {
+            const double alpha = nleaves > 0 ? sum_acc / (double)nleaves : 0.0;
+            eps = da.update(alpha, A.target_accept);
+            if (win.any && k >= win.start && k < win.end) {
+                ++wn;
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) {
+                    const double d1 = cur.q[m] - wmean[m];
+                    wmean[m] += d1 / (double)wn;
+                    wm2[m] += d1 * (cur.q[m] - wmean[m]);
+                }
+            }
+            if (win.any && k == win.end - 1) {
+                if (wn >= 2) {
+                    const double nn = (double)wn;
+#pragma unroll
+                    for (int m = 0; m < DPL; ++m)
+                        im[m] = act[m] ? (nn / (nn + 5.0)) * (wm2[m] / (nn - 1.0)) + 1e-3 * (5.0 / (nn + 5.0))
+                                       : 1.0;
+                }
+                wn = 0;
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) wmean[m] = wm2[m] = 0.0;
+                win.next();
+                eps = find_step_size<DPL>(ev, cur, eps, im, act, seed, key_chain,
+                                          (uint64_t)(A.first_iter + k + 1), &evals);
+                da.start(eps);
+            }
+            if (k == A.num_warmup - 1) eps = exp(da.log_eps_bar);
+        }
+
         // diagonal inverse mass from warmup states in [W/2, W)
-        if (A.adapt_diag && k < A.num_warmup && k >= A.num_warmup / 2) {
+        if (!adapt && A.adapt_diag && k < A.num_warmup && k >= A.num_warmup / 2) {
             ++wn;
 #pragma unroll
             for (int m = 0; m < DPL; ++m) {
@@ -598,7 +763,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 wm2[m] += d1 * (cur.q[m] - wmean[m]);
             }
         }
-        if (A.adapt_diag && k == A.num_warmup - 1 && wn >= 2) {
+        if (!adapt && A.adapt_diag && k == A.num_warmup - 1 && wn >= 2) {
             const double nn = (double)wn;
             double var[DPL], tot = 0.0;
 #pragma unroll
@@ -650,6 +815,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             if (act[m] && A.out_inv_mass) A.out_inv_mass[cidx * D + l + 64 * m] = im[m];
         }
         if (l == 0) A.grad_evals[cidx] = evals;
+        if (l == 0 && A.out_step_size) A.out_step_size[cidx] = eps;
     }
 }
 
@@ -683,7 +849,7 @@ struct WaveLds {
 // group first copies its chains' data sets into LDS (one barrier) and every
 // gradient evaluation then streams from LDS; a group is then one per CU, so
 // the register budget is the whole wave's share of the SIMD.
-template <typename T, int S, int CPS, bool RESIDENT>
+template <typename T, int S, int CPS, bool RESIDENT, bool ADAPT>
 __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3) sampler_wave_kernel(SamplerArgs A,
                                                                                                    int cpg)
 {
@@ -741,10 +907,10 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     ev.D = D;
     ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
     ev.prior_const = (double)D * (log(A.prior_scale) + kHalfLog2Pi);
-    run_chain<1>(A, ev, chain, S_arr);
+    run_chain<1, ADAPT>(A, ev, chain, S_arr);
 }
 
-template <typename T, int S, int CPS, int DPL>
+template <typename T, int S, int CPS, int DPL, bool ADAPT>
 __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(SamplerArgs A, int groups,
                                                                             double* partials, double* result,
                                                                             GridSync* sync)
@@ -770,7 +936,7 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
         ev.prior_const = (double)A.data.D * (log(A.prior_scale) + kHalfLog2Pi);
         ev.step = 0;
         ev.abort = false;
-        run_chain<DPL>(A, ev, 0, lds);
+        run_chain<DPL, ADAPT>(A, ev, 0, lds);
         ev.finish();
     } else {
         unsigned long long step = 0;
@@ -786,18 +952,18 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
 }
 
 // Kernel for a data shape (S, CPS, DPL as pass_shape gives them).
-template <typename T>
+template <typename T, bool ADAPT>
 const void* grid_kernel_for(const DataView& dv)
 {
     const int D = dv.D;
-    if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1>;
-    if (D <= 16) return (const void*)sampler_grid_kernel<T, 1, 16, 1>;
-    if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1>;
-    if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1>;
-    if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2>;
-    if (D <= 192) return (const void*)sampler_grid_kernel<T, 32, 8, 3>;
-    if (D <= 256) return (const void*)sampler_grid_kernel<T, 32, 8, 4>;
-    return (const void*)sampler_grid_kernel<T, 32, 10, 5>;
+    if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1, ADAPT>;
+    if (D <= 16) return (const void*)sampler_grid_kernel<T, 1, 16, 1, ADAPT>;
+    if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1, ADAPT>;
+    if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1, ADAPT>;
+    if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2, ADAPT>;
+    if (D <= 192) return (const void*)sampler_grid_kernel<T, 32, 8, 3, ADAPT>;
+    if (D <= 256) return (const void*)sampler_grid_kernel<T, 32, 8, 4, ADAPT>;
+    return (const void*)sampler_grid_kernel<T, 32, 10, 5, ADAPT>;
 }
 
 // Chains per group of the LDS-resident variant (the most of 4, 2, 1 whose
@@ -813,24 +979,25 @@ int resident_chains_per_group(const SamplerArgs& a)
     return 0;
 }
 
-template <typename T, int S, int CPS>
+template <typename T, int S, int CPS, bool ADAPT>
 hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
 {
     using G = WaveLds<T, S, CPS>;
     const int cpg = resident_chains_per_group<T, S, CPS>(a);
     if (cpg > 0) {
         const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg);
-        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true>;
+        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true, ADAPT>;
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         const unsigned grid = (unsigned)((a.num_chains + cpg - 1) / cpg);
-        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true>), dim3(grid), dim3(kWaveChainsPerGroup * kWave), lds,
-                           stream, a, cpg);
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true, ADAPT>), dim3(grid),
+                           dim3(kWaveChainsPerGroup * kWave), lds, stream, a, cpg);
     } else {
         const int c4 = kWaveChainsPerGroup;
         const unsigned grid = (unsigned)((a.num_chains + c4 - 1) / c4);
-        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false>), dim3(grid), dim3(kWaveChainsPerGroup * kWave),
-                           G::bytes(a.data.D, a.data.nb, a.max_depth, false, c4), stream, a, c4);
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false, ADAPT>), dim3(grid),
+                           dim3(kWaveChainsPerGroup * kWave), G::bytes(a.data.D, a.data.nb, a.max_depth, false, c4),
+                           stream, a, c4);
     }
     return hipGetLastError();
 }
@@ -847,15 +1014,15 @@ bool wave_resident_split(const SamplerArgs& a)
     return resident_chains_per_group<T, 8, 8>(a) > 0;
 }
 
-template <typename T>
+template <typename T, bool ADAPT>
 hipError_t wave_launch_split(const SamplerArgs& a, hipStream_t stream)
 {
     if (a.data.split == 1) {
-        if (a.data.cols == 16) return wave_launch<T, 1, 16>(a, stream);
-        return wave_launch<T, 1, 8>(a, stream);
+        if (a.data.cols == 16) return wave_launch<T, 1, 16, ADAPT>(a, stream);
+        return wave_launch<T, 1, 8, ADAPT>(a, stream);
     }
-    if (a.data.split == 4) return wave_launch<T, 4, 8>(a, stream);
-    return wave_launch<T, 8, 8>(a, stream);
+    if (a.data.split == 4) return wave_launch<T, 4, 8, ADAPT>(a, stream);
+    return wave_launch<T, 8, 8, ADAPT>(a, stream);
 }
 
 }  // namespace sampler
