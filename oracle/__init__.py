@@ -109,6 +109,9 @@ def lib():
         L.orc_find_step_size_at.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, P, dbl, u64, u64,
                                             u64, P]
         L.orc_find_step_size_at.restype = dbl
+        L.orc_log_likelihood.argtypes = [P, P, i64, i64, P, i64, P, P]
+        L.orc_expected_log_likelihood.argtypes = [P, i64]
+        L.orc_expected_log_likelihood.restype = dbl
         _lib = L
     return _lib
 
@@ -300,3 +303,23 @@ def find_step_size(X, y, q, eps, *, seed, chain=0, t=0, inv_mass=None, prior_sca
                                     noise_scale, _p(im), _p(_f64(q)), eps, seed, chain, t,
                                     ctypes.byref(ev))
     return e, ev.value
+
+
+# ------------------------------------------- log-likelihood over draws -----
+def log_likelihood(X, y, W):
+    """Per-draw log-likelihood ll [S] and posterior predictive mean
+    P(y_i = 1) averaged over the draws [N] (Section 3.2), fp64 sums."""
+    X = _f64(X)
+    N, D = X.shape
+    W = _f64(W).reshape(-1, D)
+    S = W.shape[0]
+    ll = np.zeros(S)
+    pm = np.zeros(N)
+    lib().orc_log_likelihood(_p(X), _p(_u8(y)), N, D, _p(W), S, _p(ll), _p(pm))
+    return ll, pm
+
+
+def expected_log_likelihood(ll):
+    """logsumexp(ll) - log S."""
+    ll = _f64(ll)
+    return lib().orc_expected_log_likelihood(_p(ll), ll.shape[0])

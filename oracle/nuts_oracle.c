@@ -210,6 +210,41 @@ double orc_logistic_ug(const double *X, const uint8_t *y, int64_t N, int64_t D, 
     return U;
 }
 
+/* Log-likelihood over a batch of draws (Section 3.2, the vectorised
+ * log-likelihood and posterior predictive of the Fig. 1 logistic model):
+ *   ll[s]        = sum_i log p(y_i | x_i, w_s) = -sum_i softplus((1 - 2 y_i) eta_is),
+ *   pred_mean[i] = (1/S) sum_s sigmoid(eta_is)   (may be NULL),
+ * eta_is = x_i . w_s; W is [S][D].  Plain sums in index order.           */
+void orc_log_likelihood(const double *X, const uint8_t *y, int64_t N, int64_t D, const double *W,
+                        int64_t S, double *ll, double *pred_mean)
+{
+    for (int64_t s = 0; s < S; ++s) ll[s] = 0.0;
+    for (int64_t i = 0; i < N; ++i) {
+        const double *xi = X + i * D;
+        double psum = 0.0;
+        for (int64_t s = 0; s < S; ++s) {
+            const double *w = W + s * D;
+            double eta = 0.0;
+            for (int64_t j = 0; j < D; ++j) eta += xi[j] * w[j];
+            double sgn = y[i] ? -1.0 : 1.0;
+            ll[s] -= orc_softplus(sgn * eta);
+            psum += orc_sigmoid(eta);
+        }
+        if (pred_mean) pred_mean[i] = psum / (double)S;
+    }
+}
+
+/* The expected log-likelihood over the draws: log((1/S) sum_s exp(ll[s])),
+ * i.e. logsumexp(ll) - log S, with the largest term factored out. */
+double orc_expected_log_likelihood(const double *ll, int64_t S)
+{
+    double m = -INFINITY;
+    for (int64_t s = 0; s < S; ++s) m = ll[s] > m ? ll[s] : m;
+    double acc = 0.0;
+    for (int64_t s = 0; s < S; ++s) acc += exp(ll[s] - m);
+    return m + log(acc) - log((double)S);
+}
+
 /* Conjugate linear-Gaussian target used to pin the sampler's statistics:
  *   U(w) = sum_i (y_i - x_i . w)^2 / (2 sn^2) + sum_j w_j^2 / (2 s^2) + const,
  * whose posterior is N(mu, Sigma), Sigma = (X^T X / sn^2 + I / s^2)^-1,
