@@ -132,6 +132,21 @@ int nuts_potential_grad(nuts_handle* h, const void* X, const uint8_t* y, int64_t
                         int dtype, double prior_scale, const double* w, double* out_U,
                         double* out_grad);
 
+/* Log-likelihood of the model at S draws W [S][D] (Section 3.2: the
+ * vectorised log-likelihood and posterior predictive of the Fig. 1 logistic
+ * model, mapped over posterior draws):
+ *   out_ll[s]        = sum_i log p(y_i | x_i, w_s) = -sum_i softplus((1 - 2 y_i) x_i . w_s),
+ *   out_elpd[0]      = log((1/S) sum_s exp(out_ll[s]))        (may be NULL),
+ *   out_pred_mean[i] = (1/S) sum_s sigmoid(x_i . w_s), [N]    (may be NULL).
+ * fp32 data with D <= 132: one pass of matrix-core products over X per 128
+ * draws (E = X W^T, fp32 products and row terms, fp64 sums); otherwise the
+ * streaming potential kernel per draw (fp64 data keeps fp64 arithmetic),
+ * and then out_pred_mean must be NULL (NUTS_EUNSUPPORTED).  One shared data
+ * set (NUTS_EINVAL for per-chain data); 1 <= S <= 65535; W, out_ll and the
+ * other outputs may be host or device memory. */
+int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W, int64_t S, double* out_ll,
+                             double* out_elpd, double* out_pred_mean);
+
 /* Options of nuts_sample_data; a NULL pointer means all defaults. */
 typedef struct {
     const double* init_q;      /* [C][D] start positions, or NULL for zeros */

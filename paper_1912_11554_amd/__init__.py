@@ -24,7 +24,7 @@ NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID, NUTS_PATH_BATCH = 0, 1, 2, 3
 EXPORTED = [
     "nuts_init", "nuts_free", "nuts_last_error", "nuts_data_create", "nuts_data_free",
     "nuts_data_potential_grad", "nuts_data_potential_grad_batched", "nuts_potential_grad",
-    "nuts_sample_data", "nuts_sample",
+    "nuts_data_log_likelihood", "nuts_sample_data", "nuts_sample",
 ]
 
 STATS_DTYPE = np.dtype([
@@ -100,6 +100,8 @@ def load_library():
     L.nuts_data_potential_grad_batched.restype = i32
     L.nuts_potential_grad.argtypes = [P, P, P, i64, i64, i32, dbl, P, P, P]
     L.nuts_potential_grad.restype = i32
+    L.nuts_data_log_likelihood.argtypes = [P, P, P, i64, P, P, P]
+    L.nuts_data_log_likelihood.restype = i32
     L.nuts_sample_data.argtypes = [P, P, u32, dbl, dbl, P, i32, i64, i64, i64, u64, P, P,
                                    ctypes.POINTER(_Opts)]
     L.nuts_sample_data.restype = i32
@@ -222,6 +224,21 @@ class Data:
             self.free()
         except Exception:
             pass
+
+    def log_likelihood(self, W, pred_mean=False, out_ll=None):
+        """Per-draw log-likelihood ll [S], the expected log-likelihood
+        log mean exp(ll), and (pred_mean=True) the mean over the draws of
+        P(y_i = 1) [N], for draws W [S, D] (numpy or device tensor)."""
+        if isinstance(W, np.ndarray):
+            W = np.ascontiguousarray(W, dtype=np.float64).reshape(-1, self.D)
+        S = W.shape[0]
+        if out_ll is None:
+            out_ll = np.zeros(S)
+        elpd = np.zeros(1)
+        pm = np.zeros(self.N) if pred_mean else None
+        self.s._check(self.s._L.nuts_data_log_likelihood(self.s._h, self._d, _ptr(W), S, _ptr(out_ll),
+                                                         _ptr(elpd), _ptr(pm)))
+        return out_ll, float(elpd[0]), pm
 
     def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None, batched=False):
         """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor).

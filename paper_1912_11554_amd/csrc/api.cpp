@@ -447,6 +447,65 @@ int nuts_data_potential_grad_batched(nuts_handle* h, const nuts_data* d, double 
     return NUTS_OK;
 }
 
+int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W, int64_t S, double* out_ll,
+                             double* out_elpd, double* out_pred_mean)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (!W || !out_ll) return fail(h, NUTS_EINVAL, "W and out_ll must be non-NULL");
+    if (S < 1 || S > kMaxPotentialItems)
+        return fail(h, NUTS_EINVAL, "S must be in [1, %d] (got %lld)", kMaxPotentialItems, (long long)S);
+    if (d->view.nds != 1) return fail(h, NUTS_EINVAL, "the log-likelihood takes one shared data set");
+    if (d->view.N < 1) return fail(h, NUTS_EINVAL, "the log-likelihood needs N >= 1");
+    DeviceScope ds(h->device);
+    const int D = d->view.D;
+    const int64_t N = d->view.N;
+    int kt = 0, tc = 0;
+    const bool mfma = d->view.dtype == NUTS_F32 && batch_shape(D, &kt, &tc);
+    if (!mfma && out_pred_mean)
+        return fail(h, NUTS_EUNSUPPORTED, "the predictive mean takes fp32 data with D <= %d", 16 * kBatchMaxKT + 4);
+    DevBuf wt, lt, et, pt;
+    const void* Wd = nullptr;
+    void *Ld = nullptr, *Ed = nullptr, *Pd = nullptr;
+    HIP_TRY(h, stage_in(W, (size_t)S * D * 8, wt, &Wd, h->stream));
+    HIP_TRY(h, stage_out(out_ll, (size_t)S * 8, lt, &Ld));
+    HIP_TRY(h, stage_out(out_elpd, 8, et, &Ed));
+    HIP_TRY(h, stage_out(out_pred_mean, (size_t)N * 8, pt, &Pd));
+    if (mfma) {
+        const int rc = ensure_batch_layout(h, d);
+        if (rc != NUTS_OK) return rc;
+        const BatchPlan plan = plan_batch_potential(d->batch, S, h->num_cu);
+        const size_t lbytes = align256((size_t)plan.tiles * plan.groups * kBatchTileChains * sizeof(double));
+        const size_t rbytes = out_pred_mean ? (size_t)plan.tiles * d->batch.ns * kBatchStageRows * sizeof(float) : 0;
+        void* scratch = nullptr;
+        HIP_TRY(h, handle_scratch(h, lbytes + rbytes, &scratch));
+        HIP_TRY(h, launch_batch_log_likelihood(d->batch, (const double*)Wd, S, plan, (double*)scratch,
+                                               (float*)((char*)scratch + lbytes), (double*)Ld, (double*)Pd,
+                                               h->stream));
+    } else {
+        // the potential at prior scale 1 per draw, then the prior taken off
+        const PotentialPlan plan = plan_potential(d->view, S, h->num_cu);
+        const size_t pbytes = align256((size_t)S * plan.groups_per_item * plan.width * sizeof(double));
+        const size_t ubytes = align256((size_t)S * sizeof(double));
+        void* scratch = nullptr;
+        HIP_TRY(h, handle_scratch(h, pbytes + ubytes + (size_t)S * D * sizeof(double), &scratch));
+        double* U = (double*)((char*)scratch + pbytes);
+        double* G = (double*)((char*)scratch + pbytes + ubytes);
+        unsigned int* counts = nullptr;
+        HIP_TRY(h, potential_counts(h, &counts));
+        HIP_TRY(h, launch_potential_grad(d->view, 1.0, (const double*)Wd, S, plan, (double*)scratch, counts, U, G,
+                                         h->stream));
+        HIP_TRY(h, launch_ll_from_potential(D, (const double*)Wd, S, U, (double*)Ld, h->stream));
+    }
+    if (out_elpd) HIP_TRY(h, launch_expected_ll((const double*)Ld, S, (double*)Ed, h->stream));
+    HIP_TRY(h, finish_out(out_ll, (size_t)S * 8, lt, h->stream));
+    HIP_TRY(h, finish_out(out_elpd, 8, et, h->stream));
+    HIP_TRY(h, finish_out(out_pred_mean, (size_t)N * 8, pt, h->stream));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    return NUTS_OK;
+}
+
 int nuts_potential_grad(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype,
                         double prior_scale, const double* w, double* out_U, double* out_grad)
 {

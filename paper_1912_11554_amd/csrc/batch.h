@@ -251,6 +251,136 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
     }
 }
 
+// ---------------------------------------------------------------------------
+// Log-likelihood over draws: the column contraction E = X Q alone, then per
+// (row, position) the loss and, with PRED, sigma(eta) summed over the
+// positions of each row.
+
+// loss = softplus(t) as in row_terms; p1 = sigmoid(eta) (the probability of
+// y = 1): sigma(t) when y = 0 (t = eta), sigma(-t) when y = 1 (t = -eta).
+__device__ __forceinline__ void ll_terms(float eta, float sgn, float& loss, float& p1)
+{
+    const float t = sgn * eta;
+    const float e = __builtin_amdgcn_exp2f(-fabsf(t) * 1.4426950408889634f);
+    const float u = 1.0f + e;
+    const float inv = __builtin_amdgcn_rcpf(u);
+    loss = __builtin_fmaf(kLn2f, __builtin_amdgcn_logf(u), fmaxf(t, 0.0f));
+    const float sig_t = t >= 0.0f ? inv : e * inv;
+    const float sig_mt = t >= 0.0f ? e * inv : inv;
+    p1 = sgn > 0.0f ? sig_t : sig_mt;
+}
+
+// Sum over the 16 positions of a wave (lanes l, l ^ 1, ..., l ^ 15 share the
+// row group l / 16); every lane of the 16 gets the same bits.
+__device__ __forceinline__ float sum16(float v)
+{
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 8);
+    return v;
+}
+
+// One LDS stage for this wave's 16 positions: the loss of every live
+// (row, position) into `loss`; with PRED, the wave's sums of sigma(eta) over
+// its live positions for each of the 64 rows into rs[0..63].
+template <int KT, bool PRED>
+__device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, const float* __restrict__ ys,
+                                                 const WaveQ& Q, float live, double& loss, float* rs)
+{
+    using G = Geo<KT>;
+    const int l = lane();
+    const int m = l & 15;
+    const int jj = l >> 4;
+    const int e_off = m * G::RS + (G::KP == 8 ? 12 * (jj >> 1) + 4 * (jj & 1) : 4 * jj);
+    constexpr int e_step = G::KP == 8 ? 24 : 16;
+#pragma unroll 1
+    for (int tp = 0; tp < kTiles; tp += 2) {
+        const float* x0 = xs + tp * kTileRows * G::RS;
+        const float* x1 = x0 + kTileRows * G::RS;
+        v4f e0 = {0.0f, 0.0f, 0.0f, 0.0f};
+        v4f e1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int t = 0; t < G::KP; ++t) {
+            const v4f a0 = *reinterpret_cast<const v4f*>(x0 + e_off + e_step * t);
+            const v4f a1 = *reinterpret_cast<const v4f*>(x1 + e_off + e_step * t);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                e0 = mfma(a0[i], Q.q[4 * t + i], e0);
+                e1 = mfma(a1[i], Q.q[4 * t + i], e1);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const v4f xr0 = *reinterpret_cast<const v4f*>(x0 + (4 * jj + r) * G::RS + 16 * G::GS);
+            const v4f xr1 = *reinterpret_cast<const v4f*>(x1 + (4 * jj + r) * G::RS + 16 * G::GS);
+            e0[r] += ((xr0[0] * Q.qt[0] + xr0[1] * Q.qt[1]) + xr0[2] * Q.qt[2]) + xr0[3] * Q.qt[3];
+            e1[r] += ((xr1[0] * Q.qt[0] + xr1[1] * Q.qt[1]) + xr1[2] * Q.qt[2]) + xr1[3] * Q.qt[3];
+        }
+        const v4f s0 = *reinterpret_cast<const v4f*>(ys + tp * kTileRows + 4 * jj);
+        const v4f s1 = *reinterpret_cast<const v4f*>(ys + (tp + 1) * kTileRows + 4 * jj);
+        float lsum = 0.0f;
+        float p0[4], p1[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float l0, l1;
+            ll_terms(e0[r], s0[r], l0, p0[r]);
+            ll_terms(e1[r], s1[r], l1, p1[r]);
+            lsum += l0 + l1;
+        }
+        loss += (double)lsum;
+        if constexpr (PRED) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float a = sum16(live * p0[r]);
+                const float b = sum16(live * p1[r]);
+                if (m == 0) {
+                    rs[tp * kTileRows + 4 * jj + r] = a;
+                    rs[(tp + 1) * kTileRows + 4 * jj + r] = b;
+                }
+            }
+        }
+    }
+}
+
+// Stage loop of the log-likelihood: as stage_loop, and with PRED the eight
+// waves' row sums of each stage (rs[buffer][wave][64]) are added in wave
+// order and stored to prow[stage * 64 + row] one stage later, after the
+// barrier that ends it.
+template <int KT, bool PRED>
+__device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, int64_t st1, int tid, float* xs,
+                                              float* ys, float* rs, const WaveQ& Q, float live, double& loss,
+                                              float* prow)
+{
+    const int widx = tid / kWave;
+    auto flush = [&](int64_t st, int b) {
+        if (PRED && tid < kBatchStageRows) {
+            float s_ = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s_ += rs[(b * kWaves + w) * kBatchStageRows + tid];
+            prow[st * kBatchStageRows + tid] = s_;
+        }
+    };
+    if (st0 < st1) {
+        StageRegs r;
+        load_stage(bv, st0, tid, r);
+        store_stage<KT>(r, tid, xs, ys);
+    }
+    __syncthreads();
+    for (int64_t st = st0; st < st1; ++st) {
+        const int b = (int)((st - st0) & 1);
+        const bool more = st + 1 < st1;
+        StageRegs r;
+        if (more) load_stage(bv, st + 1, tid, r);
+        if (st > st0) flush(st - 1, b ^ 1);
+        compute_stage_ll<KT, PRED>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, live, loss,
+                                   rs + (b * kWaves + widx) * kBatchStageRows);
+        if (more) store_stage<KT>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
+        __syncthreads();
+    }
+    if (st1 > st0) flush(st1 - 1, (int)((st1 - 1 - st0) & 1));
+}
+
 // The stage loop over [st0, st1) with double-buffered LDS stages.  Workers
 // (tid = loader index, 0 .. 511) load and compute; a non-worker wave of the
 // same group passes the same workgroup barriers (1 + st1 - st0 of them) and

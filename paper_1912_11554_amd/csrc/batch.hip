@@ -244,6 +244,127 @@ hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const
 }
 
 // ---------------------------------------------------------------------------
+// Log-likelihood over a batch of draws (fp32 matrix cores): one pass over X
+// per tile of 128 draws computing E = X W^T, then per draw the negative log
+// likelihood summed in fp64 (partial rows per group, added in group order by
+// the finish kernel), and optionally per row the sum of sigmoid(eta) over
+// the tile's live draws (one fp32 value per row and tile, added over tiles in
+// fp64 in order).
+
+namespace {
+
+template <int KT, bool PRED>
+__global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_ll_kernel(BatchView bv, const double* __restrict__ W,
+                                                                           int64_t S, int groups,
+                                                                           double* __restrict__ L,
+                                                                           float* __restrict__ Pr)
+{
+    __shared__ __align__(16) float xs[2 * batch::kStageBuf];
+    __shared__ __align__(16) float ys[2 * kBatchStageRows];
+    __shared__ float rs[PRED ? 2 * batch::kWaves * kBatchStageRows : 1];
+    const int l = lane();
+    const int m = l & 15;
+    const int jj = l >> 4;
+    const int widx = threadIdx.x / kWave;
+    const int g = blockIdx.x;
+    const int t = blockIdx.y;
+    const int D = bv.D;
+    const int64_t pos = (int64_t)t * kBatchTileChains + widx * 16 + m;
+    const bool live = pos < S;
+
+    WaveQ Q;
+    constexpr int KP = batch::Geo<KT>::KP;
+#pragma unroll
+    for (int c = 0; c < KP; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int col = batch::e_column<KT>(c, jj, i);
+            const bool used = (col / 16) < KT && col < D;
+            Q.q[4 * c + i] = (live && used) ? (float)W[pos * D + col] : 0.0f;
+        }
+#pragma unroll
+    for (int k = 0; k < batch::kTail; ++k)
+        Q.qt[k] = (live && k < bv.tc) ? (float)W[pos * D + 16 * KT + k] : 0.0f;
+
+    double loss = 0.0;
+    const int64_t st0 = (int64_t)g * bv.ns / groups;
+    const int64_t st1 = (int64_t)(g + 1) * bv.ns / groups;
+    batch::stage_loop_ll<KT, PRED>(bv, st0, st1, (int)threadIdx.x, xs, ys, rs, Q, live ? 1.0f : 0.0f, loss,
+                                   Pr + (int64_t)t * bv.ns * kBatchStageRows);
+    // the four lanes of a position hold its four row groups
+    loss += __shfl_xor(loss, 16);
+    loss += __shfl_xor(loss, 32);
+    if (jj == 0) L[((int64_t)t * groups + g) * kBatchTileChains + widx * 16 + m] = loss;
+}
+
+// ll[s] = -(sum over groups of the loss partials - the padding rows' ln 2).
+__global__ void __launch_bounds__(64) batch_ll_finish_kernel(int64_t S, int groups, int npad,
+                                                            const double* __restrict__ L,
+                                                            double* __restrict__ out_ll)
+{
+    const int64_t s = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (s >= S) return;
+    const int64_t t = s / kBatchTileChains;
+    const double* src = L + t * groups * kBatchTileChains + s % kBatchTileChains;
+    double tot = 0.0;
+    for (int g = 0; g < groups; ++g) tot += src[(int64_t)g * kBatchTileChains];
+    out_ll[s] = -(tot - (double)npad * (double)batch::kLn2f);
+}
+
+// pred_mean[i] = (sum over tiles of the row sums) / S.
+__global__ void __launch_bounds__(256) batch_pred_kernel(int64_t N, int64_t rows, int tiles, int64_t S,
+                                                        const float* __restrict__ Pr, double* __restrict__ out)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < N; i += (int64_t)gridDim.x * 256) {
+        double tot = 0.0;
+        for (int t = 0; t < tiles; ++t) tot += (double)Pr[(int64_t)t * rows + i];
+        out[i] = tot / (double)S;
+    }
+}
+
+template <int KT>
+void enqueue_ll(const BatchView& bv, const double* W, int64_t S, int tiles, int groups, double* L, float* Pr,
+                bool pred, hipStream_t stream)
+{
+    if (pred)
+        hipLaunchKernelGGL((batch_ll_kernel<KT, true>), dim3(groups, tiles), dim3(batch::kWaves * kWave), 0, stream,
+                           bv, W, S, groups, L, Pr);
+    else
+        hipLaunchKernelGGL((batch_ll_kernel<KT, false>), dim3(groups, tiles), dim3(batch::kWaves * kWave), 0,
+                           stream, bv, W, S, groups, L, Pr);
+}
+
+}  // namespace
+
+hipError_t launch_batch_log_likelihood(const BatchView& bv, const double* W, int64_t S, const BatchPlan& plan,
+                                       double* L, float* Pr, double* out_ll, double* out_pred, hipStream_t stream)
+{
+    const bool pred = out_pred != nullptr;
+    switch (bv.kt) {
+    case 0: enqueue_ll<0>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 1: enqueue_ll<1>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 2: enqueue_ll<2>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 3: enqueue_ll<3>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 4: enqueue_ll<4>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 5: enqueue_ll<5>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 6: enqueue_ll<6>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 7: enqueue_ll<7>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    case 8: enqueue_ll<8>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+    default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(batch_ll_finish_kernel, dim3((unsigned)((S + 63) / 64)), dim3(64), 0, stream, S, plan.groups,
+                       (int)(bv.ns * kBatchStageRows - bv.N), L, out_ll);
+    e = hipGetLastError();
+    if (e != hipSuccess || !pred) return e;
+    const int64_t want = (bv.N + 255) / 256;
+    hipLaunchKernelGGL(batch_pred_kernel, dim3((unsigned)(want < 4096 ? want : 4096)), dim3(256), 0, stream, bv.N,
+                       bv.ns * kBatchStageRows, plan.tiles, S, Pr, out_pred);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Persistent batched sampler.
 //
 // Tile t holds chain slots 0..127 and `groups` workgroups; group i of the

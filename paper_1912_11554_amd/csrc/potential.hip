@@ -178,6 +178,51 @@ void enqueue_shape(const DataView& dv, double prior_scale, const double* W, int6
 
 }  // namespace
 
+namespace {
+
+__global__ void __launch_bounds__(64) ll_from_potential_kernel(int D, const double* __restrict__ W, int64_t S,
+                                                              const double* __restrict__ U,
+                                                              double* __restrict__ out_ll)
+{
+    const int64_t s = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (s >= S) return;
+    double pr = 0.0;
+    for (int j = 0; j < D; ++j) pr += 0.5 * W[s * D + j] * W[s * D + j];
+    out_ll[s] = -(U[s] - pr - (double)D * kHalfLog2Pi);
+}
+
+// One wave: the largest term factored out, then the exponentials summed by
+// lane (draws l, l + 64, ... in order) and across lanes in a fixed order.
+__global__ void __launch_bounds__(64) expected_ll_kernel(const double* __restrict__ ll, int64_t S,
+                                                        double* __restrict__ out)
+{
+    const int l = lane();
+    double mx = -INFINITY;
+    for (int64_t s = l; s < S; s += 64) mx = fmax(mx, ll[s]);
+#pragma unroll
+    for (int b = 1; b < 64; b <<= 1) mx = fmax(mx, __shfl_xor(mx, b));
+    double acc = 0.0;
+    for (int64_t s = l; s < S; s += 64) acc += exp(ll[s] - mx);
+    acc = wave_sum(acc);
+    if (l == 0) *out = mx + log(acc) - log((double)S);
+}
+
+}  // namespace
+
+hipError_t launch_ll_from_potential(int D, const double* W, int64_t S, const double* U, double* out_ll,
+                                    hipStream_t stream)
+{
+    hipLaunchKernelGGL(ll_from_potential_kernel, dim3((unsigned)((S + 63) / 64)), dim3(64), 0, stream, D, W, S, U,
+                       out_ll);
+    return hipGetLastError();
+}
+
+hipError_t launch_expected_ll(const double* ll, int64_t S, double* out, hipStream_t stream)
+{
+    hipLaunchKernelGGL(expected_ll_kernel, dim3(1), dim3(64), 0, stream, ll, S, out);
+    return hipGetLastError();
+}
+
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
 {
     // one group per CU over all items, never more groups than the blocks give

@@ -2,10 +2,12 @@
 
     python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 1
     python -m paper_1912_11554_amd.microbench --workload shared256_n200000_d129_f32 --positions 256 --batched
+    python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 500 --loglik
 
 Each call evaluates U and grad U at K positions (around the data's generating
-weights) with the data already in device memory; the outputs stay on the
-device.  Prints one JSON line: microseconds per call (HIP events on the
+weights) with the data already in device memory (with --loglik: the
+log-likelihood of the K positions as draws, the expected log-likelihood and
+the predictive mean of every row); the outputs stay on the device.  Prints one JSON line: microseconds per call (HIP events on the
 stream the kernels run on; the C-ABI call is synchronous, so this includes
 its host side: pointer checks, launches, the final synchronisation), the
 algorithmic rate at that time (bytes of X and y per position for the
@@ -36,6 +38,9 @@ def main():
     ap.add_argument("--positions", type=int, default=1)
     ap.add_argument("--batched", action="store_true",
                     help="nuts_data_potential_grad_batched (fp32 matrix cores)")
+    ap.add_argument("--loglik", action="store_true",
+                    help="nuts_data_log_likelihood at the positions as draws (with the expected "
+                         "log-likelihood and the predictive mean)")
     ap.add_argument("--reps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--copy-mb", type=int, default=0,
@@ -67,22 +72,37 @@ def main():
     d = s.data(torch.from_numpy(X).cuda(), torch.from_numpy(y).cuda())
     U = torch.empty(K, dtype=torch.float64, device="cuda")
     G = torch.empty((K, wl.D), dtype=torch.float64, device="cuda")
+    if args.loglik:
+        pm = torch.empty(wl.N, dtype=torch.float64, device="cuda")
+        el = torch.empty(1, dtype=torch.float64, device="cuda")
+
+        def call():
+            s._check(s._L.nuts_data_log_likelihood(s._h, d._d, W.data_ptr(), K, U.data_ptr(),
+                                                   el.data_ptr(), pm.data_ptr()))
+    else:
+        def call():
+            d.potential_grad(W, out_U=U, out_grad=G, batched=args.batched)
     for _ in range(args.warmup):
-        d.potential_grad(W, out_U=U, out_grad=G, batched=args.batched)
+        call()
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(args.reps):
-        d.potential_grad(W, out_U=U, out_grad=G, batched=args.batched)
+        call()
     e1.record(stream)
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) * 1e3 / args.reps
     es = 8 if wl.dtype == "f64" else 4
-    out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K,
-               kernel="batch_pass_kernel" if args.batched else "potential_grad_kernel",
+    kernel = ("batch_ll_kernel" if args.loglik else
+              "batch_pass_kernel" if args.batched else "potential_grad_kernel")
+    out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K, kernel=kernel,
                reps=args.reps, us_per_call_with_host=round(us, 2))
-    if args.batched:
+    if args.loglik:
+        tflops = 2.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12   # E = X W^T only
+        out.update(bound="mfma", achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
+                   frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4))
+    elif args.batched:
         tflops = 4.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12
         out.update(bound="mfma", achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
                    frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4))
