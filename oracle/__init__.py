@@ -95,13 +95,15 @@ def lib():
         L.orc_check_range.argtypes = [u64, P, P]
         L.orc_nuts_chain.argtypes = [
             i32, P, P, P, i64, i64, dbl, dbl, dbl, P, i32, i64, i64, u64, u64, i32, i32, P,
-            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P,
+            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P, i32,
         ]
         L.orc_nuts_chain.restype = i64
         L.orc_leapfrog_steps.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, dbl, i64, P, P]
         L.orc_leapfrog_steps.restype = dbl
         L.orc_is_uturn_exported.argtypes = [P, P, P, P, i32, P, i64]
         L.orc_is_uturn_exported.restype = i32
+        L.orc_is_uturn_gen_exported.argtypes = [P, P, P, P, i64]
+        L.orc_is_uturn_gen_exported.restype = i32
         L.orc_normals_tagged.argtypes = [u64, u64, u64, u64, i64, P]
         L.orc_dual_avg_run.argtypes = [dbl, dbl, i64, P, P, P]
         L.orc_mass_windows.argtypes = [i64, P, i32]
@@ -226,13 +228,15 @@ def leapfrog(X, y, q, p, h, nsteps, inv_mass=None, prior_scale=1.0, target=TARGE
 def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chain=0,
          prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
          init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
-         trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8):
+         trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8,
+         uturn_generalized=False):
     """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
     final_q [D], inv_mass [D], step_size (the one in use at the end: the
     adapted one with adapt_step_size), grad_evals; with trace_cap the U-turn check
     trace as (first_leaf, last_leaf) pairs; with leaves_cap the generated
     leaves as records (j, n, position, H - H0).  ``sel_salt`` (test only)
-    re-keys the proposal-selection draws and nothing else."""
+    re-keys the proposal-selection draws and nothing else.  uturn_generalized
+    selects the momentum-sum criterion (reading R20)."""
     X = _f64(X)
     N, D = X.shape
     samples = np.zeros((num_samples, D), dtype=np.float64)
@@ -251,7 +255,7 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
         _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
         ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
         ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
-        ctypes.byref(eps_out),
+        ctypes.byref(eps_out), 1 if uturn_generalized else 0,
     )
     out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im,
                step_size=eps_out.value, grad_evals=nev)
@@ -323,3 +327,12 @@ def expected_log_likelihood(ll):
     """logsumexp(ll) - log S."""
     ll = _f64(ll)
     return lib().orc_expected_log_likelihood(_p(ll), ll.shape[0])
+
+
+def is_uturn_generalized(rho, pa, pb, inv_mass=None):
+    """Reading R20's test on a (sub)trajectory with momentum sum rho and end
+    momenta pa, pb."""
+    rho, pa, pb = (_f64(a) for a in (rho, pa, pb))
+    D = rho.shape[0]
+    im = _f64(np.ones(D) if inv_mass is None else inv_mass)
+    return bool(lib().orc_is_uturn_gen_exported(_p(rho), _p(pa), _p(pb), _p(im), D))

@@ -56,6 +56,13 @@
  *       below 20); at each window end the inverse mass is the regularised
  *       variance of the window's states (weight 5/(n+5) towards 1e-3, not
  *       normalised) and the heuristic and dual averaging restart.
+ *   R20 generalised U-turn criterion (optional; Betancourt 2017, App. A.4.2):
+ *       a (sub)trajectory with momentum sum rho over all its points turns
+ *       iff rho . M^-1 p <= 0 at either end.  The iterative builder keeps in
+ *       S[BitCount(n)] the leaf's momentum and the subtree's momentum sum
+ *       before that leaf, so the sum over leaves k..n is a difference of
+ *       running sums; the trajectory test uses the sum over every point
+ *       including the start.
  */
 #include <math.h>
 #include <stdint.h>
@@ -378,6 +385,24 @@ static int orc_is_uturn(const double *qa, const double *pa, const double *qb, co
     return (dl < 0.0) || (dr < 0.0);
 }
 
+/* Reading R20: rho . M^-1 p_a <= 0 or rho . M^-1 p_b <= 0 (either end). */
+static int orc_is_uturn_gen(const double *rho, const double *pa, const double *pb,
+                            const double *inv_mass, int64_t D)
+{
+    double da = 0.0, db = 0.0;
+    for (int64_t j = 0; j < D; ++j) {
+        da += rho[j] * inv_mass[j] * pa[j];
+        db += rho[j] * inv_mass[j] * pb[j];
+    }
+    return (da <= 0.0) || (db <= 0.0);
+}
+
+int orc_is_uturn_gen_exported(const double *rho, const double *pa, const double *pb,
+                              const double *inv_mass, int64_t D)
+{
+    return orc_is_uturn_gen(rho, pa, pb, inv_mass, D);
+}
+
 int orc_is_uturn_exported(const double *qa, const double *pa, const double *qb, const double *pb,
                           int v, const double *inv_mass, int64_t D)
 {
@@ -419,6 +444,8 @@ typedef struct {
     /* per-iteration totals */
     int64_t nleaves;
     double sum_accept;
+    /* reading R20: the generalised criterion instead of the endpoint one */
+    int gen;
 } orc_iter;
 
 /* What a subtree hands back: the streaming proposal and its log-weight. */
@@ -429,6 +456,7 @@ typedef struct {
     orc_node prop;
     int64_t prop_idx;     /* signed leaf offset of the proposal from q0 */
     int has_prop;
+    double *rho;          /* momentum sum over the subtree's leaves (R20) */
 } orc_sub;
 
 static void orc_trace_check(orc_iter *it, int64_t first, int64_t last)
@@ -488,12 +516,22 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
     double *Sp = (double *)malloc((size_t)nslots * (size_t)D * sizeof(double));
     int64_t S_leaf[64];
     int64_t nleaf = (int64_t)1 << j;
+    /* R20: running momentum sum of the subtree's leaves; the slots then hold
+     * (sum before the leaf, the leaf's momentum) instead of (q, p) */
+    double *rsum = sub->rho;
+    double *rho = (double *)malloc((size_t)D * sizeof(double));
+    for (int64_t k = 0; k < D; ++k) rsum[k] = 0.0;
     for (int64_t n = 0; n < nleaf; ++n) {
         orc_leapfrog(it->tg, z, (double)v * it->eps, it->inv_mass);
         if (orc_leaf(it, sub, z, j, n, e, v) != ORC_OK) break;
+        for (int64_t k = 0; k < D; ++k) rsum[k] += z->p[k];
         if ((n & 1) == 0) {
             int i = orc_bitcount((uint64_t)n);
-            memcpy(Sq + (int64_t)i * D, z->q, (size_t)D * sizeof(double));
+            if (it->gen) {
+                for (int64_t k = 0; k < D; ++k) Sq[(int64_t)i * D + k] = rsum[k] - z->p[k];
+            } else {
+                memcpy(Sq + (int64_t)i * D, z->q, (size_t)D * sizeof(double));
+            }
             memcpy(Sp + (int64_t)i * D, z->p, (size_t)D * sizeof(double));
             S_leaf[i] = n;
         } else {
@@ -502,8 +540,15 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
             int turned = 0;
             for (int k = i_max; k >= i_min; --k) {
                 orc_trace_check(it, S_leaf[k], n);
-                if (orc_is_uturn(Sq + (int64_t)k * D, Sp + (int64_t)k * D, z->q, z->p, v,
-                                 it->inv_mass, D)) {
+                int t;
+                if (it->gen) {
+                    for (int64_t c = 0; c < D; ++c) rho[c] = rsum[c] - Sq[(int64_t)k * D + c];
+                    t = orc_is_uturn_gen(rho, Sp + (int64_t)k * D, z->p, it->inv_mass, D);
+                } else {
+                    t = orc_is_uturn(Sq + (int64_t)k * D, Sp + (int64_t)k * D, z->q, z->p, v,
+                                     it->inv_mass, D);
+                }
+                if (t) {
                     turned = 1;
                     break;
                 }
@@ -515,6 +560,7 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
             }
         }
     }
+    free(rho);
     free(Sq);
     free(Sp);
 }
@@ -524,7 +570,7 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
  * the left half and the last leaf of the right half.  Leaves are numbered
  * from `offset`; the first leaf's (q, p) is returned in fq/fp. */
 static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t offset, int v,
-                                int64_t e, orc_sub *sub, double *fq, double *fp)
+                                int64_t e, orc_sub *sub, double *fq, double *fp, double *rho)
 {
     int64_t D = it->tg->D;
     if (d == 0) {
@@ -532,20 +578,26 @@ static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t
         orc_leaf(it, sub, z, j, offset, e, v);
         memcpy(fq, z->q, (size_t)D * sizeof(double));
         memcpy(fp, z->p, (size_t)D * sizeof(double));
+        memcpy(rho, z->p, (size_t)D * sizeof(double));
         return;
     }
-    orc_build_recursive(it, z, j, d - 1, offset, v, e, sub, fq, fp);
+    orc_build_recursive(it, z, j, d - 1, offset, v, e, sub, fq, fp, rho);
     if (sub->status != ORC_OK) return;
     double *rq = (double *)malloc((size_t)D * sizeof(double));
     double *rp = (double *)malloc((size_t)D * sizeof(double));
+    double *rr = (double *)malloc((size_t)D * sizeof(double));
     int64_t half = (int64_t)1 << (d - 1);
-    orc_build_recursive(it, z, j, d - 1, offset + half, v, e, sub, rq, rp);
+    orc_build_recursive(it, z, j, d - 1, offset + half, v, e, sub, rq, rp, rr);
+    for (int64_t k = 0; k < D; ++k) rho[k] += rr[k];
     free(rq);
     free(rp);
+    free(rr);
     if (sub->status != ORC_OK) return;
     int64_t last = offset + 2 * half - 1;
     orc_trace_check(it, offset, last);
-    if (orc_is_uturn(fq, fp, z->q, z->p, v, it->inv_mass, D)) {
+    int t = it->gen ? orc_is_uturn_gen(rho, fp, z->p, it->inv_mass, D)
+                    : orc_is_uturn(fq, fp, z->q, z->p, v, it->inv_mass, D);
+    if (t) {
         sub->status = ORC_TURNING;
         sub->term_leaf = last;
     }
@@ -594,8 +646,12 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
 
     orc_sub sub;
     orc_node_alloc(&sub.prop, D);
+    sub.rho = (double *)malloc((size_t)D * sizeof(double));
     double *fq = (double *)malloc((size_t)D * sizeof(double));
     double *fp = (double *)malloc((size_t)D * sizeof(double));
+    /* R20: momentum sum over every point of the trajectory */
+    double *rho_traj = (double *)malloc((size_t)D * sizeof(double));
+    memcpy(rho_traj, cur->p, (size_t)D * sizeof(double));
 
     memset(st, 0, sizeof(*st));
     st->term_leaf = -1;
@@ -610,7 +666,7 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
         sub.prop_idx = 0;
         sub.has_prop = 0;
         if (builder == ORC_BUILDER_RECURSIVE)
-            orc_build_recursive(it, &z, j, j, 0, v, e, &sub, fq, fp);
+            orc_build_recursive(it, &z, j, j, 0, v, e, &sub, fq, fp, sub.rho);
         else
             orc_build_iterative(it, &z, j, v, e, &sub);
         st->tree_depth = j + 1;
@@ -630,7 +686,9 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
         logw_traj = orc_logaddexp(logw_traj, sub.logw);
         if (v > 0) { orc_node_copy(&right, &z, D); Rpos += (int64_t)1 << j; }
         else       { orc_node_copy(&left, &z, D);  Lpos -= (int64_t)1 << j; }
-        if (orc_is_uturn(left.q, left.p, right.q, right.p, +1, im, D)) {
+        for (int64_t k = 0; k < D; ++k) rho_traj[k] += sub.rho[k];
+        if (it->gen ? orc_is_uturn_gen(rho_traj, left.p, right.p, im, D)
+                    : orc_is_uturn(left.q, left.p, right.q, right.p, +1, im, D)) {
             st->turning = 1;
             st->term_leaf = -2;
             break;
@@ -645,6 +703,8 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
     st->energy = cur->U + orc_kinetic(cur->p, im, D);
 
     free(fq); free(fp);
+    free(rho_traj);
+    free(sub.rho);
     orc_node_free(&sub.prop);
     orc_node_free(&left); orc_node_free(&right);
     orc_node_free(&prop); orc_node_free(&z);
@@ -807,7 +867,8 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
                        double *out_q, double *out_inv_mass, int64_t *trace,
                        int64_t trace_cap, int64_t *trace_len, int64_t *leaves,
                        int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt,
-                       int adapt_step, double target_accept, double *out_step_size)
+                       int adapt_step, double target_accept, double *out_step_size,
+                       int uturn_gen)
 {
     orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
     double *im = (double *)malloc((size_t)D * sizeof(double));
@@ -830,6 +891,7 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
     it.leaves = leaves;
     it.leaves_cap = leaves_cap;
     it.sel_salt = sel_salt;
+    it.gen = uturn_gen;
 
     orc_welford wf = { 0, (double *)calloc((size_t)D, sizeof(double)),
                        (double *)calloc((size_t)D, sizeof(double)) };
