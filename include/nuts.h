@@ -56,8 +56,9 @@ enum { NUTS_F64 = 0, NUTS_F32 = 1 };
 
 enum {
     NUTS_DATA_PER_CHAIN = 1u << 0,  /* X is [C][N][D] and y is [C][N]; else one shared data set */
-    NUTS_ADAPT_DIAG_MASS = 1u << 1,  /* set the diagonal inverse mass from warmup draws */
-    NUTS_ADAPT_STEP_SIZE = 1u << 3   /* adapt the step size during warmup (dual averaging) */
+    NUTS_ADAPT_DIAG_MASS = 1u << 1,    /* set the diagonal inverse mass from warmup draws */
+    NUTS_UTURN_GENERALIZED = 1u << 2,  /* U-turn on momentum sums (Betancourt 2017, App. A.4.2) */
+    NUTS_ADAPT_STEP_SIZE = 1u << 3     /* adapt the step size during warmup (dual averaging) */
 };
 
 /* Kernel path selection for nuts_sample_data (opts->path). */
@@ -191,6 +192,13 @@ typedef struct {
  * Writes out_samples [C][S][D] fp64 and out_stats [C][S] (either may be
  * NULL).  Divergences are not errors.  NUTS_EINVAL for target_accept outside
  * (0, 1). */
+/* NUTS_UTURN_GENERALIZED replaces Hoffman & Gelman's endpoint test (the
+ * default; the paper's Alg. 1/2 leave the criterion open) by the
+ * generalised one: a subtree or the whole trajectory turns when the
+ * momentum sum rho over its points has rho . M^-1 p <= 0 at either end.  The
+ * iterative builder then keeps in S[BitCount(n)] the leaf's momentum and the
+ * subtree's momentum sum before the leaf; the candidate set C(n) is
+ * unchanged. */
 int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double prior_scale,
                      double step_size, const double* inv_mass_diag, int max_tree_depth,
                      int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libnuts.so")
 
 NUTS_OK, NUTS_EINVAL, NUTS_ENOMEM, NUTS_EDEVICE, NUTS_EUNSUPPORTED = 0, -1, -2, -3, -4
 NUTS_F64, NUTS_F32 = 0, 1
-NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS, NUTS_ADAPT_STEP_SIZE = 1, 2, 8
+NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS, NUTS_UTURN_GENERALIZED, NUTS_ADAPT_STEP_SIZE = 1, 2, 4, 8
 NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID, NUTS_PATH_BATCH = 0, 1, 2, 3
 
 EXPORTED = [
@@ -259,7 +259,7 @@ class Data:
     def sample(self, *, step_size, max_tree_depth, num_warmup, num_samples, num_chains=1,
                seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None,
-               adapt_step_size=False, target_accept=0.8):
+               adapt_step_size=False, target_accept=0.8, uturn_generalized=False):
         """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
         (STATS_DTYPE), final_q [C, D], inv_mass [C, D], step_size [C] (in use
         at the end: the adapted one with adapt_step_size), grad_evals.  Outputs
@@ -268,7 +268,8 @@ class Data:
         C, D = num_chains, self.D
         flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
             NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
-            NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0)
+            NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0) | (
+            NUTS_UTURN_GENERALIZED if uturn_generalized else 0)
         if out_samples is None:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:

@@ -528,7 +528,8 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     std::memset(&o, 0, sizeof o);
     if (opts) o = *opts;
     if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
-    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE))
+    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE |
+                            NUTS_UTURN_GENERALIZED))
         return fail(h, NUTS_EINVAL, "unknown flag bits 0x%x", flags);
     const double target_accept = o.target_accept == 0.0 ? 0.8 : o.target_accept;
     if (!(target_accept > 0.0 && target_accept < 1.0))
@@ -632,6 +633,7 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     a.first_iter = o.first_iter;
     a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
     a.adapt_step = (flags & NUTS_ADAPT_STEP_SIZE) ? 1 : 0;
+    a.uturn_gen = (flags & NUTS_UTURN_GENERALIZED) ? 1 : 0;
     a.target_accept = target_accept;
     a.init_q = (const double*)iq_d;
     a.out_samples = (double*)smp_d;

@@ -664,7 +664,7 @@ struct BatchEval {
     }
 };
 
-template <int KT, int DPL, bool ADAPT>
+template <int KT, int DPL, bool EXT>
 __global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(SamplerArgs A, BatchView bv,
                                                                               int tiles, int groups, float* qbuf,
                                                                               float* P, double* L,
@@ -696,7 +696,7 @@ __global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(S
         ev.abort = false;
         const int64_t chain = (int64_t)c.t * kBatchTileChains + c.i;
         const bool host = c.i < kBatchTileChains;
-        if (host && chain < A.num_chains) sampler::run_chain<DPL, ADAPT>(A, ev, chain, lds);
+        if (host && chain < A.num_chains) sampler::run_chain<DPL, EXT>(A, ev, chain, lds);
         ev.finish(host);
     } else {
         double q[DPL], r[DPL + 1];
@@ -708,24 +708,24 @@ __global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(S
 }
 
 // Kernel for a shape: KT chunks (0..8) and DPL = ceil(D / 64) (1..3); the
-// pairs that occur for D <= 132; ADAPT compiles the warmup step-size
+// pairs that occur for D <= 132; EXT compiles the warmup step-size
 // adaptation in.
-template <bool ADAPT>
+template <bool EXT>
 const void* batch_kernel_for_t(const BatchView& bv)
 {
     const int dpl = (bv.D + 63) / 64;
     switch (bv.kt * 4 + dpl) {
-    case 0 * 4 + 1: return (const void*)sampler_batch_kernel<0, 1, ADAPT>;
-    case 1 * 4 + 1: return (const void*)sampler_batch_kernel<1, 1, ADAPT>;
-    case 2 * 4 + 1: return (const void*)sampler_batch_kernel<2, 1, ADAPT>;
-    case 3 * 4 + 1: return (const void*)sampler_batch_kernel<3, 1, ADAPT>;
-    case 4 * 4 + 1: return (const void*)sampler_batch_kernel<4, 1, ADAPT>;
-    case 4 * 4 + 2: return (const void*)sampler_batch_kernel<4, 2, ADAPT>;
-    case 5 * 4 + 2: return (const void*)sampler_batch_kernel<5, 2, ADAPT>;
-    case 6 * 4 + 2: return (const void*)sampler_batch_kernel<6, 2, ADAPT>;
-    case 7 * 4 + 2: return (const void*)sampler_batch_kernel<7, 2, ADAPT>;
-    case 8 * 4 + 2: return (const void*)sampler_batch_kernel<8, 2, ADAPT>;
-    case 8 * 4 + 3: return (const void*)sampler_batch_kernel<8, 3, ADAPT>;
+    case 0 * 4 + 1: return (const void*)sampler_batch_kernel<0, 1, EXT>;
+    case 1 * 4 + 1: return (const void*)sampler_batch_kernel<1, 1, EXT>;
+    case 2 * 4 + 1: return (const void*)sampler_batch_kernel<2, 1, EXT>;
+    case 3 * 4 + 1: return (const void*)sampler_batch_kernel<3, 1, EXT>;
+    case 4 * 4 + 1: return (const void*)sampler_batch_kernel<4, 1, EXT>;
+    case 4 * 4 + 2: return (const void*)sampler_batch_kernel<4, 2, EXT>;
+    case 5 * 4 + 2: return (const void*)sampler_batch_kernel<5, 2, EXT>;
+    case 6 * 4 + 2: return (const void*)sampler_batch_kernel<6, 2, EXT>;
+    case 7 * 4 + 2: return (const void*)sampler_batch_kernel<7, 2, EXT>;
+    case 8 * 4 + 2: return (const void*)sampler_batch_kernel<8, 2, EXT>;
+    case 8 * 4 + 3: return (const void*)sampler_batch_kernel<8, 3, EXT>;
     default: return nullptr;
     }
 }
@@ -764,7 +764,7 @@ hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int t
     SamplerArgs A = a;
     BatchView B = bv;
     void* args[] = {&A, &B, &tiles, &groups, &qbuf, &P, &L, &sync};
-    const void* k = batch_kernel_for(bv, sampler_adapts(a));
+    const void* k = batch_kernel_for(bv, sampler_extended(a));
     if (!k) return hipErrorInvalidValue;
     return hipLaunchCooperativeKernel(k, dim3((unsigned)(tiles * groups)),
                                       dim3(kGroupWaves * kWave), args, (unsigned)batch_sampler_lds(a), stream);

@@ -99,6 +99,7 @@ struct SamplerArgs {
     int adapt_diag;
     int adapt_step;           // dual-averaging step size during warmup
     double target_accept;     // its target acceptance
+    int uturn_gen;            // the generalised (momentum-sum) U-turn criterion
     const double* init_q;     // [C][D] or null
     double* out_samples;      // [C][S][D] or null
     nuts_stats* out_stats;    // [C][S] or null
@@ -228,13 +229,14 @@ bool wave_resident_f32(const SamplerArgs& a);
 bool wave_resident_f64(const SamplerArgs& a);
 const void* grid_kernel_f32(const DataView& dv);
 const void* grid_kernel_f64(const DataView& dv);
-// The same with warmup step-size adaptation compiled in (sampler_adapt_*.hip).
-hipError_t launch_sampler_wave_adapt_f32(const SamplerArgs& a, hipStream_t stream);
-hipError_t launch_sampler_wave_adapt_f64(const SamplerArgs& a, hipStream_t stream);
-const void* grid_kernel_adapt_f32(const DataView& dv);
-const void* grid_kernel_adapt_f64(const DataView& dv);
+// The same with the optional features compiled in: warmup step-size
+// adaptation, the generalised U-turn criterion (sampler_ext_*.hip).
+hipError_t launch_sampler_wave_ext_f32(const SamplerArgs& a, hipStream_t stream);
+hipError_t launch_sampler_wave_ext_f64(const SamplerArgs& a, hipStream_t stream);
+const void* grid_kernel_ext_f32(const DataView& dv);
+const void* grid_kernel_ext_f64(const DataView& dv);
 // Whether a launch needs the kernels with the adaptation.
-inline bool sampler_adapts(const SamplerArgs& a) { return a.adapt_step && a.num_warmup > 0; }
+inline bool sampler_extended(const SamplerArgs& a) { return (a.adapt_step && a.num_warmup > 0) || a.uturn_gen; }
 constexpr int kGridWaves = 16;  // per group: 1 controller + 15 workers
 
 }  // namespace nuts

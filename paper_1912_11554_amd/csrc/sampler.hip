@@ -17,7 +17,7 @@ __global__ void fill_empty_slots(double* a, int64_t na, double* b, int64_t nb)
 
 const void* pick_grid_kernel(const DataView& dv, bool adapt)
 {
-    if (adapt) return dv.dtype == NUTS_F64 ? grid_kernel_adapt_f64(dv) : grid_kernel_adapt_f32(dv);
+    if (adapt) return dv.dtype == NUTS_F64 ? grid_kernel_ext_f64(dv) : grid_kernel_ext_f32(dv);
     return dv.dtype == NUTS_F64 ? grid_kernel_f64(dv) : grid_kernel_f32(dv);
 }
 
@@ -32,9 +32,9 @@ bool wave_path_resident(const SamplerArgs& a)
 
 hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream)
 {
-    if (sampler_adapts(a))
-        return a.data.dtype == NUTS_F64 ? launch_sampler_wave_adapt_f64(a, stream)
-                                        : launch_sampler_wave_adapt_f32(a, stream);
+    if (sampler_extended(a))
+        return a.data.dtype == NUTS_F64 ? launch_sampler_wave_ext_f64(a, stream)
+                                        : launch_sampler_wave_ext_f32(a, stream);
     return a.data.dtype == NUTS_F64 ? launch_sampler_wave_f64(a, stream) : launch_sampler_wave_f32(a, stream);
 }
 
@@ -70,7 +70,7 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
     if (e != hipSuccess) return e;
     const int slots = a.max_depth > 1 ? a.max_depth : 1;
     const size_t lds = (size_t)slots * 2 * a.data.D * sizeof(double);
-    const void* k = pick_grid_kernel(a.data, sampler_adapts(a));
+    const void* k = pick_grid_kernel(a.data, sampler_extended(a));
     SamplerArgs A = a;
     void* args[] = {&A, &groups, &partials, &result, &sync};
     return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);

@@ -72,6 +72,23 @@ __device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (
     return uni((dl < 0.0) || (dr < 0.0));
 }
 
+// Generalised criterion (Betancourt 2017, App. A.4.2): a (sub)trajectory
+// with momentum sum rho turns iff rho . M^-1 p <= 0 at either end.
+template <int DPL>
+__device__ __forceinline__ bool is_uturn_gen(const double (&rho)[DPL], const double (&pa)[DPL],
+                                             const double (&pb)[DPL], const double (&im)[DPL])
+{
+    double sa = 0.0, sb = 0.0;
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        sa += rho[m] * im[m] * pa[m];
+        sb += rho[m] * im[m] * pb[m];
+    }
+    const double da = wave_sum(sa);
+    const double db = wave_sum(sb);
+    return uni((da <= 0.0) || (db <= 0.0));
+}
+
 // Evaluator interface: eval(q, U, g) with q, g lane-per-dimension arrays;
 // s_writer() says whether this wave stores the checkpoint array S,
 // out_writer() whether it stores the chain's outputs; aborted() reports a
@@ -521,9 +538,10 @@ struct MassWindows {
 
 // The whole chain: init, warmup + sampling iterations, outputs.  S_arr points
 // to this chain's checkpoint array in LDS: [max(max_depth, 1)][2][D].
-// ADAPT = false compiles the warmup adaptation of the step size out (the
-// kernels without it keep their registers for the tree and the data pass).
-template <int DPL, bool ADAPT, class Eval>
+// EXT = false compiles the optional features out (warmup adaptation of the
+// step size, the generalised U-turn criterion): the kernels without them keep
+// their registers for the tree and the data pass.
+template <int DPL, bool EXT, class Eval>
 __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double* S_arr)
 {
     const int l = lane();
@@ -559,7 +577,10 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     const int64_t iters = A.num_warmup + A.num_samples;
 
     // warmup adaptation of the step size, with windowed mass if asked
-    const bool adapt = ADAPT && A.adapt_step && A.num_warmup > 0;
+    const bool adapt = EXT && A.adapt_step && A.num_warmup > 0;
+    // generalised criterion: the slots of S hold (momentum sum of the subtree
+    // before the leaf, the leaf's momentum) instead of (q, p)
+    const bool gen = EXT && A.uturn_gen;
     DualAvg da;
     MassWindows win;
     win.any = false;
@@ -581,6 +602,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             kin += im[m] * cur.p[m] * cur.p[m];
         }
         const double H0 = cur.U + 0.5 * wave_sum(kin);
+        double rho_traj[DPL];  // momentum sum over the trajectory's points
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) rho_traj[m] = cur.p[m];
 
         // per-iteration draws, one doubling per lane: direction bits and the
         // merge uniforms
@@ -614,6 +638,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             depth = j + 1;
             const int64_t nleaf = 1ll << j;
             double u_leaf = 0.0;
+            double rsum[DPL];  // momentum sum over the subtree's leaves so far
+#pragma unroll
+            for (int m = 0; m < DPL; ++m) rsum[m] = 0.0;
 
             for (int64_t n = 0; n < nleaf; ++n) {
                 if ((n & (kWave - 1)) == 0)
@@ -636,6 +663,10 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     k2 += im[m] * z.p[m] * z.p[m];
                 }
                 ++nleaves;
+                if (gen) {
+#pragma unroll
+                    for (int m = 0; m < DPL; ++m) rsum[m] += z.p[m];
+                }
 
                 const double dH = (z.U + 0.5 * wave_sum(k2)) - H0;
                 if (dH == dH) sum_acc += dH > 0.0 ? exp_nonpos(-dH) : 1.0;
@@ -661,7 +692,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
 #pragma unroll
                         for (int m = 0; m < DPL; ++m) {
                             if (act[m]) {
-                                S_arr[(2 * i) * D + l + 64 * m] = z.q[m];
+                                S_arr[(2 * i) * D + l + 64 * m] = gen ? rsum[m] - z.p[m] : z.q[m];
                                 S_arr[(2 * i + 1) * D + l + 64 * m] = z.p[m];
                             }
                         }
@@ -679,7 +710,16 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                             sq[m] = act[m] ? S_arr[(2 * kk) * D + l + 64 * m] : 0.0;
                             sp[m] = act[m] ? S_arr[(2 * kk + 1) * D + l + 64 * m] : 0.0;
                         }
-                        if (is_uturn<DPL>(sq, sp, z.q, z.p, v, im)) {
+                        bool t_;
+                        if (gen) {
+                            double rho[DPL];
+#pragma unroll
+                            for (int m = 0; m < DPL; ++m) rho[m] = rsum[m] - sq[m];
+                            t_ = is_uturn_gen<DPL>(rho, sp, z.p, im);
+                        } else {
+                            t_ = is_uturn<DPL>(sq, sp, z.q, z.p, v, im);
+                        }
+                        if (t_) {
                             turned = true;
                             break;
                         }
@@ -712,7 +752,15 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 left = z;
                 Lpos -= nleaf;
             }
-            if (is_uturn<DPL>(left.q, left.p, right.q, right.p, 1, im)) {
+            bool traj_turn;
+            if (gen) {
+#pragma unroll
+                for (int m = 0; m < DPL; ++m) rho_traj[m] += rsum[m];
+                traj_turn = is_uturn_gen<DPL>(rho_traj, left.p, right.p, im);
+            } else {
+                traj_turn = is_uturn<DPL>(left.q, left.p, right.q, right.p, 1, im);
+            }
+            if (traj_turn) {
                 turning = 1;
                 term = -2;
                 break;
@@ -849,7 +897,7 @@ struct WaveLds {
 // group first copies its chains' data sets into LDS (one barrier) and every
 // gradient evaluation then streams from LDS; a group is then one per CU, so
 // the register budget is the whole wave's share of the SIMD.
-template <typename T, int S, int CPS, bool RESIDENT, bool ADAPT>
+template <typename T, int S, int CPS, bool RESIDENT, bool EXT>
 __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3) sampler_wave_kernel(SamplerArgs A,
                                                                                                    int cpg)
 {
@@ -907,10 +955,10 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     ev.D = D;
     ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
     ev.prior_const = (double)D * (log(A.prior_scale) + kHalfLog2Pi);
-    run_chain<1, ADAPT>(A, ev, chain, S_arr);
+    run_chain<1, EXT>(A, ev, chain, S_arr);
 }
 
-template <typename T, int S, int CPS, int DPL, bool ADAPT>
+template <typename T, int S, int CPS, int DPL, bool EXT>
 __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(SamplerArgs A, int groups,
                                                                             double* partials, double* result,
                                                                             GridSync* sync)
@@ -936,7 +984,7 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
         ev.prior_const = (double)A.data.D * (log(A.prior_scale) + kHalfLog2Pi);
         ev.step = 0;
         ev.abort = false;
-        run_chain<DPL, ADAPT>(A, ev, 0, lds);
+        run_chain<DPL, EXT>(A, ev, 0, lds);
         ev.finish();
     } else {
         unsigned long long step = 0;
@@ -952,18 +1000,18 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
 }
 
 // Kernel for a data shape (S, CPS, DPL as pass_shape gives them).
-template <typename T, bool ADAPT>
+template <typename T, bool EXT>
 const void* grid_kernel_for(const DataView& dv)
 {
     const int D = dv.D;
-    if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1, ADAPT>;
-    if (D <= 16) return (const void*)sampler_grid_kernel<T, 1, 16, 1, ADAPT>;
-    if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1, ADAPT>;
-    if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1, ADAPT>;
-    if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2, ADAPT>;
-    if (D <= 192) return (const void*)sampler_grid_kernel<T, 32, 8, 3, ADAPT>;
-    if (D <= 256) return (const void*)sampler_grid_kernel<T, 32, 8, 4, ADAPT>;
-    return (const void*)sampler_grid_kernel<T, 32, 10, 5, ADAPT>;
+    if (D <= 8) return (const void*)sampler_grid_kernel<T, 1, 8, 1, EXT>;
+    if (D <= 16) return (const void*)sampler_grid_kernel<T, 1, 16, 1, EXT>;
+    if (D <= 32) return (const void*)sampler_grid_kernel<T, 4, 8, 1, EXT>;
+    if (D <= 64) return (const void*)sampler_grid_kernel<T, 8, 8, 1, EXT>;
+    if (D <= 128) return (const void*)sampler_grid_kernel<T, 16, 8, 2, EXT>;
+    if (D <= 192) return (const void*)sampler_grid_kernel<T, 32, 8, 3, EXT>;
+    if (D <= 256) return (const void*)sampler_grid_kernel<T, 32, 8, 4, EXT>;
+    return (const void*)sampler_grid_kernel<T, 32, 10, 5, EXT>;
 }
 
 // Chains per group of the LDS-resident variant (the most of 4, 2, 1 whose
@@ -979,23 +1027,23 @@ int resident_chains_per_group(const SamplerArgs& a)
     return 0;
 }
 
-template <typename T, int S, int CPS, bool ADAPT>
+template <typename T, int S, int CPS, bool EXT>
 hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
 {
     using G = WaveLds<T, S, CPS>;
     const int cpg = resident_chains_per_group<T, S, CPS>(a);
     if (cpg > 0) {
         const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg);
-        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true, ADAPT>;
+        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true, EXT>;
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         const unsigned grid = (unsigned)((a.num_chains + cpg - 1) / cpg);
-        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true, ADAPT>), dim3(grid),
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true, EXT>), dim3(grid),
                            dim3(kWaveChainsPerGroup * kWave), lds, stream, a, cpg);
     } else {
         const int c4 = kWaveChainsPerGroup;
         const unsigned grid = (unsigned)((a.num_chains + c4 - 1) / c4);
-        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false, ADAPT>), dim3(grid),
+        hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false, EXT>), dim3(grid),
                            dim3(kWaveChainsPerGroup * kWave), G::bytes(a.data.D, a.data.nb, a.max_depth, false, c4),
                            stream, a, c4);
     }
@@ -1014,15 +1062,15 @@ bool wave_resident_split(const SamplerArgs& a)
     return resident_chains_per_group<T, 8, 8>(a) > 0;
 }
 
-template <typename T, bool ADAPT>
+template <typename T, bool EXT>
 hipError_t wave_launch_split(const SamplerArgs& a, hipStream_t stream)
 {
     if (a.data.split == 1) {
-        if (a.data.cols == 16) return wave_launch<T, 1, 16, ADAPT>(a, stream);
-        return wave_launch<T, 1, 8, ADAPT>(a, stream);
+        if (a.data.cols == 16) return wave_launch<T, 1, 16, EXT>(a, stream);
+        return wave_launch<T, 1, 8, EXT>(a, stream);
     }
-    if (a.data.split == 4) return wave_launch<T, 4, 8, ADAPT>(a, stream);
-    return wave_launch<T, 8, 8, ADAPT>(a, stream);
+    if (a.data.split == 4) return wave_launch<T, 4, 8, EXT>(a, stream);
+    return wave_launch<T, 8, 8, EXT>(a, stream);
 }
 
 }  // namespace sampler
