@@ -237,6 +237,6 @@ const void* grid_kernel_ext_f32(const DataView& dv);
 const void* grid_kernel_ext_f64(const DataView& dv);
 // Whether a launch needs the kernels with the adaptation.
 inline bool sampler_extended(const SamplerArgs& a) { return (a.adapt_step && a.num_warmup > 0) || a.uturn_gen; }
-constexpr int kGridWaves = 16;  // per group: 1 controller + 15 workers
+constexpr int kGridWaves = 12;  // per group: 1 controller + 11 workers (3 waves per SIMD: 168 registers each)
 
 }  // namespace nuts
