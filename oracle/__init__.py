@@ -45,6 +45,7 @@ assert STATS_DTYPE.itemsize == 56
 
 TARGET_LOGISTIC = 0
 TARGET_LINGAUSS = 1
+TARGET_HMM = 2
 BUILDER_ITERATIVE = 0
 BUILDER_RECURSIVE = 1
 
@@ -95,7 +96,7 @@ def lib():
         L.orc_check_range.argtypes = [u64, P, P]
         L.orc_nuts_chain.argtypes = [
             i32, P, P, P, i64, i64, dbl, dbl, dbl, P, i32, i64, i64, u64, u64, i32, i32, P,
-            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P, i32,
+            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P, i32, P, i64, i32, i32,
         ]
         L.orc_nuts_chain.restype = i64
         L.orc_leapfrog_steps.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, dbl, i64, P, P]
@@ -112,6 +113,8 @@ def lib():
                                             u64, P]
         L.orc_find_step_size_at.restype = dbl
         L.orc_log_likelihood.argtypes = [P, P, i64, i64, P, i64, P, P]
+        L.orc_hmm_ug.argtypes = [P, i64, P, i64, i32, i32, P, P]
+        L.orc_hmm_ug.restype = dbl
         L.orc_expected_log_likelihood.argtypes = [P, i64]
         L.orc_expected_log_likelihood.restype = dbl
         _lib = L
@@ -229,16 +232,26 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
          prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
          init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
          trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8,
-         uturn_generalized=False):
+         uturn_generalized=False, hmm=None):
     """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
     final_q [D], inv_mass [D], step_size (the one in use at the end: the
     adapted one with adapt_step_size), grad_evals; with trace_cap the U-turn check
     trace as (first_leaf, last_leaf) pairs; with leaves_cap the generated
     leaves as records (j, n, position, H - H0).  ``sel_salt`` (test only)
     re-keys the proposal-selection draws and nothing else.  uturn_generalized
-    selects the momentum-sum criterion (reading R20)."""
-    X = _f64(X)
-    N, D = X.shape
+    selects the momentum-sum criterion (reading R20).  With hmm = dict(w, z,
+    K, V) the target is the semi-supervised HMM (reading R21) and X, y are
+    ignored."""
+    hz = None
+    if hmm is not None:
+        target = TARGET_HMM
+        y = _u8(hmm["w"])
+        hz = _u8(hmm["z"])
+        N, D = y.shape[0], hmm_dim(hmm["K"], hmm["V"])
+        X = np.zeros((1, D))
+    else:
+        X = _f64(X)
+        N, D = X.shape
     samples = np.zeros((num_samples, D), dtype=np.float64)
     stats = np.zeros(num_samples, dtype=STATS_DTYPE)
     final_q = np.zeros(D, dtype=np.float64)
@@ -255,7 +268,9 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
         _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
         ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
         ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
-        ctypes.byref(eps_out), 1 if uturn_generalized else 0,
+        ctypes.byref(eps_out), 1 if uturn_generalized else 0, _p(hz),
+        0 if hz is None else hz.shape[0], 0 if hmm is None else hmm["K"],
+        0 if hmm is None else hmm["V"],
     )
     out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im,
                step_size=eps_out.value, grad_evals=nev)
@@ -336,3 +351,20 @@ def is_uturn_generalized(rho, pa, pb, inv_mass=None):
     D = rho.shape[0]
     im = _f64(np.ones(D) if inv_mass is None else inv_mass)
     return bool(lib().orc_is_uturn_gen_exported(_p(rho), _p(pa), _p(pb), _p(im), D))
+
+
+# ------------------------------------------------------------------- HMM ----
+def hmm_dim(K, V):
+    """Unconstrained dimension: K (K - 1) transition logits, K (V - 1)
+    emission logits."""
+    return K * (K - 1) + K * (V - 1)
+
+
+def hmm_potential_grad(w, z, K, V, q):
+    """U and grad U of the semi-supervised HMM (reading R21) at logits q."""
+    w = _u8(w)
+    z = _u8(z)
+    q = _f64(q)
+    g = np.zeros(q.shape[0])
+    U = lib().orc_hmm_ug(_p(w), w.shape[0], _p(z), z.shape[0], K, V, _p(q), _p(g))
+    return U, g

@@ -276,7 +276,125 @@ double orc_lingauss_ug(const double *X, const double *yv, int64_t N, int64_t D, 
     return U;
 }
 
-enum { ORC_TARGET_LOGISTIC = 0, ORC_TARGET_LINGAUSS = 1 };
+/* Semi-supervised hidden Markov model (reading R21; the paper's HMM
+ * benchmark, Appendix C, after Stan's semi-supervised example): K hidden
+ * states, V observation symbols, one sequence w_1..w_T whose first Tsup
+ * hidden states z_1..z_Tsup are observed.  Parameters: the K transition rows
+ * theta_j and the K emission rows phi_k, each a simplex with a uniform
+ * Dirichlet prior, sampled on the unconstrained space of additive log-ratios
+ * (row x = softmax(a_0 .. a_{n-2}, 0), |Jacobian| = prod_i x_i).  q holds the
+ * K (K - 1) transition logits (row j at j (K - 1)), then the K (V - 1)
+ * emission logits (row k at K (K - 1) + k (V - 1)).  With
+ *   f(q) = sum over rows of sum_i log x_i                       (Jacobians)
+ *        + sum_{t <= Tsup} log phi_{z_t}(w_t) + sum_{2 <= t <= Tsup} log theta_{z_{t-1}}(z_t)
+ *        + log p(w_{Tsup+1..T} | z_Tsup)                     (forward algorithm),
+ * U = -f and grad U = -df/dq.  The forward recursion runs on scaled
+ * probabilities (alpha_t normalised, log p = sum_t log c_t), starting from
+ * theta_{z_Tsup} (uniform 1/K when Tsup = 0); the backward recursion gives
+ * the expected transition counts xi and state occupancies gamma, which are
+ * d log p / d log theta and d log p / d log phi.  Through the softmax,
+ * df/da_i = G_i - x_i sum_m G_m with G = df/d log x.                        */
+static void orc_softmax_row(const double *a, int n, double *x, double *lx)
+{
+    double m = 0.0;                               /* the fixed last logit */
+    for (int i = 0; i < n - 1; ++i) m = a[i] > m ? a[i] : m;
+    double tot = 0.0;
+    for (int i = 0; i < n; ++i) tot += exp((i < n - 1 ? a[i] : 0.0) - m);
+    double lse = m + log(tot);
+    for (int i = 0; i < n; ++i) {
+        lx[i] = (i < n - 1 ? a[i] : 0.0) - lse;
+        x[i] = exp(lx[i]);
+    }
+}
+
+double orc_hmm_ug(const uint8_t *w, int64_t T, const uint8_t *z, int64_t Tsup, int K, int V,
+                  const double *q, double *grad)
+{
+    const int nt = K * (K - 1);
+    double *th = (double *)malloc((size_t)K * K * sizeof(double));
+    double *lth = (double *)malloc((size_t)K * K * sizeof(double));
+    double *ph = (double *)malloc((size_t)K * V * sizeof(double));
+    double *lph = (double *)malloc((size_t)K * V * sizeof(double));
+    double *Gt = (double *)calloc((size_t)K * K, sizeof(double));
+    double *Gp = (double *)calloc((size_t)K * V, sizeof(double));
+    for (int j = 0; j < K; ++j) orc_softmax_row(q + j * (K - 1), K, th + j * K, lth + j * K);
+    for (int k = 0; k < K; ++k) orc_softmax_row(q + nt + k * (V - 1), V, ph + k * V, lph + k * V);
+
+    double f = 0.0;
+    /* Jacobians: each entry contributes log x_i and d/d log x_i = 1 */
+    for (int i = 0; i < K * K; ++i) { f += lth[i]; Gt[i] += 1.0; }
+    for (int i = 0; i < K * V; ++i) { f += lph[i]; Gp[i] += 1.0; }
+    /* the observed states */
+    for (int64_t t = 0; t < Tsup; ++t) {
+        f += lph[z[t] * V + w[t]];
+        Gp[z[t] * V + w[t]] += 1.0;
+        if (t > 0) {
+            f += lth[z[t - 1] * K + z[t]];
+            Gt[z[t - 1] * K + z[t]] += 1.0;
+        }
+    }
+    /* forward over t = Tsup .. T-1 (0-based) */
+    int64_t Tu = T - Tsup;
+    if (Tu > 0) {
+        double *al = (double *)malloc((size_t)(Tu + 1) * K * sizeof(double));
+        double *be = (double *)malloc((size_t)Tu * K * sizeof(double));
+        double *c = (double *)malloc((size_t)Tu * sizeof(double));
+        for (int k = 0; k < K; ++k) al[k] = Tsup > 0 ? (z[Tsup - 1] == k ? 1.0 : 0.0) : 1.0 / K;
+        for (int64_t s = 0; s < Tu; ++s) {
+            const int ws = w[Tsup + s];
+            const double *prev = al + s * K;
+            double *cur = al + (s + 1) * K;
+            double tot = 0.0;
+            for (int k = 0; k < K; ++k) {
+                double acc = 0.0;
+                if (s == 0 && Tsup == 0) acc = prev[k];  /* initial distribution, no transition */
+                else for (int j = 0; j < K; ++j) acc += prev[j] * th[j * K + k];
+                cur[k] = acc * ph[k * V + ws];
+                tot += cur[k];
+            }
+            c[s] = tot;
+            for (int k = 0; k < K; ++k) cur[k] /= tot;
+            f += log(tot);
+        }
+        /* backward (scaled by the same c) */
+        for (int k = 0; k < K; ++k) be[(Tu - 1) * K + k] = 1.0;
+        for (int64_t s = Tu - 2; s >= 0; --s) {
+            const int wn = w[Tsup + s + 1];
+            for (int j = 0; j < K; ++j) {
+                double acc = 0.0;
+                for (int k = 0; k < K; ++k) acc += th[j * K + k] * ph[k * V + wn] * be[(s + 1) * K + k];
+                be[s * K + j] = acc / c[s + 1];
+            }
+        }
+        /* expected counts */
+        for (int64_t s = 0; s < Tu; ++s) {
+            const int ws = w[Tsup + s];
+            const double *prev = al + s * K;
+            const double *cur = al + (s + 1) * K;
+            for (int k = 0; k < K; ++k) Gp[k * V + ws] += cur[k] * be[s * K + k];
+            if (s == 0 && Tsup == 0) continue;
+            for (int j = 0; j < K; ++j)
+                for (int k = 0; k < K; ++k)
+                    Gt[j * K + k] += prev[j] * th[j * K + k] * ph[k * V + ws] * be[s * K + k] / c[s];
+        }
+        free(al); free(be); free(c);
+    }
+    /* through the softmax of each row, then U = -f */
+    for (int j = 0; j < K; ++j) {
+        double tot = 0.0;
+        for (int k = 0; k < K; ++k) tot += Gt[j * K + k];
+        for (int k = 0; k < K - 1; ++k) grad[j * (K - 1) + k] = -(Gt[j * K + k] - th[j * K + k] * tot);
+    }
+    for (int k = 0; k < K; ++k) {
+        double tot = 0.0;
+        for (int v = 0; v < V; ++v) tot += Gp[k * V + v];
+        for (int v = 0; v < V - 1; ++v) grad[nt + k * (V - 1) + v] = -(Gp[k * V + v] - ph[k * V + v] * tot);
+    }
+    free(th); free(lth); free(ph); free(lph); free(Gt); free(Gp);
+    return -f;
+}
+
+enum { ORC_TARGET_LOGISTIC = 0, ORC_TARGET_LINGAUSS = 1, ORC_TARGET_HMM = 2 };
 
 typedef struct {
     int kind;
@@ -287,6 +405,10 @@ typedef struct {
     double s;             /* prior scale */
     double sn;            /* noise scale (linear-Gaussian) */
     int64_t nevals;       /* gradient evaluations performed */
+    /* HMM: the observations are y (N = T symbols), then these */
+    const uint8_t *z;     /* the Tsup observed hidden states */
+    int64_t Tsup;
+    int K, V;
 } orc_target;
 
 static double orc_eval(orc_target *tg, const double *w, double *grad)
@@ -294,6 +416,8 @@ static double orc_eval(orc_target *tg, const double *w, double *grad)
     tg->nevals++;
     if (tg->kind == ORC_TARGET_LINGAUSS)
         return orc_lingauss_ug(tg->X, tg->yv, tg->N, tg->D, tg->s, tg->sn, w, grad);
+    if (tg->kind == ORC_TARGET_HMM)
+        return orc_hmm_ug(tg->y, tg->N, tg->z, tg->Tsup, tg->K, tg->V, w, grad);
     return orc_logistic_ug(tg->X, tg->y, tg->N, tg->D, tg->s, w, grad);
 }
 
@@ -868,9 +992,13 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
                        int64_t trace_cap, int64_t *trace_len, int64_t *leaves,
                        int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt,
                        int adapt_step, double target_accept, double *out_step_size,
-                       int uturn_gen)
+                       int uturn_gen, const uint8_t *hmm_z, int64_t hmm_tsup, int hmm_k, int hmm_v)
 {
     orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
+    tg.z = hmm_z;
+    tg.Tsup = hmm_tsup;
+    tg.K = hmm_k;
+    tg.V = hmm_v;
     double *im = (double *)malloc((size_t)D * sizeof(double));
     for (int64_t j = 0; j < D; ++j) im[j] = inv_mass_in ? inv_mass_in[j] : 1.0;
 

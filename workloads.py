@@ -119,3 +119,23 @@ def make_lingauss(N: int, D: int, *, key, noise_scale: float = 1.0):
     X = rng.normal(size=(N, D))
     yv = X @ w_true + noise_scale * rng.normal(size=N)
     return X, yv
+
+
+def make_hmm(T: int = 600, Tsup: int = 100, K: int = 3, V: int = 10, *, key=6, stay: float = 0.7,
+             emit_conc: float = 0.5):
+    """A semi-supervised HMM data set shaped like the paper's HMM benchmark
+    (K = 3 hidden states, V = 10 symbols, T = 600 points, the first 100 hidden
+    states observed).  The paper does not give its fixed matrices; here the
+    transition matrix keeps the state with probability ``stay`` and moves to
+    each other state equally, and the emission rows are Dirichlet(emit_conc)
+    draws.  Returns (w [T] uint8, z [Tsup] uint8, theta [K, K], phi [K, V])."""
+    rng = np.random.Generator(np.random.Philox(key=key))
+    theta = np.full((K, K), (1.0 - stay) / (K - 1))
+    np.fill_diagonal(theta, stay)
+    phi = rng.dirichlet(np.full(V, emit_conc), size=K)
+    z = np.empty(T, dtype=np.int64)
+    z[0] = rng.integers(K)
+    for t in range(1, T):
+        z[t] = rng.choice(K, p=theta[z[t - 1]])
+    w = np.array([rng.choice(V, p=phi[k]) for k in z], dtype=np.uint8)
+    return w, z[:Tsup].astype(np.uint8), theta, phi
