@@ -1,6 +1,7 @@
 /*
  * nuts.h -- C ABI of the MI355X (gfx950) iterative No-U-Turn sampler for
- * Bayesian logistic regression.
+ * Bayesian logistic regression (and a semi-supervised hidden Markov model,
+ * declared at the end).
  *
  * What is computed (arXiv 1912.11554):
  *   - the model of Appendix B / Fig. 1a: weights m ~ N(0, 1), intercept
@@ -211,6 +212,40 @@ int nuts_sample(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int6
                 uint32_t flags, double prior_scale, double step_size, const double* inv_mass_diag,
                 int max_tree_depth, int64_t num_warmup, int64_t num_samples, int64_t num_chains,
                 uint64_t seed, double* out_samples, nuts_stats* out_stats);
+
+/* Semi-supervised hidden Markov model (the HMM benchmark of Section 4 and
+ * Appendix C, built as in Stan's semi-supervised example): K hidden states,
+ * V observation symbols, one sequence w [T] (bytes < V) whose first Tsup
+ * hidden states z [Tsup] (bytes < K) are observed.  The K transition rows
+ * and K emission rows are simplexes with uniform Dirichlet priors, sampled
+ * through additive log-ratios: a row is softmax(a_0, .., a_{n-2}, 0) and
+ * its log Jacobian is the sum of the row's log entries.  A position q holds
+ * D = K (K - 1) + K (V - 1) logits: the K - 1 free logits of transition row j
+ * at j (K - 1), then those of emission row k at K (K - 1) + k (V - 1).
+ *   U(q) = -[ sum over entries x of log x  +  sum_{t < Tsup} log phi_{z_t}(w_t)
+ *             + sum_{0 < t < Tsup} log theta_{z_{t-1}}(z_t)
+ *             + log p(w_Tsup .. w_{T-1} | z_{Tsup-1}) ],
+ * the last term by the forward algorithm (from the uniform distribution,
+ * without a transition, when Tsup = 0).  The gradient comes from the
+ * backward recursion's expected counts.  Shapes: 2 <= K <= 4, V >= 2,
+ * K*K + K*V <= 64, T - Tsup <= 512 (else NUTS_EUNSUPPORTED); w and z are
+ * checked (NUTS_EINVAL for a symbol >= V or a state >= K).  fp64 throughout.
+ *
+ * nuts_hmm_potential_grad: U and grad U at num_points positions Q
+ * [num_points][D]; writes out_U [num_points] and out_grad [num_points][D]. */
+int nuts_hmm_potential_grad(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K,
+                            int V, const double* Q, int64_t num_points, double* out_U, double* out_grad);
+
+/* nuts_hmm_sample: NUTS on the model above, one wavefront per chain, with
+ * the meaning of every other argument, flag and option as in
+ * nuts_sample_data (flags NUTS_ADAPT_DIAG_MASS, NUTS_ADAPT_STEP_SIZE and
+ * NUTS_UTURN_GENERALIZED; opts->path NUTS_PATH_AUTO or NUTS_PATH_WAVE).
+ * Chains start at init_q or at q = 0 (uniform rows).  Writes out_samples
+ * [C][S][D] (the logits) and out_stats [C][S]. */
+int nuts_hmm_sample(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K, int V,
+                    uint32_t flags, double step_size, const double* inv_mass_diag, int max_tree_depth,
+                    int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed, double* out_samples,
+                    nuts_stats* out_stats, const nuts_sample_opts* opts);
 
 #ifdef __cplusplus
 }

@@ -1,4 +1,5 @@
-"""MI355X (gfx950) iterative NUTS for Bayesian logistic regression.
+"""MI355X (gfx950) iterative NUTS for Bayesian logistic regression (and a
+semi-supervised hidden Markov model, ``Sampler.hmm_sample``).
 
 Thin ctypes binding over ``libnuts.so`` (C ABI in ``include/nuts.h``): it
 marshals numpy arrays or torch tensors (host or device) into pointers and
@@ -25,6 +26,7 @@ EXPORTED = [
     "nuts_init", "nuts_free", "nuts_last_error", "nuts_data_create", "nuts_data_free",
     "nuts_data_potential_grad", "nuts_data_potential_grad_batched", "nuts_potential_grad",
     "nuts_data_log_likelihood", "nuts_sample_data", "nuts_sample",
+    "nuts_hmm_potential_grad", "nuts_hmm_sample",
 ]
 
 STATS_DTYPE = np.dtype([
@@ -108,6 +110,11 @@ def load_library():
     L.nuts_sample.argtypes = [P, P, P, i64, i64, i32, u32, dbl, dbl, P, i32, i64, i64, i64,
                               u64, P, P]
     L.nuts_sample.restype = i32
+    L.nuts_hmm_potential_grad.argtypes = [P, P, i64, P, i64, i32, i32, P, i64, P, P]
+    L.nuts_hmm_potential_grad.restype = i32
+    L.nuts_hmm_sample.argtypes = [P, P, i64, P, i64, i32, i32, u32, dbl, P, i32, i64, i64, i64, u64,
+                                  P, P, ctypes.POINTER(_Opts)]
+    L.nuts_hmm_sample.restype = i32
     _lib = L
     return L
 
@@ -206,6 +213,58 @@ class Sampler:
                             inv_mass=inv_mass, adapt_diag_mass=adapt_diag_mass, **kw)
         finally:
             d.free()
+
+
+    # ------------------------------------------------------------------
+    @staticmethod
+    def _hmm_seq(w, z):
+        w = np.ascontiguousarray(w, dtype=np.uint8)
+        z = np.zeros(0, np.uint8) if z is None else np.ascontiguousarray(z, dtype=np.uint8)
+        return w, z
+
+    def hmm_potential_grad(self, w, z, K, V, Q):
+        """Semi-supervised HMM: U [n] and grad U [n, D] at logits Q [n, D],
+        D = K (K - 1) + K (V - 1), for symbols w [T] with the first len(z)
+        hidden states z observed."""
+        w, z = self._hmm_seq(w, z)
+        D = hmm_dim(K, V)
+        Q = np.ascontiguousarray(Q, dtype=np.float64).reshape(-1, D)
+        n = Q.shape[0]
+        U, g = np.zeros(n), np.zeros((n, D))
+        self._check(self._L.nuts_hmm_potential_grad(self._h, _ptr(w), w.shape[0], _ptr(z), z.shape[0],
+                                                    K, V, _ptr(Q), n, _ptr(U), _ptr(g)))
+        return U, g
+
+    def hmm_sample(self, w, z, K, V, *, step_size, max_tree_depth, num_warmup, num_samples,
+                   num_chains=1, seed=0, inv_mass=None, adapt_diag_mass=False, init_q=None,
+                   first_iter=0, adapt_step_size=False, target_accept=0.8,
+                   uturn_generalized=False):
+        """NUTS on the semi-supervised HMM (one wavefront per chain).  Returns
+        the same dict as ``Data.sample``; samples hold the logits."""
+        w, z = self._hmm_seq(w, z)
+        C, D = num_chains, hmm_dim(K, V)
+        flags = (NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
+            NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0) | (
+            NUTS_UTURN_GENERALIZED if uturn_generalized else 0)
+        out_samples = np.zeros((C, num_samples, D))
+        out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
+        final_q, out_im, out_eps = np.zeros((C, D)), np.zeros((C, D)), np.zeros(C)
+        gev = np.zeros(1, dtype=np.int64)
+        im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)
+        iq = None if init_q is None else np.ascontiguousarray(init_q, dtype=np.float64)
+        opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), NUTS_PATH_AUTO,
+                     0, target_accept, _ptr(out_eps))
+        self._check(self._L.nuts_hmm_sample(
+            self._h, _ptr(w), w.shape[0], _ptr(z), z.shape[0], K, V, flags, step_size, _ptr(im),
+            max_tree_depth, num_warmup, num_samples, C, seed, _ptr(out_samples), _ptr(out_stats),
+            ctypes.byref(opts)))
+        return dict(samples=out_samples, stats=out_stats, final_q=final_q, inv_mass=out_im,
+                    step_size=out_eps, grad_evals=int(gev[0]))
+
+
+def hmm_dim(K, V):
+    """Number of logits of the semi-supervised HMM: K (K - 1) + K (V - 1)."""
+    return K * (K - 1) + K * (V - 1)
 
 
 class Data:

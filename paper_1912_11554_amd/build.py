@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libnuts.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 SOURCES = ["layout.hip", "potential.hip", "sampler.hip", "sampler_f32.hip", "sampler_f64.hip",
-           "sampler_ext_f32.hip", "sampler_ext_f64.hip", "batch.hip", "api.cpp"]
+           "sampler_ext_f32.hip", "sampler_ext_f64.hip", "batch.hip", "hmm.hip", "hmm_ext.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -205,6 +205,151 @@ struct DeviceScope {
     }
 };
 
+// Arguments every sampling entry point shares.
+int check_run(nuts_handle* h, uint32_t flags, uint32_t allowed, const nuts_sample_opts& o, double step_size,
+              int max_tree_depth, int64_t num_warmup, int64_t num_samples, int64_t num_chains,
+              double* target_accept)
+{
+    if (flags & ~allowed) return fail(h, NUTS_EINVAL, "unknown flag bits 0x%x", flags & ~allowed);
+    *target_accept = o.target_accept == 0.0 ? 0.8 : o.target_accept;
+    if (!(*target_accept > 0.0 && *target_accept < 1.0))
+        return fail(h, NUTS_EINVAL, "target_accept must be in (0, 1) (got %g)", o.target_accept);
+    if (!finite_pos(step_size)) return fail(h, NUTS_EINVAL, "step_size must be finite and > 0");
+    if (max_tree_depth < 1 || max_tree_depth > 30)
+        return fail(h, NUTS_EINVAL, "max_tree_depth must be in [1, 30] (got %d)", max_tree_depth);
+    if (num_warmup < 0) return fail(h, NUTS_EINVAL, "num_warmup must be >= 0");
+    if (num_samples < 1) return fail(h, NUTS_EINVAL, "num_samples must be >= 1");
+    if (num_chains < 1) return fail(h, NUTS_EINVAL, "num_chains must be >= 1");
+    if (o.first_iter < 0) return fail(h, NUTS_EINVAL, "first_iter must be >= 0");
+    return NUTS_OK;
+}
+
+int check_inv_mass(nuts_handle* h, const double* inv_mass_diag, int D)
+{
+    if (!inv_mass_diag) return NUTS_OK;
+    std::vector<double> im(D);
+    if (is_device_ptr(inv_mass_diag)) {
+        DeviceScope ds(h->device);
+        HIP_TRY(h, hipMemcpy(im.data(), inv_mass_diag, (size_t)D * 8, hipMemcpyDeviceToHost));
+    } else {
+        std::memcpy(im.data(), inv_mass_diag, (size_t)D * 8);
+    }
+    for (int i = 0; i < D; ++i)
+        if (!finite_pos(im[i])) return fail(h, NUTS_EINVAL, "inv_mass_diag[%d] must be finite and > 0", i);
+    return NUTS_OK;
+}
+
+// Device copies of a sampling call's inputs and outputs, and the sampler
+// arguments that point at them.
+struct RunBuffers {
+    DevBuf imb, iqb, smp, sts, fq, fim, fep, gev;
+    int64_t C = 0, S = 0, D = 0;
+    hipStream_t s = nullptr;
+
+    // a.data and the model fields are the caller's; the rest is set here
+    int stage(nuts_handle* h, SamplerArgs& a, uint32_t flags, const nuts_sample_opts& o, double target_accept,
+              double step_size, const double* inv_mass_diag, int max_tree_depth, int64_t num_warmup,
+              int64_t num_samples, int64_t num_chains, uint64_t seed, double* out_samples, nuts_stats* out_stats)
+    {
+        C = num_chains;
+        S = num_samples;
+        D = a.data.D;
+        s = h->stream;
+        const void *im_d = nullptr, *iq_d = nullptr;
+        void *smp_d = nullptr, *sts_d = nullptr, *fq_d = nullptr, *fim_d = nullptr, *fep_d = nullptr;
+        HIP_TRY(h, stage_in(inv_mass_diag, (size_t)D * 8, imb, &im_d, s));
+        HIP_TRY(h, stage_in(o.init_q, (size_t)C * D * 8, iqb, &iq_d, s));
+        HIP_TRY(h, stage_out(out_samples, (size_t)C * S * D * 8, smp, &smp_d));
+        HIP_TRY(h, stage_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, &sts_d));
+        HIP_TRY(h, stage_out(o.out_final_q, (size_t)C * D * 8, fq, &fq_d));
+        HIP_TRY(h, stage_out(o.out_inv_mass, (size_t)C * D * 8, fim, &fim_d));
+        HIP_TRY(h, stage_out(o.out_step_size, (size_t)C * 8, fep, &fep_d));
+        HIP_TRY(h, gev.alloc((size_t)C * sizeof(unsigned long long)));
+        a.step_size = step_size;
+        a.inv_mass = (const double*)im_d;
+        a.max_depth = max_tree_depth;
+        a.num_warmup = num_warmup;
+        a.num_samples = num_samples;
+        a.num_chains = C;
+        a.chain_offset = 0;
+        a.seed = seed;
+        a.first_iter = o.first_iter;
+        a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
+        a.adapt_step = (flags & NUTS_ADAPT_STEP_SIZE) ? 1 : 0;
+        a.uturn_gen = (flags & NUTS_UTURN_GENERALIZED) ? 1 : 0;
+        a.target_accept = target_accept;
+        a.init_q = (const double*)iq_d;
+        a.out_samples = (double*)smp_d;
+        a.out_stats = (nuts_stats*)sts_d;
+        a.out_final_q = (double*)fq_d;
+        a.out_inv_mass = (double*)fim_d;
+        a.out_step_size = (double*)fep_d;
+        a.grad_evals = (unsigned long long*)gev.p;
+        return NUTS_OK;
+    }
+
+    // copy host outputs back, sum the gradient evaluations, synchronise
+    int finish(nuts_handle* h, const nuts_sample_opts& o, double* out_samples, nuts_stats* out_stats)
+    {
+        HIP_TRY(h, finish_out(out_samples, (size_t)C * S * D * 8, smp, s));
+        HIP_TRY(h, finish_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, s));
+        HIP_TRY(h, finish_out(o.out_final_q, (size_t)C * D * 8, fq, s));
+        HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
+        HIP_TRY(h, finish_out(o.out_step_size, (size_t)C * 8, fep, s));
+        std::vector<unsigned long long> ev(C);
+        HIP_TRY(h, hipMemcpyAsync(ev.data(), gev.p, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipStreamSynchronize(s));
+        if (o.out_grad_evals) {
+            unsigned long long tot = 0;
+            for (auto v : ev) tot += v;
+            *o.out_grad_evals = (int64_t)tot;
+        }
+        return NUTS_OK;
+    }
+};
+
+
+// Check an HMM sequence on the host and put it on the device.
+int hmm_stage(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K, int V,
+              DevBuf& wb, DevBuf& zb, HmmView* hv)
+{
+    if (!w) return fail(h, NUTS_EINVAL, "w is NULL");
+    if (Tsup > 0 && !z) return fail(h, NUTS_EINVAL, "z is NULL with Tsup = %lld", (long long)Tsup);
+    if (T < 1 || Tsup < 0 || Tsup > T)
+        return fail(h, NUTS_EINVAL, "need 1 <= T and 0 <= Tsup <= T (T = %lld, Tsup = %lld)", (long long)T,
+                    (long long)Tsup);
+    if (!hmm_supported(K, V, T, Tsup))
+        return fail(h, NUTS_EUNSUPPORTED,
+                    "the HMM kernels take 2 <= K <= 4, V >= 2, K*K + K*V <= 64 and T - Tsup <= %d "
+                    "(K = %d, V = %d, T - Tsup = %lld)",
+                    kHmmMaxUnobserved, K, V, (long long)(T - Tsup));
+    std::vector<uint8_t> hw((size_t)T), hz((size_t)Tsup);
+    DeviceScope ds(h->device);
+    if (is_device_ptr(w)) HIP_TRY(h, hipMemcpy(hw.data(), w, (size_t)T, hipMemcpyDeviceToHost));
+    else std::memcpy(hw.data(), w, (size_t)T);
+    if (Tsup > 0) {
+        if (is_device_ptr(z)) HIP_TRY(h, hipMemcpy(hz.data(), z, (size_t)Tsup, hipMemcpyDeviceToHost));
+        else std::memcpy(hz.data(), z, (size_t)Tsup);
+    }
+    for (int64_t t = 0; t < T; ++t)
+        if (hw[t] >= V) return fail(h, NUTS_EINVAL, "w[%lld] = %d is not below V = %d", (long long)t, hw[t], V);
+    for (int64_t t = 0; t < Tsup; ++t)
+        if (hz[t] >= K) return fail(h, NUTS_EINVAL, "z[%lld] = %d is not below K = %d", (long long)t, hz[t], K);
+    HIP_TRY(h, wb.alloc((size_t)T));
+    HIP_TRY(h, zb.alloc((size_t)Tsup));
+    HIP_TRY(h, hipMemcpyAsync(wb.p, hw.data(), (size_t)T, hipMemcpyHostToDevice, h->stream));
+    if (Tsup > 0) HIP_TRY(h, hipMemcpyAsync(zb.p, hz.data(), (size_t)Tsup, hipMemcpyHostToDevice, h->stream));
+    // the host copies must outlive the copies
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    hv->w = (const uint8_t*)wb.p;
+    hv->z = (const uint8_t*)zb.p;
+    hv->T = (int)T;
+    hv->Tsup = (int)Tsup;
+    hv->K = K;
+    hv->V = V;
+    return NUTS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -528,20 +673,12 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     std::memset(&o, 0, sizeof o);
     if (opts) o = *opts;
     if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
-    if (flags & ~(uint32_t)(NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE |
-                            NUTS_UTURN_GENERALIZED))
-        return fail(h, NUTS_EINVAL, "unknown flag bits 0x%x", flags);
-    const double target_accept = o.target_accept == 0.0 ? 0.8 : o.target_accept;
-    if (!(target_accept > 0.0 && target_accept < 1.0))
-        return fail(h, NUTS_EINVAL, "target_accept must be in (0, 1) (got %g)", o.target_accept);
+    double target_accept = 0.0;
+    int rc = check_run(h, flags, NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE |
+                                     NUTS_UTURN_GENERALIZED,
+                       o, step_size, max_tree_depth, num_warmup, num_samples, num_chains, &target_accept);
+    if (rc != NUTS_OK) return rc;
     if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
-    if (!finite_pos(step_size)) return fail(h, NUTS_EINVAL, "step_size must be finite and > 0");
-    if (max_tree_depth < 1 || max_tree_depth > 30)
-        return fail(h, NUTS_EINVAL, "max_tree_depth must be in [1, 30] (got %d)", max_tree_depth);
-    if (num_warmup < 0) return fail(h, NUTS_EINVAL, "num_warmup must be >= 0");
-    if (num_samples < 1) return fail(h, NUTS_EINVAL, "num_samples must be >= 1");
-    if (num_chains < 1) return fail(h, NUTS_EINVAL, "num_chains must be >= 1");
-    if (o.first_iter < 0) return fail(h, NUTS_EINVAL, "first_iter must be >= 0");
     if (d->view.N < 1) return fail(h, NUTS_EINVAL, "sampling needs N >= 1");
     const bool per_chain = (flags & NUTS_DATA_PER_CHAIN) != 0;
     if (per_chain && d->view.nds != num_chains)
@@ -550,17 +687,8 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     if (!per_chain && d->view.nds != 1)
         return fail(h, NUTS_EINVAL, "data holds %lld sets; pass NUTS_DATA_PER_CHAIN", (long long)d->view.nds);
     const int D = d->view.D;
-    if (inv_mass_diag) {
-        std::vector<double> im(D);
-        if (is_device_ptr(inv_mass_diag)) {
-            DeviceScope ds(h->device);
-            HIP_TRY(h, hipMemcpy(im.data(), inv_mass_diag, (size_t)D * 8, hipMemcpyDeviceToHost));
-        } else {
-            std::memcpy(im.data(), inv_mass_diag, (size_t)D * 8);
-        }
-        for (int i = 0; i < D; ++i)
-            if (!finite_pos(im[i])) return fail(h, NUTS_EINVAL, "inv_mass_diag[%d] must be finite and > 0", i);
-    }
+    rc = check_inv_mass(h, inv_mass_diag, D);
+    if (rc != NUTS_OK) return rc;
 
     DeviceScope ds(h->device);
     int path = o.path;
@@ -604,44 +732,16 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     }
 
     hipStream_t s = h->stream;
-    const int64_t C = num_chains, S = num_samples;
-    DevBuf imb, iqb, smp, sts, fq, fim, fep, gev;
-    const void *im_d = nullptr, *iq_d = nullptr;
-    void *smp_d = nullptr, *sts_d = nullptr, *fq_d = nullptr, *fim_d = nullptr, *fep_d = nullptr;
-    HIP_TRY(h, stage_in(inv_mass_diag, (size_t)D * 8, imb, &im_d, s));
-    HIP_TRY(h, stage_in(o.init_q, (size_t)C * D * 8, iqb, &iq_d, s));
-    HIP_TRY(h, stage_out(out_samples, (size_t)C * S * D * 8, smp, &smp_d));
-    HIP_TRY(h, stage_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, &sts_d));
-    HIP_TRY(h, stage_out(o.out_final_q, (size_t)C * D * 8, fq, &fq_d));
-    HIP_TRY(h, stage_out(o.out_inv_mass, (size_t)C * D * 8, fim, &fim_d));
-    HIP_TRY(h, stage_out(o.out_step_size, (size_t)C * 8, fep, &fep_d));
-    HIP_TRY(h, gev.alloc((size_t)C * sizeof(unsigned long long)));
-
+    const int64_t C = num_chains;
+    RunBuffers rb;
     SamplerArgs a;
     std::memset(&a, 0, sizeof a);
     a.data = d->view;
     a.per_chain_data = per_chain ? 1 : 0;
     a.prior_scale = prior_scale;
-    a.step_size = step_size;
-    a.inv_mass = (const double*)im_d;
-    a.max_depth = max_tree_depth;
-    a.num_warmup = num_warmup;
-    a.num_samples = num_samples;
-    a.num_chains = C;
-    a.chain_offset = 0;
-    a.seed = seed;
-    a.first_iter = o.first_iter;
-    a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
-    a.adapt_step = (flags & NUTS_ADAPT_STEP_SIZE) ? 1 : 0;
-    a.uturn_gen = (flags & NUTS_UTURN_GENERALIZED) ? 1 : 0;
-    a.target_accept = target_accept;
-    a.init_q = (const double*)iq_d;
-    a.out_samples = (double*)smp_d;
-    a.out_stats = (nuts_stats*)sts_d;
-    a.out_final_q = (double*)fq_d;
-    a.out_inv_mass = (double*)fim_d;
-    a.out_step_size = (double*)fep_d;
-    a.grad_evals = (unsigned long long*)gev.p;
+    rc = rb.stage(h, a, flags, o, target_accept, step_size, inv_mass_diag, max_tree_depth, num_warmup, num_samples,
+                  num_chains, seed, out_samples, out_stats);
+    if (rc != NUTS_OK) return rc;
 
     if (path == NUTS_PATH_WAVE) {
         HIP_TRY(h, launch_sampler_wave(a, s));
@@ -698,20 +798,76 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
                             (long long)c);
         }
     }
-    HIP_TRY(h, finish_out(out_samples, (size_t)C * S * D * 8, smp, s));
-    HIP_TRY(h, finish_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, s));
-    HIP_TRY(h, finish_out(o.out_final_q, (size_t)C * D * 8, fq, s));
-    HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
-    HIP_TRY(h, finish_out(o.out_step_size, (size_t)C * 8, fep, s));
-    std::vector<unsigned long long> ev(C);
-    HIP_TRY(h, hipMemcpyAsync(ev.data(), gev.p, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+    return rb.finish(h, o, out_samples, out_stats);
+}
+
+int nuts_hmm_potential_grad(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K,
+                            int V, const double* Q, int64_t num_points, double* out_U, double* out_grad)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!Q || !out_U || !out_grad) return fail(h, NUTS_EINVAL, "Q, out_U and out_grad must not be NULL");
+    if (num_points < 1 || num_points > ((int64_t)1 << 31))
+        return fail(h, NUTS_EINVAL, "num_points must be in [1, 2^31] (got %lld)", (long long)num_points);
+    DevBuf wb, zb;
+    HmmView hv;
+    int rc = hmm_stage(h, w, T, z, Tsup, K, V, wb, zb, &hv);
+    if (rc != NUTS_OK) return rc;
+    DeviceScope ds(h->device);
+    hipStream_t s = h->stream;
+    const int D = hmm_dim(K, V);
+    DevBuf qb, ub, gb;
+    const void* q_d = nullptr;
+    void *u_d = nullptr, *g_d = nullptr;
+    HIP_TRY(h, stage_in(Q, (size_t)num_points * D * 8, qb, &q_d, s));
+    HIP_TRY(h, stage_out(out_U, (size_t)num_points * 8, ub, &u_d));
+    HIP_TRY(h, stage_out(out_grad, (size_t)num_points * D * 8, gb, &g_d));
+    HIP_TRY(h, launch_hmm_potential(hv, (const double*)q_d, num_points, (double*)u_d, (double*)g_d, s));
+    HIP_TRY(h, finish_out(out_U, (size_t)num_points * 8, ub, s));
+    HIP_TRY(h, finish_out(out_grad, (size_t)num_points * D * 8, gb, s));
     HIP_TRY(h, hipStreamSynchronize(s));
-    if (o.out_grad_evals) {
-        unsigned long long tot = 0;
-        for (auto v : ev) tot += v;
-        *o.out_grad_evals = (int64_t)tot;
-    }
     return NUTS_OK;
+}
+
+int nuts_hmm_sample(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K, int V,
+                    uint32_t flags, double step_size, const double* inv_mass_diag, int max_tree_depth,
+                    int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed, double* out_samples,
+                    nuts_stats* out_stats, const nuts_sample_opts* opts)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    nuts_sample_opts o;
+    std::memset(&o, 0, sizeof o);
+    if (opts) o = *opts;
+    double target_accept = 0.0;
+    int rc = check_run(h, flags, NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE | NUTS_UTURN_GENERALIZED, o, step_size,
+                       max_tree_depth, num_warmup, num_samples, num_chains, &target_accept);
+    if (rc != NUTS_OK) return rc;
+    if (o.path != NUTS_PATH_AUTO && o.path != NUTS_PATH_WAVE)
+        return fail(h, NUTS_EUNSUPPORTED, "the HMM runs on the one-wave-per-chain path only");
+    DevBuf wb, zb;
+    HmmView hv;
+    rc = hmm_stage(h, w, T, z, Tsup, K, V, wb, zb, &hv);
+    if (rc != NUTS_OK) return rc;
+    const int D = hmm_dim(K, V);
+    rc = check_inv_mass(h, inv_mass_diag, D);
+    if (rc != NUTS_OK) return rc;
+    DeviceScope ds(h->device);
+    RunBuffers rb;
+    SamplerArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.data.D = D;
+    a.data.N = T;
+    a.data.nds = 1;
+    a.prior_scale = 1.0;
+    rc = rb.stage(h, a, flags, o, target_accept, step_size, inv_mass_diag, max_tree_depth, num_warmup, num_samples,
+                  num_chains, seed, out_samples, out_stats);
+    if (rc != NUTS_OK) return rc;
+    const hipError_t e = launch_hmm_sampler(a, hv, h->stream);
+    if (e == hipErrorInvalidValue)
+        return fail(h, NUTS_EUNSUPPORTED, "max_tree_depth %d: the HMM chain's LDS does not fit", max_tree_depth);
+    HIP_TRY(h, e);
+    return rb.finish(h, o, out_samples, out_stats);
 }
 
 int nuts_sample(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int64_t D, int dtype, uint32_t flags,

@@ -239,4 +239,29 @@ const void* grid_kernel_ext_f64(const DataView& dv);
 inline bool sampler_extended(const SamplerArgs& a) { return (a.adapt_step && a.num_warmup > 0) || a.uturn_gen; }
 constexpr int kGridWaves = 12;  // per group: 1 controller + 11 workers (3 waves per SIMD: 168 registers each)
 
+// Semi-supervised hidden Markov model (hmm.hip, hmm_ext.hip): symbols w [T]
+// (< V), observed states z [Tsup] (< K), on the device.  Parameters: K (K-1)
+// transition logits, then K (V-1) emission logits.
+constexpr int kHmmSteps = 8;                     // unobserved steps per lane
+constexpr int kHmmMaxUnobserved = kHmmSteps * 64;
+struct HmmView {
+    const uint8_t* w;
+    const uint8_t* z;
+    int T, Tsup, K, V;
+};
+inline int hmm_dim(int K, int V) { return K * (K - 1) + K * (V - 1); }
+// Shapes the kernels take: 2 <= K <= 4, V >= 2, K*K + K*V <= 64 (one lane
+// per simplex entry), T - Tsup <= kHmmMaxUnobserved.
+inline bool hmm_supported(int K, int V, int64_t T, int64_t Tsup)
+{
+    return K >= 2 && K <= 4 && V >= 2 && K * K + K * V <= 64 && Tsup >= 0 && Tsup <= T && T >= 1 &&
+           T - Tsup <= kHmmMaxUnobserved;
+}
+// One wave per chain; a.data.D = hmm_dim(K, V), the other data fields unused.
+hipError_t launch_hmm_sampler(const SamplerArgs& a, const HmmView& hv, hipStream_t stream);
+hipError_t launch_hmm_sampler_ext(const SamplerArgs& a, const HmmView& hv, hipStream_t stream);
+// U and grad U at n positions Q [n][D]: out_U [n], out_grad [n][D].
+hipError_t launch_hmm_potential(const HmmView& hv, const double* Q, int64_t n, double* out_U, double* out_grad,
+                                hipStream_t stream);
+
 }  // namespace nuts
