@@ -159,8 +159,8 @@ def recorded_traffic(kernel, workload, evals):
     """HBM bytes of the timed launch from the PMC record in
     profiles/traffic.json (FETCH_SIZE + WRITE_SIZE per gradient evaluation,
     each scaled by the same counter's reading on a copy of known size), or
-    None when there is no record for this kernel and workload or the kernel
-    sources have changed since it was taken."""
+    None when there is no record for this kernel and workload or the sources
+    the kernel is built from have changed since it was taken."""
     from paper_1912_11554_amd.profiling import source_fingerprint
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -168,10 +168,8 @@ def recorded_traffic(kernel, workload, evals):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("fingerprint") != source_fingerprint():
-        return None
     e = rec.get("kernels", {}).get(f"{kernel}/{workload}")
-    if not e:
+    if not e or e.get("fingerprint") != source_fingerprint(kernel):
         return None
     out = dict(bytes=round((e["fetch_bytes_per_eval"] + e["write_bytes_per_eval"]) * evals),
                fetch_bytes_per_eval=e["fetch_bytes_per_eval"],
@@ -208,6 +206,114 @@ def cpu_baseline(name, seconds):
                 host_cores_available=len(os.sched_getaffinity(0)))
 
 
+HMM_SHAPE = dict(T=600, Tsup=100, K=3, V=10)
+
+
+def run_hmm(chains, steps, warmup):
+    """The semi-supervised HMM (T = 600 symbols, the first 100 hidden states
+    observed, K = 3, V = 10).  (1) One chain under the paper's HMM protocol
+    (1000 warmup iterations adapting the step size and the diagonal mass,
+    then 1000 draws): milliseconds per leapfrog step, the paper's HMM metric.
+    (2) `chains` chains at that step size and mass, `warmup` untimed
+    iterations, then `steps` timed ones: gradient evaluations per second."""
+    import torch
+
+    import paper_1912_11554_amd as nuts
+    import workloads
+    from paper_1912_11554_amd.diagnostics import effective_sample_size
+
+    sh = HMM_SHAPE
+    K, V = sh["K"], sh["V"]
+    w, z, _, _ = workloads.make_hmm(**sh)
+    D = nuts.hmm_dim(K, V)
+    s = nuts.Sampler(0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r1 = s.hmm_sample(w, z, K, V, step_size=0.1, max_tree_depth=10, num_warmup=1000,
+                      num_samples=1000, seed=1, adapt_step_size=True, adapt_diag_mass=True)
+    one_s = time.perf_counter() - t0
+    st1 = r1["stats"][0]
+    ess1 = effective_sample_size(r1["samples"])
+    eps, im = float(r1["step_size"][0]), r1["inv_mass"][0]
+    log(f"hmm one chain: 2000 iterations, {r1['grad_evals']} gradient evaluations in "
+        f"{one_s * 1e3:.1f} ms: {one_s * 1e3 / r1['grad_evals']:.5f} ms per leapfrog step, "
+        f"adapted step {eps:.4g}, min ESS {ess1.min():.0f}")
+
+    kw = dict(step_size=eps, inv_mass=im, max_tree_depth=10, seed=2, num_chains=chains)
+    r0 = s.hmm_sample(w, z, K, V, num_warmup=warmup, num_samples=1, **kw)
+    samples = torch.empty((chains, steps, D), dtype=torch.float64, device="cuda")
+    stats = torch.empty((chains, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    r = s.hmm_sample(w, z, K, V, num_warmup=0, num_samples=steps, init_q=r0["final_q"],
+                     first_iter=warmup + 1, out_samples=samples, out_stats=stats, **kw)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    gpu_s = ev0.elapsed_time(ev1) / 1e3
+    st = stats.cpu().numpy().reshape(chains, steps, -1).view(nuts.STATS_DTYPE)[..., 0]
+    evals = r["grad_evals"]
+    assert evals == int(st["num_steps"].sum()) + chains
+    log(f"hmm {chains} chains: {steps} iterations, {evals} evaluations in {gpu_s * 1e3:.1f} ms: "
+        f"{evals / gpu_s:.4g} evals/s, {st['num_steps'].mean():.1f} steps per iteration")
+    s.close()
+    return dict(workload="hmm_t600_tsup100_k3_v10", T=sh["T"], Tsup=sh["Tsup"], K=K, V=V, D=D,
+                one_chain=dict(warmup=1000, samples=1000, adapt="step size + diagonal mass",
+                               grad_evals=r1["grad_evals"], seconds=round(one_s, 4),
+                               ms_per_leapfrog_step=round(one_s * 1e3 / r1["grad_evals"], 6),
+                               step_size=round(eps, 6), ess_min=round(float(ess1.min()), 1),
+                               mean_steps_per_iter=round(float(st1["num_steps"].mean()), 2),
+                               divergences=int(st1["diverging"].sum())),
+                chains=chains, steps=steps, warmup=warmup, grad_evals=evals,
+                gpu_seconds=round(gpu_s, 4), evals_per_s=round(evals / gpu_s, 1),
+                mean_steps_per_iter=round(float(st["num_steps"].mean()), 2),
+                kernel="sampler_hmm_kernel")
+
+
+def hmm_cpu_baseline(seconds):
+    """The oracle's fp64 HMM gradient evaluations, one core."""
+    import oracle
+    import workloads
+
+    w, z, _, _ = workloads.make_hmm(**HMM_SHAPE)
+    D = oracle.hmm_dim(HMM_SHAPE["K"], HMM_SHAPE["V"])
+    q = np.random.default_rng(3).normal(0.0, 0.5, D)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.hmm_potential_grad(w, z, HMM_SHAPE["K"], HMM_SHAPE["V"], q)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    log(f"cpu oracle hmm: {n} gradient evaluations in {el:.1f}s")
+    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle",
+                sample=f"{n} HMM potential+gradient evaluations (T 600, Tsup 100, K 3, V 10), "
+                       f"single-threaded fp64 C, {el:.1f}s")
+
+
+def hmm_line(h, cpu):
+    """The HMM object of the JSON line, with its roofline: the wave-per-chain
+    HMM kernel is bound by vector-ALU issue (the recursions run in
+    registers, the symbols and occupancies in LDS)."""
+    traffic = recorded_traffic(h["kernel"], h["workload"], h["grad_evals"])
+    roof = None
+    if traffic and "valu_instructions_per_eval" in traffic:
+        rate = traffic["valu_instructions_per_eval"] * h["evals_per_s"] / 1e9
+        roof = {"kernel": h["kernel"], "bound": "alu", "achieved": round(rate, 1),
+                "peak": VALU_PEAK_GIPS, "unit": "G VALU wave-instructions/s",
+                "frac": round(rate / VALU_PEAK_GIPS, 4), "traffic": traffic["bytes"],
+                "valu_instructions_per_eval": traffic["valu_instructions_per_eval"]}
+    out = dict(h)
+    out["roofline"] = roof
+    out["cpu_baseline"] = cpu
+    # the paper's HMM figure (NumPyro, 32-bit, one CPU chain): context only
+    out["paper_numpyro_cpu_ms_per_leapfrog_step"] = 0.09
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -225,6 +331,11 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run a plain device copy of this many MiB (a known-size "
                          "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+    ap.add_argument("--hmm-chains", type=int, default=8192,
+                    help="chains of the semi-supervised HMM reported beside the main workload "
+                         "(0: no HMM line)")
+    ap.add_argument("--hmm-steps", type=int, default=100)
+    ap.add_argument("--hmm-only", action="store_true", help="run the HMM measurement alone")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -239,6 +350,10 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy: {args.copy_mb} MiB read + {args.copy_mb} MiB written")
         del src, dst
+    if args.hmm_only:
+        h = run_hmm(args.hmm_chains, args.hmm_steps, 20)
+        print(json.dumps(hmm_line(h, None)), flush=True)
+        return
     main_res = run_workload(args.workload, args.steps, args.warmup, args.adapt)
     other = run_workload(args.also, args.steps, args.warmup, args.adapt) if args.also else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
@@ -297,6 +412,10 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if args.hmm_chains:
+        h = run_hmm(args.hmm_chains, args.hmm_steps, 20)
+        hc = None if args.no_cpu_baseline else hmm_cpu_baseline(min(args.cpu_seconds, 10.0))
+        line["hmm"] = hmm_line(h, hc)
     if other:
         line["also"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in other.items()}
         line["also"]["frac_hbm"] = round(other["achieved_gbs"] / HBM_PEAK_GBS, 4)

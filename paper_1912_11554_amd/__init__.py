@@ -238,16 +238,19 @@ class Sampler:
     def hmm_sample(self, w, z, K, V, *, step_size, max_tree_depth, num_warmup, num_samples,
                    num_chains=1, seed=0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                    first_iter=0, adapt_step_size=False, target_accept=0.8,
-                   uturn_generalized=False):
+                   uturn_generalized=False, out_samples=None, out_stats=None):
         """NUTS on the semi-supervised HMM (one wavefront per chain).  Returns
-        the same dict as ``Data.sample``; samples hold the logits."""
+        the same dict as ``Data.sample``; samples hold the logits (numpy
+        unless device tensors are passed in out_samples / out_stats)."""
         w, z = self._hmm_seq(w, z)
         C, D = num_chains, hmm_dim(K, V)
         flags = (NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
             NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0) | (
             NUTS_UTURN_GENERALIZED if uturn_generalized else 0)
-        out_samples = np.zeros((C, num_samples, D))
-        out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
+        if out_samples is None:
+            out_samples = np.zeros((C, num_samples, D))
+        if out_stats is None:
+            out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
         final_q, out_im, out_eps = np.zeros((C, D)), np.zeros((C, D)), np.zeros(C)
         gev = np.zeros(1, dtype=np.int64)
         im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)

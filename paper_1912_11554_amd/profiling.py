@@ -5,8 +5,8 @@ ties recorded HBM-traffic figures to the kernel code they were taken on.
         kernel-trace summary (calls, total, average, min, max per kernel)
     python -m paper_1912_11554_amd.profiling counters RUN_results.db
         PMC counter values per dispatch (summed over the counter instances)
-    python -m paper_1912_11554_amd.profiling fingerprint
-        SHA-256 over the kernel sources (csrc/*)
+    python -m paper_1912_11554_amd.profiling fingerprint [KERNEL]
+        SHA-256 over the sources KERNEL is built from (default: all of csrc)
 
 The databases are the SQLite files rocprofv3 writes (`-d DIR -o NAME`).
 """
@@ -22,12 +22,25 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def source_fingerprint() -> str:
-    """SHA-256 over the device and host sources of the library (file names
-    and contents, sorted): any kernel change gives a new value."""
+# Sources that only the HMM kernels are built from; the other kernels'
+# fingerprint leaves them out (the HMM kernels include every shared header).
+HMM_ONLY_SOURCES = ("hmm_impl.h", "hmm.hip", "hmm_ext.hip")
+
+
+def is_hmm_kernel(kernel: str) -> bool:
+    return "hmm" in kernel
+
+
+def source_fingerprint(kernel: str | None = None) -> str:
+    """SHA-256 over the device and host sources a kernel is built from (file
+    names and contents, sorted): any change to them gives a new value.  With
+    no kernel named, over all of csrc."""
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
-        h.update(os.path.basename(path).encode())
+        base = os.path.basename(path)
+        if kernel is not None and not is_hmm_kernel(kernel) and base in HMM_ONLY_SOURCES:
+            continue
+        h.update(base.encode())
         with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -65,7 +78,7 @@ def main(argv):
         sys.exit(__doc__)
     cmd = argv[0]
     if cmd == "fingerprint":
-        print(source_fingerprint())
+        print(source_fingerprint(argv[1] if len(argv) > 1 else None))
     elif cmd == "kernels":
         print("| kernel | calls | total (us) | average (us) | min (us) | max (us) |")
         print("|---|---:|---:|---:|---:|---:|")
