@@ -101,12 +101,68 @@ __device__ __forceinline__ void mat_mul(const double (&A)[K][K], const double (&
         }
 }
 
+// Sums over the wave of N values per lane at once (a reduce-scatter
+// butterfly): at the stage of lane bit M each lane keeps the lower or the
+// upper part of its current values, by that bit, and adds its partner's copy
+// of them; once one value is left the butterfly goes on over the remaining
+// bits.  Returns this lane's final value: the total of value index
+// scatter_index(e) == this lane for some e, see scatter_lane.
+template <int M, int C>
+__device__ __forceinline__ double scatter_stage(const double (&cur)[C])
+{
+    if constexpr (C == 1) {
+        const double s = cur[0] + xor_move<M>(cur[0]);
+        if constexpr (M > 1) {
+            double n[1] = {s};
+            return scatter_stage<M / 2, 1>(n);
+        } else {
+            return s;
+        }
+    } else {
+        constexpr int lo = (C + 1) / 2, hi = C - lo;
+        const bool upper = (lane() & M) != 0;
+        double n[lo];
+#pragma unroll
+        for (int i = 0; i < lo; ++i) {
+            const double up = i < hi ? cur[lo + i] : 0.0;
+            const double send = upper ? cur[i] : up;
+            const double keep = upper ? up : cur[i];
+            n[i] = keep + xor_move<M>(send);
+        }
+        if constexpr (M > 1) {
+            return scatter_stage<M / 2, lo>(n);
+        } else {
+            static_assert(lo == 1, "more values than lanes");
+            return n[0];
+        }
+    }
+}
+
+// The lane left holding the total of value e by scatter_stage<32, C>.
+__host__ __device__ inline int scatter_lane(int e, int C)
+{
+    int lanebits = 0;
+    for (int M = 32; M >= 1; M >>= 1) {
+        if (C == 1) break;
+        const int lo = (C + 1) / 2;
+        if (e >= lo) {
+            lanebits |= M;
+            e -= lo;
+        }
+        C = lo;
+    }
+    return lanebits;
+}
+
 // LDS of one wave, in doubles: the checkpoint array S, the occupancies
 // (Tu x K, symbol-sorted; first used to sort the symbols), the emission
-// table (V x K).
+// table (V x K), the row table (2K rows of row_width, zero-padded).
 struct HmmLds {
-    int s_off, gam_off, phi_off, wave;
+    int s_off, gam_off, phi_off, row_off, wave;
 };
+
+// Slots of one simplex row in the row table: the longer row length, even.
+__host__ __device__ inline int hmm_row_width(int K, int V) { return ((K > V ? K : V) + 1) & ~1; }
 
 __host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, int max_depth)
 {
@@ -116,7 +172,8 @@ __host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, 
     L.s_off = 0;
     L.gam_off = slots * 2 * D;
     L.phi_off = L.gam_off + tu * K;
-    L.wave = (L.phi_off + V * K + 1) & ~1;  // 16-byte aligned waves
+    L.row_off = L.phi_off + V * K;
+    L.wave = (L.row_off + 2 * K * hmm_row_width(K, V) + 1) & ~1;  // 16-byte aligned waves
     return L;
 }
 
@@ -125,11 +182,15 @@ struct HmmEval {
     int V, D, Tsup, Tu;
     // this lane's entry
     int src;       // dimension lane of its logit; -1 for a row's fixed logit or no entry
-    int rs, rn;    // its row: first entry lane, length
+    int RW;        // row table: slots per row
+    int slot;      // this entry's slot in the row table (-1 off the entries)
+    int row0;      // first slot of its row (0 off the entries)
     double cnt1;   // 1 + its count among the observed states (0 off the entries)
-    // emission lanes: their symbol's run of occupancies in LDS
-    int g_k, g_start, g_count, g_max;  // g_max: the longest run (wave-uniform)
+    // the gather of occupancies: gather lane L takes piece L % GP of the
+    // symbol run of emission entry L / GP (GP lanes per entry)
+    int GP, g_k, g_start, g_count, g_max;  // g_max: the longest piece (wave-uniform)
     int dst;       // dimension lanes: the entry lane of the logit
+    int xi_src;    // transition lanes: the lane the wave's sum of its count ends in
     // this lane's steps: first, count, and per step symbol | position << 8
     int s0, ns;
     int sp[kHmmSteps];
@@ -137,12 +198,13 @@ struct HmmEval {
     bool no_transition0;  // Tsup == 0: step 0 emits from the initial distribution
     double* gam;
     double* phi;
+    double* rowt;
 
     __device__ bool s_writer() const { return true; }
     __device__ bool out_writer() const { return true; }
     __device__ bool aborted() const { return false; }
 
-    __device__ void init_chain(const HmmView& hv, int D_, double* gam_, double* phi_)
+    __device__ void init_chain(const HmmView& hv, int D_, double* gam_, double* phi_, double* rowt_)
     {
         const int l = lane();
         V = hv.V;
@@ -151,22 +213,28 @@ struct HmmEval {
         Tu = hv.T - hv.Tsup;
         gam = gam_;
         phi = phi_;
+        rowt = rowt_;
+        RW = hmm_row_width(K, V);
         const int KK = K * K, E = KK + K * V, nt = K * (K - 1);
         if (l < KK) {
             const int j = l / K, k = l % K;
             src = k < K - 1 ? j * (K - 1) + k : -1;
-            rs = j * K;
-            rn = K;
+            row0 = j * RW;
+            slot = row0 + k;
         } else if (l < E) {
             const int e = l - KK, k = e / V, v = e % V;
             src = v < V - 1 ? nt + k * (V - 1) + v : -1;
-            rs = KK + k * V;
-            rn = V;
+            row0 = (K + k) * RW;
+            slot = row0 + v;
         } else {
             src = -1;
-            rs = l;
-            rn = 1;
+            row0 = 0;
+            slot = -1;
         }
+        // the pads of the row table stay zero (a neutral entry for the sums,
+        // and for the maximum, which starts from the fixed logit 0)
+        for (int i = l; i < 2 * K * RW; i += kWave) rowt[i] = 0.0;
+        xi_src = scatter_lane(l < KK ? l : 0, KK);
         if (l < nt) {
             dst = (l / (K - 1)) * K + l % (K - 1);
         } else if (l < D) {
@@ -209,19 +277,26 @@ struct HmmEval {
                 if (l == v) run += __popcll(m);
             }
         }
-        g_max = 0;
+        GP = K * V * 4 <= kWave ? 4 : (K * V * 2 <= kWave ? 2 : 1);
+        int cmax = 0;
         for (int v = 0; v < V; ++v) {
             const int cv = __builtin_amdgcn_readlane(cnt, v);
-            g_max = cv > g_max ? cv : g_max;
+            cmax = cv > cmax ? cv : cmax;
         }
-        const int ev = l - KK;
-        const int gv = (l >= KK && l < E) ? ev % V : 0;
-        g_k = (l >= KK && l < E) ? ev / V : 0;
+        const int piece = (cmax + GP - 1) / GP;  // run length per piece
+        g_max = piece;
+        const int ge = l / GP, gh = l % GP;
+        const bool gl = ge < K * V;
+        const int gv = gl ? ge % V : 0;
+        g_k = gl ? ge / V : 0;
         // (cross-lane reads with every lane active: a lane outside the
         // condition would read as zero)
-        g_start = __shfl(start, gv);
+        const int st = __shfl(start, gv);
         const int gc = __shfl(cnt, gv);
-        g_count = (l >= KK && l < E) ? gc : 0;
+        const int lo = gh * piece < gc ? gh * piece : gc;
+        const int hi = (gh + 1) * piece < gc ? (gh + 1) * piece : gc;
+        g_start = st + lo;
+        g_count = gl ? hi - lo : 0;
         wave_lds_sync();
 #pragma unroll
         for (int i = 0; i < kHmmSteps; ++i) {
@@ -256,26 +331,40 @@ struct HmmEval {
         for (int k = 0; k < K; ++k) init[k] = Tsup > 0 ? (k == z0 ? 1.0 : 0.0) : 1.0 / K;
     }
 
+    // Every entry lane's value into its row slot, then over this lane's row
+    // in slot order: the maximum (from 0) or the sum (from 0).
+    template <bool MAX>
+    __device__ double row_reduce(double v)
+    {
+        wave_lds_sync();  // earlier reads of the table are done
+        if (slot >= 0) rowt[slot] = v;
+        wave_lds_sync();
+        const double* r = rowt + row0;
+        double acc = 0.0;
+        for (int i = 0; i < RW; i += 2) {
+            const double v0 = r[i], v1 = r[i + 1];
+            if constexpr (MAX) {
+                acc = v0 > acc ? v0 : acc;
+                acc = v1 > acc ? v1 : acc;
+            } else {
+                acc += v0;
+                acc += v1;
+            }
+        }
+        return acc;
+    }
+
     __device__ void eval(const double (&q)[1], double& U, double (&g)[1])
     {
         const int l = lane();
         const int KK = K * K, E = KK + K * V;
-        const int rmax = K > V ? K : V;
 
         // the rows' softmax: max with the fixed 0, then exps summed in row order
         double a = __shfl(q[0], src < 0 ? 0 : src);
         a = src < 0 ? 0.0 : a;
-        double m = 0.0;
-        for (int i = 0; i < rmax; ++i) {
-            const double ai = __shfl(a, (rs + i) & (kWave - 1));
-            if (i < rn && ai > m) m = ai;
-        }
+        const double m = row_reduce<true>(a);
         const double ex = exp_nonpos(a - m);
-        double tot = 0.0;
-        for (int i = 0; i < rmax; ++i) {
-            const double ei = __shfl(ex, (rs + i) & (kWave - 1));
-            if (i < rn) tot += ei;
-        }
+        const double tot = row_reduce<false>(ex);
         const double lx = a - (m + log(tot));
         const double x = exp_nonpos(lx);
 
@@ -471,13 +560,16 @@ struct HmmEval {
 
         // 4. G = df/d log x on the entry lanes
         double G = cnt1;
+        {
+            double flat[K * K];
 #pragma unroll
-        for (int j = 0; j < K; ++j)
+            for (int j = 0; j < K; ++j)
 #pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const double sx = wave_sum(xi[j][k]);
-                if (l == j * K + k) G += sx;
-            }
+                for (int k = 0; k < K; ++k) flat[j * K + k] = xi[j][k];
+            const double tot = scatter_stage<32, K * K>(flat);
+            const double sx = __shfl(tot, xi_src);
+            if (l < KK) G += sx;
+        }
         double gs = 0.0;
         for (int i0 = 0; i0 < g_max; i0 += 4) {
             double t4[4];
@@ -486,14 +578,15 @@ struct HmmEval {
 #pragma unroll
             for (int u = 0; u < 4; ++u) gs += t4[u];
         }
-        G += gs;
+        // an emission entry's pieces, in time order
+        const int gbase = ((l - KK) * GP) & (kWave - 1);
+        for (int h = 0; h < GP; ++h) {
+            const double ph = __shfl(gs, (gbase + h) & (kWave - 1));
+            if (l >= KK && l < E) G += ph;
+        }
 
         // 5. through the softmax, then onto the dimension lanes
-        double rowG = 0.0;
-        for (int i = 0; i < rmax; ++i) {
-            const double gi = __shfl(G, (rs + i) & (kWave - 1));
-            if (i < rn) rowG += gi;
-        }
+        const double rowG = row_reduce<false>(G);
         const double ga = -(G - x * rowG);
         const double gd = __shfl(ga, dst);
         g[0] = l < D ? gd : 0.0;
@@ -512,7 +605,7 @@ __global__ void __launch_bounds__(kHmmChainsPerGroup * kWave, 2) sampler_hmm_ker
     const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, A.data.D, A.max_depth);
     double* base = lds + (int64_t)wave * L.wave;
     HmmEval<K> ev;
-    ev.init_chain(hv, A.data.D, base + L.gam_off, base + L.phi_off);
+    ev.init_chain(hv, A.data.D, base + L.gam_off, base + L.phi_off, base + L.row_off);
     run_chain<1, EXT>(A, ev, chain, base + L.s_off);
 }
 
@@ -530,7 +623,7 @@ __global__ void __launch_bounds__(kHmmChainsPerGroup * kWave, 2) hmm_potential_k
     const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, D, 1);
     double* base = lds + (int64_t)wave * L.wave;
     HmmEval<K> ev;
-    ev.init_chain(hv, D, base + L.gam_off, base + L.phi_off);
+    ev.init_chain(hv, D, base + L.gam_off, base + L.phi_off, base + L.row_off);
     double q[1] = {l < D ? Q[p * D + l] : 0.0}, U, g[1];
     ev.eval(q, U, g);
     if (l < D) out_grad[p * D + l] = g[0];
