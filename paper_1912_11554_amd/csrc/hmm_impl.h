@@ -74,11 +74,17 @@ __device__ __forceinline__ void set_identity(double (&P)[K][K])
 template <int K>
 __device__ __forceinline__ void unit_scale(double (&P)[K][K])
 {
-    double mx = 0.0;
+    // the maximum as a tree (short dependency chains)
+    double m[K * K];
 #pragma unroll
     for (int r = 0; r < K; ++r)
 #pragma unroll
-        for (int c = 0; c < K; ++c) mx = fmax(mx, P[r][c]);
+        for (int c = 0; c < K; ++c) m[r * K + c] = P[r][c];
+#pragma unroll
+    for (int w = 1; w < K * K; w *= 2)
+#pragma unroll
+        for (int i = 0; i + w < K * K; i += 2 * w) m[i] = fmax(m[i], m[i + w]);
+    const double mx = m[0];
     int e = 0;
     (void)frexp(mx, &e);
 #pragma unroll
