@@ -243,13 +243,19 @@ def run_hmm(chains, steps, warmup):
     r0 = s.hmm_sample(w, z, K, V, num_warmup=warmup, num_samples=1, **kw)
     samples = torch.empty((chains, steps, D), dtype=torch.float64, device="cuda")
     stats = torch.empty((chains, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
+    outs = dict(out_final_q=torch.empty((chains, D), dtype=torch.float64, device="cuda"),
+                out_inv_mass=torch.empty((chains, D), dtype=torch.float64, device="cuda"),
+                out_step_size=torch.empty(chains, dtype=torch.float64, device="cuda"))
     stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
-    r = s.hmm_sample(w, z, K, V, num_warmup=0, num_samples=steps, init_q=r0["final_q"],
-                     first_iter=warmup + 1, out_samples=samples, out_stats=stats, **kw)
+    q0 = torch.from_numpy(r0["final_q"]).cuda()
+    kw["inv_mass"] = torch.from_numpy(np.ascontiguousarray(im)).cuda()
+    torch.cuda.synchronize()
+    r = s.hmm_sample(w, z, K, V, num_warmup=0, num_samples=steps, init_q=q0,
+                     first_iter=warmup + 1, out_samples=samples, out_stats=stats, **outs, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     gpu_s = ev0.elapsed_time(ev1) / 1e3

@@ -130,6 +130,18 @@ def _ptr(a):
     return a.data_ptr()
 
 
+def _as_f64(a):
+    """An fp64 input as a contiguous numpy array, or a device tensor as is
+    (it must already be contiguous fp64)."""
+    if a is None:
+        return None
+    if hasattr(a, "data_ptr") and not isinstance(a, np.ndarray):
+        if str(a.dtype) != "torch.float64" or not a.is_contiguous():
+            raise TypeError("device inputs must be contiguous float64 tensors")
+        return a
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
 def _dtype_code(X):
     name = str(X.dtype)
     if name.endswith("float64"):
@@ -238,10 +250,12 @@ class Sampler:
     def hmm_sample(self, w, z, K, V, *, step_size, max_tree_depth, num_warmup, num_samples,
                    num_chains=1, seed=0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                    first_iter=0, adapt_step_size=False, target_accept=0.8,
-                   uturn_generalized=False, out_samples=None, out_stats=None):
+                   uturn_generalized=False, out_samples=None, out_stats=None, out_final_q=None,
+                   out_inv_mass=None, out_step_size=None):
         """NUTS on the semi-supervised HMM (one wavefront per chain).  Returns
         the same dict as ``Data.sample``; samples hold the logits (numpy
-        unless device tensors are passed in out_samples / out_stats)."""
+        unless device tensors are passed in the out_* arguments, which are
+        then filled and returned)."""
         w, z = self._hmm_seq(w, z)
         C, D = num_chains, hmm_dim(K, V)
         flags = (NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
@@ -251,10 +265,12 @@ class Sampler:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:
             out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
-        final_q, out_im, out_eps = np.zeros((C, D)), np.zeros((C, D)), np.zeros(C)
+        final_q = np.zeros((C, D)) if out_final_q is None else out_final_q
+        out_im = np.zeros((C, D)) if out_inv_mass is None else out_inv_mass
+        out_eps = np.zeros(C) if out_step_size is None else out_step_size
         gev = np.zeros(1, dtype=np.int64)
-        im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)
-        iq = None if init_q is None else np.ascontiguousarray(init_q, dtype=np.float64)
+        im = _as_f64(inv_mass)
+        iq = _as_f64(init_q)
         opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), NUTS_PATH_AUTO,
                      0, target_accept, _ptr(out_eps))
         self._check(self._L.nuts_hmm_sample(
@@ -340,8 +356,8 @@ class Data:
         out_im = np.zeros((C, D))
         out_eps = np.zeros(C)
         gev = np.zeros(1, dtype=np.int64)
-        im = None if inv_mass is None else np.ascontiguousarray(inv_mass, dtype=np.float64)
-        iq = None if init_q is None else np.ascontiguousarray(init_q, dtype=np.float64)
+        im = _as_f64(inv_mass)
+        iq = _as_f64(init_q)
         opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), path, 0,
                      target_accept, _ptr(out_eps))
         self.s._check(self.s._L.nuts_sample_data(
