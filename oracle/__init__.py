@@ -96,7 +96,7 @@ def lib():
         L.orc_check_range.argtypes = [u64, P, P]
         L.orc_nuts_chain.argtypes = [
             i32, P, P, P, i64, i64, dbl, dbl, dbl, P, i32, i64, i64, u64, u64, i32, i32, P,
-            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P, i32, P, i64, i32, i32,
+            i64, P, P, P, P, P, i64, P, P, i64, P, u64, i32, dbl, P, i32, P, i64, i32, i32, i32,
         ]
         L.orc_nuts_chain.restype = i64
         L.orc_leapfrog_steps.argtypes = [i32, P, P, P, i64, i64, dbl, dbl, P, dbl, i64, P, P]
@@ -232,7 +232,7 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
          prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
          init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
          trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8,
-         uturn_generalized=False, hmm=None):
+         uturn_generalized=False, hmm=None, subtree_merge=False):
     """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
     final_q [D], inv_mass [D], step_size (the one in use at the end: the
     adapted one with adapt_step_size), grad_evals; with trace_cap the U-turn check
@@ -241,7 +241,8 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
     re-keys the proposal-selection draws and nothing else.  uturn_generalized
     selects the momentum-sum criterion (reading R20).  With hmm = dict(w, z,
     K, V) the target is the semi-supervised HMM (reading R21) and X, y are
-    ignored."""
+    ignored.  subtree_merge chooses each subtree's proposal at the merges of
+    its halves (reading R22) instead of by the streaming choice."""
     hz = None
     if hmm is not None:
         target = TARGET_HMM
@@ -270,7 +271,7 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
         ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
         ctypes.byref(eps_out), 1 if uturn_generalized else 0, _p(hz),
         0 if hz is None else hz.shape[0], 0 if hmm is None else hmm["K"],
-        0 if hmm is None else hmm["V"],
+        0 if hmm is None else hmm["V"], 1 if subtree_merge else 0,
     )
     out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im,
                step_size=eps_out.value, grad_evals=nev)

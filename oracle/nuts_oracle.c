@@ -109,7 +109,8 @@ void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint6
 }
 
 /* Draw tags: which random quantity a Philox block feeds (reading R8). */
-enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4, ORC_TAG_STEP = 5 };
+enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4, ORC_TAG_STEP = 5,
+       ORC_TAG_SUBMERGE = 6 };
 
 static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, uint64_t j,
                       uint64_t n, uint64_t out[4])
@@ -168,6 +169,16 @@ double orc_u_leaf(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_
 {
     uint64_t w[4];
     orc_block(seed, chain, t, ORC_TAG_LEAF, j, n, w);
+    return orc_u53(w[0]);
+}
+
+/* Reading R22: the uniform of the merge of two halves inside subtree j,
+ * named by its gap m = the last leaf of the left half (each of the 2^j - 1
+ * merges of a subtree has its own gap). */
+double orc_u_submerge(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_t m)
+{
+    uint64_t w[4];
+    orc_block(seed, chain, t, ORC_TAG_SUBMERGE, j, m, w);
     return orc_u53(w[0]);
 }
 
@@ -570,6 +581,10 @@ typedef struct {
     double sum_accept;
     /* reading R20: the generalised criterion instead of the endpoint one */
     int gen;
+    /* reading R22: the subtree's proposal chosen at the merges of its halves
+     * instead of by the streaming choice; -(H - H0) of the last leaf */
+    int smerge;
+    double last_lam;
 } orc_iter;
 
 /* What a subtree hands back: the streaming proposal and its log-weight. */
@@ -616,6 +631,10 @@ static int orc_leaf(orc_iter *it, orc_sub *sub, const orc_node *z, int j, int64_
         return ORC_DIVERGENT;
     }
     double lam = -dH;
+    if (it->smerge) {
+        it->last_lam = lam;
+        return ORC_OK;
+    }
     double logw_new = orc_logaddexp(sub->logw, lam);
     double u = orc_u_leaf(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j, (uint64_t)n);
     if (u < exp(lam - logw_new)) {
@@ -645,9 +664,48 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
     double *rsum = sub->rho;
     double *rho = (double *)malloc((size_t)D * sizeof(double));
     for (int64_t k = 0; k < D; ++k) rsum[k] = 0.0;
+    /* R22: the proposal, log-weight and offset of the completed left block
+     * waiting at each level, and those of the block ending at this leaf */
+    orc_node stk[64], cp;
+    double stk_lw[64], c_lw = 0.0;
+    int64_t stk_idx[64], c_idx = 0;
+    if (it->smerge) {
+        for (int k = 0; k < nslots; ++k) orc_node_alloc(&stk[k], D);
+        orc_node_alloc(&cp, D);
+    }
     for (int64_t n = 0; n < nleaf; ++n) {
         orc_leapfrog(it->tg, z, (double)v * it->eps, it->inv_mass);
         if (orc_leaf(it, sub, z, j, n, e, v) != ORC_OK) break;
+        if (it->smerge) {
+            /* the leaf is a block of one; every completed pair of equal
+             * blocks merges, the later half's proposal kept with probability
+             * its share of the weight */
+            orc_node_copy(&cp, z, D);
+            c_lw = it->last_lam;
+            c_idx = e + (int64_t)v * (n + 1);
+            int k = 0;
+            while ((n >> k) & 1) {
+                double lw = orc_logaddexp(stk_lw[k], c_lw);
+                double u = orc_u_submerge(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j,
+                                          (uint64_t)(n - ((int64_t)1 << k)));
+                if (!(u < exp(c_lw - lw))) {
+                    orc_node_copy(&cp, &stk[k], D);
+                    c_idx = stk_idx[k];
+                }
+                c_lw = lw;
+                ++k;
+            }
+            if (n + 1 < nleaf) {
+                orc_node_copy(&stk[k], &cp, D);
+                stk_lw[k] = c_lw;
+                stk_idx[k] = c_idx;
+            } else {
+                orc_node_copy(&sub->prop, &cp, D);
+                sub->prop_idx = c_idx;
+                sub->logw = c_lw;
+                sub->has_prop = 1;
+            }
+        }
         for (int64_t k = 0; k < D; ++k) rsum[k] += z->p[k];
         if ((n & 1) == 0) {
             int i = orc_bitcount((uint64_t)n);
@@ -684,6 +742,10 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
             }
         }
     }
+    if (it->smerge) {
+        for (int k = 0; k < nslots; ++k) orc_node_free(&stk[k]);
+        orc_node_free(&cp);
+    }
     free(rho);
     free(Sq);
     free(Sp);
@@ -694,7 +756,8 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
  * the left half and the last leaf of the right half.  Leaves are numbered
  * from `offset`; the first leaf's (q, p) is returned in fq/fp. */
 static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t offset, int v,
-                                int64_t e, orc_sub *sub, double *fq, double *fp, double *rho)
+                                int64_t e, orc_sub *sub, double *fq, double *fp, double *rho,
+                                orc_node *mp, double *mlw, int64_t *midx)
 {
     int64_t D = it->tg->D;
     if (d == 0) {
@@ -703,19 +766,41 @@ static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t
         memcpy(fq, z->q, (size_t)D * sizeof(double));
         memcpy(fp, z->p, (size_t)D * sizeof(double));
         memcpy(rho, z->p, (size_t)D * sizeof(double));
+        if (it->smerge) {  /* R22: a leaf is its own block's proposal */
+            orc_node_copy(mp, z, D);
+            *mlw = it->last_lam;
+            *midx = e + (int64_t)v * (offset + 1);
+        }
         return;
     }
-    orc_build_recursive(it, z, j, d - 1, offset, v, e, sub, fq, fp, rho);
+    orc_build_recursive(it, z, j, d - 1, offset, v, e, sub, fq, fp, rho, mp, mlw, midx);
     if (sub->status != ORC_OK) return;
     double *rq = (double *)malloc((size_t)D * sizeof(double));
     double *rp = (double *)malloc((size_t)D * sizeof(double));
     double *rr = (double *)malloc((size_t)D * sizeof(double));
     int64_t half = (int64_t)1 << (d - 1);
-    orc_build_recursive(it, z, j, d - 1, offset + half, v, e, sub, rq, rp, rr);
+    orc_node rprop;
+    double rlw = 0.0;
+    int64_t ridx = 0;
+    if (it->smerge) orc_node_alloc(&rprop, D);
+    orc_build_recursive(it, z, j, d - 1, offset + half, v, e, sub, rq, rp, rr, &rprop, &rlw, &ridx);
     for (int64_t k = 0; k < D; ++k) rho[k] += rr[k];
     free(rq);
     free(rp);
     free(rr);
+    if (it->smerge && sub->status == ORC_OK) {
+        /* R22: merge the halves; the later one's proposal with probability
+         * its share of the weight, drawn at the gap between them */
+        double lw = orc_logaddexp(*mlw, rlw);
+        double u = orc_u_submerge(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j,
+                                  (uint64_t)(offset + half - 1));
+        if (u < exp(rlw - lw)) {
+            orc_node_copy(mp, &rprop, D);
+            *midx = ridx;
+        }
+        *mlw = lw;
+    }
+    if (it->smerge) orc_node_free(&rprop);
     if (sub->status != ORC_OK) return;
     int64_t last = offset + 2 * half - 1;
     orc_trace_check(it, offset, last);
@@ -789,9 +874,11 @@ static void orc_iteration(orc_iter *it, orc_node *cur, int max_depth, int builde
         sub.logw = -INFINITY;
         sub.prop_idx = 0;
         sub.has_prop = 0;
-        if (builder == ORC_BUILDER_RECURSIVE)
-            orc_build_recursive(it, &z, j, j, 0, v, e, &sub, fq, fp, sub.rho);
-        else
+        if (builder == ORC_BUILDER_RECURSIVE) {
+            orc_build_recursive(it, &z, j, j, 0, v, e, &sub, fq, fp, sub.rho, &sub.prop, &sub.logw,
+                                &sub.prop_idx);
+            if (it->smerge) sub.has_prop = 1;
+        } else
             orc_build_iterative(it, &z, j, v, e, &sub);
         st->tree_depth = j + 1;
         if (sub.status != ORC_OK) {
@@ -992,7 +1079,8 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
                        int64_t trace_cap, int64_t *trace_len, int64_t *leaves,
                        int64_t leaves_cap, int64_t *leaves_len, uint64_t sel_salt,
                        int adapt_step, double target_accept, double *out_step_size,
-                       int uturn_gen, const uint8_t *hmm_z, int64_t hmm_tsup, int hmm_k, int hmm_v)
+                       int uturn_gen, const uint8_t *hmm_z, int64_t hmm_tsup, int hmm_k, int hmm_v,
+                       int sub_merge)
 {
     orc_target tg = { kind, X, y, yv, N, D, s, sn, 0 };
     tg.z = hmm_z;
@@ -1020,6 +1108,7 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
     it.leaves_cap = leaves_cap;
     it.sel_salt = sel_salt;
     it.gen = uturn_gen;
+    it.smerge = sub_merge;
 
     orc_welford wf = { 0, (double *)calloc((size_t)D, sizeof(double)),
                        (double *)calloc((size_t)D, sizeof(double)) };
