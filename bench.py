@@ -48,7 +48,7 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_workload(name, steps=None, warmup=None, adapt=False):
+def run_workload(name, steps=None, warmup=None, adapt=False, variants=None):
     import torch
 
     import paper_1912_11554_amd as nuts
@@ -85,7 +85,7 @@ def run_workload(name, steps=None, warmup=None, adapt=False):
     else:
         path, kernel = nuts.NUTS_PATH_BATCH, "sampler_batch_kernel"
     kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
-              prior_scale=wl.prior_scale, num_chains=C, path=path)
+              prior_scale=wl.prior_scale, num_chains=C, path=path, **(variants or {}))
 
     t0 = time.time()
     if adapt and C != 1:
@@ -141,7 +141,7 @@ def run_workload(name, steps=None, warmup=None, adapt=False):
     s.close()
     return dict(
         workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=kw["step_size"],
-        step_size_adapted=bool(adapt),
+        step_size_adapted=bool(adapt), variants=sorted(k for k, v in (variants or {}).items() if v),
         max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
         gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
         evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
@@ -337,6 +337,10 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run a plain device copy of this many MiB (a known-size "
                          "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+    ap.add_argument("--uturn-generalized", action="store_true",
+                    help="the generalised (momentum-sum) U-turn criterion")
+    ap.add_argument("--subtree-merge", action="store_true",
+                    help="subtree proposals chosen at the merges of halves")
     ap.add_argument("--hmm-chains", type=int, default=8192,
                     help="chains of the semi-supervised HMM reported beside the main workload "
                          "(0: no HMM line)")
@@ -360,8 +364,9 @@ def main():
         h = run_hmm(args.hmm_chains, args.hmm_steps, 20)
         print(json.dumps(hmm_line(h, None)), flush=True)
         return
-    main_res = run_workload(args.workload, args.steps, args.warmup, args.adapt)
-    other = run_workload(args.also, args.steps, args.warmup, args.adapt) if args.also else None
+    variants = dict(uturn_generalized=args.uturn_generalized, subtree_merge=args.subtree_merge)
+    main_res = run_workload(args.workload, args.steps, args.warmup, args.adapt, variants)
+    other = run_workload(args.also, args.steps, args.warmup, args.adapt, variants) if args.also else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
 
     achieved = main_res["achieved_gbs"]
@@ -404,7 +409,7 @@ def main():
         "config": {
             "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
             "chains": main_res["chains"], "step_size": main_res["step_size"],
-            "step_size_adapted": main_res["step_size_adapted"],
+            "step_size_adapted": main_res["step_size_adapted"], "variants": main_res["variants"],
             "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
             "path": main_res["kernel"],
         },

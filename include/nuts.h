@@ -59,7 +59,8 @@ enum {
     NUTS_DATA_PER_CHAIN = 1u << 0,  /* X is [C][N][D] and y is [C][N]; else one shared data set */
     NUTS_ADAPT_DIAG_MASS = 1u << 1,    /* set the diagonal inverse mass from warmup draws */
     NUTS_UTURN_GENERALIZED = 1u << 2,  /* U-turn on momentum sums (Betancourt 2017, App. A.4.2) */
-    NUTS_ADAPT_STEP_SIZE = 1u << 3     /* adapt the step size during warmup (dual averaging) */
+    NUTS_ADAPT_STEP_SIZE = 1u << 3,    /* adapt the step size during warmup (dual averaging) */
+    NUTS_SUBTREE_MERGE = 1u << 4       /* subtree proposals chosen at the merges of halves */
 };
 
 /* Kernel path selection for nuts_sample_data (opts->path). */
@@ -200,6 +201,17 @@ typedef struct {
  * iterative builder then keeps in S[BitCount(n)] the leaf's momentum and the
  * subtree's momentum sum before the leaf; the candidate set C(n) is
  * unchanged. */
+/* NUTS_SUBTREE_MERGE replaces the streaming choice of a subtree's proposal
+ * (each new leaf taken with probability its share of the weight so far) by
+ * the merge-structured one of Betancourt (2017, App. A.3): inside a subtree
+ * every pair of completed equal halves merges, keeping the later half's
+ * proposal with probability W_later / (W_earlier + W_later), one uniform per
+ * merge under tag 6 indexed by the merge's ordinal among the subtree's
+ * 2^j - 1 merges in completion order (the merge of the block of 2^d leaves
+ * ending at leaf n is number n - BitCount(n) + d - 1).  The selection distribution is the same; the
+ * draws differ.  The iterative builder keeps one waiting block per level
+ * (its proposal and weight) in LDS beside S; NUTS_EUNSUPPORTED where a
+ * path's tree state then no longer fits a CU. */
 int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double prior_scale,
                      double step_size, const double* inv_mass_diag, int max_tree_depth,
                      int64_t num_warmup, int64_t num_samples, int64_t num_chains, uint64_t seed,
@@ -238,8 +250,9 @@ int nuts_hmm_potential_grad(nuts_handle* h, const uint8_t* w, int64_t T, const u
 
 /* nuts_hmm_sample: NUTS on the model above, one wavefront per chain, with
  * the meaning of every other argument, flag and option as in
- * nuts_sample_data (flags NUTS_ADAPT_DIAG_MASS, NUTS_ADAPT_STEP_SIZE and
- * NUTS_UTURN_GENERALIZED; opts->path NUTS_PATH_AUTO or NUTS_PATH_WAVE).
+ * nuts_sample_data (flags NUTS_ADAPT_DIAG_MASS, NUTS_ADAPT_STEP_SIZE,
+ * NUTS_UTURN_GENERALIZED and NUTS_SUBTREE_MERGE; opts->path NUTS_PATH_AUTO
+ * or NUTS_PATH_WAVE).
  * Chains start at init_q or at q = 0 (uniform rows).  Writes out_samples
  * [C][S][D] (the logits) and out_stats [C][S]. */
 int nuts_hmm_sample(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int64_t Tsup, int K, int V,

@@ -172,14 +172,22 @@ double orc_u_leaf(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_
     return orc_u53(w[0]);
 }
 
-/* Reading R22: the uniform of the merge of two halves inside subtree j,
- * named by its gap m = the last leaf of the left half (each of the 2^j - 1
- * merges of a subtree has its own gap). */
-double orc_u_submerge(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_t m)
+/* Reading R22: the uniform of a merge of two halves inside subtree j, named
+ * by its ordinal P among the subtree's 2^j - 1 merges in the order they
+ * complete (the merge of the block of 2^d leaves ending at leaf n is number
+ * n - BitCount(n) + d - 1). */
+double orc_u_submerge(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_t P)
 {
     uint64_t w[4];
-    orc_block(seed, chain, t, ORC_TAG_SUBMERGE, j, m, w);
+    orc_block(seed, chain, t, ORC_TAG_SUBMERGE, j, P, w);
     return orc_u53(w[0]);
+}
+
+int orc_bitcount(uint64_t n);
+
+static uint64_t orc_merge_ordinal(int64_t n, int d)
+{
+    return (uint64_t)(n - (int64_t)orc_bitcount((uint64_t)n) + d - 1);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -687,7 +695,7 @@ static void orc_build_iterative(orc_iter *it, orc_node *z, int j, int v, int64_t
             while ((n >> k) & 1) {
                 double lw = orc_logaddexp(stk_lw[k], c_lw);
                 double u = orc_u_submerge(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j,
-                                          (uint64_t)(n - ((int64_t)1 << k)));
+                                          orc_merge_ordinal(n, k + 1));
                 if (!(u < exp(c_lw - lw))) {
                     orc_node_copy(&cp, &stk[k], D);
                     c_idx = stk_idx[k];
@@ -790,10 +798,10 @@ static void orc_build_recursive(orc_iter *it, orc_node *z, int j, int d, int64_t
     free(rr);
     if (it->smerge && sub->status == ORC_OK) {
         /* R22: merge the halves; the later one's proposal with probability
-         * its share of the weight, drawn at the gap between them */
+         * its share of the weight */
         double lw = orc_logaddexp(*mlw, rlw);
         double u = orc_u_submerge(it->seed ^ it->sel_salt, it->chain, it->t, (uint64_t)j,
-                                  (uint64_t)(offset + half - 1));
+                                  orc_merge_ordinal(offset + 2 * half - 1, d));
         if (u < exp(rlw - lw)) {
             orc_node_copy(mp, &rprop, D);
             *midx = ridx;

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libnuts.so")
 NUTS_OK, NUTS_EINVAL, NUTS_ENOMEM, NUTS_EDEVICE, NUTS_EUNSUPPORTED = 0, -1, -2, -3, -4
 NUTS_F64, NUTS_F32 = 0, 1
 NUTS_DATA_PER_CHAIN, NUTS_ADAPT_DIAG_MASS, NUTS_UTURN_GENERALIZED, NUTS_ADAPT_STEP_SIZE = 1, 2, 4, 8
+NUTS_SUBTREE_MERGE = 16
 NUTS_PATH_AUTO, NUTS_PATH_WAVE, NUTS_PATH_GRID, NUTS_PATH_BATCH = 0, 1, 2, 3
 
 EXPORTED = [
@@ -250,8 +251,8 @@ class Sampler:
     def hmm_sample(self, w, z, K, V, *, step_size, max_tree_depth, num_warmup, num_samples,
                    num_chains=1, seed=0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                    first_iter=0, adapt_step_size=False, target_accept=0.8,
-                   uturn_generalized=False, out_samples=None, out_stats=None, out_final_q=None,
-                   out_inv_mass=None, out_step_size=None):
+                   uturn_generalized=False, subtree_merge=False, out_samples=None, out_stats=None,
+                   out_final_q=None, out_inv_mass=None, out_step_size=None):
         """NUTS on the semi-supervised HMM (one wavefront per chain).  Returns
         the same dict as ``Data.sample``; samples hold the logits (numpy
         unless device tensors are passed in the out_* arguments, which are
@@ -260,7 +261,8 @@ class Sampler:
         C, D = num_chains, hmm_dim(K, V)
         flags = (NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
             NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0) | (
-            NUTS_UTURN_GENERALIZED if uturn_generalized else 0)
+            NUTS_UTURN_GENERALIZED if uturn_generalized else 0) | (
+            NUTS_SUBTREE_MERGE if subtree_merge else 0)
         if out_samples is None:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:
@@ -337,7 +339,8 @@ class Data:
     def sample(self, *, step_size, max_tree_depth, num_warmup, num_samples, num_chains=1,
                seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None,
-               adapt_step_size=False, target_accept=0.8, uturn_generalized=False):
+               adapt_step_size=False, target_accept=0.8, uturn_generalized=False,
+               subtree_merge=False):
         """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
         (STATS_DTYPE), final_q [C, D], inv_mass [C, D], step_size [C] (in use
         at the end: the adapted one with adapt_step_size), grad_evals.  Outputs
@@ -347,7 +350,8 @@ class Data:
         flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
             NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
             NUTS_ADAPT_STEP_SIZE if adapt_step_size else 0) | (
-            NUTS_UTURN_GENERALIZED if uturn_generalized else 0)
+            NUTS_UTURN_GENERALIZED if uturn_generalized else 0) | (
+            NUTS_SUBTREE_MERGE if subtree_merge else 0)
         if out_samples is None:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:

@@ -277,6 +277,7 @@ struct RunBuffers {
         a.adapt_diag = (flags & NUTS_ADAPT_DIAG_MASS) ? 1 : 0;
         a.adapt_step = (flags & NUTS_ADAPT_STEP_SIZE) ? 1 : 0;
         a.uturn_gen = (flags & NUTS_UTURN_GENERALIZED) ? 1 : 0;
+        a.sub_merge = (flags & NUTS_SUBTREE_MERGE) ? 1 : 0;
         a.target_accept = target_accept;
         a.init_q = (const double*)iq_d;
         a.out_samples = (double*)smp_d;
@@ -675,12 +676,13 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
     double target_accept = 0.0;
     int rc = check_run(h, flags, NUTS_DATA_PER_CHAIN | NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE |
-                                     NUTS_UTURN_GENERALIZED,
+                                     NUTS_UTURN_GENERALIZED | NUTS_SUBTREE_MERGE,
                        o, step_size, max_tree_depth, num_warmup, num_samples, num_chains, &target_accept);
     if (rc != NUTS_OK) return rc;
     if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
     if (d->view.N < 1) return fail(h, NUTS_EINVAL, "sampling needs N >= 1");
     const bool per_chain = (flags & NUTS_DATA_PER_CHAIN) != 0;
+    const int sub_merge = (flags & NUTS_SUBTREE_MERGE) ? 1 : 0;
     if (per_chain && d->view.nds != num_chains)
         return fail(h, NUTS_EINVAL, "NUTS_DATA_PER_CHAIN: data holds %lld sets for %lld chains",
                     (long long)d->view.nds, (long long)num_chains);
@@ -707,9 +709,10 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
         probe.data = d->view;
         probe.max_depth = max_tree_depth;
         probe.num_chains = num_chains;
+        probe.sub_merge = sub_merge;
         const bool resident = wave_path_supports(d->view) && wave_path_resident(probe);
         if (batchable && ensure_batch_layout(h, d) == NUTS_OK &&
-            batch_sampler_supported(d->batch, max_tree_depth, h->num_cu))
+            batch_sampler_supported(d->batch, max_tree_depth, sub_merge, h->num_cu))
             path = NUTS_PATH_BATCH;
         else
             path = ((per_chain || small || resident || num_chains > 1) && wave_path_supports(d->view))
@@ -726,7 +729,7 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
     if (path == NUTS_PATH_BATCH) {
         const int rc = ensure_batch_layout(h, d);
         if (rc != NUTS_OK) return rc;
-        if (!batch_sampler_supported(d->batch, max_tree_depth, h->num_cu))
+        if (!batch_sampler_supported(d->batch, max_tree_depth, sub_merge, h->num_cu))
             return fail(h, NUTS_EUNSUPPORTED, "the batch path needs >= %d compute units and D <= 132",
                         kBatchTileChains);
     }
@@ -777,7 +780,10 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
                             (long long)c0);
         }
     } else {
-        const int groups = grid_sampler_groups(d->view, max_tree_depth, h->num_cu);
+        const int groups = grid_sampler_groups(d->view, max_tree_depth, sub_merge, h->num_cu);
+        if (groups == 0)
+            return fail(h, NUTS_EUNSUPPORTED, "the grid path's tree state (D = %d, depth %d) does not fit a CU's LDS",
+                        D, max_tree_depth);
         const size_t part_bytes = align256((size_t)grid_partial_elems(D, groups) * sizeof(double));
         const size_t res_bytes = align256((size_t)grid_result_elems(D) * sizeof(double));
         void* scratch = nullptr;
@@ -840,7 +846,9 @@ int nuts_hmm_sample(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* 
     std::memset(&o, 0, sizeof o);
     if (opts) o = *opts;
     double target_accept = 0.0;
-    int rc = check_run(h, flags, NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE | NUTS_UTURN_GENERALIZED, o, step_size,
+    int rc = check_run(h, flags,
+                       NUTS_ADAPT_DIAG_MASS | NUTS_ADAPT_STEP_SIZE | NUTS_UTURN_GENERALIZED | NUTS_SUBTREE_MERGE, o,
+                       step_size,
                        max_tree_depth, num_warmup, num_samples, num_chains, &target_accept);
     if (rc != NUTS_OK) return rc;
     if (o.path != NUTS_PATH_AUTO && o.path != NUTS_PATH_WAVE)

@@ -737,18 +737,17 @@ const void* batch_kernel_for(const BatchView& bv, bool adapt)
 
 size_t batch_sampler_lds(const SamplerArgs& a)
 {
-    const int slots = a.max_depth > 1 ? a.max_depth : 1;
-    return (size_t)slots * 2 * a.data.D * sizeof(double);
+    return (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge) * sizeof(double);
 }
 
 }  // namespace
 
-bool batch_sampler_supported(const BatchView& bv, int max_depth, int num_cu)
+bool batch_sampler_supported(const BatchView& bv, int max_depth, int sub_merge, int num_cu)
 {
     if (bv.D > 64 * 3 || num_cu < kBatchTileChains) return false;
     int per_cu = 0;
-    const size_t lds = (size_t)(max_depth > 1 ? max_depth : 1) * 2 * bv.D * sizeof(double);
-    const void* k = batch_kernel_for(bv, false);
+    const size_t lds = (size_t)chain_lds_doubles(bv.D, max_depth, sub_merge) * sizeof(double);
+    const void* k = batch_kernel_for(bv, sub_merge != 0);
     if (!k) return false;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGroupWaves * kWave, lds) != hipSuccess) return false;
     return per_cu >= 1;
@@ -766,6 +765,8 @@ hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int t
     void* args[] = {&A, &B, &tiles, &groups, &qbuf, &P, &L, &sync};
     const void* k = batch_kernel_for(bv, sampler_extended(a));
     if (!k) return hipErrorInvalidValue;
+    e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)batch_sampler_lds(a));
+    if (e != hipSuccess) return e;
     return hipLaunchCooperativeKernel(k, dim3((unsigned)(tiles * groups)),
                                       dim3(kGroupWaves * kWave), args, (unsigned)batch_sampler_lds(a), stream);
 }

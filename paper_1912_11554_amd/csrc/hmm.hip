@@ -15,7 +15,7 @@ static hipError_t potential_launch(const HmmView& hv, const double* Q, int64_t n
                                    hipStream_t stream)
 {
     const int D = hmm_dim(hv.K, hv.V);
-    const hmm::HmmLds L = hmm::hmm_lds(K, hv.V, hv.T, hv.Tsup, D, 1);
+    const hmm::HmmLds L = hmm::hmm_lds(K, hv.V, hv.T, hv.Tsup, D, 1, 0);
     const int cpg = hmm::hmm_chains_per_group(L, n);
     if (cpg == 0) return hipErrorInvalidValue;
     const size_t lds = (size_t)cpg * L.wave * sizeof(double);

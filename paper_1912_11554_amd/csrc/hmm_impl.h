@@ -170,13 +170,12 @@ struct HmmLds {
 // Slots of one simplex row in the row table: the longer row length, even.
 __host__ __device__ inline int hmm_row_width(int K, int V) { return ((K > V ? K : V) + 1) & ~1; }
 
-__host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, int max_depth)
+__host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, int max_depth, int sub_merge)
 {
     HmmLds L;
-    const int slots = max_depth > 1 ? max_depth : 1;
     const int tu = T - Tsup > 1 ? T - Tsup : 1;
     L.s_off = 0;
-    L.gam_off = slots * 2 * D;
+    L.gam_off = (int)chain_lds_doubles(D, max_depth, sub_merge);
     L.phi_off = L.gam_off + tu * K;
     L.row_off = L.phi_off + V * K;
     L.wave = (L.row_off + 2 * K * hmm_row_width(K, V) + 1) & ~1;  // 16-byte aligned waves
@@ -608,7 +607,7 @@ __global__ void __launch_bounds__(kHmmChainsPerGroup * kWave, 2) sampler_hmm_ker
     const int wave = threadIdx.x / kWave;
     const int64_t chain = (int64_t)blockIdx.x * cpg + wave;
     if (wave >= cpg || chain >= A.num_chains) return;
-    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, A.data.D, A.max_depth);
+    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, A.data.D, A.max_depth, EXT ? A.sub_merge : 0);
     double* base = lds + (int64_t)wave * L.wave;
     HmmEval<K> ev;
     ev.init_chain(hv, A.data.D, base + L.gam_off, base + L.phi_off, base + L.row_off);
@@ -626,7 +625,7 @@ __global__ void __launch_bounds__(kHmmChainsPerGroup * kWave, 2) hmm_potential_k
     const int64_t p = (int64_t)blockIdx.x * cpg + wave;
     if (wave >= cpg || p >= n) return;
     const int l = lane();
-    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, D, 1);
+    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, D, 1, 0);
     double* base = lds + (int64_t)wave * L.wave;
     HmmEval<K> ev;
     ev.init_chain(hv, D, base + L.gam_off, base + L.phi_off, base + L.row_off);
@@ -649,7 +648,7 @@ inline int hmm_chains_per_group(const HmmLds& L, int64_t n)
 template <int K, bool EXT>
 hipError_t hmm_sampler_launch(const SamplerArgs& a, const HmmView& hv, hipStream_t stream)
 {
-    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, a.data.D, a.max_depth);
+    const HmmLds L = hmm_lds(K, hv.V, hv.T, hv.Tsup, a.data.D, a.max_depth, a.sub_merge);
     const int cpg = hmm_chains_per_group(L, a.num_chains);
     if (cpg == 0) return hipErrorInvalidValue;
     const size_t lds = (size_t)cpg * L.wave * sizeof(double);

@@ -100,6 +100,7 @@ struct SamplerArgs {
     int adapt_step;           // dual-averaging step size during warmup
     double target_accept;     // its target acceptance
     int uturn_gen;            // the generalised (momentum-sum) U-turn criterion
+    int sub_merge;            // subtree proposals chosen at the merges of halves
     const double* init_q;     // [C][D] or null
     double* out_samples;      // [C][S][D] or null
     nuts_stats* out_stats;    // [C][S] or null
@@ -127,7 +128,7 @@ struct GridSync {
 };
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream);
-int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu);
+int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int num_cu);
 
 // ---------------------------------------------------------------------------
 // Batched chains on shared fp32 data: the potential and gradient of K
@@ -219,7 +220,7 @@ struct BatchSync {
 // doubles.
 hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int tiles, int groups, float* qbuf,
                                 float* P, double* L, BatchSync* sync, hipStream_t stream);
-bool batch_sampler_supported(const BatchView& bv, int max_depth, int num_cu);
+bool batch_sampler_supported(const BatchView& bv, int max_depth, int sub_merge, int num_cu);
 constexpr int kBatchQWidth = 192;
 
 // Per-dtype kernel entry points (sampler_f32.hip, sampler_f64.hip).
@@ -236,7 +237,24 @@ hipError_t launch_sampler_wave_ext_f64(const SamplerArgs& a, hipStream_t stream)
 const void* grid_kernel_ext_f32(const DataView& dv);
 const void* grid_kernel_ext_f64(const DataView& dv);
 // Whether a launch needs the kernels with the adaptation.
-inline bool sampler_extended(const SamplerArgs& a) { return (a.adapt_step && a.num_warmup > 0) || a.uturn_gen; }
+inline bool sampler_extended(const SamplerArgs& a)
+{
+    return (a.adapt_step && a.num_warmup > 0) || a.uturn_gen || a.sub_merge;
+}
+// Levels of waiting blocks a subtree of at most 2^(depth-1) leaves uses.
+__host__ __device__ inline int merge_levels(int max_depth) { return max_depth > 1 ? max_depth - 1 : 1; }
+
+// Doubles of one chain's tree state in LDS: the checkpoint array S
+// [max(depth, 1)][2][D], then, with merge-structured subtree proposals, the
+// waiting block of each level: its proposal [levels][3][D] (q, p, grad U)
+// and [levels][3] scalars (log-weight, offset, U).
+__host__ __device__ inline int64_t chain_lds_doubles(int D, int max_depth, int sub_merge)
+{
+    const int slots = max_depth > 1 ? max_depth : 1;
+    int64_t n = (int64_t)slots * 2 * D;
+    if (sub_merge) n += (int64_t)merge_levels(max_depth) * (3 * D + 3);
+    return n;
+}
 constexpr int kGridWaves = 12;  // per group: 1 controller + 11 workers (3 waves per SIMD: 168 registers each)
 
 // Semi-supervised hidden Markov model (hmm.hip, hmm_ext.hip): symbols w [T]

@@ -38,15 +38,15 @@ hipError_t launch_sampler_wave(const SamplerArgs& a, hipStream_t stream)
     return a.data.dtype == NUTS_F64 ? launch_sampler_wave_f64(a, stream) : launch_sampler_wave_f32(a, stream);
 }
 
-int grid_sampler_groups(const DataView& dv, int max_depth, int num_cu)
+int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int num_cu)
 {
-    const void* k = pick_grid_kernel(dv, false);
+    const void* k = pick_grid_kernel(dv, sub_merge != 0);
     int per_cu = 0;
-    const int slots = max_depth > 1 ? max_depth : 1;
-    const size_t lds = (size_t)slots * 2 * dv.D * sizeof(double);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGridWaves * kWave, lds) != hipSuccess ||
-        per_cu < 1)
+    const size_t lds = (size_t)chain_lds_doubles(dv.D, max_depth, sub_merge) * sizeof(double);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGridWaves * kWave, lds) != hipSuccess)
         per_cu = 1;
+    else if (per_cu < 1)
+        return 0;  // the group's LDS does not fit a CU
     if (per_cu > 1) per_cu = 1;
     int64_t groups = (int64_t)num_cu * per_cu;
     const int64_t most = (dv.nb + kGridWaves - 2) / (kGridWaves - 1);
@@ -68,9 +68,10 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
                        grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int slots = a.max_depth > 1 ? a.max_depth : 1;
-    const size_t lds = (size_t)slots * 2 * a.data.D * sizeof(double);
+    const size_t lds = (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge) * sizeof(double);
     const void* k = pick_grid_kernel(a.data, sampler_extended(a));
+    e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
     SamplerArgs A = a;
     void* args[] = {&A, &groups, &partials, &result, &sync};
     return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);

@@ -581,6 +581,12 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     // generalised criterion: the slots of S hold (momentum sum of the subtree
     // before the leaf, the leaf's momentum) instead of (q, p)
     const bool gen = EXT && A.uturn_gen;
+    // merge-structured subtree proposals: the waiting block of each level
+    // sits after S (proposal q, p, grad U per level, then per level the
+    // log-weight, offset and U)
+    const bool smerge = EXT && A.sub_merge;
+    double* stk = S_arr + (int64_t)(maxd > 1 ? maxd : 1) * 2 * D;
+    double* stk_sc = stk + (int64_t)merge_levels(maxd) * 3 * D;
     DualAvg da;
     MassWindows win;
     win.any = false;
@@ -638,12 +644,14 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             depth = j + 1;
             const int64_t nleaf = 1ll << j;
             double u_leaf = 0.0;
+            double u_sm = 0.0;    // merge-structured: uniforms of merges [msub & ~63, + 64)
+            int64_t msub = 0;     // merges completed in this subtree
             double rsum[DPL];  // momentum sum over the subtree's leaves so far
 #pragma unroll
             for (int m = 0; m < DPL; ++m) rsum[m] = 0.0;
 
             for (int64_t n = 0; n < nleaf; ++n) {
-                if ((n & (kWave - 1)) == 0)
+                if (!smerge && (n & (kWave - 1)) == 0)
                     u_leaf = (n + l < nleaf)
                                  ? unit53(draw(seed, key_chain, t, kTagLeaf, (uint64_t)j, (uint64_t)(n + l)).w0)
                                  : 0.0;
@@ -675,15 +683,72 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     term = (int)n;
                     break;
                 }
-                // streaming multinomial choice inside the subtree
                 const double lam = -dH;
-                const double lw = logaddexp(logw, lam);
-                const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
-                if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
-                    sprop = z;
-                    sprop_idx = e + v * (n + 1);
+                if (smerge) {
+                    // the leaf is a block of one; every completed pair of
+                    // equal blocks merges, keeping the later block's proposal
+                    // with probability its share of the weight (the merges'
+                    // uniforms are keyed by their ordinal in completion
+                    // order, drawn 64 at a time)
+                    const int nm = __builtin_ctzll(~(unsigned long long)n);
+                    Node<DPL> cp = z;
+                    double clw = lam;
+                    int64_t cix = e + v * (n + 1);
+                    for (int k2 = 0; k2 < nm; ++k2) {
+                        if ((msub & (kWave - 1)) == 0)
+                            u_sm = (msub + l < nleaf - 1)
+                                       ? unit53(draw(seed, key_chain, t, kTagSubMerge, (uint64_t)j,
+                                                     (uint64_t)(msub + l)).w0)
+                                       : 0.0;
+                        const double um = __shfl(u_sm, (int)(msub & (kWave - 1)));
+                        ++msub;
+                        const double* lv = stk + (int64_t)k2 * 3 * D;
+                        const double* sc = stk_sc + 3 * k2;
+                        const double lw = logaddexp(sc[0], clw);
+                        if (!uni(um < exp_nonpos(clw - lw))) {  // clw <= lw
+#pragma unroll
+                            for (int m = 0; m < DPL; ++m) {
+                                cp.q[m] = act[m] ? lv[l + 64 * m] : 0.0;
+                                cp.p[m] = act[m] ? lv[D + l + 64 * m] : 0.0;
+                                cp.g[m] = act[m] ? lv[2 * D + l + 64 * m] : 0.0;
+                            }
+                            cp.U = sc[2];
+                            cix = (int64_t)sc[1];
+                        }
+                        clw = lw;
+                    }
+                    if (n + 1 < nleaf) {
+                        if (s_out) {
+                            double* lv = stk + (int64_t)nm * 3 * D;
+#pragma unroll
+                            for (int m = 0; m < DPL; ++m) {
+                                if (act[m]) {
+                                    lv[l + 64 * m] = cp.q[m];
+                                    lv[D + l + 64 * m] = cp.p[m];
+                                    lv[2 * D + l + 64 * m] = cp.g[m];
+                                }
+                            }
+                            if (l == 0) {
+                                stk_sc[3 * nm] = clw;
+                                stk_sc[3 * nm + 1] = (double)cix;
+                                stk_sc[3 * nm + 2] = cp.U;
+                            }
+                        }
+                    } else {
+                        sprop = cp;
+                        sprop_idx = cix;
+                        logw = clw;
+                    }
+                } else {
+                    // streaming multinomial choice inside the subtree
+                    const double lw = logaddexp(logw, lam);
+                    const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
+                    if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
+                        sprop = z;
+                        sprop_idx = e + v * (n + 1);
+                    }
+                    logw = lw;
                 }
-                logw = lw;
 
                 if ((n & 1) == 0) {
                     // even leaf: checkpoint into S[BitCount(n)]
@@ -877,16 +942,15 @@ constexpr size_t kMaxGroupLds = 160 * 1024;
 template <typename T, int S, int CPS>
 struct WaveLds {
     static constexpr int R = BlockShape<T, S>::R;
-    __host__ __device__ static size_t s_bytes(int D, int max_depth, int cpg)
+    __host__ __device__ static size_t s_bytes(int D, int max_depth, int sub_merge, int cpg)
     {
-        const int slots = max_depth > 1 ? max_depth : 1;
-        return (size_t)cpg * slots * 2 * D * sizeof(double);
+        return (size_t)cpg * chain_lds_doubles(D, max_depth, sub_merge) * sizeof(double);
     }
     __host__ __device__ static int64_t x_elems(int D, int64_t nb) { return nb * D * R; }
     __host__ __device__ static int64_t pad_elems(int D) { return (int64_t)(CPS * S - D) * R; }
-    static size_t bytes(int D, int64_t nb, int max_depth, bool resident, int cpg)
+    static size_t bytes(int D, int64_t nb, int max_depth, int sub_merge, bool resident, int cpg)
     {
-        size_t b = s_bytes(D, max_depth, cpg);
+        size_t b = s_bytes(D, max_depth, sub_merge, cpg);
         if (resident)
             b += (size_t)(cpg * x_elems(D, nb) + pad_elems(D)) * sizeof(T) + (size_t)cpg * nb * R;
         return b;
@@ -910,8 +974,7 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     const int64_t chain = (int64_t)blockIdx.x * cpg + wave;
     const int D = A.data.D;
     const int64_t nb = A.data.nb;
-    const int slots = A.max_depth > 1 ? A.max_depth : 1;
-    double* S_arr = lds + (int64_t)wave * slots * 2 * D;
+    double* S_arr = lds + (int64_t)wave * chain_lds_doubles(D, A.max_depth, EXT ? A.sub_merge : 0);
     const int64_t c = A.chain_offset + chain;
     const int64_t ds = A.per_chain_data ? c : 0;
     const T* Xg = (const T*)A.data.X + ds * nb * (int64_t)D * R;
@@ -919,7 +982,7 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     WaveEval<T, S, CPS> ev;
     if constexpr (RESIDENT) {
         const int64_t xe = G::x_elems(D, nb);
-        T* Xl = reinterpret_cast<T*>(reinterpret_cast<char*>(lds) + G::s_bytes(D, A.max_depth, cpg));
+        T* Xl = reinterpret_cast<T*>(reinterpret_cast<char*>(lds) + G::s_bytes(D, A.max_depth, EXT ? A.sub_merge : 0, cpg));
         T* Xw = Xl + wave * xe;
         uint8_t* yl = reinterpret_cast<uint8_t*>(Xl + cpg * xe + G::pad_elems(D));
         uint8_t* yw = yl + wave * nb * R;
@@ -1014,15 +1077,15 @@ const void* grid_kernel_for(const DataView& dv)
     return (const void*)sampler_grid_kernel<T, 32, 10, 5, EXT>;
 }
 
-// Chains per group of the LDS-resident variant (the most of 4, 2, 1 whose
+// Chains per group of the LDS-resident variant (the most of 4 .. 1 whose
 // data sets fit), or 0 if not even one chain's data fits.
 template <typename T, int S, int CPS>
 int resident_chains_per_group(const SamplerArgs& a)
 {
     using G = WaveLds<T, S, CPS>;
-    for (int cpg = kWaveChainsPerGroup; cpg >= 1; cpg /= 2) {
+    for (int cpg = kWaveChainsPerGroup; cpg >= 1; --cpg) {
         if (cpg > a.num_chains && cpg > 1) continue;
-        if (G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg) <= kMaxGroupLds) return cpg;
+        if (G::bytes(a.data.D, a.data.nb, a.max_depth, a.sub_merge, true, cpg) <= kMaxGroupLds) return cpg;
     }
     return 0;
 }
@@ -1033,7 +1096,7 @@ hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
     using G = WaveLds<T, S, CPS>;
     const int cpg = resident_chains_per_group<T, S, CPS>(a);
     if (cpg > 0) {
-        const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, true, cpg);
+        const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, a.sub_merge, true, cpg);
         const void* k = (const void*)sampler_wave_kernel<T, S, CPS, true, EXT>;
         hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
@@ -1041,11 +1104,18 @@ hipError_t wave_launch(const SamplerArgs& a, hipStream_t stream)
         hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, true, EXT>), dim3(grid),
                            dim3(kWaveChainsPerGroup * kWave), lds, stream, a, cpg);
     } else {
-        const int c4 = kWaveChainsPerGroup;
+        // chains per group whose tree state fits (four unless the merge
+        // stacks of a deep tree take more)
+        int c4 = kWaveChainsPerGroup;
+        while (c4 > 1 && G::bytes(a.data.D, a.data.nb, a.max_depth, a.sub_merge, false, c4) > kMaxGroupLds) --c4;
+        const size_t lds = G::bytes(a.data.D, a.data.nb, a.max_depth, a.sub_merge, false, c4);
+        if (lds > kMaxGroupLds) return hipErrorInvalidValue;
+        const void* k = (const void*)sampler_wave_kernel<T, S, CPS, false, EXT>;
+        hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
         const unsigned grid = (unsigned)((a.num_chains + c4 - 1) / c4);
         hipLaunchKernelGGL((sampler_wave_kernel<T, S, CPS, false, EXT>), dim3(grid),
-                           dim3(kWaveChainsPerGroup * kWave), G::bytes(a.data.D, a.data.nb, a.max_depth, false, c4),
-                           stream, a, c4);
+                           dim3(kWaveChainsPerGroup * kWave), lds, stream, a, c4);
     }
     return hipGetLastError();
 }
