@@ -199,7 +199,8 @@ def cpu_baseline(name, seconds):
         if el >= seconds:
             break
     log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
-    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle",
+    allc = cpu_all_cores(f, X, y, w_true, min(seconds, 10.0))
+    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
                 sample=f"{n} full potential+gradient evaluations of {name}"
                        f"{' (one chain data set)' if wl.per_chain_data else ''} at w_true, "
                        f"single-threaded fp64 C, {el:.1f}s",
@@ -295,7 +296,34 @@ def hmm_cpu_baseline(seconds):
         if el >= seconds:
             break
     log(f"cpu oracle hmm: {n} gradient evaluations in {el:.1f}s")
-    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle",
+    # every allowed core (at most 16) evaluating on its own, as independent
+    # chains would
+    import concurrent.futures
+
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+
+    def worker(_):
+        # the C entry point with its arguments prepared once, so that the
+        # interpreter's share of a call (which the threads take in turn)
+        # stays small
+        lib = oracle.lib()
+        wu, zu = np.ascontiguousarray(w, np.uint8), np.ascontiguousarray(z, np.uint8)
+        qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
+        args = (wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"], HMM_SHAPE["V"],
+                qq.ctypes.data, gg.ctypes.data)
+        m, t1 = 0, time.perf_counter()
+        while time.perf_counter() - t1 < min(seconds, 5.0):
+            for _ in range(20):
+                lib.orc_hmm_ug(*args)
+            m += 20
+        return m, time.perf_counter() - t1
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=cores) as ex:
+        res = list(ex.map(worker, range(cores)))
+    allc = dict(value=sum(m / t for m, t in res), unit="grad-evals/s", cores=cores,
+                sample=f"{sum(m for m, _ in res)} evaluations on {cores} threads")
+    log(f"cpu oracle hmm, {cores} threads: {allc['value']:.0f} evaluations/s")
+    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
                 sample=f"{n} HMM potential+gradient evaluations (T 600, Tsup 100, K 3, V 10), "
                        f"single-threaded fp64 C, {el:.1f}s")
 
@@ -318,6 +346,34 @@ def hmm_line(h, cpu):
     # the paper's HMM figure (NumPyro, 32-bit, one CPU chain): context only
     out["paper_numpyro_cpu_ms_per_leapfrog_step"] = 0.09
     return out
+
+
+def cpu_all_cores(f, X, y, w, seconds):
+    """The oracle's gradient on every allowed host core (at most 16): the rows
+    in one fixed chunk per thread (ctypes releases the interpreter lock
+    during the C call), the partial sums added in chunk order.  A timing
+    mode only: each chunk's call also adds the prior, which this sum does not
+    correct."""
+    import concurrent.futures
+
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    N = X.shape[0]
+    bounds = [(N * i // cores, N * (i + 1) // cores) for i in range(cores)]
+    with concurrent.futures.ThreadPoolExecutor(max_workers=cores) as ex:
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            parts = list(ex.map(lambda b: f(X[b[0]:b[1]], y[b[0]:b[1]], w), bounds))
+            g = parts[0][1].copy()
+            for p in parts[1:]:
+                g += p[1]
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
+    log(f"cpu oracle, {cores} threads: {n} gradient evaluations in {el:.1f}s")
+    return dict(value=n / el, unit="grad-evals/s", cores=cores,
+                sample=f"{n} evaluations, rows in {cores} fixed chunks, {el:.1f}s")
 
 
 def main():
