@@ -113,6 +113,8 @@ def lib():
                                             u64, P]
         L.orc_find_step_size_at.restype = dbl
         L.orc_log_likelihood.argtypes = [P, P, i64, i64, P, i64, P, P]
+        L.orc_posterior_predictive.argtypes = [P, i64, i64, P, i64, u64, P, P]
+        L.orc_posterior_predictive.restype = None
         L.orc_hmm_ug.argtypes = [P, i64, P, i64, i32, i32, P, P]
         L.orc_hmm_ug.restype = dbl
         L.orc_expected_log_likelihood.argtypes = [P, i64]
@@ -337,6 +339,20 @@ def log_likelihood(X, y, W):
     pm = np.zeros(N)
     lib().orc_log_likelihood(_p(X), _p(_u8(y)), N, D, _p(W), S, _p(ll), _p(pm))
     return ll, pm
+
+
+def posterior_predictive(X, W, seed):
+    """Posterior predictive samples y [S, N] (uint8) at draws W [S, D] and
+    the probabilities sigmoid(x_i . w_s) [S, N] they were drawn with
+    (reading R23: one keyed uniform per (draw, row))."""
+    X = _f64(X)
+    N, D = X.shape
+    W = _f64(W).reshape(-1, D)
+    S = W.shape[0]
+    y = np.zeros((S, N), dtype=np.uint8)
+    p = np.zeros((S, N))
+    lib().orc_posterior_predictive(_p(X), N, D, _p(W), S, seed, _p(y), _p(p))
+    return y, p
 
 
 def expected_log_likelihood(ll):

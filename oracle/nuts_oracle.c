@@ -110,7 +110,7 @@ void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint6
 
 /* Draw tags: which random quantity a Philox block feeds (reading R8). */
 enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4, ORC_TAG_STEP = 5,
-       ORC_TAG_SUBMERGE = 6 };
+       ORC_TAG_SUBMERGE = 6, ORC_TAG_PREDICT = 7 };
 
 static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, uint64_t j,
                       uint64_t n, uint64_t out[4])
@@ -257,6 +257,29 @@ void orc_log_likelihood(const double *X, const uint8_t *y, int64_t N, int64_t D,
             psum += orc_sigmoid(eta);
         }
         if (pred_mean) pred_mean[i] = psum / (double)S;
+    }
+}
+
+/* Posterior predictive samples (Section 3.2, Fig. 1c: the model run forward
+ * at each posterior draw; reading R23): y_si = 1 iff u_si < sigmoid(x_i .
+ * w_s), u_si the word i mod 4 of the Philox block keyed (seed, s) at counter
+ * (0, 7 << 32, floor(i / 4), 0).  Writes y [S][N] bytes and, if p is not
+ * NULL, the probabilities p [S][N].                                         */
+void orc_posterior_predictive(const double *X, int64_t N, int64_t D, const double *W, int64_t S,
+                              uint64_t seed, uint8_t *y, double *p)
+{
+    for (int64_t s = 0; s < S; ++s) {
+        const double *w = W + s * D;
+        uint64_t blk[4];
+        for (int64_t i = 0; i < N; ++i) {
+            const double *xi = X + i * D;
+            double eta = 0.0;
+            for (int64_t j = 0; j < D; ++j) eta += xi[j] * w[j];
+            double prob = orc_sigmoid(eta);
+            if ((i & 3) == 0) orc_block(seed, (uint64_t)s, 0, ORC_TAG_PREDICT, 0, (uint64_t)(i >> 2), blk);
+            y[s * N + i] = orc_u53(blk[i & 3]) < prob ? 1 : 0;
+            if (p) p[s * N + i] = prob;
+        }
     }
 }
 
