@@ -150,6 +150,19 @@ int nuts_potential_grad(nuts_handle* h, const void* X, const uint8_t* y, int64_t
 int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W, int64_t S, double* out_ll,
                              double* out_elpd, double* out_pred_mean);
 
+/* Posterior predictive samples at S draws W [S][D] (Section 3.2 / Fig. 1c:
+ * the model run forward at each posterior draw, vectorised over the draws):
+ *   out_y[s][i] = 1 if u_si < sigmoid(x_i . w_s) else 0,   [S][N] bytes,
+ * u_si the 53-bit uniform from word i % 4 of the Philox4x64-10 block keyed
+ * (seed, s) at counter (0, 7 << 32, i / 4, 0).  The prior predictive is the
+ * same call with W drawn from the prior.  Computed in the matrix-core pass of
+ * nuts_data_log_likelihood (fp32 products and fp32 sigmoid, compared with the
+ * uniform in fp64), so fp32 data with D <= 132 only (else NUTS_EUNSUPPORTED);
+ * one shared data set; 1 <= S <= 65535; W and out_y may be host or device
+ * memory. */
+int nuts_data_posterior_predictive(nuts_handle* h, const nuts_data* d, const double* W, int64_t S, uint64_t seed,
+                                   uint8_t* out_y);
+
 /* Options of nuts_sample_data; a NULL pointer means all defaults. */
 typedef struct {
     const double* init_q;      /* [C][D] start positions, or NULL for zeros */

@@ -113,7 +113,7 @@ def lib():
                                             u64, P]
         L.orc_find_step_size_at.restype = dbl
         L.orc_log_likelihood.argtypes = [P, P, i64, i64, P, i64, P, P]
-        L.orc_posterior_predictive.argtypes = [P, i64, i64, P, i64, u64, P, P]
+        L.orc_posterior_predictive.argtypes = [P, i64, i64, P, i64, u64, u64, P, P, P]
         L.orc_posterior_predictive.restype = None
         L.orc_hmm_ug.argtypes = [P, i64, P, i64, i32, i32, P, P]
         L.orc_hmm_ug.restype = dbl
@@ -341,18 +341,20 @@ def log_likelihood(X, y, W):
     return ll, pm
 
 
-def posterior_predictive(X, W, seed):
+def posterior_predictive(X, W, seed, uniforms=False, first_draw=0):
     """Posterior predictive samples y [S, N] (uint8) at draws W [S, D] and
     the probabilities sigmoid(x_i . w_s) [S, N] they were drawn with
-    (reading R23: one keyed uniform per (draw, row))."""
+    (reading R23: one keyed uniform per (draw, row)); with uniforms=True
+    also the uniforms [S, N].  Row s of W is keyed as draw first_draw + s."""
     X = _f64(X)
     N, D = X.shape
     W = _f64(W).reshape(-1, D)
     S = W.shape[0]
     y = np.zeros((S, N), dtype=np.uint8)
     p = np.zeros((S, N))
-    lib().orc_posterior_predictive(_p(X), N, D, _p(W), S, seed, _p(y), _p(p))
-    return y, p
+    u = np.zeros((S, N)) if uniforms else None
+    lib().orc_posterior_predictive(_p(X), N, D, _p(W), S, seed, first_draw, _p(y), _p(p), _p(u))
+    return (y, p, u) if uniforms else (y, p)
 
 
 def expected_log_likelihood(ll):

@@ -263,10 +263,11 @@ void orc_log_likelihood(const double *X, const uint8_t *y, int64_t N, int64_t D,
 /* Posterior predictive samples (Section 3.2, Fig. 1c: the model run forward
  * at each posterior draw; reading R23): y_si = 1 iff u_si < sigmoid(x_i .
  * w_s), u_si the word i mod 4 of the Philox block keyed (seed, s) at counter
- * (0, 7 << 32, floor(i / 4), 0).  Writes y [S][N] bytes and, if p is not
- * NULL, the probabilities p [S][N].                                         */
+ * (0, 7 << 32, floor(i / 4), 0), s counted from s0 (the index of W's first
+ * row among the draws).  Writes y [S][N] bytes and, where not NULL, the
+ * probabilities p [S][N] and the uniforms u [S][N].                        */
 void orc_posterior_predictive(const double *X, int64_t N, int64_t D, const double *W, int64_t S,
-                              uint64_t seed, uint8_t *y, double *p)
+                              uint64_t seed, uint64_t s0, uint8_t *y, double *p, double *u)
 {
     for (int64_t s = 0; s < S; ++s) {
         const double *w = W + s * D;
@@ -276,9 +277,11 @@ void orc_posterior_predictive(const double *X, int64_t N, int64_t D, const doubl
             double eta = 0.0;
             for (int64_t j = 0; j < D; ++j) eta += xi[j] * w[j];
             double prob = orc_sigmoid(eta);
-            if ((i & 3) == 0) orc_block(seed, (uint64_t)s, 0, ORC_TAG_PREDICT, 0, (uint64_t)(i >> 2), blk);
-            y[s * N + i] = orc_u53(blk[i & 3]) < prob ? 1 : 0;
+            if ((i & 3) == 0) orc_block(seed, s0 + (uint64_t)s, 0, ORC_TAG_PREDICT, 0, (uint64_t)(i >> 2), blk);
+            double ui = orc_u53(blk[i & 3]);
+            y[s * N + i] = ui < prob ? 1 : 0;
             if (p) p[s * N + i] = prob;
+            if (u) u[s * N + i] = ui;
         }
     }
 }

@@ -27,7 +27,7 @@ EXPORTED = [
     "nuts_init", "nuts_free", "nuts_last_error", "nuts_data_create", "nuts_data_free",
     "nuts_data_potential_grad", "nuts_data_potential_grad_batched", "nuts_potential_grad",
     "nuts_data_log_likelihood", "nuts_sample_data", "nuts_sample",
-    "nuts_hmm_potential_grad", "nuts_hmm_sample",
+    "nuts_hmm_potential_grad", "nuts_hmm_sample", "nuts_data_posterior_predictive",
 ]
 
 STATS_DTYPE = np.dtype([
@@ -111,6 +111,8 @@ def load_library():
     L.nuts_sample.argtypes = [P, P, P, i64, i64, i32, u32, dbl, dbl, P, i32, i64, i64, i64,
                               u64, P, P]
     L.nuts_sample.restype = i32
+    L.nuts_data_posterior_predictive.argtypes = [P, P, P, i64, u64, P]
+    L.nuts_data_posterior_predictive.restype = i32
     L.nuts_hmm_potential_grad.argtypes = [P, P, i64, P, i64, i32, i32, P, i64, P, P]
     L.nuts_hmm_potential_grad.restype = i32
     L.nuts_hmm_sample.argtypes = [P, P, i64, P, i64, i32, i32, u32, dbl, P, i32, i64, i64, i64, u64,
@@ -319,6 +321,19 @@ class Data:
         self.s._check(self.s._L.nuts_data_log_likelihood(self.s._h, self._d, _ptr(W), S, _ptr(out_ll),
                                                          _ptr(elpd), _ptr(pm)))
         return out_ll, float(elpd[0]), pm
+
+    def posterior_predictive(self, W, seed=0, out_y=None):
+        """Posterior predictive samples y [S, N] (uint8) at draws W [S, D]:
+        y_si ~ Bernoulli(sigmoid(x_i . w_s)) with keyed uniforms (fp32 data
+        on the matrix cores)."""
+        if isinstance(W, np.ndarray):
+            W = np.ascontiguousarray(W, dtype=np.float64).reshape(-1, self.D)
+        S = W.shape[0]
+        if out_y is None:
+            out_y = np.zeros((S, self.N), dtype=np.uint8)
+        self.s._check(self.s._L.nuts_data_posterior_predictive(self.s._h, self._d, _ptr(W), S, seed,
+                                                               _ptr(out_y)))
+        return out_y
 
     def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None, batched=False):
         """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor).

@@ -628,7 +628,7 @@ int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W
         HIP_TRY(h, handle_scratch(h, lbytes + rbytes, &scratch));
         HIP_TRY(h, launch_batch_log_likelihood(d->batch, (const double*)Wd, S, plan, (double*)scratch,
                                                (float*)((char*)scratch + lbytes), (double*)Ld, (double*)Pd,
-                                               h->stream));
+                                               nullptr, 0, h->stream));
     } else {
         // the potential at prior scale 1 per draw, then the prior taken off
         const PotentialPlan plan = plan_potential(d->view, S, h->num_cu);
@@ -648,6 +648,41 @@ int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W
     HIP_TRY(h, finish_out(out_ll, (size_t)S * 8, lt, h->stream));
     HIP_TRY(h, finish_out(out_elpd, 8, et, h->stream));
     HIP_TRY(h, finish_out(out_pred_mean, (size_t)N * 8, pt, h->stream));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    return NUTS_OK;
+}
+
+int nuts_data_posterior_predictive(nuts_handle* h, const nuts_data* d, const double* W, int64_t S, uint64_t seed,
+                                   uint8_t* out_y)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (!W || !out_y) return fail(h, NUTS_EINVAL, "W and out_y must be non-NULL");
+    if (S < 1 || S > kMaxPotentialItems)
+        return fail(h, NUTS_EINVAL, "S must be in [1, %d] (got %lld)", kMaxPotentialItems, (long long)S);
+    if (d->view.nds != 1) return fail(h, NUTS_EINVAL, "the predictive takes one shared data set");
+    if (d->view.N < 1) return fail(h, NUTS_EINVAL, "the predictive needs N >= 1");
+    const int D = d->view.D;
+    const int64_t N = d->view.N;
+    int kt = 0, tc = 0;
+    if (d->view.dtype != NUTS_F32 || !batch_shape(D, &kt, &tc))
+        return fail(h, NUTS_EUNSUPPORTED, "the predictive samples take fp32 data with D <= %d", 16 * kBatchMaxKT + 4);
+    DeviceScope ds(h->device);
+    DevBuf wt, yt;
+    const void* Wd = nullptr;
+    void* Yd = nullptr;
+    HIP_TRY(h, stage_in(W, (size_t)S * D * 8, wt, &Wd, h->stream));
+    HIP_TRY(h, stage_out(out_y, (size_t)S * N, yt, &Yd));
+    const int rc = ensure_batch_layout(h, d);
+    if (rc != NUTS_OK) return rc;
+    const BatchPlan plan = plan_batch_potential(d->batch, S, h->num_cu);
+    const size_t lbytes = align256((size_t)plan.tiles * plan.groups * kBatchTileChains * sizeof(double));
+    void* scratch = nullptr;
+    HIP_TRY(h, handle_scratch(h, lbytes, &scratch));
+    HIP_TRY(h, launch_batch_log_likelihood(d->batch, (const double*)Wd, S, plan, (double*)scratch, nullptr, nullptr,
+                                           nullptr, (uint8_t*)Yd, seed, h->stream));
+    HIP_TRY(h, finish_out(out_y, (size_t)S * N, yt, h->stream));
     HIP_TRY(h, hipStreamSynchronize(h->stream));
     return NUTS_OK;
 }

@@ -281,12 +281,36 @@ __device__ __forceinline__ float sum16(float v)
     return v;
 }
 
+// Posterior predictive samples of one position (draw s): y[i] = 1 iff
+// u_si < sigmoid(eta_i), the uniforms the words of the Philox block keyed
+// (seed, s) at counter (0, kTagPredict << 32, i / 4, 0), word i % 4.
+struct PredictOut {
+    uint8_t* y;     // the position's row of the [S][N] output, or null (dead position)
+    uint64_t seed;
+    uint64_t s;
+    int64_t N;
+    int64_t row0;   // first row of the stage
+};
+
+// Draw and store the samples of four consecutive rows r0 .. r0 + 3 (r0 a
+// multiple of 4) from their probabilities p.
+__device__ __forceinline__ void predict_rows(const PredictOut& po, int64_t r0, const float (&p)[4])
+{
+    const Block4 b = philox4x64_10(0, kTagPredict << 32, (uint64_t)(r0 >> 2), 0, po.seed, po.s);
+    const uint64_t w[4] = {b.w0, b.w1, b.w2, b.w3};
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+        if (r0 + r < po.N) po.y[r0 + r] = unit53(w[r]) < (double)p[r] ? 1 : 0;
+}
+
 // One LDS stage for this wave's 16 positions: the loss of every live
 // (row, position) into `loss`; with PRED, the wave's sums of sigma(eta) over
-// its live positions for each of the 64 rows into rs[0..63].
-template <int KT, bool PRED>
+// its live positions for each of the 64 rows into rs[0..63]; with SAMPLE,
+// the position's predictive samples of the stage's rows.
+template <int KT, bool PRED, bool SAMPLE>
 __device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, const float* __restrict__ ys,
-                                                 const WaveQ& Q, float live, double& loss, float* rs)
+                                                 const WaveQ& Q, float live, double& loss, float* rs,
+                                                 const PredictOut& po)
 {
     using G = Geo<KT>;
     const int l = lane();
@@ -329,6 +353,12 @@ __device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, c
             lsum += l0 + l1;
         }
         loss += (double)lsum;
+        if constexpr (SAMPLE) {
+            if (po.y) {
+                predict_rows(po, po.row0 + tp * kTileRows + 4 * jj, p0);
+                predict_rows(po, po.row0 + (tp + 1) * kTileRows + 4 * jj, p1);
+            }
+        }
         if constexpr (PRED) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -347,10 +377,10 @@ __device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, c
 // waves' row sums of each stage (rs[buffer][wave][64]) are added in wave
 // order and stored to prow[stage * 64 + row] one stage later, after the
 // barrier that ends it.
-template <int KT, bool PRED>
+template <int KT, bool PRED, bool SAMPLE>
 __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, int64_t st1, int tid, float* xs,
                                               float* ys, float* rs, const WaveQ& Q, float live, double& loss,
-                                              float* prow)
+                                              float* prow, PredictOut po)
 {
     const int widx = tid / kWave;
     auto flush = [&](int64_t st, int b) {
@@ -373,8 +403,9 @@ __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, 
         StageRegs r;
         if (more) load_stage(bv, st + 1, tid, r);
         if (st > st0) flush(st - 1, b ^ 1);
-        compute_stage_ll<KT, PRED>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, live, loss,
-                                   rs + (b * kWaves + widx) * kBatchStageRows);
+        po.row0 = st * kBatchStageRows;
+        compute_stage_ll<KT, PRED, SAMPLE>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, live, loss,
+                                           rs + (b * kWaves + widx) * kBatchStageRows, po);
         if (more) store_stage<KT>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
         __syncthreads();
     }

@@ -253,11 +253,12 @@ hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const
 
 namespace {
 
-template <int KT, bool PRED>
+template <int KT, bool PRED, bool SAMPLE>
 __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_ll_kernel(BatchView bv, const double* __restrict__ W,
                                                                            int64_t S, int groups,
                                                                            double* __restrict__ L,
-                                                                           float* __restrict__ Pr)
+                                                                           float* __restrict__ Pr,
+                                                                           uint8_t* __restrict__ Y, uint64_t seed)
 {
     __shared__ __align__(16) float xs[2 * batch::kStageBuf];
     __shared__ __align__(16) float ys[2 * kBatchStageRows];
@@ -289,8 +290,14 @@ __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_ll_kernel(Batc
     double loss = 0.0;
     const int64_t st0 = (int64_t)g * bv.ns / groups;
     const int64_t st1 = (int64_t)(g + 1) * bv.ns / groups;
-    batch::stage_loop_ll<KT, PRED>(bv, st0, st1, (int)threadIdx.x, xs, ys, rs, Q, live ? 1.0f : 0.0f, loss,
-                                   Pr + (int64_t)t * bv.ns * kBatchStageRows);
+    batch::PredictOut po;
+    po.y = (SAMPLE && live) ? Y + pos * bv.N : nullptr;
+    po.seed = seed;
+    po.s = (uint64_t)pos;
+    po.N = bv.N;
+    po.row0 = 0;
+    batch::stage_loop_ll<KT, PRED, SAMPLE>(bv, st0, st1, (int)threadIdx.x, xs, ys, rs, Q, live ? 1.0f : 0.0f,
+                                           loss, Pr + (int64_t)t * bv.ns * kBatchStageRows, po);
     // the four lanes of a position hold its four row groups
     loss += __shfl_xor(loss, 16);
     loss += __shfl_xor(loss, 32);
@@ -324,36 +331,38 @@ __global__ void __launch_bounds__(256) batch_pred_kernel(int64_t N, int64_t rows
 
 template <int KT>
 void enqueue_ll(const BatchView& bv, const double* W, int64_t S, int tiles, int groups, double* L, float* Pr,
-                bool pred, hipStream_t stream)
+                bool pred, uint8_t* Y, uint64_t seed, hipStream_t stream)
 {
-    if (pred)
-        hipLaunchKernelGGL((batch_ll_kernel<KT, true>), dim3(groups, tiles), dim3(batch::kWaves * kWave), 0, stream,
-                           bv, W, S, groups, L, Pr);
+    const dim3 grid(groups, tiles), block(batch::kWaves * kWave);
+    if (Y)
+        hipLaunchKernelGGL((batch_ll_kernel<KT, false, true>), grid, block, 0, stream, bv, W, S, groups, L, Pr, Y,
+                           seed);
+    else if (pred)
+        hipLaunchKernelGGL((batch_ll_kernel<KT, true, false>), grid, block, 0, stream, bv, W, S, groups, L, Pr, Y,
+                           seed);
     else
-        hipLaunchKernelGGL((batch_ll_kernel<KT, false>), dim3(groups, tiles), dim3(batch::kWaves * kWave), 0,
-                           stream, bv, W, S, groups, L, Pr);
+        hipLaunchKernelGGL((batch_ll_kernel<KT, false, false>), grid, block, 0, stream, bv, W, S, groups, L, Pr, Y,
+                           seed);
 }
 
 }  // namespace
 
 hipError_t launch_batch_log_likelihood(const BatchView& bv, const double* W, int64_t S, const BatchPlan& plan,
-                                       double* L, float* Pr, double* out_ll, double* out_pred, hipStream_t stream)
+                                       double* L, float* Pr, double* out_ll, double* out_pred, uint8_t* out_y,
+                                       uint64_t seed, hipStream_t stream)
 {
     const bool pred = out_pred != nullptr;
+#define NUTS_LL_CASE(k)                                                                         \
+    case k: enqueue_ll<k>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, out_y, seed, stream); break;
     switch (bv.kt) {
-    case 0: enqueue_ll<0>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 1: enqueue_ll<1>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 2: enqueue_ll<2>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 3: enqueue_ll<3>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 4: enqueue_ll<4>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 5: enqueue_ll<5>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 6: enqueue_ll<6>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 7: enqueue_ll<7>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
-    case 8: enqueue_ll<8>(bv, W, S, plan.tiles, plan.groups, L, Pr, pred, stream); break;
+        NUTS_LL_CASE(0) NUTS_LL_CASE(1) NUTS_LL_CASE(2) NUTS_LL_CASE(3) NUTS_LL_CASE(4) NUTS_LL_CASE(5)
+        NUTS_LL_CASE(6) NUTS_LL_CASE(7) NUTS_LL_CASE(8)
     default: return hipErrorInvalidValue;
     }
+#undef NUTS_LL_CASE
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (out_y) return hipSuccess;  // the predictive samples only
     hipLaunchKernelGGL(batch_ll_finish_kernel, dim3((unsigned)((S + 63) / 64)), dim3(64), 0, stream, S, plan.groups,
                        (int)(bv.ns * kBatchStageRows - bv.N), L, out_ll);
     e = hipGetLastError();

@@ -52,7 +52,8 @@ __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64
 
 // Which quantity a block feeds; part of the counter.
 enum : uint64_t {
-    kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4, kTagStepSize = 5, kTagSubMerge = 6
+    kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4, kTagStepSize = 5, kTagSubMerge = 6,
+    kTagPredict = 7
 };
 
 // Kept out of line: it is called a few times per iteration, and inlining it

@@ -195,9 +195,12 @@ hipError_t launch_batch_potential(const BatchView& bv, double prior_scale, const
 // Log-likelihood of S draws over shared fp32 data on the matrix cores (the
 // plan of plan_batch_potential for K = S): L holds tiles * groups * 128
 // doubles; Pr tiles * ns * 64 floats when out_pred (mean of sigmoid(eta)
-// over the draws, [N]) is wanted, else unused.
+// over the draws, [N]) is wanted, else unused.  With out_y ([S][N] bytes)
+// the pass writes the posterior predictive samples of the draws under
+// `seed` instead, and nothing else.
 hipError_t launch_batch_log_likelihood(const BatchView& bv, const double* W, int64_t S, const BatchPlan& plan,
-                                       double* L, float* Pr, double* out_ll, double* out_pred, hipStream_t stream);
+                                       double* L, float* Pr, double* out_ll, double* out_pred, uint8_t* out_y,
+                                       uint64_t seed, hipStream_t stream);
 // ll[s] = -(U[s] - |w_s|^2 / 2 - D ln(2 pi) / 2) for potentials U taken with
 // prior scale 1 (the streaming path's log-likelihood).
 hipError_t launch_ll_from_potential(int D, const double* W, int64_t S, const double* U, double* out_ll,

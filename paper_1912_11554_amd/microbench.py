@@ -3,6 +3,7 @@
     python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 1
     python -m paper_1912_11554_amd.microbench --workload shared256_n200000_d129_f32 --positions 256 --batched
     python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 500 --loglik
+    python -m paper_1912_11554_amd.microbench --workload covtype_n581012_d55_f32 --positions 500 --predictive
 
 Each call evaluates U and grad U at K positions (around the data's generating
 weights) with the data already in device memory (with --loglik: the
@@ -41,6 +42,9 @@ def main():
     ap.add_argument("--loglik", action="store_true",
                     help="nuts_data_log_likelihood at the positions as draws (with the expected "
                          "log-likelihood and the predictive mean)")
+    ap.add_argument("--predictive", action="store_true",
+                    help="nuts_data_posterior_predictive at the positions as draws (one byte per row "
+                         "and draw)")
     ap.add_argument("--reps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--copy-mb", type=int, default=0,
@@ -72,7 +76,12 @@ def main():
     d = s.data(torch.from_numpy(X).cuda(), torch.from_numpy(y).cuda())
     U = torch.empty(K, dtype=torch.float64, device="cuda")
     G = torch.empty((K, wl.D), dtype=torch.float64, device="cuda")
-    if args.loglik:
+    if args.predictive:
+        Y = torch.empty((K, wl.N), dtype=torch.uint8, device="cuda")
+
+        def call():
+            d.posterior_predictive(W, seed=1, out_y=Y)
+    elif args.loglik:
         pm = torch.empty(wl.N, dtype=torch.float64, device="cuda")
         el = torch.empty(1, dtype=torch.float64, device="cuda")
 
@@ -94,11 +103,19 @@ def main():
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) * 1e3 / args.reps
     es = 8 if wl.dtype == "f64" else 4
-    kernel = ("batch_ll_kernel" if args.loglik else
+    kernel = ("batch_ll_kernel" if args.loglik or args.predictive else
               "batch_pass_kernel" if args.batched else "potential_grad_kernel")
     out = dict(workload=args.workload, N=wl.N, D=wl.D, dtype=wl.dtype, positions=K, kernel=kernel,
                reps=args.reps, us_per_call_with_host=round(us, 2))
-    if args.loglik:
+    if args.predictive:
+        # per (row, draw): the product row of E = X W^T, one sigmoid, a
+        # quarter of a Philox4x64-10 block, one byte out
+        pairs = wl.N * K
+        tflops = 2.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12
+        out.update(pairs_per_s=round(pairs / (us * 1e-6), 1), bytes_out=pairs,
+                   achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
+                   frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4))
+    elif args.loglik:
         tflops = 2.0 * wl.N * wl.D * K / (us * 1e-6) / 1e12   # E = X W^T only
         out.update(bound="mfma", achieved_tflops=round(tflops, 2), peak=MFMA_F32_PEAK_TFLOPS,
                    frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4))
