@@ -161,3 +161,18 @@ def test_rejects(sampler):
     assert e.value.code == nuts.NUTS_EINVAL
     U, g = sampler.hmm_potential_grad(w, z, 3, 5, Q)
     assert np.isfinite(U).all() and np.isfinite(g).all()
+
+
+def test_sampler_bench_configuration(sampler, orc):
+    # the timed configuration of bench.py's HMM line: 8192 chains (2048
+    # groups), depth 10, with an inverse mass; five chains checked over a
+    # few iterations
+    w, z = _seq(600, 100, 3, 10, key=6)
+    hm = dict(w=w, z=z, K=3, V=10)
+    im = np.linspace(0.6, 1.4, 33)
+    kw = dict(step_size=0.15, max_tree_depth=10, num_warmup=2, num_samples=4, seed=2, inv_mass=im)
+    say("hmm sample 8192 chains")
+    r = sampler.hmm_sample(w, z, 3, 10, num_chains=8192, **kw)
+    for c in (0, 1, 4095, 4096, 8191):
+        ref = orc.nuts(None, None, hmm=hm, chain=c, **kw)
+        compare_chain(r["samples"][c], r["stats"][c], ref)
