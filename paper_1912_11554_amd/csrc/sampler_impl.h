@@ -969,7 +969,8 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     constexpr int R = G::R;
     extern __shared__ double lds[];
     const int wave = threadIdx.x / kWave;
-    if (wave >= cpg) return;
+    const bool idle = wave >= cpg;  // a group of fewer than four chains
+    if (!RESIDENT && idle) return;   // (no group barrier on this variant)
     const int l = lane();
     const int64_t chain = (int64_t)blockIdx.x * cpg + wave;
     const int D = A.data.D;
@@ -990,7 +991,9 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
         // multiple of 16 since R * sizeof(T) is 512 / S or 1024 and S <= 8
         const int64_t n16 = xe * (int64_t)sizeof(T) / 16;
         uint4* dst = reinterpret_cast<uint4*>(Xw);
-        if (chain < A.num_chains) {
+        if (idle) {
+            // an idle wave only takes part in the barrier below
+        } else if (chain < A.num_chains) {
             const uint4* src = reinterpret_cast<const uint4*>(Xg);
             for (int64_t i = l; i < n16; i += kWave) dst[i] = src[i];
             const int64_t n8 = nb * R / 8;
@@ -1000,12 +1003,12 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
             // a neighbour's last block over-reads into this region: zeros
             for (int64_t i = l; i < n16; i += kWave) dst[i] = uint4{0u, 0u, 0u, 0u};
         }
-        if (wave == cpg - 1) {
+        if (!idle && wave == cpg - 1) {
             T* pad = Xl + cpg * xe;
             for (int64_t i = l; i < G::pad_elems(D); i += kWave) pad[i] = T(0);
         }
         __syncthreads();
-        if (chain >= A.num_chains) return;
+        if (idle || chain >= A.num_chains) return;
         ev.X = Xw;
         ev.y = yw;
     } else {
