@@ -101,6 +101,26 @@ def test_full_size_covtype(sampler, orc, name):
         _check(sampler, orc, X, y, w, 1.0, wl.dtype)
 
 
+def test_full_size_streaming(sampler, orc):
+    # the 4,000,000 x 257 fp32 set (4.1 GB, 10 % of the features zero) of
+    # the streaming workload, at zero and near its generating weights; the
+    # oracle promotes the fp32 rows to fp64 one at a time
+    wl = workloads.WORKLOADS["stream_n4m_d257_f32"]
+    X, y = workloads.make_workload(wl)
+    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+    colsum = np.abs(X).sum(axis=0, dtype=np.float64)
+    d = sampler.data(X, y)
+    rng = np.random.default_rng(8)
+    for w in (np.zeros(wl.D), w_true + 0.01 * rng.normal(size=wl.D)):
+        say("potential_grad full-size streaming", X.shape)
+        U, G = d.potential_grad(w[None, :])
+        U_ref, g_ref = orc.logistic_potential_grad_f32(X, y, w)
+        assert abs(U[0] - U_ref) <= RTOL["f32"] * abs(U_ref), (U[0], U_ref)
+        tol = RTOL["f32"] * (np.abs(g_ref) + colsum + np.abs(w) + 1.0)
+        assert (np.abs(G[0] - g_ref) <= tol).all(), np.max(np.abs(G[0] - g_ref) / tol)
+    d.free()
+
+
 def test_errors_are_reported(sampler):
     import paper_1912_11554_amd as nuts
     X = np.zeros((10, 3))
