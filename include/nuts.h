@@ -253,7 +253,7 @@ int nuts_sample(nuts_handle* h, const void* X, const uint8_t* y, int64_t N, int6
  * the last term by the forward algorithm (from the uniform distribution,
  * without a transition, when Tsup = 0).  The gradient comes from the
  * backward recursion's expected counts.  Shapes: 2 <= K <= 4, V >= 2,
- * K*K + K*V <= 64, T - Tsup <= 512 (else NUTS_EUNSUPPORTED); w and z are
+ * K*K + K*V <= 64, T - Tsup <= 512 (else NUTS_EUNSUPPORTED), T <= 2^30; w and z are
  * checked (NUTS_EINVAL for a symbol >= V or a state >= K).  fp64 throughout.
  *
  * nuts_hmm_potential_grad: U and grad U at num_points positions Q

@@ -316,9 +316,9 @@ int hmm_stage(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* z, int
 {
     if (!w) return fail(h, NUTS_EINVAL, "w is NULL");
     if (Tsup > 0 && !z) return fail(h, NUTS_EINVAL, "z is NULL with Tsup = %lld", (long long)Tsup);
-    if (T < 1 || Tsup < 0 || Tsup > T)
-        return fail(h, NUTS_EINVAL, "need 1 <= T and 0 <= Tsup <= T (T = %lld, Tsup = %lld)", (long long)T,
-                    (long long)Tsup);
+    if (T < 1 || Tsup < 0 || Tsup > T || T > ((int64_t)1 << 30))
+        return fail(h, NUTS_EINVAL, "need 1 <= T <= 2^30 and 0 <= Tsup <= T (T = %lld, Tsup = %lld)",
+                    (long long)T, (long long)Tsup);
     if (!hmm_supported(K, V, T, Tsup))
         return fail(h, NUTS_EUNSUPPORTED,
                     "the HMM kernels take 2 <= K <= 4, V >= 2, K*K + K*V <= 64 and T - Tsup <= %d "
