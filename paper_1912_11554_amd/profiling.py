@@ -25,6 +25,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # Sources that only the HMM kernels are built from; the other kernels'
 # fingerprint leaves them out (the HMM kernels include every shared header).
 HMM_ONLY_SOURCES = ("hmm_impl.h", "hmm.hip", "hmm_ext.hip")
+# Host-only sources (argument checks, staging, launch choices): no kernel is
+# built from them, so no kernel's fingerprint covers them.
+HOST_ONLY_SOURCES = ("api.cpp",)
 
 
 def is_hmm_kernel(kernel: str) -> bool:
@@ -38,6 +41,8 @@ def source_fingerprint(kernel: str | None = None) -> str:
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
         base = os.path.basename(path)
+        if kernel is not None and base in HOST_ONLY_SOURCES:
+            continue
         if kernel is not None and not is_hmm_kernel(kernel) and base in HMM_ONLY_SOURCES:
             continue
         h.update(base.encode())
