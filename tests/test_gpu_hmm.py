@@ -56,7 +56,10 @@ def test_potential_matches_oracle(sampler, orc, T, Tsup, K, V):
     w, z = _seq(T, Tsup, K, V, key=[7, T * 100 + Tsup])
     D = orc.hmm_dim(K, V)
     rng = np.random.default_rng([8, T, K, V])
-    Q = np.concatenate([np.zeros((1, D)), rng.normal(0.0, 1.0, (5, D)), rng.normal(0.0, 6.0, (2, D))])
+    # zero, moderate and large logits (at scale 30 emission probabilities
+    # reach ~1e-26: the segment products lean on their rescaling)
+    Q = np.concatenate([np.zeros((1, D)), rng.normal(0.0, 1.0, (5, D)), rng.normal(0.0, 6.0, (2, D)),
+                        rng.normal(0.0, 30.0, (2, D))])
     say("hmm potential", T, Tsup, K, V)
     _check_potential(sampler, orc, w, z, K, V, Q)
 
