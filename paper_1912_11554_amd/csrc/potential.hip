@@ -21,6 +21,14 @@ constexpr double kHalfLog2Pi = 0.91893853320467274178032973640562;
 // per-lane state needs more registers than that
 template <int S, int CPS>
 constexpr int pot_waves() { return (S == 1 && CPS == 16) || CPS > 8 ? 8 : 16; }
+// two block register sets in the stream for the 8-wave shapes and for fp64
+// rows shared by several lanes (16 waves of fp32 rows hide the loads as well
+// with one set, and fp64 rows of one lane would spill with two); the
+// lane-masked loads of the last column slots in the 8-wave shapes
+template <typename T, int S, int CPS>
+constexpr bool pot_pipe() { return pot_waves<S, CPS>() == 8 || (sizeof(T) == 8 && S > 1); }
+template <int S, int CPS>
+constexpr bool pot_mask() { return pot_waves<S, CPS>() == 8; }
 static_assert(kMaxDim + 1 <= 8 * kWave, "one thread per used column in the final sum");
 
 __device__ __forceinline__ void store_agent(double* p, double v)
@@ -64,7 +72,7 @@ __global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_
 #pragma unroll
     for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
     double loss = 0.0;
-    stream_blocks<T, CPS, S>(X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv,
+    stream_blocks<T, CPS, S, pot_pipe<T, S, CPS>(), pot_mask<S, CPS>()>(X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv,
                              acc, loss);
 
     double* row = part + wave * width;

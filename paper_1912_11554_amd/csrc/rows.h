@@ -17,6 +17,8 @@
 // CPS == R, and in a fixed lane computed by column_source_lane otherwise.
 #pragma once
 
+#include <type_traits>
+
 #include "device.h"
 
 namespace nuts {
@@ -58,22 +60,36 @@ struct BlockShape {
 };
 
 // Raw registers of one block for one lane: CPS column slots of RPL rows,
-// and the RPL labels.
+// and the RPL labels as loaded (one byte each, row i in bits 8 i .. 8 i + 7;
+// they are taken apart where they are used, so a loaded block needs no work
+// before its computation starts).
 template <typename T, int CPS, int S>
 struct BlockRegs {
     using V = typename VecOf<T, BlockShape<T, S>::RPL>::type;
+    using Y = typename std::conditional<BlockShape<T, S>::RPL == 2, uint16_t, uint8_t>::type;
     V x[CPS];
-    uint8_t y[BlockShape<T, S>::RPL];
+    Y y;
 };
 
-// Issue the loads of one block.  The loads are unconditional: a slot past
-// column D - 1 reads the next block's memory (or the zeroed tail of the
-// allocation, at least kTailElems long), a finite value that meets a zero
-// position component in eta and only feeds an accumulator slot that is
-// never output.
-template <typename T, int CPS, int S>
+__device__ __forceinline__ void set_zero(float2& v) { v = make_float2(0.0f, 0.0f); }
+__device__ __forceinline__ void set_zero(double2& v) { v = make_double2(0.0, 0.0); }
+__device__ __forceinline__ void set_zero(double& v) { v = 0.0; }
+
+// Issue the loads of one block.  By default the loads are unconditional: a
+// slot past column D - 1 reads the next block's memory (or the zeroed tail of
+// the allocation, at least kTailElems long), a finite value that meets a zero
+// position component in eta and only feeds an accumulator slot that is never
+// output.  For rows of at most 8 lanes those bytes are a small share of a
+// block and mostly L2 hits.  For rows of 16 or 32 lanes they can be a quarter
+// to a half of the block (D = 257 in 320 slots, D = 129 in 256), and part of
+// them came from HBM a second time (8 % over the algorithmic bytes at
+// D = 257); with MASK such rows skip every slot whose column is past D - 1
+// (it holds zero; slots whose columns are all used load without a lane
+// test), at the cost of registers, so the callers with registers to spare
+// ask for it.
+template <typename T, int CPS, int S, bool MASK>
 __device__ __forceinline__ BlockRegs<T, CPS, S> load_block(const T* __restrict__ blk,
-                                                           const uint8_t* __restrict__ yb)
+                                                           const uint8_t* __restrict__ yb, int D)
 {
     using B = BlockRegs<T, CPS, S>;
     constexpr int RPL = BlockShape<T, S>::RPL;
@@ -84,9 +100,22 @@ __device__ __forceinline__ BlockRegs<T, CPS, S> load_block(const T* __restrict__
     const T* base = blk + p * R + row0;
     B out;
 #pragma unroll
-    for (int k = 0; k < CPS; ++k) out.x[k] = *reinterpret_cast<const typename B::V*>(base + k * S * R);
-#pragma unroll
-    for (int i = 0; i < RPL; ++i) out.y[i] = yb[row0 + i];
+    for (int k = 0; k < CPS; ++k) {
+        const typename B::V* src = reinterpret_cast<const typename B::V*>(base + k * S * R);
+        if constexpr (MASK && S >= 16) {
+            if ((k + 1) * S <= D) {  // wave-uniform: every lane's column is used
+                out.x[k] = *src;
+            } else {
+                typename B::V v;
+                set_zero(v);
+                if (k * S + p < D) v = *src;
+                out.x[k] = v;
+            }
+        } else {
+            out.x[k] = *src;
+        }
+    }
+    out.y = *reinterpret_cast<const typename B::Y*>(yb + row0);  // row0 is a multiple of RPL
     return out;
 }
 
@@ -121,7 +150,7 @@ __device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, in
         if constexpr (S >= 8) eta += pair_move<4>(eta);
         if constexpr (S >= 16) eta += pair_move<8>(eta);
         if constexpr (S >= 32) eta += pair_move<16>(eta);
-        const RowTerms rt = logistic_row_t<T>(eta, in.y[i] != 0);
+        const RowTerms rt = logistic_row_t<T>(eta, ((in.y >> (8 * i)) & 0xff) != 0);
         const bool valid = row0 + i < rows_left;
         r[i] = valid ? rt.resid : 0.0;
         loss += (valid && p == 0) ? rt.loss : 0.0;
@@ -133,27 +162,63 @@ __device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, in
     }
 }
 
-// The blocks first, first + stride, ... < nb of one data set, with the next
-// block's loads in flight while the current block is computed.
-template <typename T, int CPS, int S>
+// The blocks first, first + stride, ... < nb of one data set.
+//
+// PIPE (the grid-wide and standalone passes, where each wave streams many
+// blocks from HBM): the next block's loads are in flight while the current
+// block is computed.  Two register sets take turns (the loop body handles
+// two blocks), so no loaded block is copied from one set to the other: such
+// a copy waits for the loads to land and would leave the wave with no loads
+// in flight at the end of each block.  The loop runs a known count, so no
+// path out of the body leaves a prefetched block unused (with an exit test
+// after the computation the compiler moves the loads behind it, onto the
+// path that uses them).
+//
+// Without PIPE (where the extra register set would not fit beside the rest of
+// the kernel's state): one register set; the next block's loads are issued
+// while the current block's gradient terms are added.  MASK as for
+// load_block.
+template <typename T, int CPS, int S, bool PIPE, bool MASK>
 __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
                                               int64_t N, int64_t nb, int64_t first, int64_t stride,
                                               const double (&qv)[CPS], double (&acc)[CPS], double& loss)
 {
     constexpr int R = BlockShape<T, S>::R;
+    if (first >= nb) return;
     int64_t b = first;
-    if (b >= nb) return;
-    BlockRegs<T, CPS, S> cur = load_block<T, CPS, S>(X + b * D * R, y + b * R);
+    BlockRegs<T, CPS, S> a = load_block<T, CPS, S, MASK>(X + b * D * R, y + b * R, D);
+    if constexpr (PIPE) {
+        const int64_t count = (nb - 1 - first) / stride + 1;  // blocks of this wave
+        int64_t i = 1;                                         // blocks loaded so far
 #pragma unroll 1
-    for (;;) {
-        const int64_t nx = b + stride;
-        const bool more = nx < nb;
-        const int64_t lb = more ? nx : b;  // a valid block either way
-        const BlockRegs<T, CPS, S> nxt = load_block<T, CPS, S>(X + lb * D * R, y + lb * R);
-        compute_block<T, CPS, S>(cur, N - b * R, qv, acc, loss);
-        if (!more) break;
-        cur = nxt;
-        b = nx;
+        for (; i + 1 < count; i += 2) {
+            const int64_t b1 = b + stride, b2 = b1 + stride;
+            const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+            a = load_block<T, CPS, S, MASK>(X + b2 * D * R, y + b2 * R, D);
+            compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
+            b = b2;
+        }
+        if (i < count) {
+            const int64_t b1 = b + stride;
+            const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+            compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
+        } else {
+            compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+        }
+    } else {
+#pragma unroll 1
+        for (;;) {
+            const int64_t nx = b + stride;
+            const bool more = nx < nb;
+            const int64_t lb = more ? nx : b;  // a valid block either way
+            const BlockRegs<T, CPS, S> nxt = load_block<T, CPS, S, MASK>(X + lb * D * R, y + lb * R, D);
+            compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+            if (!more) break;
+            a = nxt;
+            b = nx;
+        }
     }
 }
 

@@ -114,7 +114,7 @@ struct WaveEval {
 #pragma unroll
         for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
         double loss = 0.0;
-        stream_blocks<T, CPS, S>(X, y, D, N, nb, 0, 1, qv, acc, loss);
+        stream_blocks<T, CPS, S, false, false>(X, y, D, N, nb, 0, 1, qv, acc, loss);
         const double col = finish_pass<CPS, S>(acc, loss);
         const double prior = wave_sum(0.5 * q[0] * q[0] * inv_s2);
         U = loss + prior + prior_const;
@@ -126,6 +126,12 @@ struct WaveEval {
 // Grid path.
 
 constexpr int kCmdEval = 1, kCmdExit = 2;
+
+// The grid workers' stream: two block register sets and lane-masked loads of
+// the last column slots for fp32 data; fp64 keeps one set (with two, its
+// kernels spill registers in the stream).
+template <typename T>
+constexpr bool kGridPipe = sizeof(T) == 4;
 
 template <int DPL, int NW>
 struct GridShared {
@@ -273,7 +279,7 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
         const int workers = NW - 1;
-        stream_blocks<T, CPS, S>((const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
+        stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>>((const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
                                  (int64_t)G * workers, qv, acc, loss);
         if constexpr (S <= 8 && CPS == 8) {
             const double col = finish_pass<CPS, S>(acc, loss);
