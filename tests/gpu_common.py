@@ -20,15 +20,18 @@ DECISION_FIELDS = ("tree_depth", "num_steps", "proposal_index", "term_leaf", "di
                    "diverging", "turning", "hit_max_depth")
 
 
-def compare_chain(gpu_samples, gpu_stats, ref, atol=1e-9):
+def compare_chain(gpu_samples, gpu_stats, ref, atol=1e-9, accept_atol=None):
     """Decisions bit-exact, positions and energies within atol (relative to
-    magnitude).  Returns the number of iterations compared."""
+    magnitude), the mean acceptance statistic within accept_atol (default
+    atol).  Returns the number of iterations compared."""
     rs, rst = ref["samples"], ref["stats"]
     n = len(rst)
     for f in DECISION_FIELDS:
         bad = np.flatnonzero(gpu_stats[f][:n] != rst[f])
         assert bad.size == 0, f"{f} differs first at iteration {bad[0]}: gpu {gpu_stats[f][bad[0]]} ref {rst[f][bad[0]]}"
     np.testing.assert_allclose(gpu_samples[:n], rs, rtol=atol, atol=atol)
-    for f in ("potential_energy", "energy", "accept_prob"):
+    for f in ("potential_energy", "energy"):
         np.testing.assert_allclose(gpu_stats[f][:n], rst[f], rtol=atol, atol=atol)
+    ta = atol if accept_atol is None else accept_atol
+    np.testing.assert_allclose(gpu_stats["accept_prob"][:n], rst["accept_prob"], rtol=ta, atol=ta)
     return n
