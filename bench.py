@@ -199,7 +199,13 @@ def cpu_baseline(name, seconds):
         if el >= seconds:
             break
     log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
-    allc = cpu_all_cores(f, X, y, w_true, min(seconds, 10.0))
+    if wl.per_chain_data or wl.num_chains > 1 or wl.N * wl.D < 1_000_000:
+        # many chains, or one small data set: independent evaluations on
+        # every core (each thread its own chain's data set where chains have
+        # their own, else its own position), as independent chains would run
+        allc = cpu_independent(wl, min(seconds, 10.0))
+    else:
+        allc = cpu_all_cores(f, X, y, w_true, min(seconds, 10.0))
     return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
                 sample=f"{n} full potential+gradient evaluations of {name}"
                        f"{' (one chain data set)' if wl.per_chain_data else ''} at w_true, "
@@ -346,6 +352,54 @@ def hmm_line(h, cpu):
     # the paper's HMM figure (NumPyro, 32-bit, one CPU chain): context only
     out["paper_numpyro_cpu_ms_per_leapfrog_step"] = 0.09
     return out
+
+
+def cpu_independent(wl, seconds):
+    """The oracle's gradient on every allowed host core (at most 16), each
+    thread evaluating on its own: chain t's data set for per-chain data,
+    else the shared data at its own position.  Each call of the oracle's
+    timing loop runs about 10 ms of evaluations, so the interpreter's share
+    (which the threads take in turn) stays small."""
+    import concurrent.futures
+
+    import oracle
+    import workloads
+
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    if wl.per_chain_data:
+        Xs, ys = workloads.make_workload(wl, chains=list(range(cores)))
+        sets = [(np.ascontiguousarray(Xs[t]), np.ascontiguousarray(ys[t])) for t in range(cores)]
+    else:
+        X, y = workloads.make_workload(wl)
+        sets = [(X, y)] * cores
+    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+    lib = oracle.lib()
+    f32 = 1 if wl.dtype == "f32" else 0
+    rng = np.random.default_rng(11)
+    pos = [np.ascontiguousarray(w_true + (0.01 * rng.normal(size=wl.D) if t else 0.0), np.float64)
+           for t in range(cores)]
+
+    def worker(t):
+        Xt, yt = sets[t]
+        w = pos[t]
+        g = np.zeros(wl.D)
+        reps = max(1, int(20_000_000 // (Xt.shape[0] * wl.D)))  # about 10 ms per call
+        args = (Xt.ctypes.data, yt.ctypes.data, Xt.shape[0], wl.D, wl.prior_scale, w.ctypes.data,
+                g.ctypes.data, reps, f32)
+        m, t1 = 0, time.perf_counter()
+        while time.perf_counter() - t1 < seconds:
+            lib.orc_logistic_ug_repeat(*args)
+            m += reps
+        return m, time.perf_counter() - t1
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=cores) as ex:
+        res = list(ex.map(worker, range(cores)))
+    v = sum(m / t for m, t in res)
+    log(f"cpu oracle, {cores} threads, independent evaluations: {v:.0f} evaluations/s")
+    what = "its own chain's data set" if wl.per_chain_data else "its own position"
+    return dict(value=v, unit="grad-evals/s", cores=cores,
+                sample=f"{sum(m for m, _ in res)} evaluations, each thread on {what}, "
+                       f"{max(t for _, t in res):.1f}s")
 
 
 def cpu_all_cores(f, X, y, w, seconds):

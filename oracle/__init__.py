@@ -87,6 +87,8 @@ def lib():
         L.orc_logistic_ug.restype = dbl
         L.orc_logistic_ug_f32.argtypes = [P, P, i64, i64, dbl, P, P]
         L.orc_logistic_ug_f32.restype = dbl
+        L.orc_logistic_ug_repeat.argtypes = [P, P, i64, i64, dbl, P, P, i64, i32]
+        L.orc_logistic_ug_repeat.restype = dbl
         L.orc_lingauss_ug.argtypes = [P, P, i64, i64, dbl, dbl, P, P]
         L.orc_lingauss_ug.restype = dbl
         L.orc_bitcount.argtypes = [u64]

@@ -1272,3 +1272,18 @@ double orc_logistic_ug_f32(const float *Xf, const uint8_t *y, int64_t N, int64_t
     U += (double)D * (log(s) + half_log_2pi);
     return U;
 }
+
+/* Timing loop for the benchmark's CPU baseline (no arithmetic of its own):
+ * reps evaluations of the logistic potential and gradient at the same point,
+ * over fp64 rows, or fp32 rows promoted one at a time when f32 is nonzero,
+ * so that a caller's threads spend their time here rather than in the
+ * interpreter between calls.  Returns the last U. */
+double orc_logistic_ug_repeat(const void *X, const uint8_t *y, int64_t N, int64_t D, double s,
+                              const double *w, double *grad, int64_t reps, int f32)
+{
+    double U = 0.0;
+    for (int64_t r = 0; r < reps; ++r)
+        U = f32 ? orc_logistic_ug_f32((const float *)X, y, N, D, s, w, grad)
+                : orc_logistic_ug((const double *)X, y, N, D, s, w, grad);
+    return U;
+}
