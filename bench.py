@@ -190,14 +190,24 @@ def cpu_baseline(name, seconds):
         X, y = X[0], y[0]
     _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
     f = oracle.logistic_potential_grad_f32 if wl.dtype == "f32" else oracle.logistic_potential_grad
+    U_check = f(X, y, w_true)[0]
+    # the oracle's timing loop (about 10 ms of evaluations per call, or one
+    # evaluation when that takes longer), so that small data sets are not
+    # timed with the interpreter's share of each call
+    Xc, yc = np.ascontiguousarray(X), np.ascontiguousarray(y, np.uint8)
+    w, g = np.ascontiguousarray(w_true, np.float64), np.zeros(wl.D)
+    reps = max(1, int(20_000_000 // (Xc.shape[0] * wl.D)))
+    lib = oracle.lib()
     n = 0
     t0 = time.perf_counter()
     while True:
-        f(X, y, w_true)
-        n += 1
+        U = lib.orc_logistic_ug_repeat(Xc.ctypes.data, yc.ctypes.data, Xc.shape[0], wl.D, wl.prior_scale,
+                                       w.ctypes.data, g.ctypes.data, reps, 1 if wl.dtype == "f32" else 0)
+        n += reps
         el = time.perf_counter() - t0
         if el >= seconds:
             break
+    assert U == U_check, (U, U_check)  # the loop evaluates what the entry point does
     log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
     if wl.per_chain_data or wl.num_chains > 1 or wl.N * wl.D < 1_000_000:
         # many chains, or one small data set: independent evaluations on
@@ -293,14 +303,20 @@ def hmm_cpu_baseline(seconds):
     w, z, _, _ = workloads.make_hmm(**HMM_SHAPE)
     D = oracle.hmm_dim(HMM_SHAPE["K"], HMM_SHAPE["V"])
     q = np.random.default_rng(3).normal(0.0, 0.5, D)
+    U_check = oracle.hmm_potential_grad(w, z, HMM_SHAPE["K"], HMM_SHAPE["V"], q)[0]
+    lib = oracle.lib()
+    wu, zu = np.ascontiguousarray(w, np.uint8), np.ascontiguousarray(z, np.uint8)
+    qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
     n = 0
     t0 = time.perf_counter()
-    while True:
-        oracle.hmm_potential_grad(w, z, HMM_SHAPE["K"], HMM_SHAPE["V"], q)
-        n += 1
+    while True:  # the oracle's timing loop, 500 evaluations per call
+        U = lib.orc_hmm_ug_repeat(wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"],
+                                  HMM_SHAPE["V"], qq.ctypes.data, gg.ctypes.data, 500)
+        n += 500
         el = time.perf_counter() - t0
         if el >= seconds:
             break
+    assert U == U_check, (U, U_check)
     log(f"cpu oracle hmm: {n} gradient evaluations in {el:.1f}s")
     # every allowed core (at most 16) evaluating on its own, as independent
     # chains would
@@ -309,19 +325,19 @@ def hmm_cpu_baseline(seconds):
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
 
     def worker(_):
-        # the C entry point with its arguments prepared once, so that the
-        # interpreter's share of a call (which the threads take in turn)
-        # stays small
+        # the oracle's timing loop, about 10 ms of evaluations per call, so
+        # that the interpreter's share (which the threads take in turn) stays
+        # small
         lib = oracle.lib()
         wu, zu = np.ascontiguousarray(w, np.uint8), np.ascontiguousarray(z, np.uint8)
         qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
+        reps = 500
         args = (wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"], HMM_SHAPE["V"],
-                qq.ctypes.data, gg.ctypes.data)
+                qq.ctypes.data, gg.ctypes.data, reps)
         m, t1 = 0, time.perf_counter()
         while time.perf_counter() - t1 < min(seconds, 5.0):
-            for _ in range(20):
-                lib.orc_hmm_ug(*args)
-            m += 20
+            lib.orc_hmm_ug_repeat(*args)
+            m += reps
         return m, time.perf_counter() - t1
 
     with concurrent.futures.ThreadPoolExecutor(max_workers=cores) as ex:

@@ -119,6 +119,8 @@ def lib():
         L.orc_posterior_predictive.restype = None
         L.orc_hmm_ug.argtypes = [P, i64, P, i64, i32, i32, P, P]
         L.orc_hmm_ug.restype = dbl
+        L.orc_hmm_ug_repeat.argtypes = [P, i64, P, i64, i32, i32, P, P, i64]
+        L.orc_hmm_ug_repeat.restype = dbl
         L.orc_expected_log_likelihood.argtypes = [P, i64]
         L.orc_expected_log_likelihood.restype = dbl
         _lib = L

@@ -439,6 +439,16 @@ double orc_hmm_ug(const uint8_t *w, int64_t T, const uint8_t *z, int64_t Tsup, i
     return -f;
 }
 
+/* Timing loop for the benchmark's CPU baseline (no arithmetic of its own):
+ * reps evaluations of orc_hmm_ug at the same point.  Returns the last U. */
+double orc_hmm_ug_repeat(const uint8_t *w, int64_t T, const uint8_t *z, int64_t Tsup, int K, int V,
+                         const double *q, double *grad, int64_t reps)
+{
+    double U = 0.0;
+    for (int64_t r = 0; r < reps; ++r) U = orc_hmm_ug(w, T, z, Tsup, K, V, q, grad);
+    return U;
+}
+
 enum { ORC_TARGET_LOGISTIC = 0, ORC_TARGET_LINGAUSS = 1, ORC_TARGET_HMM = 2 };
 
 typedef struct {
