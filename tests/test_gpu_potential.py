@@ -35,7 +35,8 @@ def _check(sampler, orc, X, y, w, s, dt):
 @pytest.mark.parametrize("dt", ["f64", "f32"])
 @pytest.mark.parametrize("N,D", [(1, 1), (63, 2), (64, 5), (65, 11), (1000, 11), (4097, 9),
                                  (777, 33), (3000, 55), (130, 63), (500, 64), (301, 65),
-                                 (1000, 129), (777, 200), (513, 257), (200, 320)])
+                                 (1000, 129), (777, 200), (513, 257), (200, 320),
+                                 (301, 288), (299, 289), (203, 319)])
 def test_random_positions(sampler, orc, dt, N, D):
     X, y, w_true = workloads.make_logistic(N, D, w_scale=0.7, key=[50, N * 1000 + D],
                                            dtype=dt)

@@ -169,3 +169,21 @@ def test_streaming_workload_first_iterations(sampler, orc):
     # H - H0, so the statistic is compared within 2e-4 (the energies
     # themselves, about 2e6, within 1e-6 relative)
     compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6, accept_atol=2e-4)
+
+
+@pytest.mark.parametrize("D", [65, 80, 128, 129, 160, 256, 257, 288, 289, 320])
+def test_grid_fp32_wide_rows(sampler, orc, D):
+    # fp32 data on the grid path, rows of 16 and 32 lanes: the loads of the
+    # column slots past D - 1 are lane-masked and the streaming waves
+    # alternate two block register sets; D at and around the slot
+    # boundaries, a ragged last block
+    N = 1237
+    X, y, _ = workloads.make_logistic(N, D, w_scale=0.1, key=[67, D], dtype="f32")
+    say("sampler grid fp32 wide", N, D)
+    kw = dict(step_size=0.02, max_tree_depth=5, num_warmup=1, num_samples=4, seed=7)
+    r = sampler.sample(X, y, path=2, **kw)
+    ref = orc.nuts(X.astype(np.float64), y, **kw)
+    # the acceptance statistic averages exp(-(H - H0)) over the leaves; each
+    # row's fp32-evaluated loss carries about 3e-8 absolute error, so with no
+    # cancellation between the two sums H - H0 is off by at most 3e-8 N
+    compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6, accept_atol=3e-8 * N)
