@@ -121,6 +121,9 @@ def lib():
         L.orc_hmm_ug.restype = dbl
         L.orc_hmm_ug_repeat.argtypes = [P, i64, P, i64, i32, i32, P, P, i64]
         L.orc_hmm_ug_repeat.restype = dbl
+        L.orc_set_warmup_trace.argtypes = [P, i64]
+        L.orc_logistic_laplace.argtypes = [P, i32, P, i64, i64, dbl, P, P, P]
+        L.orc_logistic_laplace.restype = i64
         L.orc_expected_log_likelihood.argtypes = [P, i64]
         L.orc_expected_log_likelihood.restype = dbl
         _lib = L
@@ -195,6 +198,26 @@ def logistic_potential_grad_f32(Xf, y, w, prior_scale=1.0):
     return U, g
 
 
+def logistic_laplace(X, y, prior_scale=1.0):
+    """Normal approximation of the logistic posterior: the MAP by Newton's
+    method (iteratively reweighted least squares), the Laplace covariance
+    (the inverse Hessian of U there) and the posterior mean to order 1/N^2
+    (the mode moved by the skewness of U).  X may be fp64 or fp32 (promoted
+    row by row).  Returns dict(w_map, cov, mean, newton_steps)."""
+    f32 = X.dtype == np.float32
+    X = np.ascontiguousarray(X, dtype=np.float32 if f32 else np.float64)
+    y = _u8(y)
+    N, D = X.shape
+    w = np.zeros(D)
+    cov = np.zeros((D, D))
+    mean = np.zeros(D)
+    steps = lib().orc_logistic_laplace(_p(X), 1 if f32 else 0, _p(y), N, D, prior_scale, _p(w),
+                                       _p(cov), _p(mean))
+    if steps < 0:
+        raise RuntimeError("Newton's method did not converge")
+    return dict(w_map=w, cov=cov, mean=mean, newton_steps=int(steps))
+
+
 def lingauss_potential_grad(X, yv, w, prior_scale=1.0, noise_scale=1.0):
     X = _f64(X)
     yv = _f64(yv)
@@ -238,14 +261,16 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
          prior_scale=1.0, inv_mass=None, builder=BUILDER_ITERATIVE, adapt_diag_mass=False,
          init_q=None, first_iter=0, target=TARGET_LOGISTIC, yv=None, noise_scale=1.0,
          trace_cap=0, leaves_cap=0, sel_salt=0, adapt_step_size=False, target_accept=0.8,
-         uturn_generalized=False, hmm=None, subtree_merge=False):
+         uturn_generalized=False, hmm=None, subtree_merge=False, warmup_trace=False):
     """One chain of NUTS.  Returns a dict with samples [S, D], stats [S],
     final_q [D], inv_mass [D], step_size (the one in use at the end: the
     adapted one with adapt_step_size), grad_evals; with trace_cap the U-turn check
     trace as (first_leaf, last_leaf) pairs; with leaves_cap the generated
     leaves as records (j, n, position, H - H0).  ``sel_salt`` (test only)
     re-keys the proposal-selection draws and nothing else.  uturn_generalized
-    selects the momentum-sum criterion (reading R20).  With hmm = dict(w, z,
+    selects the momentum-sum criterion (reading R20).  warmup_trace=True
+    adds "warmup_q" [W, D] (the state after each warmup iteration) and
+    "warmup_eps" [W] (the step size each warmup iteration ran with).  With hmm = dict(w, z,
     K, V) the target is the semi-supervised HMM (reading R21) and X, y are
     ignored.  subtree_merge chooses each subtree's proposal at the merges of
     its halves (reading R22) instead of by the streaming choice."""
@@ -268,19 +293,29 @@ def nuts(X, y, *, step_size, max_tree_depth, num_warmup, num_samples, seed, chai
     lv = np.zeros(max(4 * leaves_cap, 1), dtype=np.int64)
     lvlen = ctypes.c_int64(0)
     eps_out = ctypes.c_double(0.0)
-    nev = lib().orc_nuts_chain(
-        target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale, noise_scale, step_size,
-        _p(_f64(inv_mass)), max_tree_depth, num_warmup, num_samples, seed, chain, builder,
-        1 if adapt_diag_mass else 0, _p(_f64(init_q)), first_iter, _p(samples), _p(stats),
-        _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
-        ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
-        ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
-        ctypes.byref(eps_out), 1 if uturn_generalized else 0, _p(hz),
-        0 if hz is None else hz.shape[0], 0 if hmm is None else hmm["K"],
-        0 if hmm is None else hmm["V"], 1 if subtree_merge else 0,
-    )
+    wt = np.zeros((max(num_warmup, 1), D + 1)) if warmup_trace else None
+    if warmup_trace:
+        lib().orc_set_warmup_trace(_p(wt), num_warmup)
+    try:
+        nev = lib().orc_nuts_chain(
+            target, _p(X), _p(_u8(y)), _p(_f64(yv)), N, D, prior_scale, noise_scale, step_size,
+            _p(_f64(inv_mass)), max_tree_depth, num_warmup, num_samples, seed, chain, builder,
+            1 if adapt_diag_mass else 0, _p(_f64(init_q)), first_iter, _p(samples), _p(stats),
+            _p(final_q), _p(out_im), _p(tr) if trace_cap else None, 2 * trace_cap,
+            ctypes.byref(trlen), _p(lv) if leaves_cap else None, 4 * leaves_cap,
+            ctypes.byref(lvlen), sel_salt, 1 if adapt_step_size else 0, target_accept,
+            ctypes.byref(eps_out), 1 if uturn_generalized else 0, _p(hz),
+            0 if hz is None else hz.shape[0], 0 if hmm is None else hmm["K"],
+            0 if hmm is None else hmm["V"], 1 if subtree_merge else 0,
+        )
+    finally:
+        if warmup_trace:
+            lib().orc_set_warmup_trace(None, 0)
     out = dict(samples=samples, stats=stats, final_q=final_q, inv_mass=out_im,
                step_size=eps_out.value, grad_evals=nev)
+    if warmup_trace:
+        out["warmup_q"] = wt[:num_warmup, :D].copy()
+        out["warmup_eps"] = wt[:num_warmup, D].copy()
     if trace_cap:
         out["trace"] = tr[: trlen.value].reshape(-1, 2)
     if leaves_cap:

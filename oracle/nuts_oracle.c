@@ -1109,6 +1109,18 @@ typedef struct {
     double *mean, *m2;
 } orc_welford;
 
+/* Test hook: when set, every warmup iteration k < cap writes the state after
+ * it and the step size it ran with into buf [k][D + 1] (the state, then the
+ * step size), so that tests can recompute the mass rule from the states. */
+static double *orc_wtrace_buf = NULL;
+static int64_t orc_wtrace_cap = 0;
+
+void orc_set_warmup_trace(double *buf, int64_t cap)
+{
+    orc_wtrace_buf = buf;
+    orc_wtrace_cap = buf ? cap : 0;
+}
+
 /* Full chain: init at q0, then num_warmup + num_samples iterations whose
  * global indices start at first_iter.  Kept samples go to out_samples
  * [num_samples][D] and out_stats [num_samples].  The final state goes to
@@ -1171,7 +1183,12 @@ int64_t orc_nuts_chain(int kind, const double *X, const uint8_t *y, const double
     orc_stats st;
     for (int64_t k = 0; k < num_warmup + num_samples; ++k) {
         it.t = (uint64_t)(first_iter + k);
+        double eps_used = it.eps;
         orc_iteration(&it, &cur, max_depth, builder, &st);
+        if (k < num_warmup && k < orc_wtrace_cap) {
+            memcpy(orc_wtrace_buf + k * (D + 1), cur.q, (size_t)D * sizeof(double));
+            orc_wtrace_buf[k * (D + 1) + D] = eps_used;
+        }
         if (adapt && k < num_warmup) {
             it.eps = orc_da_update(&da, st.accept_prob, target_accept);
             if (wi < nwin && k >= win[2 * wi] && k < win[2 * wi + 1]) {
@@ -1296,4 +1313,164 @@ double orc_logistic_ug_repeat(const void *X, const uint8_t *y, int64_t N, int64_
         U = f32 ? orc_logistic_ug_f32((const float *)X, y, N, D, s, w, grad)
                 : orc_logistic_ug((const double *)X, y, N, D, s, w, grad);
     return U;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Normal approximation of the logistic posterior (tests only): the sampler's
+ * long runs are checked against it where no sampler of the oracle can run
+ * long enough (hundreds of thousands of rows).
+ *
+ * MAP by Newton's method on U, which for this model is iteratively
+ * reweighted least squares: with c_i = sigma(eta_i) sigma(-eta_i) the Hessian
+ * is H(w) = X^T diag(c) X + I / s^2 and each step solves H d = grad U and
+ * sets w <- w - d, from w = 0 until no coordinate moves by more than
+ * 1e-13 (1 + |w_j|) (at most 100 steps).  The Laplace covariance is H^-1 at
+ * the MAP.  The posterior mean differs from the mode at order 1/N through
+ * the skewness of U: expanding exp(-U) around the mode to the cubic term
+ * T_jkl = sum_i sigma''(eta_i) x_ij x_ik x_il (sigma'' = c (1 - 2 sigma), the
+ * third derivative of U; the prior adds none) gives
+ *   E[w] = w_map - (1/2) H^-1 b,   b_j = sum_kl T_jkl (H^-1)_kl
+ *        = sum_i sigma''(eta_i) x_ij (x_i^T H^-1 x_i),
+ * with an error of order 1/N^2.  X is fp64, or fp32 promoted one row at a
+ * time when f32 is nonzero.  Plain loops, the Cholesky factorisation written
+ * out. */
+static void orc_row(const void *X, int f32, int64_t i, int64_t D, double *row)
+{
+    if (f32) {
+        const float *xf = (const float *)X + i * D;
+        for (int64_t j = 0; j < D; ++j) row[j] = (double)xf[j];
+    } else {
+        const double *xd = (const double *)X + i * D;
+        for (int64_t j = 0; j < D; ++j) row[j] = xd[j];
+    }
+}
+
+/* H = X^T diag(c) X + I / s^2 at w, and the gradient of U at w. */
+static void orc_logistic_hessian(const void *X, int f32, const uint8_t *y, int64_t N, int64_t D,
+                                 double s, const double *w, double *H, double *grad)
+{
+    double *row = (double *)malloc((size_t)D * sizeof(double));
+    for (int64_t j = 0; j < D * D; ++j) H[j] = 0.0;
+    for (int64_t j = 0; j < D; ++j) grad[j] = 0.0;
+    for (int64_t i = 0; i < N; ++i) {
+        orc_row(X, f32, i, D, row);
+        double eta = 0.0;
+        for (int64_t j = 0; j < D; ++j) eta += row[j] * w[j];
+        double c = orc_sigmoid(eta) * orc_sigmoid(-eta);
+        double sgn = y[i] ? -1.0 : 1.0;
+        double r = sgn * orc_sigmoid(sgn * eta);
+        for (int64_t j = 0; j < D; ++j) {
+            grad[j] += r * row[j];
+            double cj = c * row[j];
+            for (int64_t k = 0; k <= j; ++k) H[j * D + k] += cj * row[k];
+        }
+    }
+    double inv_s2 = 1.0 / (s * s);
+    for (int64_t j = 0; j < D; ++j) {
+        grad[j] += w[j] * inv_s2;
+        H[j * D + j] += inv_s2;
+        for (int64_t k = 0; k < j; ++k) H[k * D + j] = H[j * D + k];
+    }
+    free(row);
+}
+
+/* Lower Cholesky factor L of a symmetric positive definite A (in place of
+ * the lower triangle of L); returns 0 if A is not positive definite. */
+static int orc_cholesky(const double *A, int64_t D, double *L)
+{
+    for (int64_t j = 0; j < D * D; ++j) L[j] = 0.0;
+    for (int64_t j = 0; j < D; ++j) {
+        double d = A[j * D + j];
+        for (int64_t k = 0; k < j; ++k) d -= L[j * D + k] * L[j * D + k];
+        if (!(d > 0.0)) return 0;
+        double ljj = sqrt(d);
+        L[j * D + j] = ljj;
+        for (int64_t i = j + 1; i < D; ++i) {
+            double v = A[i * D + j];
+            for (int64_t k = 0; k < j; ++k) v -= L[i * D + k] * L[j * D + k];
+            L[i * D + j] = v / ljj;
+        }
+    }
+    return 1;
+}
+
+/* x = A^-1 b with A = L L^T (forward, then backward substitution). */
+static void orc_chol_solve(const double *L, int64_t D, const double *b, double *x)
+{
+    for (int64_t i = 0; i < D; ++i) {
+        double v = b[i];
+        for (int64_t k = 0; k < i; ++k) v -= L[i * D + k] * x[k];
+        x[i] = v / L[i * D + i];
+    }
+    for (int64_t i = D - 1; i >= 0; --i) {
+        double v = x[i];
+        for (int64_t k = i + 1; k < D; ++k) v -= L[k * D + i] * x[k];
+        x[i] = v / L[i * D + i];
+    }
+}
+
+/* Writes w_map [D], cov [D][D] (H^-1 at the MAP) and mean [D] (the
+ * skewness-corrected mean); returns the Newton steps taken, or -1 if a
+ * Hessian was not positive definite or the steps did not converge. */
+int64_t orc_logistic_laplace(const void *X, int f32, const uint8_t *y, int64_t N, int64_t D,
+                             double s, double *w_map, double *cov, double *mean)
+{
+    double *H = (double *)malloc((size_t)(D * D) * sizeof(double));
+    double *L = (double *)malloc((size_t)(D * D) * sizeof(double));
+    double *g = (double *)malloc((size_t)D * sizeof(double));
+    double *d = (double *)malloc((size_t)D * sizeof(double));
+    double *e = (double *)calloc((size_t)D, sizeof(double));
+    double *row = (double *)malloc((size_t)D * sizeof(double));
+    double *b = (double *)calloc((size_t)D, sizeof(double));
+    int64_t steps = -1;
+    for (int64_t j = 0; j < D; ++j) w_map[j] = 0.0;
+    for (int64_t it = 1; it <= 100; ++it) {
+        orc_logistic_hessian(X, f32, y, N, D, s, w_map, H, g);
+        if (!orc_cholesky(H, D, L)) goto done;
+        orc_chol_solve(L, D, g, d);
+        int moved = 0;
+        for (int64_t j = 0; j < D; ++j) {
+            w_map[j] -= d[j];
+            if (fabs(d[j]) > 1e-13 * (1.0 + fabs(w_map[j]))) moved = 1;
+        }
+        if (!moved) {
+            steps = it;
+            break;
+        }
+    }
+    if (steps < 0) goto done;
+    /* H^-1 at the MAP, column by column */
+    orc_logistic_hessian(X, f32, y, N, D, s, w_map, H, g);
+    if (!orc_cholesky(H, D, L)) {
+        steps = -1;
+        goto done;
+    }
+    for (int64_t k = 0; k < D; ++k) {
+        for (int64_t j = 0; j < D; ++j) e[j] = (j == k) ? 1.0 : 0.0;
+        orc_chol_solve(L, D, e, d);
+        for (int64_t j = 0; j < D; ++j) cov[j * D + k] = d[j];
+    }
+    /* b_j = sum_i sigma''(eta_i) x_ij (x_i^T cov x_i) */
+    for (int64_t i = 0; i < N; ++i) {
+        orc_row(X, f32, i, D, row);
+        double eta = 0.0;
+        for (int64_t j = 0; j < D; ++j) eta += row[j] * w_map[j];
+        double sp = orc_sigmoid(eta), sm = orc_sigmoid(-eta);
+        double s2 = sp * sm * (sm - sp);
+        double quad = 0.0;
+        for (int64_t j = 0; j < D; ++j) {
+            double cj = 0.0;
+            for (int64_t k = 0; k < D; ++k) cj += cov[j * D + k] * row[k];
+            quad += row[j] * cj;
+        }
+        for (int64_t j = 0; j < D; ++j) b[j] += s2 * quad * row[j];
+    }
+    for (int64_t j = 0; j < D; ++j) {
+        double cb = 0.0;
+        for (int64_t k = 0; k < D; ++k) cb += cov[j * D + k] * b[k];
+        mean[j] = w_map[j] - 0.5 * cb;
+    }
+done:
+    free(H); free(L); free(g); free(d); free(e); free(row); free(b);
+    return steps;
 }
