@@ -147,6 +147,34 @@ def test_covtype_first_iterations(sampler, orc, name):
     compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-9 if wl.dtype == "f64" else 1e-6)
 
 
+@pytest.mark.parametrize("name", ["covtype_n581012_d55_f64", "covtype_n581012_d55_f32"])
+def test_covtype_50_iterations_from_generating_weights(sampler, orc, name):
+    # the 581,012 x 55 workload on the grid path in the benchmark's launch
+    # shape, 50 iterations from the generating weights (in the posterior's
+    # bulk: trees of typical length), every decision and position checked
+    wl = workloads.WORKLOADS[name]
+    X, y = workloads.make_workload(wl)
+    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+    iters = 50
+    say("sampler covtype grid from w_true", name, "iters", iters)
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=iters, seed=wl.seed, path=2, init_q=w_true)
+    ref = _oracle_chain(orc, X, y, wl, 0, iters, init_q=w_true)
+    # The acceptance statistic averages exp(-(H - H0)) over the leaves, an
+    # absolute quantity from the difference of two energies of ~5e4.  fp64:
+    # the two sides' energies agree to ~1e-13 of their size (summation order,
+    # carried along 50 iterations of trajectories), so it is compared within
+    # 1e-12 |H|.  fp32: each row's loss is evaluated in fp32 (~3e-8 absolute
+    # error), so H - H0 carries a random walk of sqrt(2 N) 3e-8 = 3.2e-5 at
+    # N = 581,012; compared within 1.5e-4 (about 4.5 of those).
+    H = np.abs(ref["stats"]["energy"]).max()
+    n = compare_chain(r["samples"][0], r["stats"][0], ref,
+                      atol=1e-9 if wl.dtype == "f64" else 1e-6,
+                      accept_atol=1e-12 * H if wl.dtype == "f64" else 1.5e-4)
+    assert n == iters
+    assert r["grad_evals"] == ref["grad_evals"]
+
+
 def test_streaming_workload_first_iterations(sampler, orc):
     # the 4,000,000 x 257 fp32 set (10 % of the features zero) on the grid
     # path in the launch shape the benchmark times (32-lane rows, 10 column
@@ -160,7 +188,9 @@ def test_streaming_workload_first_iterations(sampler, orc):
     say("sampler 4M x 257 grid", "iters", iters)
     r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
                        num_warmup=0, num_samples=iters, seed=wl.seed, path=2, init_q=w_true)
-    ref = _oracle_chain(orc, X, y, wl, 0, iters, init_q=w_true)
+    X64 = X.astype(np.float64)
+    ref = orc.nuts(X64, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                   num_warmup=0, num_samples=iters, seed=wl.seed, init_q=w_true)
     assert ref["stats"]["num_steps"].sum() >= 4  # real trees, not a divergence at the first leaf
     # the acceptance statistic averages exp(-(H - H0)) over the leaves, and
     # H - H0 is the difference of two 4,000,000-row sums whose row terms use
@@ -168,6 +198,21 @@ def test_streaming_workload_first_iterations(sampler, orc):
     # row): as a random walk that is sqrt(N) x 3e-8 = 6e-5 absolute in
     # H - H0, so the statistic is compared within 2e-4 (the energies
     # themselves, about 2e6, within 1e-6 relative)
+    compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6, accept_atol=2e-4)
+    # the workload's diagonal mass (reading R13) across the end of warmup:
+    # 4 warmup iterations (the mass from the states after iterations 2 and 3),
+    # then 2 with it; depth 3 keeps the oracle's share to about 40 full
+    # evaluations of the 4,000,000 rows
+    say("sampler 4M x 257 grid, diagonal mass across the end of warmup")
+    kw = dict(step_size=wl.step_size, max_tree_depth=3, num_warmup=4, num_samples=2,
+              seed=wl.seed, init_q=w_true, adapt_diag_mass=True)
+    r = sampler.sample(X, y, path=2, **kw)
+    del X
+    ref = orc.nuts(X64, y, **kw)
+    np.testing.assert_allclose(r["inv_mass"][0], ref["inv_mass"], rtol=1e-5)
+    # the rule's 1e-3 regularisation outweighs these states' variances
+    # (~1e-6), so the normalised mass moves off one only slightly, but it moves
+    assert np.abs(ref["inv_mass"] - 1.0).max() > 1e-6
     compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6, accept_atol=2e-4)
 
 
