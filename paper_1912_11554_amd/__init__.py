@@ -28,6 +28,7 @@ EXPORTED = [
     "nuts_data_potential_grad", "nuts_data_potential_grad_batched", "nuts_potential_grad",
     "nuts_data_log_likelihood", "nuts_sample_data", "nuts_sample",
     "nuts_hmm_potential_grad", "nuts_hmm_sample", "nuts_data_posterior_predictive",
+    "nuts_data_potential_grad_noalloc",
 ]
 
 STATS_DTYPE = np.dtype([
@@ -99,6 +100,8 @@ def load_library():
     L.nuts_data_free.restype = None
     L.nuts_data_potential_grad.argtypes = [P, P, dbl, P, i64, P, P]
     L.nuts_data_potential_grad.restype = i32
+    L.nuts_data_potential_grad_noalloc.argtypes = [P, P, dbl, P, i64, P, P]
+    L.nuts_data_potential_grad_noalloc.restype = i32
     L.nuts_data_potential_grad_batched.argtypes = [P, P, dbl, P, i64, P, P]
     L.nuts_data_potential_grad_batched.restype = i32
     L.nuts_potential_grad.argtypes = [P, P, P, i64, i64, i32, dbl, P, P, P]
@@ -335,9 +338,13 @@ class Data:
                                                                _ptr(out_y)))
         return out_y
 
-    def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None, batched=False):
+    def potential_grad(self, W, prior_scale=1.0, out_U=None, out_grad=None, batched=False,
+                       no_alloc=False):
         """U [K] and grad [K, D] at positions W [K, D] (numpy or device tensor).
-        batched=True uses nuts_data_potential_grad_batched (fp32 matrix cores)."""
+        batched=True uses nuts_data_potential_grad_batched (fp32 matrix cores).
+        no_alloc=True uses nuts_data_potential_grad_noalloc: W, out_U and
+        out_grad must then be device tensors, and the call returns once the
+        work is enqueued on the handle's stream (synchronise before reading)."""
         if isinstance(W, np.ndarray):
             W = np.ascontiguousarray(W, dtype=np.float64).reshape(-1, self.D)
         K = W.shape[0]
@@ -346,6 +353,7 @@ class Data:
         if out_grad is None:
             out_grad = np.zeros((K, self.D))
         fn = (self.s._L.nuts_data_potential_grad_batched if batched
+              else self.s._L.nuts_data_potential_grad_noalloc if no_alloc
               else self.s._L.nuts_data_potential_grad)
         self.s._check(fn(self.s._h, self._d, prior_scale, _ptr(W), K, _ptr(out_U),
                          _ptr(out_grad)))

@@ -49,6 +49,9 @@ struct nuts_handle {
     // arrival counts of the potential kernel, one per item; zeroed once, the
     // kernel leaves them zero
     unsigned int* pot_counts = nullptr;
+    // this device's copy of the fixed workspace of the allocation-free entry
+    // point (set up by nuts_init; never freed)
+    void* static_ws = nullptr;
 };
 
 static hipError_t potential_counts(nuts_handle* h, unsigned int** out)
@@ -385,6 +388,12 @@ int nuts_init(nuts_handle** out, int device_ordinal, void* hip_stream)
         }
         h->own_stream = true;
     }
+    e = static_workspace_setup(device_ordinal, h->stream, &h->static_ws);
+    if (e != hipSuccess) {
+        if (h->own_stream) (void)hipStreamDestroy(h->stream);
+        delete h;
+        return fail(nullptr, NUTS_EDEVICE, "nuts_init: fixed workspace: %s", hipGetErrorString(e));
+    }
     *out = h;
     return NUTS_OK;
 }
@@ -514,6 +523,34 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
     HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
     HIP_TRY(h, hipStreamSynchronize(h->stream));
+    return NUTS_OK;
+}
+
+int nuts_data_potential_grad_noalloc(nuts_handle* h, const nuts_data* d, double prior_scale, const double* W,
+                                     int64_t K, double* out_U, double* out_grad)
+{
+    if (!h) return NUTS_EINVAL;
+    h->err.clear();
+    if (!d) return fail(h, NUTS_EINVAL, "data is NULL");
+    if (!W || !out_U || !out_grad) return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be non-NULL");
+    if (K < 1 || K > kStaticMaxItems)
+        return fail(h, NUTS_EINVAL, "K must be in [1, %lld] (got %lld)", (long long)kStaticMaxItems, (long long)K);
+    if (d->view.nds > 1 && K != d->view.nds)
+        return fail(h, NUTS_EINVAL, "per-chain data: K (%lld) must equal the number of data sets (%lld)",
+                    (long long)K, (long long)d->view.nds);
+    if (!finite_pos(prior_scale)) return fail(h, NUTS_EINVAL, "prior_scale must be finite and > 0");
+    if (!is_device_ptr(W) || !is_device_ptr(out_U) || !is_device_ptr(out_grad))
+        return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be device memory (this entry point copies nothing)");
+    const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
+    const size_t need = (size_t)K * plan.groups_per_item * plan.width * sizeof(double);
+    if (need > kStaticPartialBytes)
+        return fail(h, NUTS_EINVAL,
+                    "K = %lld positions need %zu bytes of partial sums (%d groups of %d doubles each), more than "
+                    "the %zu bytes of the fixed workspace",
+                    (long long)K, need, plan.groups_per_item, plan.width, kStaticPartialBytes);
+    DeviceScope ds(h->device);
+    HIP_TRY(h, launch_potential_grad_static(h->static_ws, d->view, prior_scale, W, K, plan, out_U, out_grad,
+                                            h->stream));
     return NUTS_OK;
 }
 

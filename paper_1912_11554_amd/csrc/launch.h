@@ -83,6 +83,22 @@ hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const d
                                  const PotentialPlan& plan, double* partials, unsigned int* counters,
                                  double* out_U, double* out_grad, hipStream_t stream);
 
+// The allocation-free form of launch_potential_grad: its arrival counts and
+// partial rows live in a fixed device array of kStaticScratchBytes (the
+// counts in its first kStaticCountBytes, the partial rows after them).
+// static_workspace_setup, called once per device with that device current
+// (nuts_init does), finds this device's copy of the array and zeroes the
+// counts; it returns the array's device address.  Calls that overlap on one
+// device race on the array.
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+constexpr size_t kStaticCountBytes = (size_t)64 << 10;
+constexpr int64_t kStaticMaxItems = (int64_t)(kStaticCountBytes / sizeof(unsigned int));
+constexpr size_t kStaticPartialBytes = kStaticScratchBytes - kStaticCountBytes;
+hipError_t static_workspace_setup(int device, hipStream_t stream, void** out);
+hipError_t launch_potential_grad_static(void* workspace, const DataView& dv, double prior_scale, const double* W,
+                                        int64_t K, const PotentialPlan& plan, double* out_U, double* out_grad,
+                                        hipStream_t stream);
+
 // Sampler arguments common to both paths (device pointers).
 struct SamplerArgs {
     DataView data;

@@ -8,8 +8,17 @@
 // completes an item's count adds the item's G partial rows in a fixed order
 // and the Gaussian prior terms, writes U and grad U, and re-zeroes the count.
 // No floating-point atomics anywhere, so results are bitwise reproducible.
+#include <mutex>
+
 #include "launch.h"
 #include "rows.h"
+
+// Workspace of the allocation-free potential entry point: the arrival counts
+// (kStaticCountBytes), then the partial rows.  Every device the library runs
+// on holds its own copy until the process ends.  Host code never passes this
+// name to a kernel or a copy (on the host it only stands for the symbol):
+// it uses the address hipGetSymbolAddress gives for the current device.
+static __device__ __align__(256) unsigned char scratch[nuts::kStaticScratchBytes];
 
 namespace nuts {
 
@@ -229,6 +238,58 @@ hipError_t launch_expected_ll(const double* ll, int64_t S, double* out, hipStrea
 {
     hipLaunchKernelGGL(expected_ll_kernel, dim3(1), dim3(64), 0, stream, ll, S, out);
     return hipGetLastError();
+}
+
+namespace {
+
+__global__ void __launch_bounds__(256) zero_counts_kernel(unsigned int* __restrict__ c, int n)
+{
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) c[i] = 0u;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mutex;
+void* g_static_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+hipError_t static_workspace_setup(int device, hipStream_t stream, void** out)
+{
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_static_mutex);
+    if (!g_static_ptr[device]) {
+        // the caller has made `device` current: the symbol's address is this
+        // device's copy of the array
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        // the counts start at zero (each call clears the ones it uses as well)
+        const int n = (int)(kStaticCountBytes / sizeof(unsigned int));
+        hipLaunchKernelGGL(zero_counts_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, (unsigned int*)p, n);
+        e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return e;
+        g_static_ptr[device] = p;
+    }
+    *out = g_static_ptr[device];
+    return hipSuccess;
+}
+
+hipError_t launch_potential_grad_static(void* workspace, const DataView& dv, double prior_scale, const double* W,
+                                        int64_t K, const PotentialPlan& plan, double* out_U, double* out_grad,
+                                        hipStream_t stream)
+{
+    unsigned int* counts = (unsigned int*)workspace;
+    double* partials = (double*)((char*)workspace + kStaticCountBytes);
+    // a call that overlapped another one on this device may have left its
+    // counts anywhere: clear this call's counts first (a kernel, not a
+    // memset, so that the call can be captured into a graph)
+    hipLaunchKernelGGL(zero_counts_kernel, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, stream, counts, (int)K);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_potential_grad(dv, prior_scale, W, K, plan, partials, counts, out_U, out_grad, stream);
 }
 
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)

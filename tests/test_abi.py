@@ -47,6 +47,7 @@ def test_null_handle_is_rejected():
     assert L.nuts_sample_data(None, None, 0, 1.0, 0.1, None, 5, 0, 1, 1, 0, None, None,
                               None) == nuts.NUTS_EINVAL
     assert L.nuts_data_potential_grad(None, None, 1.0, None, 1, None, None) == nuts.NUTS_EINVAL
+    assert L.nuts_data_potential_grad_noalloc(None, None, 1.0, None, 1, None, None) == nuts.NUTS_EINVAL
     L.nuts_free(None)                    # no-op
     L.nuts_data_free(None, None)         # no-op
     assert L.nuts_last_error(None) is not None
