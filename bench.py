@@ -4,8 +4,7 @@
 Default workload: the covtype-shaped logistic regression (N = 581,012 rows,
 D = 55 columns with the intercept, synthetic iid N(0, 1) features, fp32),
 one chain.  `--workload` selects another configured workload (see
-workloads.py), e.g. the 4,096 small per-chain models or the 4,000,000 x 257
-streaming model.
+workloads.py).
 
 A "step" is one NUTS iteration of every chain: momentum, trajectory
 doubling with the iterative tree builder, every leapfrog step's fused
@@ -16,10 +15,19 @@ iterations with the data already in HBM.  Defaults: the workload's own
 warmup / sample counts.
 
 The JSON line reports leapfrog gradient evaluations per second (`value`,
-summed over chains), ESS/s, the roofline of the sampler kernel
+summed over chains) of that timed call and the roofline of its kernel
 (algorithmic bytes = one read of X and y per gradient evaluation, over the
-kernel's time measured with HIP events on the launch stream) and the CPU
-oracle's gradient rate on the same data as a baseline.
+call's time from HIP events on the stream the kernel runs on).  Beside it:
+  - ESS/s from the metric workload's full protocol (1000 warmup + 1000
+    draws, fp32 and fp64), the only run long enough for an ESS;
+  - the standalone gradient pass (the potential kernel alone, one position
+    per call, back-to-back calls) for fp32 and fp64;
+  - the other workloads' own lines (4,096 small per-chain models, 256
+    chains on shared data on the matrix cores, the 4,000,000 x 257 stream),
+    each with its roofline and CPU baseline;
+  - the semi-supervised HMM;
+  - the CPU oracle's gradient rate on the same data (one core, and all
+    allowed cores up to 16) as a baseline.
 """
 from __future__ import annotations
 
@@ -42,13 +50,94 @@ MFMA_F32_PEAK_TFLOPS = 157.3   # dense fp32 matrix-core peak of the MI355X
 # lane that is the 78.6 TFLOP/s fp64 vector peak)
 VALU_PEAK_GIPS = 614.4
 METRIC = "leapfrog grad-evals/s + ESS/s, logistic N=581012 D=55; % HBM roofline"
+SUB_WORKLOADS = ("chains4096_n500_d9_f64", "shared256_n200000_d129_f32", "stream_n4m_d257_f32")
+# iterations (warmup, timed) of the other workloads' lines
+SUB_STEPS = {"chains4096_n500_d9_f64": (100, 200), "shared256_n200000_d129_f32": (50, 50),
+             "stream_n4m_d257_f32": (30, 20)}
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_workload(name, steps=None, warmup=None, adapt=False, variants=None):
+def _stream():
+    """A torch stream of default priority that the library and the timing
+    events share, so that the events bracket exactly the library's work."""
+    import torch
+    return torch.cuda.Stream()
+
+
+def generate_on_device(wl):
+    """The workload's recipe drawn on the device (torch's generator): used for
+    the 4,000,000 x 257 set, whose numpy draw takes minutes.  w_true ~
+    N(0, w_scale^2); features N(0, 1), zeroed with probability zero_frac; a
+    ones column; y ~ Bernoulli(sigmoid(X w_true)).  Returns device X, y and
+    host w_true."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1000 + wl.data_seed)
+    D = wl.D
+    w = torch.randn(D, generator=g, device="cuda", dtype=torch.float64) * wl.w_scale
+    dt = torch.float32 if wl.dtype == "f32" else torch.float64
+    X = torch.empty((wl.N, D), dtype=dt, device="cuda")
+    y = torch.empty(wl.N, dtype=torch.uint8, device="cuda")
+    chunk = 1 << 18
+    for r0 in range(0, wl.N, chunk):
+        r1 = min(wl.N, r0 + chunk)
+        f = torch.randn((r1 - r0, D - 1), generator=g, device="cuda", dtype=torch.float64)
+        if wl.zero_frac > 0:
+            f *= torch.rand(f.shape, generator=g, device="cuda", dtype=torch.float64) >= wl.zero_frac
+        X[r0:r1, :D - 1] = f.to(dt)
+        X[r0:r1, D - 1] = 1.0
+        eta = X[r0:r1].double() @ w
+        u = torch.rand(r1 - r0, generator=g, device="cuda", dtype=torch.float64)
+        y[r0:r1] = (u < torch.sigmoid(eta)).to(torch.uint8)
+    torch.cuda.synchronize()
+    return X, y, w.cpu().numpy()
+
+
+def load_workload(name):
+    """(host X or None, host y or None, device X, device y, w_true)."""
+    import torch
+
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    t0 = time.time()
+    if wl.N * wl.D >= 100_000_000:
+        Xd, yd, w_true = generate_on_device(wl)
+        X = y = None
+        log(f"{name}: drew X {tuple(Xd.shape)} {wl.dtype} on the device in {time.time() - t0:.1f}s")
+    else:
+        X, y = workloads.make_workload(wl)
+        _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
+        Xd = torch.from_numpy(X).cuda()
+        yd = torch.from_numpy(y).cuda()
+        log(f"{name}: generated X {X.shape} {X.dtype} in {time.time() - t0:.1f}s")
+    torch.cuda.synchronize()
+    return X, y, Xd, yd, w_true
+
+
+def path_of(wl):
+    """The path the library's AUTO rule takes for this shape, named
+    explicitly, with its kernel and how it accumulates."""
+    import paper_1912_11554_amd as nuts
+
+    es = 8 if wl.dtype == "f64" else 4
+    rows = "f32" if wl.dtype == "f32" else "f64"
+    if wl.num_chains == 1 and wl.N * wl.D * es > 120 * 1024:
+        return nuts.NUTS_PATH_GRID, "sampler_grid_kernel", f"{rows} row terms, f64 sums"
+    if wl.num_chains == 1 or wl.per_chain_data or wl.dtype != "f32":
+        return nuts.NUTS_PATH_WAVE, "sampler_wave_kernel", f"{rows} row terms, f64 sums"
+    return (nuts.NUTS_PATH_BATCH, "sampler_batch_kernel",
+            "f32 positions and f32 matrix-core products within each group's row range, "
+            "f32 row terms, f64 sums across groups and of the loss")
+
+
+def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, variants=None):
+    """--warmup untimed iterations, then exactly --steps timed ones resumed
+    from that state, every buffer on the device."""
     import torch
 
     import paper_1912_11554_amd as nuts
@@ -59,59 +148,44 @@ def run_workload(name, steps=None, warmup=None, adapt=False, variants=None):
     wl = workloads.WORKLOADS[name]
     steps = wl.num_samples if steps is None else steps
     warmup = wl.num_warmup if warmup is None else warmup
-    C = wl.num_chains
-    t0 = time.time()
-    X, y = workloads.make_workload(wl)
-    log(f"{name}: generated X {X.shape} {X.dtype} in {time.time() - t0:.1f}s")
-    Xd = torch.from_numpy(X).cuda()
-    yd = torch.from_numpy(y).cuda()
-    del X
-    torch.cuda.synchronize()
-    s = nuts.Sampler(0)
+    C, D = wl.num_chains, wl.D
+    _, _, Xd, yd, _ = data
     t0 = time.time()
     d = s.data(Xd, yd, per_chain=wl.per_chain_data)
     torch.cuda.synchronize()
     layout_s = time.time() - t0
-    del Xd
-    # the path the library's AUTO rule takes for this shape, named explicitly
-    es = 8 if wl.dtype == "f64" else 4
-    if C == 1 and wl.N * wl.D * es > 120 * 1024:
-        path, kernel = nuts.NUTS_PATH_GRID, "sampler_grid_kernel"
-    elif C == 1:
-        # a data set that fits one group's LDS: one wavefront, data resident
-        path, kernel = nuts.NUTS_PATH_WAVE, "sampler_wave_kernel"
-    elif wl.per_chain_data or wl.dtype != "f32":
-        path, kernel = nuts.NUTS_PATH_WAVE, "sampler_wave_kernel"
-    else:
-        path, kernel = nuts.NUTS_PATH_BATCH, "sampler_batch_kernel"
+    path, kernel, accumulate = path_of(wl)
     kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
               prior_scale=wl.prior_scale, num_chains=C, path=path, **(variants or {}))
-
-    t0 = time.time()
     if adapt and C != 1:
         sys.exit("--adapt takes single-chain workloads (the timed call shares one step size)")
+
+    dev = dict(dtype=torch.float64, device="cuda")
+    q = torch.empty((C, D), **dev)
+    im = torch.empty((C, D), **dev)
+    eps = torch.empty(C, **dev)
+    t0 = time.time()
     r0 = d.sample(num_warmup=warmup, num_samples=1, adapt_diag_mass=wl.adapt_diag_mass,
-                  adapt_step_size=adapt, **kw)
+                  adapt_step_size=adapt, out_final_q=q, out_inv_mass=im, out_step_size=eps, **kw)
     log(f"{name}: warmup {warmup} iterations x {C} chains, {r0['grad_evals']} gradient "
         f"evaluations, {time.time() - t0:.2f}s")
-    q = r0["final_q"]
-    inv_mass = r0["inv_mass"][0] if wl.adapt_diag_mass else None
+    inv_mass = im[0].contiguous() if wl.adapt_diag_mass else None
     if adapt:
         # the paper's covtype protocol: the step size from warmup adaptation
-        kw["step_size"] = float(r0["step_size"][0])
+        kw["step_size"] = float(eps[0])
         log(f"{name}: step size adapted over {warmup} warmup iterations: {kw['step_size']:.6g}")
 
-    D = wl.D
-    samples = torch.empty((C, steps, D), dtype=torch.float64, device="cuda")
+    samples = torch.empty((C, steps, D), **dev)
     stats = torch.empty((C, steps, nuts.STATS_DTYPE.itemsize), dtype=torch.uint8, device="cuda")
-    stream = torch.cuda.current_stream()
+    outs = dict(out_final_q=torch.empty((C, D), **dev), out_inv_mass=torch.empty((C, D), **dev),
+                out_step_size=torch.empty(C, **dev))
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     ev0.record(stream)
     r = d.sample(num_warmup=0, num_samples=steps, init_q=q, first_iter=warmup + 1,
-                 inv_mass=inv_mass, out_samples=samples, out_stats=stats, **kw)
+                 inv_mass=inv_mass, out_samples=samples, out_stats=stats, **outs, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -136,23 +210,108 @@ def run_workload(name, steps=None, warmup=None, adapt=False, variants=None):
     tflops = evals * flops_per_eval / gpu_s / 1e12
     log(f"{name}: {steps} iterations x {C} chains, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
         f"({wall * 1e3:.1f} ms wall): {evals / gpu_s:.0f} evals/s, {achieved:.0f} GB/s, "
-        f"{tflops:.1f} TFLOP/s, min ESS {ess.min():.0f}")
-    d.free()
-    s.close()
-    return dict(
+        f"{tflops:.1f} TFLOP/s")
+    return d, dict(
         workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=kw["step_size"],
         step_size_adapted=bool(adapt), variants=sorted(k for k, v in (variants or {}).items() if v),
         max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
         gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
         evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
-        ess_min=float(ess.min()), ess_median=float(np.median(ess)),
-        ess_per_s=float(ess.min() / wall), bytes_per_eval=bytes_per_eval, achieved_gbs=achieved,
+        ess_min_timed_call=float(ess.min()), bytes_per_eval=bytes_per_eval, achieved_gbs=achieved,
         mean_tree_depth=float(st["tree_depth"].mean()),
         mean_steps_per_iter=float(st["num_steps"].mean()),
         divergences=int(st["diverging"].sum()), accept_prob=float(st["accept_prob"].mean()),
-        path=path, kernel=kernel, flops_per_eval=flops_per_eval, achieved_tflops=tflops,
-        passes=passes, pass_fill=evals / (passes * C), ms_per_pass=1e3 * gpu_s / passes,
+        path=path, kernel=kernel, accumulate=accumulate, flops_per_eval=flops_per_eval,
+        achieved_tflops=tflops, passes=passes, pass_fill=evals / (passes * C),
+        ms_per_pass=1e3 * gpu_s / passes,
     )
+
+
+def run_protocol(name, d, stream):
+    """The workload's full single-chain protocol (num_warmup warmup + num_samples
+    draws from q = 0, fixed step size) as two calls, all warmup iterations
+    then all sampling iterations (resuming is exact: the counter-based draws
+    make (q, t) the whole state), timed with HIP events; ESS over the draws."""
+    import torch
+
+    import paper_1912_11554_amd as nuts
+    import workloads
+    from paper_1912_11554_amd.diagnostics import effective_sample_size
+
+    wl = workloads.WORKLOADS[name]
+    W, S, D = wl.num_warmup, wl.num_samples, wl.D
+    path, _, _ = path_of(wl)
+    assert wl.num_chains == 1 and not wl.adapt_diag_mass and W >= 1
+    kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
+              prior_scale=wl.prior_scale, path=path)
+    dev = dict(dtype=torch.float64, device="cuda")
+    q = torch.empty((1, D), **dev)
+    sb = nuts.STATS_DTYPE.itemsize
+    junk = dict(out_samples=torch.empty((1, 1, D), **dev), out_inv_mass=torch.empty((1, D), **dev),
+                out_step_size=torch.empty(1, **dev),
+                out_stats=torch.empty((1, 1, sb), dtype=torch.uint8, device="cuda"))
+    samples = torch.empty((1, S, D), **dev)
+    outs = dict(out_final_q=torch.empty((1, D), **dev), out_inv_mass=torch.empty((1, D), **dev),
+                out_step_size=torch.empty(1, **dev),
+                out_stats=torch.empty((1, S, sb), dtype=torch.uint8, device="cuda"))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    r1 = d.sample(num_warmup=W - 1, num_samples=1, out_final_q=q, **junk, **kw)
+    ev[1].record(stream)
+    r2 = d.sample(num_warmup=0, num_samples=S, init_q=q, first_iter=W, out_samples=samples,
+                  **outs, **kw)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    t_all = ev[0].elapsed_time(ev[2]) / 1e3
+    t_samp = ev[1].elapsed_time(ev[2]) / 1e3
+    ess = effective_sample_size(samples.cpu().numpy())
+    evals = r1["grad_evals"] + r2["grad_evals"]
+    log(f"{name}: protocol {W} + {S}: {evals} evaluations in {t_all * 1e3:.1f} ms, "
+        f"min ESS {ess.min():.0f}, ESS/s {ess.min() / t_all:.0f}")
+    return dict(workload=name, warmup=W, samples=S, grad_evals=evals, seconds=round(t_all, 4),
+                sampling_seconds=round(t_samp, 4), sampling_grad_evals=r2["grad_evals"],
+                ess_min=round(float(ess.min()), 1), ess_median=round(float(np.median(ess)), 1),
+                ess_per_s=round(float(ess.min() / t_all), 1),
+                ess_per_s_sampling=round(float(ess.min() / t_samp), 1),
+                evals_per_s=round(evals / t_all, 1),
+                note="ESS/s = min-coordinate ESS of the draws / GPU seconds of warmup and sampling")
+
+
+def run_standalone(name, d, w_true, stream, launches=400):
+    """The potential kernel alone: one position per call (the generating
+    weights), back-to-back calls of the allocation-free entry point (which
+    only enqueues), HIP events around all of them on the kernel's stream."""
+    import torch
+
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    W = torch.from_numpy(np.ascontiguousarray(w_true[None, :])).cuda()
+    U = torch.empty(1, dtype=torch.float64, device="cuda")
+    G = torch.empty((1, wl.D), dtype=torch.float64, device="cuda")
+    for _ in range(20):
+        d.potential_grad(W, out_U=U, out_grad=G, no_alloc=True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(launches):
+        d.potential_grad(W, out_U=U, out_grad=G, no_alloc=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) * 1e3 / launches
+    es = 8 if wl.dtype == "f64" else 4
+    bytes_per_eval = wl.N * wl.D * es + wl.N
+    gbs = bytes_per_eval / (us * 1e-6) / 1e9
+    log(f"{name}: standalone gradient pass {us:.2f} us per call, {gbs:.0f} GB/s")
+    return dict(workload=name, kernel="potential_grad_kernel", positions_per_call=1, calls=launches,
+                us_per_call=round(us, 3), evals_per_s=round(1e6 / us, 1),
+                roofline={"kernel": "potential_grad_kernel", "bound": "hbm", "achieved": round(gbs, 1),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                          "bytes_per_eval": bytes_per_eval},
+                note="per call: a small kernel clearing the arrival count, then the potential "
+                     "kernel; back-to-back, so launch gaps are included")
 
 
 def recorded_traffic(kernel, workload, evals):
@@ -179,16 +338,51 @@ def recorded_traffic(kernel, workload, evals):
     return out
 
 
-def cpu_baseline(name, seconds):
-    """The oracle's fp64 gradient evaluations on the same data, one core."""
+def roofline(res):
+    """Roofline of a timed sampler call: HBM for the streaming paths, fp32
+    matrix cores for the batched path, vector-ALU issue for the wave path
+    with the data resident in LDS (from the recorded instruction count)."""
+    kernel = res["kernel"]
+    traffic = recorded_traffic(kernel, res["workload"], res["grad_evals"])
+    if kernel == "sampler_batch_kernel":
+        return {"kernel": kernel, "bound": "mfma", "achieved": round(res["achieved_tflops"], 2),
+                "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(res["achieved_tflops"] / MFMA_F32_PEAK_TFLOPS, 4),
+                "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
+                "flops_per_eval": res["flops_per_eval"], "passes": res["passes"],
+                "pass_fill": round(res["pass_fill"], 4), "ms_per_pass": round(res["ms_per_pass"], 4)}
+    if kernel == "sampler_wave_kernel" and traffic and "valu_instructions_per_eval" in traffic:
+        rate = traffic["valu_instructions_per_eval"] * res["evals_per_s"] / 1e9
+        return {"kernel": kernel, "bound": "alu", "achieved": round(rate, 1), "peak": VALU_PEAK_GIPS,
+                "unit": "G VALU wave-instructions/s", "frac": round(rate / VALU_PEAK_GIPS, 4),
+                "traffic": traffic["bytes"], "traffic_detail": traffic,
+                "valu_instructions_per_eval": traffic["valu_instructions_per_eval"],
+                "bytes_per_eval": res["bytes_per_eval"], "algorithmic_gbs": round(res["achieved_gbs"], 1)}
+    return {"kernel": kernel, "bound": "hbm", "achieved": round(res["achieved_gbs"], 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(res["achieved_gbs"] / HBM_PEAK_GBS, 4),
+            "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
+            "bytes_per_eval": res["bytes_per_eval"]}
+
+
+def cpu_baseline(name, data, seconds):
+    """The oracle's fp64 gradient evaluations on the same data, one core,
+    and on every allowed core up to 16.  For the 4,000,000-row set a slice of
+    its first rows stands in (the time per evaluation is linear in N), and
+    the rate is scaled to the full set."""
     import oracle
     import workloads
 
     wl = workloads.WORKLOADS[name]
-    X, y = workloads.make_workload(wl, chains=[0] if wl.per_chain_data else None)
+    X, y, Xd, yd, w_true = data
+    scale, what = 1.0, ""
+    if X is None:
+        rows = 400_000
+        X = Xd[:rows].cpu().numpy()
+        y = yd[:rows].cpu().numpy()
+        scale = rows / wl.N
+        what = f" on its first {rows} rows (rate scaled by {rows}/{wl.N})"
     if wl.per_chain_data:
         X, y = X[0], y[0]
-    _, _, w_true = workloads.make_logistic(1, wl.D, w_scale=wl.w_scale, key=wl.data_seed)
     f = oracle.logistic_potential_grad_f32 if wl.dtype == "f32" else oracle.logistic_potential_grad
     U_check = f(X, y, w_true)[0]
     # the oracle's timing loop (about 10 ms of evaluations per call, or one
@@ -208,17 +402,18 @@ def cpu_baseline(name, seconds):
         if el >= seconds:
             break
     assert U == U_check, (U, U_check)  # the loop evaluates what the entry point does
-    log(f"cpu oracle: {n} gradient evaluations in {el:.1f}s")
+    log(f"cpu oracle {name}: {n} gradient evaluations in {el:.1f}s{what}")
     if wl.per_chain_data or wl.num_chains > 1 or wl.N * wl.D < 1_000_000:
         # many chains, or one small data set: independent evaluations on
         # every core (each thread its own chain's data set where chains have
         # their own, else its own position), as independent chains would run
-        allc = cpu_independent(wl, min(seconds, 10.0))
+        allc = cpu_independent(wl, min(seconds, 5.0))
     else:
-        allc = cpu_all_cores(f, X, y, w_true, min(seconds, 10.0))
-    return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
+        f_rows = oracle.logistic_potential_grad_f32 if wl.dtype == "f32" else oracle.logistic_potential_grad
+        allc = cpu_all_cores(f_rows, Xc, yc, w_true, min(seconds, 5.0), scale)
+    return dict(value=n / el * scale, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
                 sample=f"{n} full potential+gradient evaluations of {name}"
-                       f"{' (one chain data set)' if wl.per_chain_data else ''} at w_true, "
+                       f"{' (one chain data set)' if wl.per_chain_data else ''}{what} at w_true, "
                        f"single-threaded fp64 C, {el:.1f}s",
                 host_cores_available=len(os.sched_getaffinity(0)))
 
@@ -243,7 +438,9 @@ def run_hmm(chains, steps, warmup):
     K, V = sh["K"], sh["V"]
     w, z, _, _ = workloads.make_hmm(**sh)
     D = nuts.hmm_dim(K, V)
-    s = nuts.Sampler(0)
+    stream = _stream()
+    with torch.cuda.stream(stream):
+        s = nuts.Sampler(0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     r1 = s.hmm_sample(w, z, K, V, step_size=0.1, max_tree_depth=10, num_warmup=1000,
@@ -263,14 +460,12 @@ def run_hmm(chains, steps, warmup):
     outs = dict(out_final_q=torch.empty((chains, D), dtype=torch.float64, device="cuda"),
                 out_inv_mass=torch.empty((chains, D), dtype=torch.float64, device="cuda"),
                 out_step_size=torch.empty(chains, dtype=torch.float64, device="cuda"))
-    stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
     q0 = torch.from_numpy(r0["final_q"]).cuda()
     kw["inv_mass"] = torch.from_numpy(np.ascontiguousarray(im)).cuda()
     torch.cuda.synchronize()
+    ev0.record(stream)
     r = s.hmm_sample(w, z, K, V, num_warmup=0, num_samples=steps, init_q=q0,
                      first_iter=warmup + 1, out_samples=samples, out_stats=stats, **outs, **kw)
     ev1.record(stream)
@@ -296,7 +491,10 @@ def run_hmm(chains, steps, warmup):
 
 
 def hmm_cpu_baseline(seconds):
-    """The oracle's fp64 HMM gradient evaluations, one core."""
+    """The oracle's fp64 HMM gradient evaluations, one core and every
+    allowed core up to 16."""
+    import concurrent.futures
+
     import oracle
     import workloads
 
@@ -306,44 +504,27 @@ def hmm_cpu_baseline(seconds):
     U_check = oracle.hmm_potential_grad(w, z, HMM_SHAPE["K"], HMM_SHAPE["V"], q)[0]
     lib = oracle.lib()
     wu, zu = np.ascontiguousarray(w, np.uint8), np.ascontiguousarray(z, np.uint8)
-    qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
-    n = 0
-    t0 = time.perf_counter()
-    while True:  # the oracle's timing loop, 500 evaluations per call
-        U = lib.orc_hmm_ug_repeat(wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"],
-                                  HMM_SHAPE["V"], qq.ctypes.data, gg.ctypes.data, 500)
-        n += 500
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
+
+    def loop(limit):
+        # the oracle's timing loop, 500 evaluations per call, so that the
+        # interpreter's share (which threads take in turn) stays small
+        qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
+        args = (wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"], HMM_SHAPE["V"],
+                qq.ctypes.data, gg.ctypes.data, 500)
+        m, t1, U = 0, time.perf_counter(), None
+        while time.perf_counter() - t1 < limit:
+            U = lib.orc_hmm_ug_repeat(*args)
+            m += 500
+        return m, time.perf_counter() - t1, U
+
+    n, el, U = loop(seconds)
     assert U == U_check, (U, U_check)
     log(f"cpu oracle hmm: {n} gradient evaluations in {el:.1f}s")
-    # every allowed core (at most 16) evaluating on its own, as independent
-    # chains would
-    import concurrent.futures
-
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
-
-    def worker(_):
-        # the oracle's timing loop, about 10 ms of evaluations per call, so
-        # that the interpreter's share (which the threads take in turn) stays
-        # small
-        lib = oracle.lib()
-        wu, zu = np.ascontiguousarray(w, np.uint8), np.ascontiguousarray(z, np.uint8)
-        qq, gg = np.ascontiguousarray(q, np.float64), np.zeros(D)
-        reps = 500
-        args = (wu.ctypes.data, wu.shape[0], zu.ctypes.data, zu.shape[0], HMM_SHAPE["K"], HMM_SHAPE["V"],
-                qq.ctypes.data, gg.ctypes.data, reps)
-        m, t1 = 0, time.perf_counter()
-        while time.perf_counter() - t1 < min(seconds, 5.0):
-            lib.orc_hmm_ug_repeat(*args)
-            m += reps
-        return m, time.perf_counter() - t1
-
     with concurrent.futures.ThreadPoolExecutor(max_workers=cores) as ex:
-        res = list(ex.map(worker, range(cores)))
-    allc = dict(value=sum(m / t for m, t in res), unit="grad-evals/s", cores=cores,
-                sample=f"{sum(m for m, _ in res)} evaluations on {cores} threads")
+        res = list(ex.map(lambda _: loop(min(seconds, 5.0)), range(cores)))
+    allc = dict(value=sum(m / t for m, t, _ in res), unit="grad-evals/s", cores=cores,
+                sample=f"{sum(m for m, _, _ in res)} evaluations on {cores} threads")
     log(f"cpu oracle hmm, {cores} threads: {allc['value']:.0f} evaluations/s")
     return dict(value=n / el, unit="grad-evals/s", cores=1, kind="oracle", all_cores=allc,
                 sample=f"{n} HMM potential+gradient evaluations (T 600, Tsup 100, K 3, V 10), "
@@ -418,12 +599,12 @@ def cpu_independent(wl, seconds):
                        f"{max(t for _, t in res):.1f}s")
 
 
-def cpu_all_cores(f, X, y, w, seconds):
+def cpu_all_cores(f, X, y, w, seconds, scale=1.0):
     """The oracle's gradient on every allowed host core (at most 16): the rows
     in one fixed chunk per thread (ctypes releases the interpreter lock
     during the C call), the partial sums added in chunk order.  A timing
     mode only: each chunk's call also adds the prior, which this sum does not
-    correct."""
+    correct.  `scale` converts the rate on a row slice to the full set."""
     import concurrent.futures
 
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
@@ -442,8 +623,21 @@ def cpu_all_cores(f, X, y, w, seconds):
             if el >= seconds:
                 break
     log(f"cpu oracle, {cores} threads: {n} gradient evaluations in {el:.1f}s")
-    return dict(value=n / el, unit="grad-evals/s", cores=cores,
+    return dict(value=n / el * scale, unit="grad-evals/s", cores=cores,
                 sample=f"{n} evaluations, rows in {cores} fixed chunks, {el:.1f}s")
+
+
+def sub_line(name, s, stream, cpu_seconds):
+    """Another workload's line: its own short protocol, roofline and CPU
+    baseline."""
+    data = load_workload(name)
+    warmup, steps = SUB_STEPS[name]
+    d, res = run_workload(name, data, s, stream, steps=steps, warmup=warmup)
+    d.free()
+    out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in res.items()}
+    out["roofline"] = roofline(res)
+    out["cpu_baseline"] = None if cpu_seconds <= 0 else cpu_baseline(name, data, cpu_seconds)
+    return out
 
 
 def main():
@@ -454,8 +648,11 @@ def main():
     ap.add_argument("--workload", default="covtype_n581012_d55_f32")
     ap.add_argument("--also", default="covtype_n581012_d55_f64",
                     help="second workload reported beside the first ('' for none)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-protocol", action="store_true",
+                    help="skip the full-protocol ESS runs and the standalone gradient pass")
+    ap.add_argument("--no-sub", action="store_true", help="skip the other workloads' lines")
     ap.add_argument("--adapt", action="store_true",
                     help="adapt the step size during warmup (dual averaging, target acceptance "
                          "0.8) and time the sampling at the adapted step size (the paper's covtype "
@@ -478,8 +675,12 @@ def main():
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
+    import torch
+
+    import paper_1912_11554_amd as nuts
+    import workloads
+
     if args.copy_mb:
-        import torch
         src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -490,35 +691,34 @@ def main():
         h = run_hmm(args.hmm_chains, args.hmm_steps, 20)
         print(json.dumps(hmm_line(h, None)), flush=True)
         return
+    cpu_s = 0.0 if args.no_cpu_baseline else args.cpu_seconds
+    stream = _stream()
+    with torch.cuda.stream(stream):
+        s = nuts.Sampler(0)   # the library runs on `stream`
     variants = dict(uturn_generalized=args.uturn_generalized, subtree_merge=args.subtree_merge)
-    main_res = run_workload(args.workload, args.steps, args.warmup, args.adapt, variants)
-    other = run_workload(args.also, args.steps, args.warmup, args.adapt, variants) if args.also else None
-    cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload, args.cpu_seconds)
 
-    achieved = main_res["achieved_gbs"]
-    kernel = main_res["kernel"]
-    traffic = recorded_traffic(kernel, main_res["workload"], main_res["grad_evals"])
-    if kernel == "sampler_batch_kernel":
-        roof = {"kernel": kernel, "bound": "mfma", "achieved": round(main_res["achieved_tflops"], 2),
-                "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(main_res["achieved_tflops"] / MFMA_F32_PEAK_TFLOPS, 4),
-                "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
-                "flops_per_eval": main_res["flops_per_eval"], "passes": main_res["passes"],
-                "pass_fill": round(main_res["pass_fill"], 4),
-                "ms_per_pass": round(main_res["ms_per_pass"], 4)}
-    elif kernel == "sampler_wave_kernel" and traffic and "valu_instructions_per_eval" in traffic:
-        # data sets resident in LDS: the vector ALU issue rate bounds the kernel
-        rate = traffic["valu_instructions_per_eval"] * main_res["evals_per_s"] / 1e9
-        roof = {"kernel": kernel, "bound": "alu", "achieved": round(rate, 1), "peak": VALU_PEAK_GIPS,
-                "unit": "G VALU wave-instructions/s", "frac": round(rate / VALU_PEAK_GIPS, 4),
-                "traffic": traffic["bytes"], "traffic_detail": traffic,
-                "valu_instructions_per_eval": traffic["valu_instructions_per_eval"],
-                "bytes_per_eval": main_res["bytes_per_eval"], "algorithmic_gbs": round(achieved, 1)}
-    else:
-        roof = {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
-                "bytes_per_eval": main_res["bytes_per_eval"]}
+    def one(name):
+        data = load_workload(name)
+        d, res = run_workload(name, data, s, stream, args.steps, args.warmup, args.adapt, variants)
+        wl = workloads.WORKLOADS[name]
+        extra = {}
+        if not args.no_protocol and wl.num_chains == 1 and not wl.adapt_diag_mass:
+            extra["protocol"] = run_protocol(name, d, stream)
+            extra["standalone_grad"] = run_standalone(name, d, data[4], stream)
+        d.free()
+        return data, res, extra
+
+    main_data, main_res, main_extra = one(args.workload)
+    other = None
+    if args.also:
+        _, other_res, other_extra = one(args.also)
+        other = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in other_res.items()}
+        other["frac_hbm"] = round(other_res["achieved_gbs"] / HBM_PEAK_GBS, 4)
+        other.update(other_extra)
+    cpu = None if cpu_s <= 0 else cpu_baseline(args.workload, main_data, cpu_s)
+    del main_data
+
+    proto = main_extra.get("protocol")
     line = {
         "metric": METRIC,
         "value": round(main_res["evals_per_s"], 1),
@@ -536,26 +736,33 @@ def main():
             "workload": main_res["workload"], "N": main_res["N"], "D": main_res["D"],
             "chains": main_res["chains"], "step_size": main_res["step_size"],
             "step_size_adapted": main_res["step_size_adapted"], "variants": main_res["variants"],
-            "max_tree_depth": main_res["max_tree_depth"], "accumulate": "f64",
+            "max_tree_depth": main_res["max_tree_depth"], "accumulate": main_res["accumulate"],
             "path": main_res["kernel"],
         },
-        "ess_per_s": round(main_res["ess_per_s"], 2),
-        "ess_min": round(main_res["ess_min"], 1),
-        "ess_median": round(main_res["ess_median"], 1),
+        # ESS needs the full protocol: the --steps timed iterations start in
+        # the chain's transient (see ess_min_timed_call)
+        "ess_per_s": proto and proto["ess_per_s"],
+        "ess_min": proto and proto["ess_min"],
+        "ess_protocol": proto,
+        "ess_min_timed_call": round(main_res["ess_min_timed_call"], 1),
         "grad_evals": main_res["grad_evals"],
         "mean_steps_per_iter": round(main_res["mean_steps_per_iter"], 2),
         "divergences": main_res["divergences"],
         "layout_seconds": round(main_res["layout_seconds"], 4),
-        "roofline": roof,
+        "roofline": roofline(main_res),
         "cpu_baseline": cpu,
+        "standalone_grad": main_extra.get("standalone_grad"),
     }
+    if other:
+        line["also"] = other
+    if not args.no_sub:
+        line["workloads"] = {name: sub_line(name, s, stream, min(cpu_s, 5.0))
+                             for name in SUB_WORKLOADS if name != args.workload}
+    s.close()
     if args.hmm_chains:
         h = run_hmm(args.hmm_chains, args.hmm_steps, 20)
-        hc = None if args.no_cpu_baseline else hmm_cpu_baseline(min(args.cpu_seconds, 10.0))
+        hc = None if cpu_s <= 0 else hmm_cpu_baseline(min(cpu_s, 10.0))
         line["hmm"] = hmm_line(h, hc)
-    if other:
-        line["also"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in other.items()}
-        line["also"]["frac_hbm"] = round(other["achieved_gbs"] / HBM_PEAK_GBS, 4)
     print(json.dumps(line), flush=True)
 
 

@@ -363,12 +363,12 @@ class Data:
                seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None,
                adapt_step_size=False, target_accept=0.8, uturn_generalized=False,
-               subtree_merge=False):
+               subtree_merge=False, out_final_q=None, out_inv_mass=None, out_step_size=None):
         """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
         (STATS_DTYPE), final_q [C, D], inv_mass [C, D], step_size [C] (in use
         at the end: the adapted one with adapt_step_size), grad_evals.  Outputs
-        are numpy unless device tensors are passed in out_samples /
-        out_stats (then those are filled and returned)."""
+        are numpy unless device tensors are passed in the out_* arguments
+        (then those are filled and returned)."""
         C, D = num_chains, self.D
         flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
             NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
@@ -379,9 +379,9 @@ class Data:
             out_samples = np.zeros((C, num_samples, D))
         if out_stats is None:
             out_stats = np.zeros((C, num_samples), dtype=STATS_DTYPE)
-        final_q = np.zeros((C, D))
-        out_im = np.zeros((C, D))
-        out_eps = np.zeros(C)
+        final_q = np.zeros((C, D)) if out_final_q is None else out_final_q
+        out_im = np.zeros((C, D)) if out_inv_mass is None else out_inv_mass
+        out_eps = np.zeros(C) if out_step_size is None else out_step_size
         gev = np.zeros(1, dtype=np.int64)
         im = _as_f64(inv_mass)
         iq = _as_f64(init_q)

@@ -52,7 +52,30 @@ struct nuts_handle {
     // this device's copy of the fixed workspace of the allocation-free entry
     // point (set up by nuts_init; never freed)
     void* static_ws = nullptr;
+    // per-chain gradient-evaluation counts of a sampling call, grow-only, so
+    // that a call on device-resident buffers allocates nothing before its
+    // kernel starts
+    unsigned long long* evals = nullptr;
+    int64_t evals_cap = 0;
 };
+
+static hipError_t handle_evals(nuts_handle* h, int64_t C, unsigned long long** out)
+{
+    if (C > h->evals_cap) {
+        if (h->evals) {
+            hipError_t e = hipStreamSynchronize(h->stream);
+            if (e != hipSuccess) return e;
+            (void)hipFree(h->evals);
+            h->evals = nullptr;
+            h->evals_cap = 0;
+        }
+        hipError_t e = hipMalloc(&h->evals, (size_t)C * sizeof(unsigned long long));
+        if (e != hipSuccess) return e;
+        h->evals_cap = C;
+    }
+    *out = h->evals;
+    return hipSuccess;
+}
 
 static hipError_t potential_counts(nuts_handle* h, unsigned int** out)
 {
@@ -245,7 +268,8 @@ int check_inv_mass(nuts_handle* h, const double* inv_mass_diag, int D)
 // Device copies of a sampling call's inputs and outputs, and the sampler
 // arguments that point at them.
 struct RunBuffers {
-    DevBuf imb, iqb, smp, sts, fq, fim, fep, gev;
+    DevBuf imb, iqb, smp, sts, fq, fim, fep;
+    unsigned long long* gev = nullptr;  // the handle's counts
     int64_t C = 0, S = 0, D = 0;
     hipStream_t s = nullptr;
 
@@ -267,7 +291,7 @@ struct RunBuffers {
         HIP_TRY(h, stage_out(o.out_final_q, (size_t)C * D * 8, fq, &fq_d));
         HIP_TRY(h, stage_out(o.out_inv_mass, (size_t)C * D * 8, fim, &fim_d));
         HIP_TRY(h, stage_out(o.out_step_size, (size_t)C * 8, fep, &fep_d));
-        HIP_TRY(h, gev.alloc((size_t)C * sizeof(unsigned long long)));
+        HIP_TRY(h, handle_evals(h, C, &gev));
         a.step_size = step_size;
         a.inv_mass = (const double*)im_d;
         a.max_depth = max_tree_depth;
@@ -288,7 +312,7 @@ struct RunBuffers {
         a.out_final_q = (double*)fq_d;
         a.out_inv_mass = (double*)fim_d;
         a.out_step_size = (double*)fep_d;
-        a.grad_evals = (unsigned long long*)gev.p;
+        a.grad_evals = gev;
         return NUTS_OK;
     }
 
@@ -301,7 +325,7 @@ struct RunBuffers {
         HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
         HIP_TRY(h, finish_out(o.out_step_size, (size_t)C * 8, fep, s));
         std::vector<unsigned long long> ev(C);
-        HIP_TRY(h, hipMemcpyAsync(ev.data(), gev.p, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipMemcpyAsync(ev.data(), gev, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
         HIP_TRY(h, hipStreamSynchronize(s));
         if (o.out_grad_evals) {
             unsigned long long tot = 0;
@@ -405,6 +429,7 @@ void nuts_free(nuts_handle* h)
     (void)hipStreamSynchronize(h->stream);
     if (h->scratch) (void)hipFree(h->scratch);
     if (h->pot_counts) (void)hipFree(h->pot_counts);
+    if (h->evals) (void)hipFree(h->evals);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
 }
