@@ -50,16 +50,26 @@ BUILDER_ITERATIVE = 0
 BUILDER_RECURSIVE = 1
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain C, -ffp-contract=off)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
+SANITIZED_LIB = os.path.join(_HERE, "liboracle_asan.so")
+
+
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (plain C, -ffp-contract=off).  With
+    sanitize=True, a separate copy with AddressSanitizer and
+    UndefinedBehaviorSanitizer (liboracle_asan.so, aborting on the first
+    report); load it by pointing NUTS_ORACLE_LIB at it, with libasan
+    preloaded into the interpreter."""
+    out = SANITIZED_LIB if sanitize else _LIB
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+        tmp = out + ".tmp%d" % os.getpid()
+        extra = (["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all"] if sanitize else ["-O2"])
         subprocess.check_call(
-            ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+            ["gcc", *extra, "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
              "-Wall", "-o", tmp, _SRC, "-lm"]
         )
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, out)
+    return out
 
 
 _lib = None

@@ -624,6 +624,7 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
 
 template <int KT, int DPL>
 struct BatchEval {
+    static constexpr bool kSpeculative = false;
     BatchCtx c;
     BatchShared<DPL>* sh;
     double inv_s2, prior_const;

@@ -184,6 +184,7 @@ __host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, 
 
 template <int K>
 struct HmmEval {
+    static constexpr bool kSpeculative = false;
     int V, D, Tsup, Tu;
     // this lane's entry
     int src;       // dimension lane of its logit; -1 for a row's fixed logit or no entry

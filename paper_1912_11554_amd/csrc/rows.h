@@ -178,10 +178,25 @@ __device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, in
 // the kernel's state): one register set; the next block's loads are issued
 // while the current block's gradient terms are added.  MASK as for
 // load_block.
-template <typename T, int CPS, int S, bool PIPE, bool MASK>
+//
+// ABORT: the pass may be called off while it runs (its result is then not
+// used): the LDS word *stop is read before each block (PIPE: each pair of
+// blocks) is loaded, and once it holds `token` the wave finishes the block it
+// holds and stops.  The block in hand is always computed, so no loaded
+// registers are dead on that path and the loads keep their place ahead of
+// the computation.
+template <bool ABORT>
+__device__ __forceinline__ bool stop_requested(const int* stop, int token)
+{
+    if constexpr (ABORT) return __hip_atomic_load(stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == token;
+    return false;
+}
+
+template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false>
 __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
                                               int64_t N, int64_t nb, int64_t first, int64_t stride,
-                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss)
+                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss,
+                                              const int* stop = nullptr, int token = 0)
 {
     constexpr int R = BlockShape<T, S>::R;
     if (first >= nb) return;
@@ -189,9 +204,14 @@ __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uin
     BlockRegs<T, CPS, S> a = load_block<T, CPS, S, MASK>(X + b * D * R, y + b * R, D);
     if constexpr (PIPE) {
         const int64_t count = (nb - 1 - first) / stride + 1;  // blocks of this wave
+        int64_t count_left = count;
         int64_t i = 1;                                         // blocks loaded so far
 #pragma unroll 1
-        for (; i + 1 < count; i += 2) {
+        for (; i + 1 < count_left; i += 2) {
+            if (stop_requested<ABORT>(stop, token)) {
+                count_left = i;  // no more loads: the tail computes the block in hand
+                break;
+            }
             const int64_t b1 = b + stride, b2 = b1 + stride;
             const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
@@ -199,7 +219,7 @@ __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uin
             compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
             b = b2;
         }
-        if (i < count) {
+        if (i < count_left) {
             const int64_t b1 = b + stride;
             const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
@@ -211,7 +231,7 @@ __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uin
 #pragma unroll 1
         for (;;) {
             const int64_t nx = b + stride;
-            const bool more = nx < nb;
+            const bool more = nx < nb && !stop_requested<ABORT>(stop, token);
             const int64_t lb = more ? nx : b;  // a valid block either way
             const BlockRegs<T, CPS, S> nxt = load_block<T, CPS, S, MASK>(X + lb * D * R, y + lb * R, D);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);

@@ -96,6 +96,7 @@ __device__ __forceinline__ bool is_uturn_gen(const double (&rho)[DPL], const dou
 
 template <typename T, int S, int CPS>
 struct WaveEval {
+    static constexpr bool kSpeculative = false;
     const T* X;
     const uint8_t* y;
     int64_t N, nb;
@@ -142,6 +143,8 @@ struct GridShared {
         double red_flat[(NW - 1) * kWave];  // the gathered partials of the group's columns
     };
     int cmd;
+    int gen;   // number of the current collective (counted by wave 0 from 1)
+    int stop;  // number of the last collective wave 0 called off (0: none)
 };
 
 struct GridCtx {
@@ -230,12 +233,25 @@ __device__ __forceinline__ bool wait_slot(const GridCtx& c, const double* p, dou
 // Position in a result row of used column ci (0..D-1, or D for the loss).
 __device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < D ? ci : 64 * DPL; }
 
-// One collective evaluation for the whole group.  Wave 0 passes the position
-// and the command; with kCmdEval every worker streams its blocks and the
-// group joins the grid-wide sum.  Returns the command; on return wave 0 finds
+// One collective evaluation for the whole group, in two halves so that wave
+// 0 (the controller) can work between them while the workers stream.
+//
+// grid_begin: wave 0 passes the position, the command and the collective's
+// number; with kCmdEval every worker streams its blocks and leaves its column
+// sums in LDS.  Returns the command (and, to the workers, the number).
+//
+// grid_end: wave 0 says whether the evaluation still counts.  If it called
+// it off (a speculative next position the tree logic turned out not to
+// need), the workers stop streaming at their next block and the whole group
+// returns false from here: nothing is published and the step does not
+// advance, identically in every group since every controller takes the same
+// decisions.  Otherwise the group joins the grid-wide sum and wave 0 finds
 // the full sums in out_r: component m of lane l is column l + 64 m, and
 // component DPL of lane 0 is the loss.  Controller and workers execute the
 // same workgroup barriers; the workers return as soon as their part is done.
+// The numbers make the stop word unambiguous: wave 0 writes a collective's
+// number into it before that collective's second barrier, and a worker
+// compares it with the number it read after the first one.
 //
 // Step s uses phase s mod 3 of the buffers.  Each group stores its partial of
 // every used column (the D gradient columns and the loss) into that column's
@@ -248,30 +264,30 @@ __device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < 
 // after its controller read all of step s - 1's results, and the next write
 // of an emptied slot comes only after the worker that emptied it has waited
 // for its own stores (s_waitcnt at its next step, before it stores the next
-// result that every writer must first read).
+// result that every writer must first read).  A called-off collective writes
+// and empties nothing, so the next one reuses its step.
 template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
-__device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step,
-                               const double (&q)[DPL], int cmd_in, double (&out_r)[DPL + 1], bool* aborted)
+__device__ int grid_begin(const GridCtx& c, GridShared<DPL, NW>& sh, const double (&q)[DPL], int cmd_in,
+                          int gen_in, int* gen_out)
 {
-    constexpr int W = GridShared<DPL, NW>::W;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
-    const int ph = (int)(step % kGridPhases);
     if (wave == 0) {
 #pragma unroll
         for (int m = 0; m < DPL; ++m) sh.qbuf[l + 64 * m] = q[m];
-        if (l == 0) sh.cmd = cmd_in;
+        if (l == 0) {
+            sh.cmd = cmd_in;
+            sh.gen = gen_in;
+        }
     }
-    __syncthreads();  // position and command published
+    __syncthreads();  // position, command and number published
     const int cmd = sh.cmd;
+    *gen_out = sh.gen;
     if (cmd == kCmdExit) return cmd;
-
-    const int D = c.D;
-    const int used = D + 1;
-    const int G = c.groups;
-    const int g = blockIdx.x;
-    double* part = c.partials + (int64_t)ph * used * G;
     if (WORKER) {
+        const int D = c.D;
+        const int G = c.groups;
+        const int g = blockIdx.x;
         double qv[CPS];
         spread_position_lds<CPS, S>(sh.qbuf, D, qv);
         double acc[CPS];
@@ -279,8 +295,10 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
         const int workers = NW - 1;
-        stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>>((const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
-                                 (int64_t)G * workers, qv, acc, loss);
+        stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>((const T*)c.X, c.y, D, c.N, c.nb,
+                                                                  (int64_t)g * workers + (wave - 1),
+                                                                  (int64_t)G * workers, qv, acc, loss,
+                                                                  &sh.stop, *gen_out);
         if constexpr (S <= 8 && CPS == 8) {
             const double col = finish_pass<CPS, S>(acc, loss);
             if (l < D) sh.red[wave][l] = col;
@@ -289,7 +307,27 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
             finish_pass_to_row<CPS, S>(acc, loss, sh.red[wave], D, 64 * DPL);
         }
     }
-    __syncthreads();  // per-worker sums in LDS
+    return cmd;
+}
+
+template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
+__device__ bool grid_end(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step, int gen, bool stop,
+                         double (&out_r)[DPL + 1], bool* aborted)
+{
+    constexpr int W = GridShared<DPL, NW>::W;
+    const int l = lane();
+    const int wave = threadIdx.x / kWave;
+    if (!WORKER && stop && l == 0)
+        __hip_atomic_store(&sh.stop, gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __syncthreads();  // per-worker sums in LDS, or the pass called off
+    if (__hip_atomic_load(&sh.stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == gen) return false;
+
+    const int ph = (int)(step % kGridPhases);
+    const int D = c.D;
+    const int used = D + 1;
+    const int G = c.groups;
+    const int g = blockIdx.x;
+    double* part = c.partials + (int64_t)ph * used * G;
 
     if (WORKER && wave == 1) {
         // the group's partial of each used column, workers in wave order
@@ -337,7 +375,7 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
             }
         }
     }
-    if (WORKER) return cmd;
+    if (WORKER) return true;
 
     // controller: wait for this lane's result slots, all at once
     const double* row = &c.result[ph * W];
@@ -372,26 +410,40 @@ __device__ int grid_collective(const GridCtx& c, GridShared<DPL, NW>& sh, unsign
     *aborted = bad;
 #pragma unroll
     for (int m = 0; m <= DPL; ++m) out_r[m] = bad ? 0.0 : __builtin_bit_cast(double, bits[m]);
-    return cmd;
+    return true;
 }
 
+// The grid path's evaluator.  Besides eval(), it can start an evaluation
+// (begin) and collect it later (end), so that run_chain hands the workers the
+// next leapfrog position before it does the tree logic of the current leaf;
+// cancel() calls a started evaluation off.
 template <typename T, int S, int CPS, int DPL, int NW>
 struct GridEval {
+    static constexpr bool kSpeculative = true;
     GridCtx c;
     GridShared<DPL, NW>* sh;
     double inv_s2, prior_const;
     unsigned long long step;
+    int gen;
     bool abort;
 
     __device__ bool s_writer() const { return true; }  // only the controller runs the chain
     __device__ bool out_writer() const { return blockIdx.x == 0; }
     __device__ bool aborted() const { return abort; }
 
-    __device__ void eval(const double (&q)[DPL], double& U, double (&g)[DPL])
+    __device__ void begin(const double (&q)[DPL])
+    {
+        int gn;
+        grid_begin<T, S, CPS, DPL, NW, false>(c, *sh, q, kCmdEval, ++gen, &gn);
+    }
+
+    // U and grad U of the started evaluation, at the position q it was
+    // started with
+    __device__ void end(const double (&q)[DPL], double& U, double (&g)[DPL])
     {
         double r[DPL + 1];
         bool ab = false;
-        grid_collective<T, S, CPS, DPL, NW, false>(c, *sh, step, q, kCmdEval, r, &ab);
+        grid_end<T, S, CPS, DPL, NW, false>(c, *sh, step, gen, false, r, &ab);
         abort = ab;
         step++;
         double pr = 0.0;
@@ -404,14 +456,26 @@ struct GridEval {
         for (int m = 0; m < DPL; ++m) g[m] = (l + 64 * m < c.D) ? r[m] + q[m] * inv_s2 : 0.0;
     }
 
-    __device__ void finish()
+    __device__ void cancel()
     {
         double r[DPL + 1];
-        bool ab;
+        bool ab = false;
+        grid_end<T, S, CPS, DPL, NW, false>(c, *sh, step, gen, true, r, &ab);
+    }
+
+    __device__ void eval(const double (&q)[DPL], double& U, double (&g)[DPL])
+    {
+        begin(q);
+        end(q, U, g);
+    }
+
+    __device__ void finish()
+    {
         double q[DPL];
 #pragma unroll
         for (int m = 0; m < DPL; ++m) q[m] = 0.0;
-        grid_collective<T, S, CPS, DPL, NW, false>(c, *sh, step, q, kCmdExit, r, &ab);
+        int gn;
+        grid_begin<T, S, CPS, DPL, NW, false>(c, *sh, q, kCmdExit, ++gen, &gn);
     }
 };
 
@@ -542,6 +606,24 @@ struct MassWindows {
     }
 };
 
+// First half of a leapfrog step from (q, p, grad U = g) with step h: the
+// half-kicked momentum ph and the drifted position q_out (which may alias
+// q).  Contraction is off, so every call site rounds alike: the grid path
+// computes a position once to start its evaluation and again when it takes
+// the results, and both must give the same bits.
+template <int DPL>
+__device__ __forceinline__ void leapfrog_drift(const double (&q)[DPL], const double (&p)[DPL],
+                                               const double (&g)[DPL], double h, const double (&im)[DPL],
+                                               double (&ph)[DPL], double (&q_out)[DPL])
+{
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int m = 0; m < DPL; ++m) {
+        ph[m] = p[m] - 0.5 * h * g[m];
+        q_out[m] = q[m] + h * im[m] * ph[m];
+    }
+}
+
 // The whole chain: init, warmup + sampling iterations, outputs.  S_arr points
 // to this chain's checkpoint array in LDS: [max(max_depth, 1)][2][D].
 // EXT = false compiles the optional features out (warmup adaptation of the
@@ -629,6 +711,10 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         const uint64_t dirmask = __ballot(dir_bit);
 
         Node<DPL> left = cur, right = cur, prop = cur;
+        // a speculative evaluation: the next leapfrog position, handed to the
+        // evaluator before the bookkeeping of the current leaf decides
+        // whether the trajectory goes on (evaluators that can start one)
+        bool pend = false;
         int64_t prop_idx = 0, Lpos = 0, Rpos = 0;
         double logw_traj = 0.0;
         int nleaves = 0;
@@ -663,12 +749,21 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                                  : 0.0;
                 // leapfrog: half kick, drift, gradient, half kick
                 double ph[DPL];
+                if constexpr (Eval::kSpeculative) {
+                    // the same bits the speculative start computed from
+                    // this node (or the edge it was started from)
+                    leapfrog_drift<DPL>(z.q, z.p, z.g, h, im, ph, z.q);
+                    if (!pend) ev.begin(z.q);
+                    pend = false;
+                    ev.end(z.q, z.U, z.g);
+                } else {
 #pragma unroll
-                for (int m = 0; m < DPL; ++m) {
-                    ph[m] = z.p[m] - 0.5 * h * z.g[m];
-                    z.q[m] = z.q[m] + h * im[m] * ph[m];
+                    for (int m = 0; m < DPL; ++m) {
+                        ph[m] = z.p[m] - 0.5 * h * z.g[m];
+                        z.q[m] = z.q[m] + h * im[m] * ph[m];
+                    }
+                    ev.eval(z.q, z.U, z.g);
                 }
-                ev.eval(z.q, z.U, z.g);
                 if (ev.aborted()) break;
                 double k2 = 0.0;
 #pragma unroll
@@ -677,6 +772,30 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     k2 += im[m] * z.p[m] * z.p[m];
                 }
                 ++nleaves;
+                if constexpr (Eval::kSpeculative) {
+                    // Start the next evaluation now, so that the workers
+                    // stream while the bookkeeping below runs: the next leaf
+                    // of this subtree, or else the first leaf of the next
+                    // doubling from the trajectory edge it starts at (this
+                    // leaf, once merged, if it goes the same way).  If the
+                    // bookkeeping ends the trajectory it is called off.
+                    const bool more = n + 1 < nleaf;
+                    if (more || j + 1 < maxd) {
+                        const int vn = more ? v : (((dirmask >> (j + 1)) & 1ull) ? 1 : -1);
+                        const bool from_z = more || vn == v;
+                        const double hn = vn * eps;
+                        double bq[DPL], bp[DPL], bg[DPL], nph[DPL], nq[DPL];
+#pragma unroll
+                        for (int m = 0; m < DPL; ++m) {
+                            bq[m] = from_z ? z.q[m] : (vn > 0 ? right.q[m] : left.q[m]);
+                            bp[m] = from_z ? z.p[m] : (vn > 0 ? right.p[m] : left.p[m]);
+                            bg[m] = from_z ? z.g[m] : (vn > 0 ? right.g[m] : left.g[m]);
+                        }
+                        leapfrog_drift<DPL>(bq, bp, bg, hn, im, nph, nq);
+                        ev.begin(nq);
+                        pend = true;
+                    }
+                }
                 if (gen) {
 #pragma unroll
                     for (int m = 0; m < DPL; ++m) rsum[m] += z.p[m];
@@ -837,6 +956,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 break;
             }
             if (j == maxd - 1) maxhit = 1;
+        }
+        if constexpr (Eval::kSpeculative) {
+            if (pend) ev.cancel();  // the trajectory ended before that position
         }
         evals += (unsigned long long)nleaves;
         cur = prop;
@@ -1049,12 +1171,15 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
     c.sync = sync;
     const int wave = threadIdx.x / kWave;
     if (wave == 0) {
+        // published by the first collective's barrier
+        if (lane() == 0) __hip_atomic_store(&sh.stop, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         GridEval<T, S, CPS, DPL, kGridWaves> ev;
         ev.c = c;
         ev.sh = &sh;
         ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
         ev.prior_const = (double)A.data.D * (log(A.prior_scale) + kHalfLog2Pi);
         ev.step = 0;
+        ev.gen = 0;
         ev.abort = false;
         run_chain<DPL, EXT>(A, ev, 0, lds);
         ev.finish();
@@ -1065,8 +1190,9 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
         for (int m = 0; m < DPL; ++m) q[m] = 0.0;
         for (;;) {
             bool ab;
-            if (grid_collective<T, S, CPS, DPL, kGridWaves, true>(c, sh, step, q, 0, r, &ab) == kCmdExit) break;
-            step++;
+            int gen = 0;
+            if (grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen) == kCmdExit) break;
+            if (grid_end<T, S, CPS, DPL, kGridWaves, true>(c, sh, step, gen, false, r, &ab)) step++;
         }
     }
 }
