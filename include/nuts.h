@@ -118,23 +118,24 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the
  * quantities of nuts_data_potential_grad from the same kernel, with its
- * partial sums and arrival counts in a fixed device array of the library
- * (8 MiB per device, held from nuts_init until the process ends) instead of
- * handle memory.  It allocates nothing, copies nothing and does not wait:
+ * partial-sum slots in a fixed device array of the library (8 MiB per
+ * device, held from nuts_init until the process ends) instead of handle
+ * memory.  It allocates nothing, copies nothing and does not wait:
  *   - W [K][D], out_U [K] and out_grad [K][D] must be device memory
  *     (NUTS_EINVAL otherwise);
- *   - the call only enqueues its work (a small kernel that clears the K
- *     arrival counts, then the potential kernel) on the handle's stream and
+ *   - the call only enqueues the potential kernel on the handle's stream and
  *     returns; the outputs are ready once that stream has reached this
  *     point (synchronise it, or order later work after it);
  *   - 1 <= K <= 16384, and K x G x partial_width(D) doubles of partial sums
- *     must fit in the array's 8 MiB - 64 KiB (G = groups per position, about
+ *     must fit in the array's 8 MiB (G = groups per position, about
  *     num_CUs / K; one group per position for K >= num_CUs): with D <= 64 up
  *     to about 8 000 positions, with D <= 320 about 2 700; larger requests
  *     fail with NUTS_EINVAL and a message giving the sizes;
- *   - every call on one device shares that device's array: calls that
- *     overlap on one device (different streams or handles, or host threads)
- *     race and give wrong results; calls in one stream are ordered and safe.
+ *   - every call on one device shares that device's array (each call leaves
+ *     the slots it used empty for the next): calls that overlap on one
+ *     device (different streams or handles, or host threads) race and give
+ *     wrong results (a position whose partial sums another call took gets
+ *     NaN after about 2 s); calls in one stream are ordered and safe.
  * Results are bitwise identical to nuts_data_potential_grad's. */
 int nuts_data_potential_grad_noalloc(nuts_handle* h, const nuts_data* d, double prior_scale,
                                      const double* W, int64_t K, double* out_U, double* out_grad);

@@ -46,9 +46,10 @@ struct nuts_handle {
     // uses it between its launches and its final stream synchronisation
     void* scratch = nullptr;
     size_t scratch_bytes = 0;
-    // arrival counts of the potential kernel, one per item; zeroed once, the
-    // kernel leaves them zero
-    unsigned int* pot_counts = nullptr;
+    // partial-sum slots of the potential kernel, grow-only, marked empty on
+    // allocation; every launch leaves the slots it used empty again
+    double* pot_slots = nullptr;
+    size_t pot_slot_bytes = 0;
     // this device's copy of the fixed workspace of the allocation-free entry
     // point (set up by nuts_init; never freed)
     void* static_ws = nullptr;
@@ -77,23 +78,31 @@ static hipError_t handle_evals(nuts_handle* h, int64_t C, unsigned long long** o
     return hipSuccess;
 }
 
-static hipError_t potential_counts(nuts_handle* h, unsigned int** out)
+// Partial-sum slots of the potential kernel for `bytes`, all empty.
+static hipError_t potential_slots(nuts_handle* h, size_t bytes, double** out)
 {
-    if (!h->pot_counts) {
-        const size_t bytes = (size_t)kMaxPotentialItems * sizeof(unsigned int);
-        hipError_t e = hipMalloc(&h->pot_counts, bytes);
+    if (bytes > h->pot_slot_bytes) {
+        if (h->pot_slots) {
+            hipError_t e = hipStreamSynchronize(h->stream);
+            if (e != hipSuccess) return e;
+            (void)hipFree(h->pot_slots);
+            h->pot_slots = nullptr;
+            h->pot_slot_bytes = 0;
+        }
+        hipError_t e = hipMalloc(&h->pot_slots, bytes);
         if (e != hipSuccess) {
-            h->pot_counts = nullptr;
+            h->pot_slots = nullptr;
             return e;
         }
-        e = hipMemsetAsync(h->pot_counts, 0, bytes, h->stream);
+        e = mark_partials_empty(h->pot_slots, (int64_t)(bytes / sizeof(double)), h->stream);
         if (e != hipSuccess) {
-            (void)hipFree(h->pot_counts);
-            h->pot_counts = nullptr;
+            (void)hipFree(h->pot_slots);
+            h->pot_slots = nullptr;
             return e;
         }
+        h->pot_slot_bytes = bytes;
     }
-    *out = h->pot_counts;
+    *out = h->pot_slots;
     return hipSuccess;
 }
 
@@ -428,7 +437,7 @@ void nuts_free(nuts_handle* h)
     DeviceScope ds(h->device);
     (void)hipStreamSynchronize(h->stream);
     if (h->scratch) (void)hipFree(h->scratch);
-    if (h->pot_counts) (void)hipFree(h->pot_counts);
+    if (h->pot_slots) (void)hipFree(h->pot_slots);
     if (h->evals) (void)hipFree(h->evals);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
@@ -539,12 +548,10 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
     HIP_TRY(h, stage_out(out_U, (size_t)K * 8, ut, &Ud));
     HIP_TRY(h, stage_out(out_grad, (size_t)K * D * 8, gt, &Gd));
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
-    void* part = nullptr;
-    HIP_TRY(h, handle_scratch(h, (size_t)K * plan.groups_per_item * plan.width * sizeof(double), &part));
-    unsigned int* counts = nullptr;
-    HIP_TRY(h, potential_counts(h, &counts));
-    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, (double*)part, counts,
-                                     (double*)Ud, (double*)Gd, h->stream));
+    double* part = nullptr;
+    HIP_TRY(h, potential_slots(h, (size_t)K * plan.groups_per_item * plan.width * sizeof(double), &part));
+    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, (const double*)Wd, K, plan, part, (double*)Ud,
+                                     (double*)Gd, h->stream));
     HIP_TRY(h, finish_out(out_U, (size_t)K * 8, ut, h->stream));
     HIP_TRY(h, finish_out(out_grad, (size_t)K * D * 8, gt, h->stream));
     HIP_TRY(h, hipStreamSynchronize(h->stream));
@@ -568,14 +575,14 @@ int nuts_data_potential_grad_noalloc(nuts_handle* h, const nuts_data* d, double 
         return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be device memory (this entry point copies nothing)");
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
     const size_t need = (size_t)K * plan.groups_per_item * plan.width * sizeof(double);
-    if (need > kStaticPartialBytes)
+    if (need > kStaticScratchBytes)
         return fail(h, NUTS_EINVAL,
                     "K = %lld positions need %zu bytes of partial sums (%d groups of %d doubles each), more than "
                     "the %zu bytes of the fixed workspace",
-                    (long long)K, need, plan.groups_per_item, plan.width, kStaticPartialBytes);
+                    (long long)K, need, plan.groups_per_item, plan.width, kStaticScratchBytes);
     DeviceScope ds(h->device);
-    HIP_TRY(h, launch_potential_grad_static(h->static_ws, d->view, prior_scale, W, K, plan, out_U, out_grad,
-                                            h->stream));
+    HIP_TRY(h, launch_potential_grad(d->view, prior_scale, W, K, plan, (double*)h->static_ws, out_U, out_grad,
+                                     h->stream));
     return NUTS_OK;
 }
 
@@ -694,16 +701,14 @@ int nuts_data_log_likelihood(nuts_handle* h, const nuts_data* d, const double* W
     } else {
         // the potential at prior scale 1 per draw, then the prior taken off
         const PotentialPlan plan = plan_potential(d->view, S, h->num_cu);
-        const size_t pbytes = align256((size_t)S * plan.groups_per_item * plan.width * sizeof(double));
         const size_t ubytes = align256((size_t)S * sizeof(double));
         void* scratch = nullptr;
-        HIP_TRY(h, handle_scratch(h, pbytes + ubytes + (size_t)S * D * sizeof(double), &scratch));
-        double* U = (double*)((char*)scratch + pbytes);
-        double* G = (double*)((char*)scratch + pbytes + ubytes);
-        unsigned int* counts = nullptr;
-        HIP_TRY(h, potential_counts(h, &counts));
-        HIP_TRY(h, launch_potential_grad(d->view, 1.0, (const double*)Wd, S, plan, (double*)scratch, counts, U, G,
-                                         h->stream));
+        HIP_TRY(h, handle_scratch(h, ubytes + (size_t)S * D * sizeof(double), &scratch));
+        double* U = (double*)scratch;
+        double* G = (double*)((char*)scratch + ubytes);
+        double* part = nullptr;
+        HIP_TRY(h, potential_slots(h, (size_t)S * plan.groups_per_item * plan.width * sizeof(double), &part));
+        HIP_TRY(h, launch_potential_grad(d->view, 1.0, (const double*)Wd, S, plan, part, U, G, h->stream));
         HIP_TRY(h, launch_ll_from_potential(D, (const double*)Wd, S, U, (double*)Ld, h->stream));
     }
     if (out_elpd) HIP_TRY(h, launch_expected_ll((const double*)Ld, S, (double*)Ed, h->stream));

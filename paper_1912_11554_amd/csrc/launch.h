@@ -70,9 +70,9 @@ hipError_t launch_to_blocks(const void* X_rowmajor, const uint8_t* y_in, DataVie
                             void* X_out, uint8_t* y_out, unsigned int* bad_label,
                             hipStream_t stream);
 
-// Workspace of the batched potential/gradient: partial sums [K][G][width]
-// and one arrival count per item, [K] unsigned ints that must be zero before
-// the launch and are zero again after it (the kernel re-arms them).
+// Workspace of the batched potential/gradient: partial-sum slots
+// [K][G][width] doubles, every slot marked empty (mark_partials_empty)
+// before the first launch; each launch leaves every slot it used empty again.
 struct PotentialPlan {
     int groups_per_item;  // G
     int width;            // partial_width(D)
@@ -80,24 +80,20 @@ struct PotentialPlan {
 constexpr int kMaxPotentialItems = 65535;
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu);
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
-                                 const PotentialPlan& plan, double* partials, unsigned int* counters,
-                                 double* out_U, double* out_grad, hipStream_t stream);
+                                 const PotentialPlan& plan, double* partials, double* out_U, double* out_grad,
+                                 hipStream_t stream);
+// Mark n partial-sum slots empty (a kernel on `stream`).
+hipError_t mark_partials_empty(double* p, int64_t n, hipStream_t stream);
 
-// The allocation-free form of launch_potential_grad: its arrival counts and
-// partial rows live in a fixed device array of kStaticScratchBytes (the
-// counts in its first kStaticCountBytes, the partial rows after them).
+// The allocation-free form of launch_potential_grad keeps its partial-sum
+// slots in a fixed device array of kStaticScratchBytes.
 // static_workspace_setup, called once per device with that device current
-// (nuts_init does), finds this device's copy of the array and zeroes the
-// counts; it returns the array's device address.  Calls that overlap on one
+// (nuts_init does), finds this device's copy of the array and marks its slots
+// empty; it returns the array's device address.  Calls that overlap on one
 // device race on the array.
 constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
-constexpr size_t kStaticCountBytes = (size_t)64 << 10;
-constexpr int64_t kStaticMaxItems = (int64_t)(kStaticCountBytes / sizeof(unsigned int));
-constexpr size_t kStaticPartialBytes = kStaticScratchBytes - kStaticCountBytes;
+constexpr int64_t kStaticMaxItems = 16384;
 hipError_t static_workspace_setup(int device, hipStream_t stream, void** out);
-hipError_t launch_potential_grad_static(void* workspace, const DataView& dv, double prior_scale, const double* W,
-                                        int64_t K, const PotentialPlan& plan, double* out_U, double* out_grad,
-                                        hipStream_t stream);
 
 // Sampler arguments common to both paths (device pointers).
 struct SamplerArgs {

@@ -1,23 +1,29 @@
 // Batched potential and gradient of the logistic log-joint at K positions,
 // in one launch.  A grid of (G groups) x (K items); the NW waves of a group
-// (16, or 8 where a lane holds many columns and needs the registers) stream
-// the blocks b = g * NW + w, g * NW + w + G * NW, ... of their item's
-// data set, the group adds its waves' column sums in wave order and stores
-// one fp64 partial row of width partial_width(D) (columns 0..D-1, the loss at
-// 64 * ceil(D / 64)), then counts itself in for its item.  The group that
-// completes an item's count adds the item's G partial rows in a fixed order
-// and the Gaussian prior terms, writes U and grad U, and re-zeroes the count.
-// No floating-point atomics anywhere, so results are bitwise reproducible.
+// (8 for fp32 rows and wide fp64 rows, 16 for fp64 rows of at most 8 column
+// slots) stream the blocks b = g * NW + w, g * NW + w + G * NW, ... of their
+// item's data set, the group adds its waves' column sums in wave order and
+// stores one fp64 partial row of width partial_width(D) (columns 0..D-1, the
+// loss at 64 * ceil(D / 64)) into its slots, and every group but the item's
+// first is done.  The first group, once its own rows are in, gathers the G
+// partial rows: each slot holds a signalling-NaN pattern until it is written,
+// so the gatherer waits on the values themselves (no counter, no ordering
+// point between a group's stores and a count).  It adds them in a fixed
+// order, adds the Gaussian prior terms, writes U and grad U, and marks every
+// slot it read empty again for the next call.  No floating-point atomics
+// anywhere, so results are bitwise reproducible.
+#include <algorithm>
 #include <mutex>
 
 #include "launch.h"
 #include "rows.h"
 
-// Workspace of the allocation-free potential entry point: the arrival counts
-// (kStaticCountBytes), then the partial rows.  Every device the library runs
-// on holds its own copy until the process ends.  Host code never passes this
-// name to a kernel or a copy (on the host it only stands for the symbol):
-// it uses the address hipGetSymbolAddress gives for the current device.
+// Workspace of the allocation-free potential entry point: partial-row slots,
+// marked empty when the library sets the device up.  Every device the
+// library runs on holds its own copy until the process ends.  Host code
+// never passes this name to a kernel or a copy (on the host it only stands
+// for the symbol): it uses the address hipGetSymbolAddress gives for the
+// current device.
 static __device__ __align__(256) unsigned char scratch[nuts::kStaticScratchBytes];
 
 namespace nuts {
@@ -26,45 +32,64 @@ namespace {
 
 constexpr double kHalfLog2Pi = 0.91893853320467274178032973640562;
 
-// waves per group: 16 (4 per SIMD, 128 registers a lane) unless the shape's
-// per-lane state needs more registers than that
-template <int S, int CPS>
-constexpr int pot_waves() { return (S == 1 && CPS == 16) || CPS > 8 ? 8 : 16; }
-// two block register sets in the stream for the 8-wave shapes and for fp64
-// rows shared by several lanes (16 waves of fp32 rows hide the loads as well
-// with one set, and fp64 rows of one lane would spill with two); the
-// lane-masked loads of the last column slots in the 8-wave shapes
+// waves per group: fp64 rows of at most 8 column slots take 16 waves (4 per
+// SIMD, 128 registers a lane, one block register set); every other shape
+// takes 8 waves, whose registers hold two block register sets (fp32 rows
+// carry two rows a lane, converted to fp64 in registers, and wide rows carry
+// 10 or 16 slots)
 template <typename T, int S, int CPS>
-constexpr bool pot_pipe() { return pot_waves<S, CPS>() == 8 || (sizeof(T) == 8 && S > 1); }
+constexpr int pot_waves() { return (sizeof(T) == 8 && CPS == 8) ? 16 : 8; }
+// two block register sets in the stream for the 8-wave shapes and for fp64
+// rows shared by several lanes (fp64 rows of one lane would spill with two);
+// the lane-masked loads of the last column slots for wide rows
+template <typename T, int S, int CPS>
+constexpr bool pot_pipe() { return pot_waves<T, S, CPS>() == 8 || S > 1; }
 template <int S, int CPS>
-constexpr bool pot_mask() { return pot_waves<S, CPS>() == 8; }
+constexpr bool pot_mask() { return S >= 16; }
 static_assert(kMaxDim + 1 <= 8 * kWave, "one thread per used column in the final sum");
+
+// A slot not written yet: a signalling-NaN bit pattern that no arithmetic
+// produces (sums of finite or non-finite values give quiet NaNs).
+constexpr unsigned long long kEmptyPartial = 0x7FF4DEADBEEF0002ull;
+// about 2 s of the 100 MHz constant clock: a slot that stays empty that long
+// means another call overlapped this one on the device
+constexpr uint64_t kGatherWaitTicks = 200000000ull;
+// slots a gathering thread has in flight at once: enough for every slot of
+// the covtype-sized shapes (G = 256 groups, D + 1 = 56 used columns) in one
+// batch, 32 with 512 threads, 16 with 1024
+template <int NW>
+constexpr int gather_batch() { return NW == 16 ? 16 : 32; }
 
 __device__ __forceinline__ void store_agent(double* p, double v)
 {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ double load_agent(const double* p)
+__device__ __forceinline__ unsigned long long load_bits(const double* p)
 {
-    return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return __hip_atomic_load(reinterpret_cast<unsigned long long*>(const_cast<double*>(p)), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void drain()
+__device__ __forceinline__ void empty_slot(double* p)
 {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), kEmptyPartial, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void __launch_bounds__(256) fill_empty_kernel(unsigned long long* __restrict__ p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        p[i] = kEmptyPartial;
 }
 
 template <typename T, int S, int CPS>
-__global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_kernel(
+__global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave)) potential_grad_kernel(
     DataView dv, const double* __restrict__ W, int G, int width, double* __restrict__ partials,
-    unsigned int* __restrict__ counters, double prior_scale, double* __restrict__ out_U,
-    double* __restrict__ out_grad)
+    double prior_scale, double* __restrict__ out_U, double* __restrict__ out_grad)
 {
     constexpr int R = BlockShape<T, S>::R;
-    constexpr int NW = pot_waves<S, CPS>();
+    constexpr int NW = pot_waves<T, S, CPS>();
     extern __shared__ double part[];  // [NW][width], later the per-set sums
-    __shared__ int last;
+    __shared__ int failed;
     const int l = lane();
     const int wave = threadIdx.x / kWave;
     const int64_t k = blockIdx.y;
@@ -81,8 +106,8 @@ __global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_
 #pragma unroll
     for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
     double loss = 0.0;
-    stream_blocks<T, CPS, S, pot_pipe<T, S, CPS>(), pot_mask<S, CPS>()>(X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv,
-                             acc, loss);
+    stream_blocks<T, CPS, S, pot_pipe<T, S, CPS>(), pot_mask<S, CPS>()>(
+        X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv, acc, loss);
 
     double* row = part + wave * width;
     if constexpr (S <= 8 && CPS == 8) {
@@ -92,9 +117,11 @@ __global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_
     } else {
         finish_pass_to_row<CPS, S>(acc, loss, row, D, loss_slot);
     }
+    if (threadIdx.x == 0) failed = 0;
     __syncthreads();  // per-wave sums in LDS
+    double* item = partials + k * G * width;
     if (wave == 0) {
-        double* mine = partials + (k * G + g) * width;
+        double* mine = item + (int64_t)g * width;
         for (int col = l; col < width; col += 64) {
             if (col < D || col == loss_slot) {
                 double s = 0.0;
@@ -103,46 +130,66 @@ __global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_
                 store_agent(mine + col, s);
             }
         }
-        drain();  // the partial row is out before the count
-        int is_last = 0;
-        if (l == 0) {
-            const unsigned int o =
-                __hip_atomic_fetch_add(&counters[k], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            is_last = o + 1 == (unsigned int)G ? 1 : 0;
-        }
-        is_last = __shfl(is_last, 0);
-        if (l == 0) last = is_last;
     }
-    __syncthreads();  // the count is taken
-    if (!last) return;
+    if (g != 0) return;
 
-    // Every group of item k is in.  Thread t takes used column c = t mod
+    // The item's first group gathers.  Thread t takes used column c = t mod
     // (D + 1) (column c < D, or the loss for c = D) of the groups j, j + J,
-    // j + 2 J, ... (j = t div (D + 1), J sets) in increasing order.
+    // j + 2 J, ... (j = t div (D + 1), J sets) in increasing order, waiting on
+    // each slot until it holds a value.
     const int used = D + 1;
     const int t = threadIdx.x;
     const int sets = (NW * kWave) / used;
     const int j = t / used;
     const int c = t - j * used;
+    constexpr int kGatherBatch = gather_batch<NW>();
     double s = 0.0;
+    bool ok = true;
     if (j < sets) {
-        const double* src = partials + k * G * width + (c < D ? c : loss_slot);
-        constexpr int B = 16;
-        for (int g0 = j; g0 < G; g0 += B * sets) {
-            double v[B];
+        double* src = item + (c < D ? c : loss_slot);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        for (int g0 = j; g0 < G; g0 += kGatherBatch * sets) {
+            unsigned long long v[kGatherBatch];
 #pragma unroll
-            for (int i = 0; i < B; ++i) {
+            for (int i = 0; i < kGatherBatch; ++i) {
                 const int gg = g0 + i * sets;
-                v[i] = gg < G ? load_agent(src + (int64_t)gg * width) : 0.0;
+                v[i] = gg < G ? load_bits(src + (int64_t)gg * width) : 0ull;
+            }
+            for (;;) {
+                bool pending = false;
+#pragma unroll
+                for (int i = 0; i < kGatherBatch; ++i) {
+                    const int gg = g0 + i * sets;
+                    if (gg < G && v[i] == kEmptyPartial) {
+                        v[i] = load_bits(src + (int64_t)gg * width);
+                        pending = true;
+                    }
+                }
+                if (!pending) break;
+                if (__builtin_amdgcn_s_memrealtime() - t0 > kGatherWaitTicks) {
+                    ok = false;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
             }
 #pragma unroll
-            for (int i = 0; i < B; ++i) s += v[i];
+            for (int i = 0; i < kGatherBatch; ++i) {
+                const int gg = g0 + i * sets;
+                if (gg < G) {
+                    s += __builtin_bit_cast(double, v[i]);
+                    empty_slot(src + (int64_t)gg * width);  // for the next call
+                }
+            }
         }
     }
+    if (!ok) __hip_atomic_store(&failed, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     __syncthreads();  // no wave reads its LDS row any more
     if (j < sets) part[j * used + c] = s;
     __syncthreads();  // per-set sums in LDS
     if (wave != 0) return;
+    // a slot that never filled: another call overlapped this one; the
+    // results are NaN (every slot this group read is empty again)
+    const double bad = failed ? __builtin_nan("") : 0.0;
     const double inv_s2 = 1.0 / (prior_scale * prior_scale);
     double pr = 0.0;
     double lossv = 0.0;
@@ -152,37 +199,33 @@ __global__ void __launch_bounds__((pot_waves<S, CPS>() * kWave)) potential_grad_
         if (col < D) {
             const double w = W[k * D + col];
             pr += 0.5 * w * w * inv_s2;
-            out_grad[k * D + col] = tot + w * inv_s2;
+            out_grad[k * D + col] = tot + w * inv_s2 + bad;
         } else {
             lossv = tot;
         }
     }
     const double prior = wave_sum(pr);
     lossv = readlane_f64(lossv, D & 63);  // column D sits in lane D mod 64
-    if (l == 0) {
-        out_U[k] = lossv + prior + (double)D * (log(prior_scale) + kHalfLog2Pi);
-        // re-arm the count for the next call (kernels on one stream are ordered)
-        __hip_atomic_store(&counters[k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (l == 0) out_U[k] = lossv + prior + (double)D * (log(prior_scale) + kHalfLog2Pi) + bad;
 }
 
 template <typename T, int S, int CPS>
 void enqueue(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-             double* partials, unsigned int* counters, double* out_U, double* out_grad, hipStream_t stream)
+             double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
-    constexpr int NW = pot_waves<S, CPS>();
+    constexpr int NW = pot_waves<T, S, CPS>();
     hipLaunchKernelGGL((potential_grad_kernel<T, S, CPS>), dim3(G, (unsigned)K), dim3(NW * kWave),
-                       (size_t)NW * width * sizeof(double), stream, dv, W, G, width, partials, counters,
-                       prior_scale, out_U, out_grad);
+                       (size_t)NW * width * sizeof(double), stream, dv, W, G, width, partials, prior_scale,
+                       out_U, out_grad);
 }
 
 template <typename T>
 void enqueue_shape(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-                   double* partials, unsigned int* counters, double* out_U, double* out_grad, hipStream_t stream)
+                   double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
     const int D = dv.D;
 #define NUTS_POT(S_, C_) \
-    enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, counters, out_U, out_grad, stream)
+    enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, out_U, out_grad, stream)
     if (D <= 8) NUTS_POT(1, 8);
     else if (D <= 16) NUTS_POT(1, 16);
     else if (D <= 32) NUTS_POT(4, 8);
@@ -242,17 +285,20 @@ hipError_t launch_expected_ll(const double* ll, int64_t S, double* out, hipStrea
 
 namespace {
 
-__global__ void __launch_bounds__(256) zero_counts_kernel(unsigned int* __restrict__ c, int n)
-{
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i < n) c[i] = 0u;
-}
-
 constexpr int kMaxDevices = 64;
 std::mutex g_static_mutex;
 void* g_static_ptr[kMaxDevices] = {};
 
 }  // namespace
+
+hipError_t mark_partials_empty(double* p, int64_t n, hipStream_t stream)
+{
+    if (n <= 0) return hipSuccess;
+    const int64_t groups = std::min<int64_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(fill_empty_kernel, dim3((unsigned)groups), dim3(256), 0, stream,
+                       reinterpret_cast<unsigned long long*>(p), n);
+    return hipGetLastError();
+}
 
 hipError_t static_workspace_setup(int device, hipStream_t stream, void** out)
 {
@@ -265,31 +311,14 @@ hipError_t static_workspace_setup(int device, hipStream_t stream, void** out)
         hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
         if (e != hipSuccess) return e;
         if (!p) return hipErrorInvalidSymbol;
-        // the counts start at zero (each call clears the ones it uses as well)
-        const int n = (int)(kStaticCountBytes / sizeof(unsigned int));
-        hipLaunchKernelGGL(zero_counts_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, (unsigned int*)p, n);
-        e = hipGetLastError();
+        // every slot starts empty (each call leaves the slots it used empty)
+        e = mark_partials_empty((double*)p, (int64_t)(kStaticScratchBytes / sizeof(double)), stream);
         if (e == hipSuccess) e = hipStreamSynchronize(stream);
         if (e != hipSuccess) return e;
         g_static_ptr[device] = p;
     }
     *out = g_static_ptr[device];
     return hipSuccess;
-}
-
-hipError_t launch_potential_grad_static(void* workspace, const DataView& dv, double prior_scale, const double* W,
-                                        int64_t K, const PotentialPlan& plan, double* out_U, double* out_grad,
-                                        hipStream_t stream)
-{
-    unsigned int* counts = (unsigned int*)workspace;
-    double* partials = (double*)((char*)workspace + kStaticCountBytes);
-    // a call that overlapped another one on this device may have left its
-    // counts anywhere: clear this call's counts first (a kernel, not a
-    // memset, so that the call can be captured into a graph)
-    hipLaunchKernelGGL(zero_counts_kernel, dim3((unsigned)((K + 255) / 256)), dim3(256), 0, stream, counts, (int)K);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_potential_grad(dv, prior_scale, W, K, plan, partials, counts, out_U, out_grad, stream);
 }
 
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
@@ -304,15 +333,15 @@ PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
 }
 
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
-                                 const PotentialPlan& plan, double* partials, unsigned int* counters,
-                                 double* out_U, double* out_grad, hipStream_t stream)
+                                 const PotentialPlan& plan, double* partials, double* out_U, double* out_grad,
+                                 hipStream_t stream)
 {
     if (dv.dtype == NUTS_F64)
-        enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, counters, out_U,
-                              out_grad, stream);
+        enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
+                              stream);
     else
-        enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, counters,
-                             out_U, out_grad, stream);
+        enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
+                             stream);
     return hipGetLastError();
 }
 
