@@ -58,7 +58,33 @@ struct nuts_handle {
     // kernel starts
     unsigned long long* evals = nullptr;
     int64_t evals_cap = 0;
+    // pinned host memory for the small read-backs that end a call (the
+    // evaluation counts, a kernel's error flag), so that they are
+    // asynchronous copies ahead of one stream synchronisation
+    void* pinned = nullptr;
+    size_t pinned_bytes = 0;
 };
+
+static hipError_t handle_pinned(nuts_handle* h, size_t bytes, void** out)
+{
+    if (bytes > h->pinned_bytes) {
+        if (h->pinned) {
+            hipError_t e = hipStreamSynchronize(h->stream);
+            if (e != hipSuccess) return e;
+            (void)hipHostFree(h->pinned);
+            h->pinned = nullptr;
+            h->pinned_bytes = 0;
+        }
+        hipError_t e = hipHostMalloc(&h->pinned, bytes, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            h->pinned = nullptr;
+            return e;
+        }
+        h->pinned_bytes = bytes;
+    }
+    *out = h->pinned;
+    return hipSuccess;
+}
 
 static hipError_t handle_evals(nuts_handle* h, int64_t C, unsigned long long** out)
 {
@@ -325,20 +351,30 @@ struct RunBuffers {
         return NUTS_OK;
     }
 
-    // copy host outputs back, sum the gradient evaluations, synchronise
-    int finish(nuts_handle* h, const nuts_sample_opts& o, double* out_samples, nuts_stats* out_stats)
+    // copy host outputs back, sum the gradient evaluations, synchronise.
+    // With `flag` (a kernel's device error word), also read it back and
+    // fail with `flag_msg` if it is set.
+    int finish(nuts_handle* h, const nuts_sample_opts& o, double* out_samples, nuts_stats* out_stats,
+               const unsigned int* flag = nullptr, const char* flag_msg = nullptr)
     {
         HIP_TRY(h, finish_out(out_samples, (size_t)C * S * D * 8, smp, s));
         HIP_TRY(h, finish_out(out_stats, (size_t)C * S * sizeof(nuts_stats), sts, s));
         HIP_TRY(h, finish_out(o.out_final_q, (size_t)C * D * 8, fq, s));
         HIP_TRY(h, finish_out(o.out_inv_mass, (size_t)C * D * 8, fim, s));
         HIP_TRY(h, finish_out(o.out_step_size, (size_t)C * 8, fep, s));
-        std::vector<unsigned long long> ev(C);
-        HIP_TRY(h, hipMemcpyAsync(ev.data(), gev, (size_t)C * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+        void* pin = nullptr;
+        const size_t eb = (size_t)C * sizeof(unsigned long long);
+        HIP_TRY(h, handle_pinned(h, eb + 8, &pin));
+        unsigned long long* ev = (unsigned long long*)pin;
+        unsigned int* fl = (unsigned int*)((char*)pin + eb);
+        *fl = 0u;
+        HIP_TRY(h, hipMemcpyAsync(ev, gev, eb, hipMemcpyDeviceToHost, s));
+        if (flag) HIP_TRY(h, hipMemcpyAsync(fl, flag, sizeof(unsigned int), hipMemcpyDeviceToHost, s));
         HIP_TRY(h, hipStreamSynchronize(s));
+        if (flag && *fl) return fail(h, NUTS_EDEVICE, "%s", flag_msg);
         if (o.out_grad_evals) {
             unsigned long long tot = 0;
-            for (auto v : ev) tot += v;
+            for (int64_t c = 0; c < C; ++c) tot += ev[c];
             *o.out_grad_evals = (int64_t)tot;
         }
         return NUTS_OK;
@@ -439,6 +475,7 @@ void nuts_free(nuts_handle* h)
     if (h->scratch) (void)hipFree(h->scratch);
     if (h->pot_slots) (void)hipFree(h->pot_slots);
     if (h->evals) (void)hipFree(h->evals);
+    if (h->pinned) (void)hipHostFree(h->pinned);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
 }
@@ -898,13 +935,19 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
             ac.num_chains = 1;
             ac.chain_offset = c;
             HIP_TRY(h, launch_sampler_grid(ac, groups, part, res, sync, s));
-            GridSync hs;
-            HIP_TRY(h, hipMemcpyAsync(&hs, sync, sizeof hs, hipMemcpyDeviceToHost, s));
-            HIP_TRY(h, hipStreamSynchronize(s));
-            if (hs.error)
-                return fail(h, NUTS_EDEVICE, "grid barrier timed out in chain %lld (a group stopped responding)",
-                            (long long)c);
+            if (c + 1 < C) {
+                // the next chain's launch clears the flag: check this one's first
+                GridSync hs;
+                HIP_TRY(h, hipMemcpyAsync(&hs, sync, sizeof hs, hipMemcpyDeviceToHost, s));
+                HIP_TRY(h, hipStreamSynchronize(s));
+                if (hs.error)
+                    return fail(h, NUTS_EDEVICE, "grid barrier timed out in chain %lld (a group stopped responding)",
+                                (long long)c);
+            }
         }
+        // the last chain's flag is read with the outputs
+        return rb.finish(h, o, out_samples, out_stats, &sync->error,
+                         "grid barrier timed out in the last chain (a group stopped responding)");
     }
     return rb.finish(h, o, out_samples, out_stats);
 }

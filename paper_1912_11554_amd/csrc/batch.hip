@@ -72,6 +72,19 @@ __device__ __forceinline__ void put_d(double* p, double v)
     if constexpr (ATOMIC) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else *p = v;
 }
+// Two consecutive floats (8-byte aligned) as one store: agent-scope stores
+// are 8 bytes at most, and one per pair halves the store transactions of
+// four separate floats.
+template <bool ATOMIC>
+__device__ __forceinline__ void put_f2(float* p, float a, float b)
+{
+    const unsigned long long v = (unsigned long long)__builtin_bit_cast(uint32_t, a) |
+                                 ((unsigned long long)__builtin_bit_cast(uint32_t, b) << 32);
+    if constexpr (ATOMIC)
+        __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        *reinterpret_cast<unsigned long long*>(p) = v;
+}
 
 template <int KT, bool ATOMIC>
 __device__ __forceinline__ void store_partials(const BatchView& bv, WaveAcc& acc, int widx, int pw, float* P,
@@ -85,8 +98,9 @@ __device__ __forceinline__ void store_partials(const BatchView& bv, WaveAcc& acc
     float* row = P + (int64_t)slot * pw;
 #pragma unroll
     for (int mt = 0; mt < KT; ++mt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) put_f<ATOMIC>(row + 16 * mt + 4 * jj + r, acc.g[mt][r]);
+        float* dst = row + 16 * mt + 4 * jj;  // 16-byte aligned: pw and 4 jj are multiples of 4
+        put_f2<ATOMIC>(dst, acc.g[mt][0], acc.g[mt][1]);
+        put_f2<ATOMIC>(dst + 2, acc.g[mt][2], acc.g[mt][3]);
     }
     if (jj == 0) {
 #pragma unroll
@@ -572,7 +586,9 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         double s[DPL + 1];
 #pragma unroll
         for (int mm = 0; mm <= DPL; ++mm) s[mm] = 0.0;
-        constexpr int B = 4;
+        // every load of a wave's share in flight at once: one round trip for
+        // up to 16 groups per wave (144 groups of 9 waves)
+        constexpr int B = 16;
         int g = wave;
         for (; g + (B - 1) * kGroupWaves < c.groups; g += B * kGroupWaves) {
             float v[B][DPL];

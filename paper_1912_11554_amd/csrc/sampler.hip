@@ -6,10 +6,13 @@ namespace nuts {
 
 namespace {
 
-__global__ void fill_empty_slots(double* a, int64_t na, double* b, int64_t nb)
+// Every exchange slot empty and the error flag clear, before a launch.
+__global__ void fill_empty_slots(double* a, int64_t na, double* b, int64_t nb, GridSync* sync)
 {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < na + nb; i += stride) {
+    const int64_t first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (first == 0) sync->error = 0u;
+    for (int64_t i = first; i < na + nb; i += stride) {
         unsigned long long* p = reinterpret_cast<unsigned long long*>(i < na ? a + i : b + (i - na));
         *p = sampler::kEmptySlot;
     }
@@ -62,11 +65,9 @@ int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int nu
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
                                GridSync* sync, hipStream_t stream)
 {
-    hipError_t e = hipMemsetAsync(sync, 0, sizeof(GridSync), stream);
-    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fill_empty_slots, dim3(64), dim3(256), 0, stream, partials,
-                       grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D));
-    e = hipGetLastError();
+                       grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D), sync);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const size_t lds = (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge) * sizeof(double);
     const void* k = pick_grid_kernel(a.data, sampler_extended(a));
