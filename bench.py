@@ -138,9 +138,27 @@ def path_of(wl):
             "f32 row terms, f64 sums across groups and of the loss")
 
 
-def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, variants=None):
+def make_data(name, data, s):
+    """The library's device layout of the workload's data, and its seconds."""
+    import torch
+
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    _, _, Xd, yd, _ = data
+    t0 = time.time()
+    d = s.data(Xd, yd, per_chain=wl.per_chain_data)
+    torch.cuda.synchronize()
+    return d, time.time() - t0
+
+
+def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, variants=None, prepared=None):
     """--warmup untimed iterations, then exactly --steps timed ones resumed
-    from that state, every buffer on the device."""
+    from that state, every buffer on the device.  `prepared`: (d, layout
+    seconds) from make_data, else the layout is made here.  The line's rate
+    is over the whole call (HIP events around it); the roofline uses the
+    sampler kernel's own time (events the library records right around its
+    launch, which is what a kernel trace measures)."""
     import torch
 
     import paper_1912_11554_amd as nuts
@@ -152,11 +170,7 @@ def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, va
     steps = wl.num_samples if steps is None else steps
     warmup = wl.num_warmup if warmup is None else warmup
     C, D = wl.num_chains, wl.D
-    _, _, Xd, yd, _ = data
-    t0 = time.time()
-    d = s.data(Xd, yd, per_chain=wl.per_chain_data)
-    torch.cuda.synchronize()
-    layout_s = time.time() - t0
+    d, layout_s = prepared if prepared is not None else make_data(name, data, s)
     path, kernel, accumulate = path_of(wl)
     kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, seed=wl.seed,
               prior_scale=wl.prior_scale, num_chains=C, path=path, **(variants or {}))
@@ -188,11 +202,12 @@ def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, va
     w0 = time.perf_counter()
     ev0.record(stream)
     r = d.sample(num_warmup=0, num_samples=steps, init_q=q, first_iter=warmup + 1,
-                 inv_mass=inv_mass, out_samples=samples, out_stats=stats, **outs, **kw)
+                 inv_mass=inv_mass, out_samples=samples, out_stats=stats, time_kernel=True, **outs, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     gpu_s = ev0.elapsed_time(ev1) / 1e3
+    kernel_s = r["kernel_ms"] / 1e3
     st = stats.cpu().numpy().reshape(C, steps, -1).view(nuts.STATS_DTYPE)[..., 0]
     draws = samples.cpu().numpy()
     evals = r["grad_evals"]
@@ -203,22 +218,22 @@ def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, va
            else effective_sample_size(draws))
     es = 8 if wl.dtype == "f64" else 4
     bytes_per_eval = wl.N * wl.D * es + wl.N
-    achieved = evals * bytes_per_eval / gpu_s / 1e9
+    achieved = evals * bytes_per_eval / kernel_s / 1e9
     # batched path: every chain of a 128-chain tile takes one leapfrog step
     # per pass until the tile's last chain is done; passes = the most
     # evaluations of any chain of the tile
     per_chain = 1 + st["num_steps"].sum(axis=1)
     passes = max(int(per_chain[t:t + 128].max()) for t in range(0, C, 128))
     flops_per_eval = 4.0 * wl.N * wl.D       # E = X q and G = X^T r, 2 flops per multiply-add
-    tflops = evals * flops_per_eval / gpu_s / 1e12
-    log(f"{name}: {steps} iterations x {C} chains, {evals} evaluations in {gpu_s * 1e3:.1f} ms GPU "
-        f"({wall * 1e3:.1f} ms wall): {evals / gpu_s:.0f} evals/s, {achieved:.0f} GB/s, "
-        f"{tflops:.1f} TFLOP/s")
+    tflops = evals * flops_per_eval / kernel_s / 1e12
+    log(f"{name}: {steps} iterations x {C} chains, {evals} evaluations in {gpu_s * 1e3:.2f} ms GPU "
+        f"({wall * 1e3:.2f} ms wall, sampler kernel {kernel_s * 1e3:.2f} ms): {evals / gpu_s:.0f} evals/s, "
+        f"kernel {achieved:.0f} GB/s, {tflops:.1f} TFLOP/s")
     return d, dict(
         workload=name, N=wl.N, D=wl.D, dtype=wl.dtype, chains=C, step_size=kw["step_size"],
         step_size_adapted=bool(adapt), variants=sorted(k for k, v in (variants or {}).items() if v),
         max_tree_depth=wl.max_tree_depth, steps=steps, warmup=warmup, grad_evals=evals,
-        gpu_seconds=gpu_s, wall_seconds=wall, layout_seconds=layout_s,
+        gpu_seconds=gpu_s, kernel_seconds=kernel_s, wall_seconds=wall, layout_seconds=layout_s,
         evals_per_s=evals / gpu_s, ms_per_step=1e3 * wall / steps,
         ess_min_timed_call=float(ess.min()), bytes_per_eval=bytes_per_eval, achieved_gbs=achieved,
         mean_tree_depth=float(st["tree_depth"].mean()),
@@ -226,7 +241,7 @@ def run_workload(name, data, s, stream, steps=None, warmup=None, adapt=False, va
         divergences=int(st["diverging"].sum()), accept_prob=float(st["accept_prob"].mean()),
         path=path, kernel=kernel, accumulate=accumulate, flops_per_eval=flops_per_eval,
         achieved_tflops=tflops, passes=passes, pass_fill=evals / (passes * C),
-        ms_per_pass=1e3 * gpu_s / passes,
+        ms_per_pass=1e3 * kernel_s / passes,
     )
 
 
@@ -355,7 +370,7 @@ def roofline(res):
                 "flops_per_eval": res["flops_per_eval"], "passes": res["passes"],
                 "pass_fill": round(res["pass_fill"], 4), "ms_per_pass": round(res["ms_per_pass"], 4)}
     if kernel == "sampler_wave_kernel" and traffic and "valu_instructions_per_eval" in traffic:
-        rate = traffic["valu_instructions_per_eval"] * res["evals_per_s"] / 1e9
+        rate = traffic["valu_instructions_per_eval"] * res["grad_evals"] / res["kernel_seconds"] / 1e9
         return {"kernel": kernel, "bound": "alu", "achieved": round(rate, 1), "peak": VALU_PEAK_GIPS,
                 "unit": "G VALU wave-instructions/s", "frac": round(rate / VALU_PEAK_GIPS, 4),
                 "traffic": traffic["bytes"], "traffic_detail": traffic,
@@ -479,10 +494,12 @@ def run_hmm(chains, steps, warmup):
     torch.cuda.synchronize()
     ev0.record(stream)
     r = s.hmm_sample(w, z, K, V, num_warmup=0, num_samples=steps, init_q=q0,
-                     first_iter=warmup + 1, out_samples=samples, out_stats=stats, **outs, **kw)
+                     first_iter=warmup + 1, out_samples=samples, out_stats=stats, time_kernel=True,
+                     **outs, **kw)
     ev1.record(stream)
     torch.cuda.synchronize()
     gpu_s = ev0.elapsed_time(ev1) / 1e3
+    kernel_s = r["kernel_ms"] / 1e3
     st = stats.cpu().numpy().reshape(chains, steps, -1).view(nuts.STATS_DTYPE)[..., 0]
     evals = r["grad_evals"]
     assert evals == int(st["num_steps"].sum()) + chains
@@ -497,7 +514,8 @@ def run_hmm(chains, steps, warmup):
                                mean_steps_per_iter=round(float(st1["num_steps"].mean()), 2),
                                divergences=int(st1["diverging"].sum())),
                 chains=chains, steps=steps, warmup=warmup, grad_evals=evals,
-                gpu_seconds=round(gpu_s, 4), evals_per_s=round(evals / gpu_s, 1),
+                gpu_seconds=round(gpu_s, 4), kernel_seconds=round(kernel_s, 5),
+                evals_per_s=round(evals / gpu_s, 1), kernel_evals_per_s=round(evals / kernel_s, 1),
                 mean_steps_per_iter=round(float(st["num_steps"].mean()), 2),
                 kernel="sampler_hmm_kernel")
 
@@ -550,7 +568,7 @@ def hmm_line(h, cpu):
     traffic = recorded_traffic(h["kernel"], h["workload"], h["grad_evals"])
     roof = None
     if traffic and "valu_instructions_per_eval" in traffic:
-        rate = traffic["valu_instructions_per_eval"] * h["evals_per_s"] / 1e9
+        rate = traffic["valu_instructions_per_eval"] * h["kernel_evals_per_s"] / 1e9
         roof = {"kernel": h["kernel"], "bound": "alu", "achieved": round(rate, 1),
                 "peak": VALU_PEAK_GIPS, "unit": "G VALU wave-instructions/s",
                 "frac": round(rate / VALU_PEAK_GIPS, 4), "traffic": traffic["bytes"],
@@ -711,12 +729,17 @@ def main():
 
     def one(name):
         data = load_workload(name)
-        d, res = run_workload(name, data, s, stream, args.steps, args.warmup, args.adapt, variants)
         wl = workloads.WORKLOADS[name]
+        prepared = make_data(name, data, s)
         extra = {}
+        # the full-protocol and standalone measurements first: the timed
+        # call then finds the device at the clocks of sustained work, as in
+        # any sampling run longer than the few milliseconds it lasts
         if not args.no_protocol and wl.num_chains == 1 and not wl.adapt_diag_mass:
-            extra["protocol"] = run_protocol(name, d, stream)
-            extra["standalone_grad"] = run_standalone(name, d, data[4], stream)
+            extra["protocol"] = run_protocol(name, prepared[0], stream)
+            extra["standalone_grad"] = run_standalone(name, prepared[0], data[4], stream)
+        d, res = run_workload(name, data, s, stream, args.steps, args.warmup, args.adapt, variants,
+                              prepared=prepared)
         d.free()
         return data, res, extra
 

@@ -199,6 +199,9 @@ typedef struct {
     int32_t _reserved;
     double target_accept;      /* NUTS_ADAPT_STEP_SIZE: target acceptance in (0, 1); 0 = 0.8 */
     double* out_step_size;     /* [C] step size in use at the end (the adapted one), or NULL */
+    double* out_kernel_ms;     /* [1] milliseconds between HIP events recorded on the handle's stream
+                                  right before the first sampler kernel launch and right after the
+                                  last (set-up kernels and read-backs excluded), or NULL */
 } nuts_sample_opts;
 
 /* Run num_chains chains for num_warmup + num_samples iterations on prepared

@@ -57,6 +57,7 @@ class _Opts(ctypes.Structure):
         ("_reserved", ctypes.c_int32),
         ("target_accept", ctypes.c_double),
         ("out_step_size", ctypes.c_void_p),
+        ("out_kernel_ms", ctypes.c_void_p),
     ]
 
 
@@ -257,7 +258,7 @@ class Sampler:
                    num_chains=1, seed=0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                    first_iter=0, adapt_step_size=False, target_accept=0.8,
                    uturn_generalized=False, subtree_merge=False, out_samples=None, out_stats=None,
-                   out_final_q=None, out_inv_mass=None, out_step_size=None):
+                   out_final_q=None, out_inv_mass=None, out_step_size=None, time_kernel=False):
         """NUTS on the semi-supervised HMM (one wavefront per chain).  Returns
         the same dict as ``Data.sample``; samples hold the logits (numpy
         unless device tensors are passed in the out_* arguments, which are
@@ -278,14 +279,16 @@ class Sampler:
         gev = np.zeros(1, dtype=np.int64)
         im = _as_f64(inv_mass)
         iq = _as_f64(init_q)
+        kms = np.zeros(1) if time_kernel else None
         opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), NUTS_PATH_AUTO,
-                     0, target_accept, _ptr(out_eps))
+                     0, target_accept, _ptr(out_eps), _ptr(kms))
         self._check(self._L.nuts_hmm_sample(
             self._h, _ptr(w), w.shape[0], _ptr(z), z.shape[0], K, V, flags, step_size, _ptr(im),
             max_tree_depth, num_warmup, num_samples, C, seed, _ptr(out_samples), _ptr(out_stats),
             ctypes.byref(opts)))
         return dict(samples=out_samples, stats=out_stats, final_q=final_q, inv_mass=out_im,
-                    step_size=out_eps, grad_evals=int(gev[0]))
+                    step_size=out_eps, grad_evals=int(gev[0]),
+                    kernel_ms=None if kms is None else float(kms[0]))
 
 
 def hmm_dim(K, V):
@@ -363,12 +366,14 @@ class Data:
                seed=0, prior_scale=1.0, inv_mass=None, adapt_diag_mass=False, init_q=None,
                first_iter=0, path=NUTS_PATH_AUTO, out_samples=None, out_stats=None,
                adapt_step_size=False, target_accept=0.8, uturn_generalized=False,
-               subtree_merge=False, out_final_q=None, out_inv_mass=None, out_step_size=None):
+               subtree_merge=False, out_final_q=None, out_inv_mass=None, out_step_size=None,
+               time_kernel=False):
         """Run the chains.  Returns a dict: samples [C, S, D], stats [C, S]
         (STATS_DTYPE), final_q [C, D], inv_mass [C, D], step_size [C] (in use
-        at the end: the adapted one with adapt_step_size), grad_evals.  Outputs
-        are numpy unless device tensors are passed in the out_* arguments
-        (then those are filled and returned)."""
+        at the end: the adapted one with adapt_step_size), grad_evals, and
+        with time_kernel the milliseconds of the sampler kernel launches
+        (kernel_ms).  Outputs are numpy unless device tensors are passed in
+        the out_* arguments (then those are filled and returned)."""
         C, D = num_chains, self.D
         flags = (NUTS_DATA_PER_CHAIN if self.num_sets > 1 else 0) | (
             NUTS_ADAPT_DIAG_MASS if adapt_diag_mass else 0) | (
@@ -385,11 +390,13 @@ class Data:
         gev = np.zeros(1, dtype=np.int64)
         im = _as_f64(inv_mass)
         iq = _as_f64(init_q)
+        kms = np.zeros(1) if time_kernel else None
         opts = _Opts(_ptr(iq), first_iter, _ptr(final_q), _ptr(out_im), _ptr(gev), path, 0,
-                     target_accept, _ptr(out_eps))
+                     target_accept, _ptr(out_eps), _ptr(kms))
         self.s._check(self.s._L.nuts_sample_data(
             self.s._h, self._d, flags, prior_scale, step_size, _ptr(im), max_tree_depth,
             num_warmup, num_samples, C, seed, _ptr(out_samples), _ptr(out_stats),
             ctypes.byref(opts)))
         return dict(samples=out_samples, stats=out_stats, final_q=final_q, inv_mass=out_im,
-                    step_size=out_eps, grad_evals=int(gev[0]))
+                    step_size=out_eps, grad_evals=int(gev[0]),
+                    kernel_ms=None if kms is None else float(kms[0]))

@@ -63,7 +63,25 @@ struct nuts_handle {
     // asynchronous copies ahead of one stream synchronisation
     void* pinned = nullptr;
     size_t pinned_bytes = 0;
+    // the events of nuts_sample_opts.out_kernel_ms, created on first use
+    hipEvent_t kev[2] = {nullptr, nullptr};
 };
+
+// The handle's two timing events (created on first use).
+static hipError_t handle_events(nuts_handle* h, hipEvent_t** out)
+{
+    for (int i = 0; i < 2; ++i) {
+        if (!h->kev[i]) {
+            hipError_t e = hipEventCreate(&h->kev[i]);
+            if (e != hipSuccess) {
+                h->kev[i] = nullptr;
+                return e;
+            }
+        }
+    }
+    *out = h->kev;
+    return hipSuccess;
+}
 
 static hipError_t handle_pinned(nuts_handle* h, size_t bytes, void** out)
 {
@@ -372,6 +390,11 @@ struct RunBuffers {
         if (flag) HIP_TRY(h, hipMemcpyAsync(fl, flag, sizeof(unsigned int), hipMemcpyDeviceToHost, s));
         HIP_TRY(h, hipStreamSynchronize(s));
         if (flag && *fl) return fail(h, NUTS_EDEVICE, "%s", flag_msg);
+        if (o.out_kernel_ms) {
+            float ms = 0.0f;
+            HIP_TRY(h, hipEventElapsedTime(&ms, h->kev[0], h->kev[1]));
+            *o.out_kernel_ms = ms;
+        }
         if (o.out_grad_evals) {
             unsigned long long tot = 0;
             for (int64_t c = 0; c < C; ++c) tot += ev[c];
@@ -476,6 +499,8 @@ void nuts_free(nuts_handle* h)
     if (h->pot_slots) (void)hipFree(h->pot_slots);
     if (h->evals) (void)hipFree(h->evals);
     if (h->pinned) (void)hipHostFree(h->pinned);
+    for (hipEvent_t ev : h->kev)
+        if (ev) (void)hipEventDestroy(ev);
     if (h->own_stream) (void)hipStreamDestroy(h->stream);
     delete h;
 }
@@ -885,8 +910,12 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
                   num_chains, seed, out_samples, out_stats);
     if (rc != NUTS_OK) return rc;
 
+    hipEvent_t* kev = nullptr;
+    if (o.out_kernel_ms) HIP_TRY(h, handle_events(h, &kev));
     if (path == NUTS_PATH_WAVE) {
+        if (kev) HIP_TRY(h, hipEventRecord(kev[0], s));
         HIP_TRY(h, launch_sampler_wave(a, s));
+        if (kev) HIP_TRY(h, hipEventRecord(kev[1], s));
     } else if (path == NUTS_PATH_BATCH) {
         // launches of up to kBatchMaxTiles tiles of 128 chains, the groups of
         // the device split evenly between the tiles of a launch
@@ -910,7 +939,9 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
             ac.chain_offset = c0;
             const int tiles = (int)((ac.num_chains + kBatchTileChains - 1) / kBatchTileChains);
             const int groups = h->num_cu / tiles;
-            HIP_TRY(h, launch_sampler_batch(ac, d->batch, tiles, groups, qbuf, P, L, sync, s));
+            HIP_TRY(h, launch_sampler_batch(ac, d->batch, tiles, groups, qbuf, P, L, sync, s,
+                                            kev && c0 == 0 ? kev[0] : nullptr));
+            if (kev) HIP_TRY(h, hipEventRecord(kev[1], s));
             unsigned int err = 0;
             HIP_TRY(h, hipMemcpyAsync(&err, &sync->error, sizeof err, hipMemcpyDeviceToHost, s));
             HIP_TRY(h, hipStreamSynchronize(s));
@@ -934,7 +965,8 @@ int nuts_sample_data(nuts_handle* h, const nuts_data* d, uint32_t flags, double 
             SamplerArgs ac = a;
             ac.num_chains = 1;
             ac.chain_offset = c;
-            HIP_TRY(h, launch_sampler_grid(ac, groups, part, res, sync, s));
+            HIP_TRY(h, launch_sampler_grid(ac, groups, part, res, sync, s, kev && c == 0 ? kev[0] : nullptr));
+            if (kev) HIP_TRY(h, hipEventRecord(kev[1], s));
             if (c + 1 < C) {
                 // the next chain's launch clears the flag: check this one's first
                 GridSync hs;
@@ -1016,7 +1048,11 @@ int nuts_hmm_sample(nuts_handle* h, const uint8_t* w, int64_t T, const uint8_t* 
     rc = rb.stage(h, a, flags, o, target_accept, step_size, inv_mass_diag, max_tree_depth, num_warmup, num_samples,
                   num_chains, seed, out_samples, out_stats);
     if (rc != NUTS_OK) return rc;
+    hipEvent_t* kev = nullptr;
+    if (o.out_kernel_ms) HIP_TRY(h, handle_events(h, &kev));
+    if (kev) HIP_TRY(h, hipEventRecord(kev[0], h->stream));
     const hipError_t e = launch_hmm_sampler(a, hv, h->stream);
+    if (kev && e == hipSuccess) HIP_TRY(h, hipEventRecord(kev[1], h->stream));
     if (e == hipErrorInvalidValue)
         return fail(h, NUTS_EUNSUPPORTED, "max_tree_depth %d: the HMM chain's LDS does not fit", max_tree_depth);
     HIP_TRY(h, e);

@@ -780,7 +780,7 @@ bool batch_sampler_supported(const BatchView& bv, int max_depth, int sub_merge, 
 }
 
 hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int tiles, int groups, float* qbuf,
-                                float* P, double* L, BatchSync* sync, hipStream_t stream)
+                                float* P, double* L, BatchSync* sync, hipStream_t stream, hipEvent_t at_launch)
 {
     hipError_t e = hipMemsetAsync(sync, 0, sizeof(BatchSync), stream);
     if (e != hipSuccess) return e;
@@ -793,6 +793,10 @@ hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int t
     if (!k) return hipErrorInvalidValue;
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)batch_sampler_lds(a));
     if (e != hipSuccess) return e;
+    if (at_launch) {
+        e = hipEventRecord(at_launch, stream);
+        if (e != hipSuccess) return e;
+    }
     return hipLaunchCooperativeKernel(k, dim3((unsigned)(tiles * groups)),
                                       dim3(kGroupWaves * kWave), args, (unsigned)batch_sampler_lds(a), stream);
 }

@@ -138,8 +138,10 @@ struct GridSync {
     unsigned int error;  // a wait timed out
     unsigned int pad[63];
 };
+// `at_launch` (optional): an event recorded right before the sampler kernel,
+// after the set-up kernel.
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
-                               GridSync* sync, hipStream_t stream);
+                               GridSync* sync, hipStream_t stream, hipEvent_t at_launch = nullptr);
 int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int num_cu);
 
 // ---------------------------------------------------------------------------
@@ -232,9 +234,10 @@ struct BatchSync {
 // Sampler on `tiles` tiles of `groups` groups (groups >= 128): chain slot i
 // of tile t is run by group t * groups + i.  qbuf holds [2][tiles * 128][192]
 // floats, P [2][tiles][groups][128][pw] floats, L [2][tiles][groups][128]
-// doubles.
+// doubles.  `at_launch` as for launch_sampler_grid.
 hipError_t launch_sampler_batch(const SamplerArgs& a, const BatchView& bv, int tiles, int groups, float* qbuf,
-                                float* P, double* L, BatchSync* sync, hipStream_t stream);
+                                float* P, double* L, BatchSync* sync, hipStream_t stream,
+                                hipEvent_t at_launch = nullptr);
 bool batch_sampler_supported(const BatchView& bv, int max_depth, int sub_merge, int num_cu);
 constexpr int kBatchQWidth = 192;
 

@@ -192,16 +192,20 @@ __device__ __forceinline__ bool stop_requested(const int* stop, int token)
     return false;
 }
 
+//
+// stream_blocks_from takes block `first` already loaded (its loads may still
+// be in flight), so that a caller can issue them before the position is
+// known; stream_blocks loads it itself.
 template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false>
-__device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
-                                              int64_t N, int64_t nb, int64_t first, int64_t stride,
-                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss,
-                                              const int* stop = nullptr, int token = 0)
+__device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const T* __restrict__ X,
+                                                   const uint8_t* __restrict__ y, int D, int64_t N, int64_t nb,
+                                                   int64_t first, int64_t stride, const double (&qv)[CPS],
+                                                   double (&acc)[CPS], double& loss, const int* stop = nullptr,
+                                                   int token = 0)
 {
     constexpr int R = BlockShape<T, S>::R;
     if (first >= nb) return;
     int64_t b = first;
-    BlockRegs<T, CPS, S> a = load_block<T, CPS, S, MASK>(X + b * D * R, y + b * R, D);
     if constexpr (PIPE) {
         const int64_t count = (nb - 1 - first) / stride + 1;  // blocks of this wave
         int64_t count_left = count;
@@ -240,6 +244,18 @@ __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uin
             b = nx;
         }
     }
+}
+
+template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false>
+__device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
+                                              int64_t N, int64_t nb, int64_t first, int64_t stride,
+                                              const double (&qv)[CPS], double (&acc)[CPS], double& loss,
+                                              const int* stop = nullptr, int token = 0)
+{
+    constexpr int R = BlockShape<T, S>::R;
+    if (first >= nb) return;
+    const BlockRegs<T, CPS, S> a = load_block<T, CPS, S, MASK>(X + first * D * R, y + first * R, D);
+    stream_blocks_from<T, CPS, S, PIPE, MASK, ABORT>(a, X, y, D, N, nb, first, stride, qv, acc, loss, stop, token);
 }
 
 // Lane that holds column c after reduce_rows<CPS, S>.

@@ -63,7 +63,7 @@ int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int nu
 }
 
 hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partials, double* result,
-                               GridSync* sync, hipStream_t stream)
+                               GridSync* sync, hipStream_t stream, hipEvent_t at_launch)
 {
     hipLaunchKernelGGL(fill_empty_slots, dim3(64), dim3(256), 0, stream, partials,
                        grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D), sync);
@@ -73,6 +73,10 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
     const void* k = pick_grid_kernel(a.data, sampler_extended(a));
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
+    if (at_launch) {
+        e = hipEventRecord(at_launch, stream);
+        if (e != hipSuccess) return e;
+    }
     SamplerArgs A = a;
     void* args[] = {&A, &groups, &partials, &result, &sync};
     return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);

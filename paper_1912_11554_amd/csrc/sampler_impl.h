@@ -134,6 +134,12 @@ constexpr int kCmdEval = 1, kCmdExit = 2;
 template <typename T>
 constexpr bool kGridPipe = sizeof(T) == 4;
 
+// The grid workers load the first block of their share before the position
+// arrives (fp32: 0.7 % faster per evaluation on the 581,012 x 55 set; fp64:
+// 3 % slower, the held block costs registers beside the exchange code).
+template <typename T>
+constexpr bool kGridPrefetch = sizeof(T) == 4;
+
 template <int DPL, int NW>
 struct GridShared {
     static constexpr int W = 64 * (DPL + 1);  // partial_width(D)
@@ -268,7 +274,7 @@ __device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < 
 // and empties nothing, so the next one reuses its step.
 template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
 __device__ int grid_begin(const GridCtx& c, GridShared<DPL, NW>& sh, const double (&q)[DPL], int cmd_in,
-                          int gen_in, int* gen_out)
+                          int gen_in, int* gen_out, const BlockRegs<T, CPS, S>* first_block = nullptr)
 {
     const int l = lane();
     const int wave = threadIdx.x / kWave;
@@ -295,10 +301,15 @@ __device__ int grid_begin(const GridCtx& c, GridShared<DPL, NW>& sh, const doubl
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
         const int workers = NW - 1;
-        stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>((const T*)c.X, c.y, D, c.N, c.nb,
-                                                                  (int64_t)g * workers + (wave - 1),
-                                                                  (int64_t)G * workers, qv, acc, loss,
-                                                                  &sh.stop, *gen_out);
+        if constexpr (kGridPrefetch<T>)
+            stream_blocks_from<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>(
+                *first_block, (const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
+                (int64_t)G * workers, qv, acc, loss, &sh.stop, *gen_out);
+        else
+            stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>((const T*)c.X, c.y, D, c.N, c.nb,
+                                                                      (int64_t)g * workers + (wave - 1),
+                                                                      (int64_t)G * workers, qv, acc, loss,
+                                                                      &sh.stop, *gen_out);
         if constexpr (S <= 8 && CPS == 8) {
             const double col = finish_pass<CPS, S>(acc, loss);
             if (l < D) sh.red[wave][l] = col;
@@ -1188,10 +1199,27 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
         double q[DPL], r[DPL + 1];
 #pragma unroll
         for (int m = 0; m < DPL; ++m) q[m] = 0.0;
+        // kGridPrefetch: the first block of the wave's share does not depend
+        // on the position, so its loads are issued while the wave waits for
+        // the next command (they land during the exchange and the
+        // controller's step) and every collective starts on a block already
+        // in registers.
+        constexpr int R = BlockShape<T, S>::R;
+        const int64_t first = (int64_t)blockIdx.x * (kGridWaves - 1) + (wave - 1);
+        const int64_t fb = first < c.nb ? first : 0;  // a valid block either way
+        const T* Xf = (const T*)c.X + fb * c.D * R;
+        const uint8_t* yf = c.y + fb * R;
         for (;;) {
             bool ab;
             int gen = 0;
-            if (grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen) == kCmdExit) break;
+            int cmd;
+            if constexpr (kGridPrefetch<T>) {
+                const BlockRegs<T, CPS, S> pre = load_block<T, CPS, S, kGridPipe<T>>(Xf, yf, c.D);
+                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen, &pre);
+            } else {
+                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen);
+            }
+            if (cmd == kCmdExit) break;
             if (grid_end<T, S, CPS, DPL, kGridWaves, true>(c, sh, step, gen, false, r, &ab)) step++;
         }
     }

@@ -232,3 +232,26 @@ def test_grid_fp32_wide_rows(sampler, orc, D):
     # row's fp32-evaluated loss carries about 3e-8 absolute error, so with no
     # cancellation between the two sums H - H0 is off by at most 3e-8 N
     compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6, accept_atol=3e-8 * N)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_kernel_time_is_reported(sampler, path):
+    # nuts_sample_opts.out_kernel_ms: events around the sampler kernel alone,
+    # so positive and no longer than the whole call; the draws are the same
+    # with and without the timing
+    import time
+    wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
+    X, y = workloads.make_workload(wl)
+    say("kernel time path", path)
+    d = sampler.data(X, y)
+    kw = dict(step_size=wl.step_size, max_tree_depth=wl.max_tree_depth, num_warmup=5, num_samples=20,
+              seed=wl.seed, path=path)
+    r0 = d.sample(**kw)
+    t0 = time.perf_counter()
+    r1 = d.sample(time_kernel=True, **kw)
+    wall_ms = (time.perf_counter() - t0) * 1e3
+    d.free()
+    assert r0["kernel_ms"] is None
+    assert 0.0 < r1["kernel_ms"] <= wall_ms
+    np.testing.assert_array_equal(r0["samples"], r1["samples"])
+    assert r0["grad_evals"] == r1["grad_evals"]
