@@ -442,8 +442,23 @@ struct GridEval {
     __device__ bool out_writer() const { return blockIdx.x == 0; }
     __device__ bool aborted() const { return abort; }
 
+    // A called-off collective's second barrier, which the workers wait at
+    // once they have stopped: the controller takes it at its next command
+    // (it finishes the iteration meanwhile), never before the workers could
+    // read the stop word.
+    bool owed = false;
+
+    __device__ void pay_barrier()
+    {
+        if (owed) {
+            __syncthreads();
+            owed = false;
+        }
+    }
+
     __device__ void begin(const double (&q)[DPL])
     {
+        pay_barrier();
         int gn;
         grid_begin<T, S, CPS, DPL, NW, false>(c, *sh, q, kCmdEval, ++gen, &gn);
     }
@@ -469,9 +484,10 @@ struct GridEval {
 
     __device__ void cancel()
     {
-        double r[DPL + 1];
-        bool ab = false;
-        grid_end<T, S, CPS, DPL, NW, false>(c, *sh, step, gen, true, r, &ab);
+        // the stop word, as grid_end stores it for a called-off collective;
+        // the barrier after it is taken at the next command
+        if (lane() == 0) __hip_atomic_store(&sh->stop, gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        owed = true;
     }
 
     __device__ void eval(const double (&q)[DPL], double& U, double (&g)[DPL])
@@ -482,6 +498,7 @@ struct GridEval {
 
     __device__ void finish()
     {
+        pay_barrier();
         double q[DPL];
 #pragma unroll
         for (int m = 0; m < DPL; ++m) q[m] = 0.0;
@@ -695,15 +712,41 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         if (A.adapt_diag) win.init(A.num_warmup);
     }
 
+    // An iteration's draws: the momentum's standard normals (component l +
+    // 64 m in lane l) and, one doubling per lane, the direction bit and the
+    // merge uniform.  None depends on the chain's state, so with a
+    // speculative evaluator the next iteration's are drawn while the first
+    // leaf of this one is evaluated, off the path between iterations.
+    struct IterDraws {
+        double xi[DPL];
+        int dir_bit;
+        double u_merge;
+    };
+    const auto draw_iteration = [&](uint64_t t, IterDraws& dr) {
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) dr.xi[m] = act[m] ? momentum_normal(seed, key_chain, t, l + 64 * m) : 0.0;
+        dr.dir_bit = 0;
+        dr.u_merge = 0.0;
+        if (l < maxd) {
+            dr.dir_bit = (int)(draw(seed, key_chain, t, kTagDirection, (uint64_t)l, 0).w0 & 1ull);
+            dr.u_merge = unit53(draw(seed, key_chain, t, kTagMerge, (uint64_t)l, 0).w0);
+        }
+    };
+    IterDraws next_draws;
+    bool have_next = false;
+
     for (int64_t k = 0; k < iters && !ev.aborted(); ++k) {
         const uint64_t t = (uint64_t)(A.first_iter + k);
+        IterDraws dr;
+        if (Eval::kSpeculative && have_next) dr = next_draws;
+        else draw_iteration(t, dr);
+        have_next = false;
 
         // momentum and initial energy
         double kin = 0.0;
 #pragma unroll
         for (int m = 0; m < DPL; ++m) {
-            const double xi = act[m] ? momentum_normal(seed, key_chain, t, l + 64 * m) : 0.0;
-            cur.p[m] = act[m] ? xi / sqrt(im[m]) : 0.0;
+            cur.p[m] = act[m] ? dr.xi[m] / sqrt(im[m]) : 0.0;
             kin += im[m] * cur.p[m] * cur.p[m];
         }
         const double H0 = cur.U + 0.5 * wave_sum(kin);
@@ -711,15 +754,8 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
 #pragma unroll
         for (int m = 0; m < DPL; ++m) rho_traj[m] = cur.p[m];
 
-        // per-iteration draws, one doubling per lane: direction bits and the
-        // merge uniforms
-        int dir_bit = 0;
-        double u_merge = 0.0;
-        if (l < maxd) {
-            dir_bit = (int)(draw(seed, key_chain, t, kTagDirection, (uint64_t)l, 0).w0 & 1ull);
-            u_merge = unit53(draw(seed, key_chain, t, kTagMerge, (uint64_t)l, 0).w0);
-        }
-        const uint64_t dirmask = __ballot(dir_bit);
+        const double u_merge = dr.u_merge;
+        const uint64_t dirmask = __ballot(dr.dir_bit);
 
         Node<DPL> left = cur, right = cur, prop = cur;
         // a speculative evaluation: the next leapfrog position, handed to the
@@ -766,6 +802,10 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     leapfrog_drift<DPL>(z.q, z.p, z.g, h, im, ph, z.q);
                     if (!pend) ev.begin(z.q);
                     pend = false;
+                    if (nleaves == 0 && k + 1 < iters) {
+                        draw_iteration(t + 1, next_draws);  // while the first leaf streams
+                        have_next = true;
+                    }
                     ev.end(z.q, z.U, z.g);
                 } else {
 #pragma unroll
