@@ -70,14 +70,17 @@ hipError_t launch_to_blocks(const void* X_rowmajor, const uint8_t* y_in, DataVie
                             void* X_out, uint8_t* y_out, unsigned int* bad_label,
                             hipStream_t stream);
 
-// Workspace of the batched potential/gradient: partial-sum slots
-// [K][G][width] doubles, every slot marked empty (mark_partials_empty)
-// before the first launch; each launch leaves every slot it used empty again.
+// Workspace of the batched potential/gradient: K * G * width doubles of
+// partial-sum slots (item k's used columns c = 0..D, the loss last, as rows
+// of G group slots at k * G * width + c * G), every slot marked empty
+// (mark_partials_empty) before the first launch; each launch leaves every
+// slot it used empty again.
 struct PotentialPlan {
     int groups_per_item;  // G
     int width;            // partial_width(D)
 };
 constexpr int kMaxPotentialItems = 65535;
+constexpr int kMaxPotentialGroups = 256;  // groups per item
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu);
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
                                  const PotentialPlan& plan, double* partials, double* out_U, double* out_grad,

@@ -2,15 +2,17 @@
 // in one launch.  A grid of (G groups) x (K items); the NW waves of a group
 // (8 for fp32 rows and wide fp64 rows, 16 for fp64 rows of at most 8 column
 // slots) stream the blocks b = g * NW + w, g * NW + w + G * NW, ... of their
-// item's data set, the group adds its waves' column sums in wave order and
-// stores one fp64 partial row of width partial_width(D) (columns 0..D-1, the
-// loss at 64 * ceil(D / 64)) into its slots, and every group but the item's
-// first is done.  The first group, once its own rows are in, gathers the G
-// partial rows: each slot holds a signalling-NaN pattern until it is written,
-// so the gatherer waits on the values themselves (no counter, no ordering
-// point between a group's stores and a count).  It adds them in a fixed
-// order, adds the Gaussian prior terms, writes U and grad U, and marks every
-// slot it read empty again for the next call.  No floating-point atomics
+// item's data set, and the group adds its waves' column sums in wave order
+// and stores its partial of each used column (the D gradient columns, then
+// the loss) as one row of slots.  The used columns are cut into tiles of 16
+// (one 128-byte line of each row); group g of the item owns the tiles g,
+// g + G, ...: each slot holds a signalling-NaN pattern until it is written,
+// so the owner's threads wait on the values themselves (no counter, no
+// ordering point between a group's stores and a count).  The owner adds the
+// G rows of each of its columns in a fixed order, adds the Gaussian prior
+// term, writes its outputs (components of grad U, and U) and then marks the
+// slots empty again for the next call.  One hop between groups per call;
+// every transfer between groups moves whole lines; no floating-point atomics
 // anywhere, so results are bitwise reproducible.
 #include <algorithm>
 #include <mutex>
@@ -46,7 +48,6 @@ template <typename T, int S, int CPS>
 constexpr bool pot_pipe() { return pot_waves<T, S, CPS>() == 8 || S > 1; }
 template <int S, int CPS>
 constexpr bool pot_mask() { return S >= 16; }
-static_assert(kMaxDim + 1 <= 8 * kWave, "one thread per used column in the final sum");
 
 // A slot not written yet: a signalling-NaN bit pattern that no arithmetic
 // produces (sums of finite or non-finite values give quiet NaNs).
@@ -54,11 +55,6 @@ constexpr unsigned long long kEmptyPartial = 0x7FF4DEADBEEF0002ull;
 // about 2 s of the 100 MHz constant clock: a slot that stays empty that long
 // means another call overlapped this one on the device
 constexpr uint64_t kGatherWaitTicks = 200000000ull;
-// slots a gathering thread has in flight at once: enough for every slot of
-// the covtype-sized shapes (G = 256 groups, D + 1 = 56 used columns) in one
-// batch, 32 with 512 threads, 16 with 1024
-template <int NW>
-constexpr int gather_batch() { return NW == 16 ? 16 : 32; }
 
 __device__ __forceinline__ void store_agent(double* p, double v)
 {
@@ -81,8 +77,12 @@ __global__ void __launch_bounds__(256) fill_empty_kernel(unsigned long long* __r
         p[i] = kEmptyPartial;
 }
 
+// The 8-wave shapes run two waves per SIMD (one group per CU), so the
+// compiler may give a lane up to 256 registers: left to aim at four waves
+// per SIMD it squeezed the fp32 stream into 120 and the pass ran slower.
 template <typename T, int S, int CPS>
-__global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave)) potential_grad_kernel(
+__global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave))
+    __attribute__((amdgpu_waves_per_eu(1, pot_waves<T, S, CPS>() == 8 ? 2 : 4))) potential_grad_kernel(
     DataView dv, const double* __restrict__ W, int G, int width, double* __restrict__ partials,
     double prior_scale, double* __restrict__ out_U, double* __restrict__ out_grad)
 {
@@ -119,120 +119,146 @@ __global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave)) potential_gr
     }
     if (threadIdx.x == 0) failed = 0;
     __syncthreads();  // per-wave sums in LDS
+    // Row g of the item's slots (at item + g * width) holds the group's
+    // partial of each used column: columns 0..D-1, the loss at D, then zeros
+    // up to a whole number of 128-byte lines, so that every store and every
+    // read between groups moves whole lines (a partial-line write to HBM is
+    // a read-modify-write, and those slowed the other groups' streams).
+    constexpr int kLine = 16;  // doubles in a 128-byte line
+    const int used = D + 1;
+    const int ntiles = (used + kLine - 1) / kLine;
     double* item = partials + k * G * width;
     if (wave == 0) {
-        double* mine = item + (int64_t)g * width;
-        for (int col = l; col < width; col += 64) {
-            if (col < D || col == loss_slot) {
-                double s = 0.0;
+        double* row = item + (int64_t)g * width;
+        for (int col = l; col < ntiles * kLine; col += 64) {
+            const int src = col < D ? col : (col == D ? loss_slot : -1);
+            double s = 0.0;
+            if (src >= 0) {
 #pragma unroll
-                for (int w = 0; w < NW; ++w) s += part[w * width + col];
-                store_agent(mine + col, s);
+                for (int w = 0; w < NW; ++w) s += part[w * width + src];
             }
+            store_agent(row + col, s);
         }
     }
-    if (g != 0) return;
-
-    // The item's first group gathers.  Thread t takes used column c = t mod
-    // (D + 1) (column c < D, or the loss for c = D) of the groups j, j + J,
-    // j + 2 J, ... (j = t div (D + 1), J sets) in increasing order, waiting on
-    // each slot until it holds a value.
-    const int used = D + 1;
+    // Group g owns the tiles g, g + G, ... (tile j: used columns 16 j ..
+    // 16 j + 15).  Its thread t takes column i = t mod 16 of the tile in rows
+    // t / 16, t / 16 + RS, ... (RS = threads / 16), so that each load and
+    // store of a wave covers whole lines, and waits for those slots; the
+    // group adds the G rows of each column in a fixed order (each thread its
+    // rows in order, then the four lanes of a wave that share the column,
+    // then the waves in order) and writes the outputs, and only then marks
+    // the slots empty again for the next call.
+    constexpr int NT = NW * kWave;
+    constexpr int RS = NT / kLine;
+    constexpr int kMaxRows = (kMaxPotentialGroups + RS - 1) / RS;
+    const int mine = g < ntiles ? (ntiles - 1 - g) / G + 1 : 0;
+    if (mine == 0) return;  // uniform over the group
     const int t = threadIdx.x;
-    const int sets = (NW * kWave) / used;
-    const int j = t / used;
-    const int c = t - j * used;
-    constexpr int kGatherBatch = gather_batch<NW>();
-    double s = 0.0;
-    bool ok = true;
-    if (j < sets) {
-        double* src = item + (c < D ? c : loss_slot);
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        for (int g0 = j; g0 < G; g0 += kGatherBatch * sets) {
-            unsigned long long v[kGatherBatch];
-#pragma unroll
-            for (int i = 0; i < kGatherBatch; ++i) {
-                const int gg = g0 + i * sets;
-                v[i] = gg < G ? load_bits(src + (int64_t)gg * width) : 0ull;
-            }
-            for (;;) {
-                bool pending = false;
-#pragma unroll
-                for (int i = 0; i < kGatherBatch; ++i) {
-                    const int gg = g0 + i * sets;
-                    if (gg < G && v[i] == kEmptyPartial) {
-                        v[i] = load_bits(src + (int64_t)gg * width);
-                        pending = true;
-                    }
-                }
-                if (!pending) break;
-                if (__builtin_amdgcn_s_memrealtime() - t0 > kGatherWaitTicks) {
-                    ok = false;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(2);
-            }
-#pragma unroll
-            for (int i = 0; i < kGatherBatch; ++i) {
-                const int gg = g0 + i * sets;
-                if (gg < G) {
-                    s += __builtin_bit_cast(double, v[i]);
-                    empty_slot(src + (int64_t)gg * width);  // for the next call
-                }
-            }
-        }
-    }
-    if (!ok) __hip_atomic_store(&failed, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    __syncthreads();  // no wave reads its LDS row any more
-    if (j < sets) part[j * used + c] = s;
-    __syncthreads();  // per-set sums in LDS
-    if (wave != 0) return;
-    // a slot that never filled: another call overlapped this one; the
-    // results are NaN (every slot this group read is empty again)
-    const double bad = failed ? __builtin_nan("") : 0.0;
+    const int ic = t & (kLine - 1);
+    const int r0 = t / kLine;
     const double inv_s2 = 1.0 / (prior_scale * prior_scale);
-    double pr = 0.0;
-    double lossv = 0.0;
-    for (int col = l; col < used; col += 64) {
-        double tot = 0.0;
-        for (int jj = 0; jj < sets; ++jj) tot += part[jj * used + col];
-        if (col < D) {
-            const double w = W[k * D + col];
-            pr += 0.5 * w * w * inv_s2;
-            out_grad[k * D + col] = tot + w * inv_s2 + bad;
-        } else {
-            lossv = tot;
+    __syncthreads();  // the waves' rows are consumed: LDS is reused below
+    for (int jt = 0; jt < mine; ++jt) {
+        const int c0 = (g + jt * G) * kLine;
+        const int col = c0 + ic;
+        // what the outputs add besides the sums, read before the wait
+        double extra = 0.0;
+        if (col < D) extra = W[k * D + col] * inv_s2;
+        if (wave == 0 && c0 <= D && D < c0 + kLine) {
+            double pr = 0.0;
+            for (int j = l; j < D; j += kWave) pr += 0.5 * W[k * D + j] * W[k * D + j] * inv_s2;
+            const double prior = wave_sum(pr) + (double)D * (log(prior_scale) + kHalfLog2Pi);
+            if (col == D) extra = prior;
         }
+        // (one poll of the thread's slots at a time: more polls in flight, a
+        // fraction of a round trip apart, made the slots arrive later)
+        unsigned long long v[kMaxRows];
+#pragma unroll
+        for (int m = 0; m < kMaxRows; ++m) {
+            const int r = r0 + m * RS;
+            v[m] = r < G ? load_bits(item + (int64_t)r * width + col) : 0ull;  // 0: +0.0
+        }
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        for (;;) {
+            bool pending = false;
+#pragma unroll
+            for (int m = 0; m < kMaxRows; ++m) {
+                const int r = r0 + m * RS;
+                if (r < G && v[m] == kEmptyPartial) {
+                    v[m] = load_bits(item + (int64_t)r * width + col);
+                    pending = true;
+                }
+            }
+            if (!pending) break;
+            if (__builtin_amdgcn_s_memrealtime() - t0 > kGatherWaitTicks) {
+                // another call overlapped this one: the results are NaN
+                __hip_atomic_store(&failed, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+                for (int m = 0; m < kMaxRows; ++m) v[m] = v[m] == kEmptyPartial ? 0ull : v[m];
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        double s = 0.0;
+#pragma unroll
+        for (int m = 0; m < kMaxRows; ++m) s += __builtin_bit_cast(double, v[m]);
+        s += xor_move<16>(s);
+        s += xor_move<32>(s);
+        if (l < kLine) part[wave * kLine + l] = s;
+        __syncthreads();  // the waves' sums (and any failure) in LDS
+        if (t < kLine && col <= D) {
+            double tot = 0.0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += part[w * kLine + t];
+            const double bad = failed ? __builtin_nan("") : 0.0;
+            if (col < D) out_grad[k * D + col] = tot + extra + bad;
+            else out_U[k] = tot + extra + bad;
+        }
+#pragma unroll
+        for (int m = 0; m < kMaxRows; ++m) {
+            const int r = r0 + m * RS;
+            if (r < G) empty_slot(item + (int64_t)r * width + col);  // for the next call
+        }
+        __syncthreads();  // part[] is reused by the next tile
     }
-    const double prior = wave_sum(pr);
-    lossv = readlane_f64(lossv, D & 63);  // column D sits in lane D mod 64
-    if (l == 0) out_U[k] = lossv + prior + (double)D * (log(prior_scale) + kHalfLog2Pi) + bad;
 }
 
+// The 8-wave shapes use at most 128 registers a lane, so two of their groups
+// would fit in one CU, and the dispatcher does place two groups on one CU
+// while another CU idles (the pass over the 581,012 x 55 fp32 set ran about
+// 8 % slower that way).  Asking for more than half of a CU's 160 KiB of LDS
+// gives every group a CU of its own, as the sizing of the grid assumes.
+constexpr size_t kOwnCuLds = 96 * 1024;
+
 template <typename T, int S, int CPS>
-void enqueue(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-             double* partials, double* out_U, double* out_grad, hipStream_t stream)
+hipError_t enqueue(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
+                   double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
     constexpr int NW = pot_waves<T, S, CPS>();
-    hipLaunchKernelGGL((potential_grad_kernel<T, S, CPS>), dim3(G, (unsigned)K), dim3(NW * kWave),
-                       (size_t)NW * width * sizeof(double), stream, dv, W, G, width, partials, prior_scale,
-                       out_U, out_grad);
+    size_t lds = (size_t)NW * width * sizeof(double);
+    if (NW == 8 && lds < kOwnCuLds) lds = kOwnCuLds;
+    const void* k = (const void*)potential_grad_kernel<T, S, CPS>;
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((potential_grad_kernel<T, S, CPS>), dim3(G, (unsigned)K), dim3(NW * kWave), lds, stream, dv,
+                       W, G, width, partials, prior_scale, out_U, out_grad);
+    return hipGetLastError();
 }
 
 template <typename T>
-void enqueue_shape(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-                   double* partials, double* out_U, double* out_grad, hipStream_t stream)
+hipError_t enqueue_shape(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
+                         double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
     const int D = dv.D;
 #define NUTS_POT(S_, C_) \
-    enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, out_U, out_grad, stream)
+    return enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, out_U, out_grad, stream)
     if (D <= 8) NUTS_POT(1, 8);
-    else if (D <= 16) NUTS_POT(1, 16);
-    else if (D <= 32) NUTS_POT(4, 8);
-    else if (D <= 64) NUTS_POT(8, 8);
-    else if (D <= 128) NUTS_POT(16, 8);
-    else if (D <= 256) NUTS_POT(32, 8);
-    else NUTS_POT(32, 10);
+    if (D <= 16) NUTS_POT(1, 16);
+    if (D <= 32) NUTS_POT(4, 8);
+    if (D <= 64) NUTS_POT(8, 8);
+    if (D <= 128) NUTS_POT(16, 8);
+    if (D <= 256) NUTS_POT(32, 8);
+    NUTS_POT(32, 10);
 #undef NUTS_POT
 }
 
@@ -328,6 +354,7 @@ PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
     int64_t want = ((int64_t)num_cu + K - 1) / K;
     int64_t most = (dv.nb + 15) / 16;
     if (want > most) want = most;
+    if (want > kMaxPotentialGroups) want = kMaxPotentialGroups;
     if (want < 1) want = 1;
     return PotentialPlan{(int)want, partial_width(dv.D)};
 }
@@ -337,12 +364,10 @@ hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const d
                                  hipStream_t stream)
 {
     if (dv.dtype == NUTS_F64)
-        enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
-                              stream);
-    else
-        enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
-                             stream);
-    return hipGetLastError();
+        return enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U,
+                                     out_grad, stream);
+    return enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
+                                stream);
 }
 
 }  // namespace nuts

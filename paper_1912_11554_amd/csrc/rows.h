@@ -71,9 +71,42 @@ struct BlockRegs {
     Y y;
 };
 
+// An empty instruction that reads and rewrites a loaded block's registers:
+// the compiler waits for the block's loads right there and cannot move work
+// that uses them above it.  The stream loop below places it after the
+// computation of the other block, so that the loads stay in flight across
+// that computation whatever the scheduler would otherwise choose (left to
+// itself it has converted a block right after issuing its loads, waiting for
+// them at once, when the kernel around the loop changed).
+template <typename V>
+__device__ __forceinline__ void hold_value(V& v)
+{
+    if constexpr (sizeof(V) == 8) {
+        uint64_t u = __builtin_bit_cast(uint64_t, v);
+        asm volatile("" : "+v"(u));
+        v = __builtin_bit_cast(V, u);
+    } else {
+        static_assert(sizeof(V) == 16, "8- or 16-byte column slots");
+        struct U2 { uint64_t a, b; };
+        U2 u = __builtin_bit_cast(U2, v);
+        asm volatile("" : "+v"(u.a), "+v"(u.b));
+        v = __builtin_bit_cast(V, u);
+    }
+}
+
 __device__ __forceinline__ void set_zero(float2& v) { v = make_float2(0.0f, 0.0f); }
 __device__ __forceinline__ void set_zero(double2& v) { v = make_double2(0.0, 0.0); }
 __device__ __forceinline__ void set_zero(double& v) { v = 0.0; }
+
+template <typename T, int CPS, int S>
+__device__ __forceinline__ void hold_block(BlockRegs<T, CPS, S>& b)
+{
+#pragma unroll
+    for (int k = 0; k < CPS; ++k) hold_value(b.x[k]);
+    uint32_t y = b.y;
+    asm volatile("" : "+v"(y));
+    b.y = (typename BlockRegs<T, CPS, S>::Y)y;
+}
 
 // Issue the loads of one block.  By default the loads are unconditional: a
 // slot past column D - 1 reads the next block's memory (or the zeroed tail of
@@ -217,16 +250,25 @@ __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const
                 break;
             }
             const int64_t b1 = b + stride, b2 = b1 + stride;
-            const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            __builtin_amdgcn_sched_barrier(0);  // the loads are issued before the computation
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+            __builtin_amdgcn_sched_barrier(0);  // and it is done before the wait for the loads
+            hold_block(c);
             a = load_block<T, CPS, S, MASK>(X + b2 * D * R, y + b2 * R, D);
+            __builtin_amdgcn_sched_barrier(0);
             compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
+            __builtin_amdgcn_sched_barrier(0);
+            hold_block(a);
             b = b2;
         }
         if (i < count_left) {
             const int64_t b1 = b + stride;
-            const BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            BlockRegs<T, CPS, S> c = load_block<T, CPS, S, MASK>(X + b1 * D * R, y + b1 * R, D);
+            __builtin_amdgcn_sched_barrier(0);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
+            __builtin_amdgcn_sched_barrier(0);
+            hold_block(c);
             compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
         } else {
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
