@@ -170,8 +170,11 @@ __device__ __forceinline__ void store_stage(const StageRegs& r, int tid, float* 
 // they add nothing).
 //
 // `flip` reverses the pair order: the two waves that share a SIMD (loader
-// index w and w + 4) take the pairs in opposite orders, so that one is on
-// the matrix core while the other evaluates its row terms.
+// index w and w + 4) take the pairs in opposite orders.  Each wave raises its
+// issue priority while it feeds the matrix core and lowers it for the row
+// terms: left to the default (the older wave first), the younger wave of a
+// SIMD fell a third behind within each stage and the older one waited for it
+// at the stage barrier.
 template <int KT>
 __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, const float* __restrict__ ys,
                                               const WaveQ& Q, WaveAcc& acc, bool flip)
@@ -191,6 +194,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
         const float* x1 = x0 + kTileRows * G::RS;
         v4f e0 = {0.0f, 0.0f, 0.0f, 0.0f};
         v4f e1 = {0.0f, 0.0f, 0.0f, 0.0f};
+        __builtin_amdgcn_s_setprio(2);
 #pragma unroll
         for (int t = 0; t < G::KP; ++t) {
             const v4f a0 = *reinterpret_cast<const v4f*>(x0 + e_off + e_step * t);
@@ -201,6 +205,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
                 e1 = mfma(a1[i], Q.q[4 * t + i], e1);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         // tail slots of this lane's four rows 4 jj + r of both tiles
         v4f xr0[4], xr1[4];
 #pragma unroll
@@ -222,6 +227,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
             lsum += l0 + l1;
         }
         acc.loss += (double)lsum;
+        __builtin_amdgcn_s_setprio(2);
         // G: residue m of row 4 jj + r holds chunks 4 h .. 4 h + 3 in piece h
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -243,6 +249,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
                     if (4 * h + i < KT) acc.g[4 * h + i] = mfma(b1[i], r1[r], acc.g[4 * h + i]);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int k = 0; k < kTail; ++k) {
             acc.gt[k] += ((xr0[0][k] * r0[0] + xr0[1][k] * r0[1]) + xr0[2][k] * r0[2]) + xr0[3][k] * r0[3];

@@ -587,36 +587,31 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
 #pragma unroll
         for (int mm = 0; mm <= DPL; ++mm) s[mm] = 0.0;
         // every load of a wave's share in flight at once: one round trip for
-        // up to 16 groups per wave (144 groups of 9 waves)
+        // up to 16 groups per wave (144 groups of 9 waves); a group past the
+        // last re-reads the wave's first group and is not added
         constexpr int B = 16;
-        int g = wave;
-        for (; g + (B - 1) * kGroupWaves < c.groups; g += B * kGroupWaves) {
+        for (int g0 = wave; g0 < c.groups; g0 += B * kGroupWaves) {
             float v[B][DPL];
             double lv[B];
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const int64_t gg = g + b * kGroupWaves;
+                const int gg = g0 + b * kGroupWaves;
+                const int64_t gq = gg < c.groups ? gg : g0;
 #pragma unroll
                 for (int mm = 0; mm < DPL; ++mm) {
                     const int col = l + 64 * mm;
-                    v[b][mm] = col < c.bv.D ? load_f(src + gg * rstride + col) : 0.0f;
+                    v[b][mm] = col < c.bv.D ? load_f(src + gq * rstride + col) : 0.0f;
                 }
-                lv[b] = l == 0 ? sampler::load_shared(lsrc + gg * kBatchTileChains) : 0.0;
+                lv[b] = l == 0 ? sampler::load_shared(lsrc + gq * kBatchTileChains) : 0.0;
             }
 #pragma unroll
             for (int b = 0; b < B; ++b) {
+                if (g0 + b * kGroupWaves < c.groups) {
 #pragma unroll
-                for (int mm = 0; mm < DPL; ++mm) s[mm] += (double)v[b][mm];
-                s[DPL] += lv[b];
+                    for (int mm = 0; mm < DPL; ++mm) s[mm] += (double)v[b][mm];
+                    s[DPL] += lv[b];
+                }
             }
-        }
-        for (; g < c.groups; g += kGroupWaves) {
-#pragma unroll
-            for (int mm = 0; mm < DPL; ++mm) {
-                const int col = l + 64 * mm;
-                s[mm] += col < c.bv.D ? (double)load_f(src + (int64_t)g * rstride + col) : 0.0;
-            }
-            s[DPL] += l == 0 ? sampler::load_shared(lsrc + (int64_t)g * kBatchTileChains) : 0.0;
         }
 #pragma unroll
         for (int mm = 0; mm <= DPL; ++mm) sh.red[wave][mm * 64 + l] = s[mm];
