@@ -6,7 +6,9 @@ ties recorded HBM-traffic figures to the kernel code they were taken on.
     python -m paper_1912_11554_amd.profiling counters RUN_results.db
         PMC counter values per dispatch (summed over the counter instances)
     python -m paper_1912_11554_amd.profiling fingerprint [KERNEL]
-        SHA-256 over the sources KERNEL is built from (default: all of csrc)
+        SHA-256 over the sources KERNEL is built from (its translation units,
+        the csrc headers they include and include/nuts.h; default: all of
+        csrc)
 
 The databases are the SQLite files rocprofv3 writes (`-d DIR -o NAME`).
 """
@@ -22,31 +24,57 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-# Sources that only the HMM kernels are built from; the other kernels'
-# fingerprint leaves them out (the HMM kernels include every shared header).
-HMM_ONLY_SOURCES = ("hmm_impl.h", "hmm.hip", "hmm_ext.hip")
-# Host-only sources (argument checks, staging, launch choices): no kernel is
-# built from them, so no kernel's fingerprint covers them.
-HOST_ONLY_SOURCES = ("api.cpp",)
+# The translation units each kernel is compiled in; its fingerprint covers
+# them and every csrc header they include, directly or through another
+# header (the include directive lines are followed, nothing else).
+KERNEL_UNITS = {
+    "potential_grad_kernel": ("potential.hip",),
+    "sampler_grid_kernel": ("sampler.hip", "sampler_f32.hip", "sampler_f64.hip", "sampler_ext_f32.hip",
+                            "sampler_ext_f64.hip"),
+    "sampler_wave_kernel": ("sampler.hip", "sampler_f32.hip", "sampler_f64.hip", "sampler_ext_f32.hip",
+                            "sampler_ext_f64.hip"),
+    "sampler_batch_kernel": ("batch.hip",),
+    "batch_pass_kernel": ("batch.hip",),
+    "batch_ll_kernel": ("batch.hip",),
+    "sampler_hmm_kernel": ("hmm.hip", "hmm_ext.hip"),
+    "hmm_potential_kernel": ("hmm.hip", "hmm_ext.hip"),
+}
 
 
-def is_hmm_kernel(kernel: str) -> bool:
-    return "hmm" in kernel
+def kernel_sources(kernel: str) -> list[str]:
+    """The csrc files a kernel is built from: its translation units and the
+    closure of their local includes."""
+    csrc = os.path.join(HERE, "csrc")
+    todo = list(KERNEL_UNITS[kernel])
+    seen = set()
+    while todo:
+        base = todo.pop()
+        if base in seen or not os.path.exists(os.path.join(csrc, base)):
+            continue
+        seen.add(base)
+        with open(os.path.join(csrc, base)) as f:
+            for line in f:
+                line = line.strip()
+                if line.startswith("#include \""):
+                    inc = line.split('"')[1]
+                    if "/" not in inc:
+                        todo.append(inc)
+    # the public header's record layouts (nuts_stats) are written by the kernels
+    return sorted(seen) + ["../../include/nuts.h"]
 
 
 def source_fingerprint(kernel: str | None = None) -> str:
-    """SHA-256 over the device and host sources a kernel is built from (file
-    names and contents, sorted): any change to them gives a new value.  With
-    no kernel named, over all of csrc."""
+    """SHA-256 over the sources a kernel is built from (file names and
+    contents, sorted): a change to any of them gives a new value, a change
+    elsewhere does not.  With no kernel named, over all of csrc."""
     h = hashlib.sha256()
-    for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
-        base = os.path.basename(path)
-        if kernel is not None and base in HOST_ONLY_SOURCES:
-            continue
-        if kernel is not None and not is_hmm_kernel(kernel) and base in HMM_ONLY_SOURCES:
-            continue
+    if kernel is None:
+        files = sorted(os.path.basename(p) for p in glob.glob(os.path.join(HERE, "csrc", "*")))
+    else:
+        files = kernel_sources(kernel)
+    for base in files:
         h.update(base.encode())
-        with open(path, "rb") as f:
+        with open(os.path.normpath(os.path.join(HERE, "csrc", base)), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
