@@ -60,6 +60,19 @@ using batch::WaveQ;
 // matrix-core accumulators, the tail columns and the loss from the lanes of
 // the first row group.  ATOMIC selects agent-scope stores (read by other
 // groups of the same launch).
+// Buffer resource word 3 for raw dword access on gfx9-family devices, and the
+// cache-policy operand of a buffer access at agent scope (the sc1 bit: the
+// access is coherent across the device's L2 caches, as an agent-scope atomic
+// load or store is).  Buffer accesses give 16-byte agent-scope transfers,
+// which the atomic builtins (8 bytes at most) do not.
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kCachePolicyAgent = 16;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* base)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, kBufferWord3);
+}
+
 template <bool ATOMIC>
 __device__ __forceinline__ void put_f(float* p, float v)
 {
@@ -72,20 +85,6 @@ __device__ __forceinline__ void put_d(double* p, double v)
     if constexpr (ATOMIC) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else *p = v;
 }
-// Two consecutive floats (8-byte aligned) as one store: agent-scope stores
-// are 8 bytes at most, and one per pair halves the store transactions of
-// four separate floats.
-template <bool ATOMIC>
-__device__ __forceinline__ void put_f2(float* p, float a, float b)
-{
-    const unsigned long long v = (unsigned long long)__builtin_bit_cast(uint32_t, a) |
-                                 ((unsigned long long)__builtin_bit_cast(uint32_t, b) << 32);
-    if constexpr (ATOMIC)
-        __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else
-        *reinterpret_cast<unsigned long long*>(p) = v;
-}
-
 template <int KT, bool ATOMIC>
 __device__ __forceinline__ void store_partials(const BatchView& bv, WaveAcc& acc, int widx, int pw, float* P,
                                                double* L)
@@ -98,9 +97,12 @@ __device__ __forceinline__ void store_partials(const BatchView& bv, WaveAcc& acc
     float* row = P + (int64_t)slot * pw;
 #pragma unroll
     for (int mt = 0; mt < KT; ++mt) {
-        float* dst = row + 16 * mt + 4 * jj;  // 16-byte aligned: pw and 4 jj are multiples of 4
-        put_f2<ATOMIC>(dst, acc.g[mt][0], acc.g[mt][1]);
-        put_f2<ATOMIC>(dst + 2, acc.g[mt][2], acc.g[mt][3]);
+        // 16-byte aligned: pw and 4 jj are multiples of 4
+        if constexpr (ATOMIC)
+            __builtin_amdgcn_raw_buffer_store_b128(acc.g[mt], buffer_of(row), (16 * mt + 4 * jj) * 4, 0,
+                                                   kCachePolicyAgent);
+        else
+            *reinterpret_cast<batch::v4f*>(row + 16 * mt + 4 * jj) = acc.g[mt];
     }
     if (jj == 0) {
 #pragma unroll
@@ -442,10 +444,6 @@ __device__ __forceinline__ void store_u64(unsigned long long* p, unsigned long l
 {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float load_f(const float* p)
-{
-    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 constexpr uint64_t kWaitTicks = 1000000000ull;  // ~10 s of the 100 MHz real-time counter
 
@@ -458,9 +456,25 @@ __device__ __forceinline__ void raise_error(const BatchCtx& c)
     if (lane() == 0) __hip_atomic_store(&c.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int DPL>
+// Slot of column `col` in a published position: the matrix-core operand
+// order of the column contraction, lane group jj's 4 KP values contiguous
+// (Q.q of load_q), so that a worker lane reads its share with 16-byte loads;
+// the four tail columns after the 16 KP permuted ones.  Columns of chunks
+// past KT have a slot and hold zero.
+template <int KT>
+__device__ __forceinline__ int q_slot(int col)
+{
+    constexpr int KP = batch::Geo<KT>::KP;
+    const int c = col >> 4, g = col & 15;
+    const int i = c & 3, h = c >> 2;
+    const int f = KP == 8 ? 2 * g + h : g;
+    return (f & 3) * 4 * KP + (f >> 2) * 4 + i;
+}
+
+template <int KT, int DPL>
 __device__ void publish(const BatchCtx& c, unsigned long long step, const double (&q)[DPL], bool mark_done)
 {
+    constexpr int KP = batch::Geo<KT>::KP;
     const int l = lane();
     const int par = (int)(step & 1);
     const int64_t slot = (int64_t)c.t * kBatchTileChains + c.i;
@@ -470,7 +484,11 @@ __device__ void publish(const BatchCtx& c, unsigned long long step, const double
         const int col = l + 64 * m;
         float v = 0.0f;
         if (m < DPL && col < c.bv.D) v = (float)q[m < DPL ? m : 0];
-        __hip_atomic_store(dst + col, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (col < 16 * KP)
+            __hip_atomic_store(dst + q_slot<KT>(col), (col >> 4) < KT ? v : 0.0f, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        if (col >= 16 * KT && col < 16 * KT + batch::kTail)
+            __hip_atomic_store(dst + 16 * KP + (col - 16 * KT), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     sampler::drain_memory_ops();
     if (mark_done) {
@@ -534,7 +552,7 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
     const int par = (int)(step & 1);
     const bool host = c.i < kBatchTileChains;
     if (LEADER) {
-        if (publish_q && host) publish<DPL>(c, step, q, mark_done);
+        if (publish_q && host) publish<KT, DPL>(c, step, q, mark_done);
         const int cmd = wait_positions(c, step);
         if (l == 0) sh.cmd = cmd;
     }
@@ -554,17 +572,21 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         const int jj = l >> 4;
         const float* qsrc = c.qbuf + ((int64_t)par * c.tiles * kBatchTileChains +
                                       (int64_t)c.t * kBatchTileChains + widx * 16 + m) * kBatchQWidth;
+        // the position in the order publish wrote it: this lane's 4 KP
+        // operand values, then the tail, in 16-byte agent-scope loads
         WaveQ Q;
         constexpr int KP = batch::Geo<KT>::KP;
+        const __amdgpu_buffer_rsrc_t qr = buffer_of(qsrc);
 #pragma unroll
-        for (int t = 0; t < KP; ++t)
+        for (int t = 0; t < KP; ++t) {
+            const batch::v4f v = __builtin_amdgcn_raw_buffer_load_b128(qr, (jj * 4 * KP + 4 * t) * 4, 0,
+                                                                       kCachePolicyAgent);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int col = batch::e_column<KT>(t, jj, i);
-                Q.q[4 * t + i] = (col / 16) < KT ? load_f(qsrc + col) : 0.0f;
-            }
+            for (int i = 0; i < 4; ++i) Q.q[4 * t + i] = v[i];
+        }
+        const batch::v4f tv = __builtin_amdgcn_raw_buffer_load_b128(qr, 16 * KP * 4, 0, kCachePolicyAgent);
 #pragma unroll
-        for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = load_f(qsrc + 16 * KT + k);
+        for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = tv[k];
         WaveAcc acc;
         batch::zero(acc);
         batch::stage_loop<KT, true>(c.bv, c.st0, c.st1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
@@ -583,38 +605,48 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         // this wave's share of the groups, in group order
         const float* src = c.P + tile_base * rstride + (int64_t)c.i * c.pw;
         const double* lsrc = c.L + tile_base * kBatchTileChains + c.i;
-        double s[DPL + 1];
-#pragma unroll
-        for (int mm = 0; mm <= DPL; ++mm) s[mm] = 0.0;
-        // every load of a wave's share in flight at once: one round trip for
-        // up to 16 groups per wave (144 groups of 9 waves); a group past the
-        // last re-reads the wave's first group and is not added
+        // Lane l adds columns 4 l .. 4 l + 3 with 16-byte loads at agent
+        // scope (buffer loads with the sc1 bit); every load of a wave's share
+        // in flight at once: one round trip for up to 16 groups per wave (144
+        // groups of 9 waves); a group past the last re-reads the wave's first
+        // group and is not added.  (4-byte loads of the same rows took three
+        // times as long: the gather is bound by the count of uncached
+        // requests, not by bytes.)
+        const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(src), (short)0, 0x7fffffff, kBufferWord3);
+        const int nl = (c.bv.D + 3) / 4;
+        const int lc = l < nl ? l : nl - 1;
+        double s4[4] = {0.0, 0.0, 0.0, 0.0};
+        double sl = 0.0;
         constexpr int B = 16;
         for (int g0 = wave; g0 < c.groups; g0 += B * kGroupWaves) {
-            float v[B][DPL];
+            batch::v4f v[B];
             double lv[B];
 #pragma unroll
             for (int b = 0; b < B; ++b) {
                 const int gg = g0 + b * kGroupWaves;
-                const int64_t gq = gg < c.groups ? gg : g0;
-#pragma unroll
-                for (int mm = 0; mm < DPL; ++mm) {
-                    const int col = l + 64 * mm;
-                    v[b][mm] = col < c.bv.D ? load_f(src + gq * rstride + col) : 0.0f;
-                }
-                lv[b] = l == 0 ? sampler::load_shared(lsrc + gq * kBatchTileChains) : 0.0;
+                const int gq = gg < c.groups ? gg : g0;
+                v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)((gq * rstride + 4 * lc) * 4), 0, kCachePolicyAgent);
+                lv[b] = l == 0 ? sampler::load_shared(lsrc + (int64_t)gq * kBatchTileChains) : 0.0;
             }
 #pragma unroll
             for (int b = 0; b < B; ++b) {
                 if (g0 + b * kGroupWaves < c.groups) {
 #pragma unroll
-                    for (int mm = 0; mm < DPL; ++mm) s[mm] += (double)v[b][mm];
-                    s[DPL] += lv[b];
+                    for (int k = 0; k < 4; ++k) s4[k] += (double)v[b][k];
+                    sl += lv[b];
                 }
             }
         }
+        // column c at sh.red[wave][c] (component c / 64 of lane c % 64), the
+        // loss at (DPL) * 64; columns from D on hold zero
 #pragma unroll
-        for (int mm = 0; mm <= DPL; ++mm) sh.red[wave][mm * 64 + l] = s[mm];
+        for (int k = 0; k < 4; ++k) {
+            const int col = 4 * l + k;
+            if (l < nl) sh.red[wave][col] = col < c.bv.D ? s4[k] : 0.0;
+        }
+        for (int col = 4 * nl + l; col < DPL * 64; col += 64) sh.red[wave][col] = 0.0;
+        sh.red[wave][DPL * 64 + l] = l == 0 ? sl : 0.0;
     }
     __syncthreads();  // per-wave sums in LDS
     if (LEADER && host) {
