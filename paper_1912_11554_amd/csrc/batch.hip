@@ -665,9 +665,12 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
     return LEADER ? status : kCmdEval;
 }
 
-template <int KT, int DPL>
+template <int KT, int DPL, bool EXT>
 struct BatchEval {
     static constexpr bool kSpeculative = false;
+    // the edge and proposal nodes in LDS where the kernel without the
+    // extended features has the room (see EdgeNodes and batch_edge_nodes)
+    static constexpr bool kNodesInLds = DPL >= 3 && !EXT;
     BatchCtx c;
     BatchShared<DPL>* sh;
     double inv_s2, prior_const;
@@ -740,7 +743,7 @@ __global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(S
     c.sync = sync;
     const int wave = threadIdx.x / kWave;
     if (wave == 0) {
-        BatchEval<KT, DPL> ev;
+        BatchEval<KT, DPL, EXT> ev;
         ev.c = c;
         ev.sh = &sh;
         ev.inv_s2 = 1.0 / (A.prior_scale * A.prior_scale);
@@ -790,7 +793,9 @@ const void* batch_kernel_for(const BatchView& bv, bool adapt)
 
 size_t batch_sampler_lds(const SamplerArgs& a)
 {
-    return (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge) * sizeof(double);
+    return (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge,
+                                     batch_edge_nodes(a.data.D, sampler_extended(a))) *
+           sizeof(double);
 }
 
 }  // namespace
@@ -799,7 +804,8 @@ bool batch_sampler_supported(const BatchView& bv, int max_depth, int sub_merge, 
 {
     if (bv.D > 64 * 3 || num_cu < kBatchTileChains) return false;
     int per_cu = 0;
-    const size_t lds = (size_t)chain_lds_doubles(bv.D, max_depth, sub_merge) * sizeof(double);
+    const size_t lds =
+        (size_t)chain_lds_doubles(bv.D, max_depth, sub_merge, batch_edge_nodes(bv.D, sub_merge != 0)) * sizeof(double);
     const void* k = batch_kernel_for(bv, sub_merge != 0);
     if (!k) return false;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGroupWaves * kWave, lds) != hipSuccess) return false;

@@ -175,7 +175,7 @@ __host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, 
     HmmLds L;
     const int tu = T - Tsup > 1 ? T - Tsup : 1;
     L.s_off = 0;
-    L.gam_off = (int)chain_lds_doubles(D, max_depth, sub_merge);
+    L.gam_off = (int)chain_lds_doubles(D, max_depth, sub_merge, false);
     L.phi_off = L.gam_off + tu * K;
     L.row_off = L.phi_off + V * K;
     L.wave = (L.row_off + 2 * K * hmm_row_width(K, V) + 1) & ~1;  // 16-byte aligned waves
@@ -185,6 +185,7 @@ __host__ __device__ inline HmmLds hmm_lds(int K, int V, int T, int Tsup, int D, 
 template <int K>
 struct HmmEval {
     static constexpr bool kSpeculative = false;
+    static constexpr bool kNodesInLds = false;
     int V, D, Tsup, Tu;
     // this lane's entry
     int src;       // dimension lane of its logit; -1 for a row's fixed logit or no entry

@@ -269,13 +269,23 @@ __host__ __device__ inline int merge_levels(int max_depth) { return max_depth > 
 // [max(depth, 1)][2][D], then, with merge-structured subtree proposals, the
 // waiting block of each level: its proposal [levels][3][D] (q, p, grad U)
 // and [levels][3] scalars (log-weight, offset, U).
-__host__ __device__ inline int64_t chain_lds_doubles(int D, int max_depth, int sub_merge)
+// LDS of one chain's tree state: the checkpoint array S, the waiting blocks
+// of the merge-structured subtree proposals, and with edge_nodes the two
+// trajectory edges and the two proposals (4 nodes of 3 * 64 * ceil(D / 64)
+// + 1 doubles).
+__host__ __device__ inline int64_t chain_lds_doubles(int D, int max_depth, int sub_merge, bool edge_nodes)
 {
     const int slots = max_depth > 1 ? max_depth : 1;
     int64_t n = (int64_t)slots * 2 * D;
     if (sub_merge) n += (int64_t)merge_levels(max_depth) * (3 * D + 3);
+    if (edge_nodes) n += 4 * (3 * 64 * (int64_t)((D + 63) / 64) + 1);
     return n;
 }
+// Whether the grid path's controller keeps its edge and proposal nodes in
+// LDS (three or more components a lane), and the batch path's (the same,
+// for the kernel without the extended features, whose LDS has the room).
+__host__ __device__ inline bool grid_edge_nodes(int D) { return D > 128; }
+__host__ __device__ inline bool batch_edge_nodes(int D, bool extended) { return D > 128 && !extended; }
 constexpr int kGridWaves = 12;  // per group: 1 controller + 11 workers (3 waves per SIMD: 168 registers each)
 
 // Semi-supervised hidden Markov model (hmm.hip, hmm_ext.hip): symbols w [T]

@@ -45,7 +45,7 @@ int grid_sampler_groups(const DataView& dv, int max_depth, int sub_merge, int nu
 {
     const void* k = pick_grid_kernel(dv, sub_merge != 0);
     int per_cu = 0;
-    const size_t lds = (size_t)chain_lds_doubles(dv.D, max_depth, sub_merge) * sizeof(double);
+    const size_t lds = (size_t)chain_lds_doubles(dv.D, max_depth, sub_merge, grid_edge_nodes(dv.D)) * sizeof(double);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kGridWaves * kWave, lds) != hipSuccess)
         per_cu = 1;
     else if (per_cu < 1)
@@ -69,7 +69,8 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
                        grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D), sync);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t lds = (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge) * sizeof(double);
+    const size_t lds =
+        (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge, grid_edge_nodes(a.data.D)) * sizeof(double);
     const void* k = pick_grid_kernel(a.data, sampler_extended(a));
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;

@@ -43,6 +43,89 @@ struct Node {
     double U;                       // wave-uniform
 };
 
+// The trajectory's two edges, its proposal and the current subtree's
+// proposal.  In registers, or (LDS: the wide shapes of the grid and batch
+// paths, whose controller would otherwise spill them to scratch memory) in
+// a region of the chain's LDS: node k at base + k * kStride holds q, p and
+// grad U (lane l's component m at l + 64 m of each of the three vectors),
+// then U.  Only the chain's own wave reads and writes the region.
+template <int DPL, bool LDS>
+struct EdgeNodes;
+
+template <int DPL>
+struct EdgeNodes<DPL, false> {
+    Node<DPL> left, right, prop, sprop;
+    __device__ void bind(double*) {}
+    __device__ void reset(const Node<DPL>& c) { left = right = prop = c; }
+    __device__ Node<DPL> edge(bool r) const { return r ? right : left; }
+    __device__ void set_edge(bool r, const Node<DPL>& z)
+    {
+        if (r) right = z;
+        else left = z;
+    }
+    __device__ double edge_q(bool r, int m) const { return r ? right.q[m] : left.q[m]; }
+    __device__ double edge_p(bool r, int m) const { return r ? right.p[m] : left.p[m]; }
+    __device__ double edge_g(bool r, int m) const { return r ? right.g[m] : left.g[m]; }
+    __device__ void set_sprop(const Node<DPL>& z) { sprop = z; }
+    __device__ void accept_sprop() { prop = sprop; }
+    __device__ Node<DPL> get_prop() const { return prop; }
+};
+
+template <int DPL>
+struct EdgeNodes<DPL, true> {
+    static constexpr int kVec = 64 * DPL;
+    static constexpr int kStride = 3 * kVec + 1;
+    static constexpr int kLeft = 0, kRight = 1, kProp = 2, kSprop = 3;
+    double* base;
+    __device__ void bind(double* b) { base = b; }
+    __device__ void store(int k, const Node<DPL>& n)
+    {
+        const int l = lane();
+        double* b = base + k * kStride;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) {
+            b[l + 64 * m] = n.q[m];
+            b[kVec + l + 64 * m] = n.p[m];
+            b[2 * kVec + l + 64 * m] = n.g[m];
+        }
+        if (l == 0) b[3 * kVec] = n.U;
+    }
+    __device__ Node<DPL> load(int k) const
+    {
+        const int l = lane();
+        const double* b = base + k * kStride;
+        Node<DPL> n;
+#pragma unroll
+        for (int m = 0; m < DPL; ++m) {
+            n.q[m] = b[l + 64 * m];
+            n.p[m] = b[kVec + l + 64 * m];
+            n.g[m] = b[2 * kVec + l + 64 * m];
+        }
+        n.U = b[3 * kVec];
+        return n;
+    }
+    __device__ void reset(const Node<DPL>& c)
+    {
+        store(kLeft, c);
+        store(kRight, c);
+        store(kProp, c);
+    }
+    __device__ Node<DPL> edge(bool r) const { return load(r ? kRight : kLeft); }
+    __device__ void set_edge(bool r, const Node<DPL>& z) { store(r ? kRight : kLeft, z); }
+    __device__ double edge_q(bool r, int m) const { return base[(r ? kRight : kLeft) * kStride + lane() + 64 * m]; }
+    __device__ double edge_p(bool r, int m) const
+    {
+        return base[(r ? kRight : kLeft) * kStride + kVec + lane() + 64 * m];
+    }
+    __device__ double edge_g(bool r, int m) const
+    {
+        return base[(r ? kRight : kLeft) * kStride + 2 * kVec + lane() + 64 * m];
+    }
+    __device__ void set_sprop(const Node<DPL>& z) { store(kSprop, z); }
+    __device__ void accept_sprop() { store(kProp, load(kSprop)); }
+    __device__ Node<DPL> get_prop() const { return load(kProp); }
+};
+
 template <int DPL>
 __device__ __forceinline__ double dot3(const double (&a)[DPL], const double (&b)[DPL], const double (&c)[DPL])
 {
@@ -97,6 +180,7 @@ __device__ __forceinline__ bool is_uturn_gen(const double (&rho)[DPL], const dou
 template <typename T, int S, int CPS>
 struct WaveEval {
     static constexpr bool kSpeculative = false;
+    static constexpr bool kNodesInLds = false;
     const T* X;
     const uint8_t* y;
     int64_t N, nb;
@@ -431,6 +515,7 @@ __device__ bool grid_end(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned lon
 template <typename T, int S, int CPS, int DPL, int NW>
 struct GridEval {
     static constexpr bool kSpeculative = true;
+    static constexpr bool kNodesInLds = DPL >= 3;  // the edge and proposal nodes in LDS (see EdgeNodes)
     GridCtx c;
     GridShared<DPL, NW>* sh;
     double inv_s2, prior_const;
@@ -703,6 +788,8 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     const bool smerge = EXT && A.sub_merge;
     double* stk = S_arr + (int64_t)(maxd > 1 ? maxd : 1) * 2 * D;
     double* stk_sc = stk + (int64_t)merge_levels(maxd) * 3 * D;
+    EdgeNodes<DPL, Eval::kNodesInLds> nodes;
+    nodes.bind(S_arr + chain_lds_doubles(D, maxd, smerge ? 1 : 0, false));
     DualAvg da;
     MassWindows win;
     win.any = false;
@@ -757,7 +844,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         const double u_merge = dr.u_merge;
         const uint64_t dirmask = __ballot(dr.dir_bit);
 
-        Node<DPL> left = cur, right = cur, prop = cur;
+        nodes.reset(cur);
         // a speculative evaluation: the next leapfrog position, handed to the
         // evaluator before the bookkeeping of the current leaf decides
         // whether the trajectory goes on (evaluators that can start one)
@@ -773,11 +860,11 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
         for (int j = 0; j < maxd; ++j) {
             const int v = ((dirmask >> j) & 1ull) ? 1 : -1;
             if (v > 0) dirbits |= 1u << j;
-            Node<DPL> z = v > 0 ? right : left;
+            Node<DPL> z = nodes.edge(v > 0);
             const int64_t e = v > 0 ? Rpos : Lpos;
             const double h = v * eps;
             double logw = -INFINITY;
-            Node<DPL> sprop = z;
+            nodes.set_sprop(z);
             int64_t sprop_idx = 0;
             int status = kTreeOk;
             depth = j + 1;
@@ -838,9 +925,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                         double bq[DPL], bp[DPL], bg[DPL], nph[DPL], nq[DPL];
 #pragma unroll
                         for (int m = 0; m < DPL; ++m) {
-                            bq[m] = from_z ? z.q[m] : (vn > 0 ? right.q[m] : left.q[m]);
-                            bp[m] = from_z ? z.p[m] : (vn > 0 ? right.p[m] : left.p[m]);
-                            bg[m] = from_z ? z.g[m] : (vn > 0 ? right.g[m] : left.g[m]);
+                            bq[m] = from_z ? z.q[m] : nodes.edge_q(vn > 0, m);
+                            bp[m] = from_z ? z.p[m] : nodes.edge_p(vn > 0, m);
+                            bg[m] = from_z ? z.g[m] : nodes.edge_g(vn > 0, m);
                         }
                         leapfrog_drift<DPL>(bq, bp, bg, hn, im, nph, nq);
                         ev.begin(nq);
@@ -911,7 +998,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                             }
                         }
                     } else {
-                        sprop = cp;
+                        nodes.set_sprop(cp);
                         sprop_idx = cix;
                         logw = clw;
                     }
@@ -920,7 +1007,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     const double lw = logaddexp(logw, lam);
                     const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
                     if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
-                        sprop = z;
+                        nodes.set_sprop(z);
                         sprop_idx = e + v * (n + 1);
                     }
                     logw = lw;
@@ -982,24 +1069,28 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             const double um = __shfl(u_merge, j);
             const double dw = logw - logw_traj;
             if (uni(um < (dw >= 0.0 ? 1.0 : exp_nonpos(dw)))) {
-                prop = sprop;
+                nodes.accept_sprop();
                 prop_idx = sprop_idx;
             }
             logw_traj = logaddexp(logw_traj, logw);
-            if (v > 0) {
-                right = z;
-                Rpos += nleaf;
-            } else {
-                left = z;
-                Lpos -= nleaf;
-            }
-            bool traj_turn;
+            nodes.set_edge(v > 0, z);
+            if (v > 0) Rpos += nleaf;
+            else Lpos -= nleaf;
             if (gen) {
 #pragma unroll
                 for (int m = 0; m < DPL; ++m) rho_traj[m] += rsum[m];
-                traj_turn = is_uturn_gen<DPL>(rho_traj, left.p, right.p, im);
+            }
+            bool traj_turn;
+            if constexpr (Eval::kNodesInLds) {
+                // the edge just extended is z, the other one is read back
+                const Node<DPL> other = nodes.edge(v < 0);
+                const Node<DPL>& le = v > 0 ? other : z;
+                const Node<DPL>& ri = v > 0 ? z : other;
+                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, le.p, ri.p, im)
+                                : is_uturn<DPL>(le.q, le.p, ri.q, ri.p, 1, im);
             } else {
-                traj_turn = is_uturn<DPL>(left.q, left.p, right.q, right.p, 1, im);
+                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, nodes.left.p, nodes.right.p, im)
+                                : is_uturn<DPL>(nodes.left.q, nodes.left.p, nodes.right.q, nodes.right.p, 1, im);
             }
             if (traj_turn) {
                 turning = 1;
@@ -1012,7 +1103,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             if (pend) ev.cancel();  // the trajectory ended before that position
         }
         evals += (unsigned long long)nleaves;
-        cur = prop;
+        cur = nodes.get_prop();
 
         if (adapt && k < A.num_warmup) {
             const double alpha = nleaves > 0 ? sum_acc / (double)nleaves : 0.0;
@@ -1123,7 +1214,7 @@ struct WaveLds {
     static constexpr int R = BlockShape<T, S>::R;
     __host__ __device__ static size_t s_bytes(int D, int max_depth, int sub_merge, int cpg)
     {
-        return (size_t)cpg * chain_lds_doubles(D, max_depth, sub_merge) * sizeof(double);
+        return (size_t)cpg * chain_lds_doubles(D, max_depth, sub_merge, false) * sizeof(double);
     }
     __host__ __device__ static int64_t x_elems(int D, int64_t nb) { return nb * D * R; }
     __host__ __device__ static int64_t pad_elems(int D) { return (int64_t)(CPS * S - D) * R; }
@@ -1154,7 +1245,7 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
     const int64_t chain = (int64_t)blockIdx.x * cpg + wave;
     const int D = A.data.D;
     const int64_t nb = A.data.nb;
-    double* S_arr = lds + (int64_t)wave * chain_lds_doubles(D, A.max_depth, EXT ? A.sub_merge : 0);
+    double* S_arr = lds + (int64_t)wave * chain_lds_doubles(D, A.max_depth, EXT ? A.sub_merge : 0, false);
     const int64_t c = A.chain_offset + chain;
     const int64_t ds = A.per_chain_data ? c : 0;
     const T* Xg = (const T*)A.data.X + ds * nb * (int64_t)D * R;
