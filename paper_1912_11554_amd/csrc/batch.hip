@@ -179,8 +179,19 @@ __global__ void __launch_bounds__(kFinishWaves * kWave) batch_finish_kernel(int 
     const double* lsrc = L + t * groups * kBatchTileChains + slot;
     for (int col = l; col < pw; col += 64) {
         double s = 0.0;
-        if (col < D)
-            for (int g = wave; g < groups; g += kFinishWaves) s += (double)src[g * rstride + col];
+        if (col < D) {
+            // eight groups' loads in flight at a time, added in group order
+            constexpr int U = 8;
+            int g = wave;
+            for (; g + (U - 1) * kFinishWaves < groups; g += U * kFinishWaves) {
+                float v[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) v[u] = src[(int64_t)(g + u * kFinishWaves) * rstride + col];
+#pragma unroll
+                for (int u = 0; u < U; ++u) s += (double)v[u];
+            }
+            for (; g < groups; g += kFinishWaves) s += (double)src[(int64_t)g * rstride + col];
+        }
         red[wave * rw + col] = s;
     }
     // loss partials: lane l of wave w takes groups w + 4 l, w + 4 (l + 64), ...
@@ -215,7 +226,8 @@ BatchPlan plan_batch_potential(const BatchView& bv, int64_t K, int num_cu)
 {
     BatchPlan p;
     p.tiles = (int)((K + kBatchTileChains - 1) / kBatchTileChains);
-    int64_t g = (int64_t)num_cu * 2 / p.tiles;
+    // one group per CU (a group's two LDS stages take most of a CU's LDS)
+    int64_t g = (int64_t)num_cu / p.tiles;
     if (g > bv.ns) g = bv.ns;
     if (g < 1) g = 1;
     p.groups = (int)g;
