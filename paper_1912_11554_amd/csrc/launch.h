@@ -134,9 +134,15 @@ bool wave_path_resident(const SamplerArgs& a);
 // One chain over the whole device.  `sync` holds the error flag, zeroed by
 // this call; `partials` holds grid_partial_elems(D, groups) doubles and
 // `result` grid_result_elems(D) doubles, both marked empty by this call.
+// The result row of each phase is kept in kGridReplicas copies, kReplicaStride
+// doubles apart (4 KiB + 256 B, so that the copies fall in different memory
+// channels): every controller polls its row once per round trip, and 256 of
+// them on one row queue at the channel that holds it.
 constexpr int kGridPhases = 3;
+constexpr int kGridReplicas = 16;
+constexpr int kReplicaStride = 544;  // >= partial_width(D) for D <= 448
 inline int64_t grid_partial_elems(int D, int groups) { return (int64_t)kGridPhases * (D + 1) * groups; }
-inline int64_t grid_result_elems(int D) { return (int64_t)kGridPhases * partial_width(D); }
+inline int64_t grid_result_elems(int) { return (int64_t)kGridPhases * kGridReplicas * kReplicaStride; }
 struct GridSync {
     unsigned int error;  // a wait timed out
     unsigned int pad[63];

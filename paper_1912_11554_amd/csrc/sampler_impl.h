@@ -244,7 +244,7 @@ struct GridCtx {
     int D;
     int groups;
     double* partials;  // [kGridPhases][D + 1][groups]
-    double* result;    // [kGridPhases][W]
+    double* result;    // [kGridPhases][kGridReplicas][kReplicaStride], W used of each row
     GridSync* sync;
 };
 
@@ -298,21 +298,30 @@ __device__ __forceinline__ void raise_grid_error(const GridCtx& c)
 // about 10 s of the 100 MHz constant clock: a wait that long means a broken
 // invariant, and every group then gives up instead of hanging the device
 constexpr uint64_t kGridWaitTicks = 1000000000ull;
+// Waits look at the error flag (which another group raises when its own wait
+// timed out) only after 20 us, and then every 16th poll: on the short waits
+// of every step its loads would only queue beside the slot polls of every
+// group at the one channel that holds the flag.
+constexpr uint64_t kErrorPollTicks = 2000ull;
+
+__device__ __forceinline__ bool error_poll_due(uint64_t waited, unsigned polls)
+{
+    return waited > kErrorPollTicks && (polls & 15u) == 0u;
+}
 
 // Wait until *p holds a value; false if the exchange failed meanwhile.
 __device__ __forceinline__ bool wait_slot(const GridCtx& c, const double* p, double& v)
 {
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    for (;;) {
-        // both loads in flight together: one round trip per poll
+    for (unsigned polls = 1;; ++polls) {
         const unsigned long long b = slot_bits(p);
-        const bool err = grid_error(c);
         if (b != kEmptySlot) {
             v = __builtin_bit_cast(double, b);
             return true;
         }
-        if (err) return false;
-        if (__builtin_amdgcn_s_memrealtime() - t0 > kGridWaitTicks) {
+        const uint64_t waited = __builtin_amdgcn_s_memrealtime() - t0;
+        if (error_poll_due(waited, polls) && grid_error(c)) return false;
+        if (waited > kGridWaitTicks) {
             raise_grid_error(c);
             return false;
         }
@@ -320,8 +329,12 @@ __device__ __forceinline__ bool wait_slot(const GridCtx& c, const double* p, dou
     }
 }
 
+// Position of the loss in a result row: right after the D gradient columns
+// when the row has room there (so that it shares their cache lines), else
+// the first slot of the extra lane-row.
+__device__ __forceinline__ int loss_pos(int D, int DPL) { return D < 64 * DPL ? D : 64 * DPL; }
 // Position in a result row of used column ci (0..D-1, or D for the loss).
-__device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < D ? ci : 64 * DPL; }
+__device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < D ? ci : loss_pos(D, DPL); }
 
 // One collective evaluation for the whole group, in two halves so that wave
 // 0 (the controller) can work between them while the workers stream.
@@ -348,9 +361,10 @@ __device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < 
 // row of group slots.  Group g owns the used columns g, g + G, ...: its
 // workers wait for the G slots of each, empty them again, add them in a fixed
 // order (lane l takes groups l, l + 64, ... in increasing order, then the
-// lanes in butterfly order), store the column's result slot and empty the
-// same slot of the previous phase.  Controllers wait for the result slots of
-// their lanes.  Emptying is safe: a group's partial of step s is written
+// lanes in butterfly order), store the column's result slot in every copy of
+// the result row and empty the same slots of the previous phase.  The
+// controller of group g waits for the result slots of its lanes in copy
+// g mod kGridReplicas.  Emptying is safe: a group's partial of step s is written
 // after its controller read all of step s - 1's results, and the next write
 // of an emptied slot comes only after the worker that emptied it has waited
 // for its own stores (s_waitcnt at its next step, before it stores the next
@@ -409,7 +423,7 @@ template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
 __device__ bool grid_end(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned long long step, int gen, bool stop,
                          double (&out_r)[DPL + 1], bool* aborted)
 {
-    constexpr int W = GridShared<DPL, NW>::W;
+    static_assert(GridShared<DPL, NW>::W <= kReplicaStride, "a result row fits its copy");
     const int l = lane();
     const int wave = threadIdx.x / kWave;
     if (!WORKER && stop && l == 0)
@@ -461,11 +475,12 @@ __device__ bool grid_end(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned lon
                 const int ci = g + jc * G;
                 double s = 0.0;
                 for (int t = l; t < G; t += kWave) s += sh.red_flat[jc * G + t];
-                s = wave_sum(s);
-                if (l == 0) {
+                s = wave_sum(s);  // the same bits in every lane
+                if (l < kGridReplicas) {
                     const int pos = result_pos(ci, D, DPL);
-                    store_shared(&c.result[ph * W + pos], s);
-                    empty_slot(&c.result[((ph + kGridPhases - 1) % kGridPhases) * W + pos]);
+                    const int prev = (ph + kGridPhases - 1) % kGridPhases;
+                    store_shared(&c.result[(ph * kGridReplicas + l) * kReplicaStride + pos], s);
+                    empty_slot(&c.result[(prev * kGridReplicas + l) * kReplicaStride + pos]);
                 }
             }
         }
@@ -473,29 +488,31 @@ __device__ bool grid_end(const GridCtx& c, GridShared<DPL, NW>& sh, unsigned lon
     if (WORKER) return true;
 
     // controller: wait for this lane's result slots, all at once
-    const double* row = &c.result[ph * W];
+    const double* row = &c.result[(ph * kGridReplicas + g % kGridReplicas) * kReplicaStride];
+    const int lp = loss_pos(D, DPL);
     unsigned long long bits[DPL + 1];
 #pragma unroll
     for (int m = 0; m <= DPL; ++m) {
-        const bool used_slot = m < DPL ? l + 64 * m < D : l == 0;
+        const int pos = l + 64 * m;
+        const bool used_slot = pos < D || pos == lp;
         bits[m] = used_slot ? kEmptySlot : 0ull;  // 0ull: +0.0, nothing to wait for
     }
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     bool bad = false;
-    for (;;) {
+    for (unsigned polls = 1;; ++polls) {
 #pragma unroll
         for (int m = 0; m <= DPL; ++m)
             if (bits[m] == kEmptySlot) bits[m] = slot_bits(row + l + 64 * m);
-        const bool err = grid_error(c);  // in flight with the slot loads
         bool ready = true;
 #pragma unroll
         for (int m = 0; m <= DPL; ++m) ready = ready && bits[m] != kEmptySlot;
         if (__all(ready)) break;
-        if (err) {
+        const uint64_t waited = __builtin_amdgcn_s_memrealtime() - t0;
+        if (error_poll_due(waited, polls) && grid_error(c)) {
             bad = true;
             break;
         }
-        if (__builtin_amdgcn_s_memrealtime() - t0 > kGridWaitTicks) {
+        if (waited > kGridWaitTicks) {
             if (l == 0) raise_grid_error(c);
             bad = true;
             break;
@@ -561,7 +578,12 @@ struct GridEval {
 #pragma unroll
         for (int m = 0; m < DPL; ++m) pr += 0.5 * q[m] * q[m] * inv_s2;
         const double prior = wave_sum(pr);
-        U = readlane_f64(r[DPL], 0) + prior + prior_const;
+        const int lp = loss_pos(c.D, DPL);
+        double loss = r[DPL];
+#pragma unroll
+        for (int m = 0; m < DPL; ++m)
+            if (m == lp / 64) loss = r[m];
+        U = readlane_f64(loss, lp % 64) + prior + prior_const;
         const int l = lane();
 #pragma unroll
         for (int m = 0; m < DPL; ++m) g[m] = (l + 64 * m < c.D) ? r[m] + q[m] * inv_s2 : 0.0;
