@@ -294,6 +294,25 @@ __host__ __device__ inline bool grid_edge_nodes(int D) { return D > 128; }
 __host__ __device__ inline bool batch_edge_nodes(int D, bool extended) { return D > 128 && !extended; }
 constexpr int kGridWaves = 12;  // per group: 1 controller + 11 workers (3 waves per SIMD: 168 registers each)
 
+// Grid path: every worker keeps the last blocks of its share in LDS for the
+// whole launch (as many as the group's LDS beside the chain's state holds),
+// so they are read from memory once per launch instead of once per
+// evaluation.  A block takes lds_block_bytes: the registers one lane loads
+// for it (cols slots of two rows for fp32 or one lane per row, else one
+// row), 64 lanes, then the lanes' labels (one byte a row).  They start at
+// byte grid_resident_offset of the group's dynamic LDS, after the chain's
+// state.
+__host__ __device__ constexpr int lds_block_bytes(int dtype, int split, int cols)
+{
+    const int rows_per_lane = (dtype == NUTS_F32 || split == 1) ? 2 : 1;
+    return cols * 64 * rows_per_lane * (dtype == NUTS_F64 ? 8 : 4) + 64 * rows_per_lane;
+}
+__host__ __device__ inline size_t grid_resident_offset(int D, int max_depth, int sub_merge)
+{
+    const size_t b = (size_t)chain_lds_doubles(D, max_depth, sub_merge, grid_edge_nodes(D)) * sizeof(double);
+    return (b + 15) & ~(size_t)15;
+}
+
 // Semi-supervised hidden Markov model (hmm.hip, hmm_ext.hip): symbols w [T]
 // (< V), observed states z [Tsup] (< K), on the device.  Parameters: K (K-1)
 // transition logits, then K (V-1) emission logits.

@@ -152,6 +152,47 @@ __device__ __forceinline__ BlockRegs<T, CPS, S> load_block(const T* __restrict__
     return out;
 }
 
+// A block kept in LDS from one pass to the next, as the registers a lane
+// loads for it: slot k of lane L at element k * 64 + L, then the lanes'
+// label words (one or two bytes a lane).  Writing a loaded block and reading
+// it back gives the same registers, so a pass computes the same rows from
+// either copy.
+template <typename T, int CPS, int S>
+struct LdsBlock {
+    using B = BlockRegs<T, CPS, S>;
+    using V = typename B::V;
+    using Y = typename B::Y;
+    static constexpr int kSlotBytes = CPS * kWave * (int)sizeof(V);
+    static constexpr int kBytes = kSlotBytes + kWave * (int)sizeof(Y);  // a multiple of 16
+
+    __device__ static void store(char* base, const B& b)
+    {
+        const int L = lane();
+        V* slots = reinterpret_cast<V*>(base);
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) slots[k * kWave + L] = b.x[k];
+        reinterpret_cast<Y*>(base + kSlotBytes)[L] = b.y;
+    }
+    __device__ static B load(const char* base)
+    {
+        const int L = lane();
+        const V* slots = reinterpret_cast<const V*>(base);
+        B b;
+#pragma unroll
+        for (int k = 0; k < CPS; ++k) b.x[k] = slots[k * kWave + L];
+        b.y = reinterpret_cast<const Y*>(base + kSlotBytes)[L];
+        return b;
+    }
+};
+
+// The blocks of a wave's share that sit in LDS: `count` of them from `base`,
+// LdsBlock::kBytes apart, holding blocks first_block, first_block + stride, ...
+struct ResidentBlocks {
+    const char* base = nullptr;
+    int count = 0;
+    int64_t first_block = 0;
+};
+
 // Rows of one loaded block.  qv[k] must hold q[k * S + L % S] (zero for
 // columns c >= D).  Rows at or past rows_left add nothing.
 template <typename T, int CPS, int S>
@@ -218,6 +259,11 @@ __device__ __forceinline__ void compute_block(const BlockRegs<T, CPS, S>& in, in
 // holds and stops.  The block in hand is always computed, so no loaded
 // registers are dead on that path and the loads keep their place ahead of
 // the computation.
+//
+// RES: besides the blocks first, first + stride, ... < nb from memory, the
+// wave computes the LDS-resident blocks `res`: one after each block from
+// memory whose successor's loads are in flight (its registers are free
+// then), the rest after the last one.
 template <bool ABORT>
 __device__ __forceinline__ bool stop_requested(const int* stop, int token)
 {
@@ -229,16 +275,29 @@ __device__ __forceinline__ bool stop_requested(const int* stop, int token)
 // stream_blocks_from takes block `first` already loaded (its loads may still
 // be in flight), so that a caller can issue them before the position is
 // known; stream_blocks loads it itself.
-template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false>
+template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false, bool RES = false>
 __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const T* __restrict__ X,
                                                    const uint8_t* __restrict__ y, int D, int64_t N, int64_t nb,
                                                    int64_t first, int64_t stride, const double (&qv)[CPS],
                                                    double (&acc)[CPS], double& loss, const int* stop = nullptr,
-                                                   int token = 0)
+                                                   int token = 0, const ResidentBlocks& res = ResidentBlocks())
 {
     constexpr int R = BlockShape<T, S>::R;
+    using LB = LdsBlock<T, CPS, S>;
     if (first >= nb) return;
     int64_t b = first;
+    int r = 0;            // resident blocks done
+    bool called_off = false;
+    // one resident block into the free register set `dst`, if any is left
+    const auto resident_step = [&](BlockRegs<T, CPS, S>& dst) {
+        if constexpr (RES) {
+            if (uni(r < res.count)) {
+                dst = LB::load(res.base + r * LB::kBytes);
+                compute_block<T, CPS, S>(dst, N - (res.first_block + r * stride) * R, qv, acc, loss);
+                ++r;
+            }
+        }
+    };
     if constexpr (PIPE) {
         const int64_t count = (nb - 1 - first) / stride + 1;  // blocks of this wave
         int64_t count_left = count;
@@ -247,6 +306,7 @@ __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const
         for (; i + 1 < count_left; i += 2) {
             if (stop_requested<ABORT>(stop, token)) {
                 count_left = i;  // no more loads: the tail computes the block in hand
+                called_off = true;
                 break;
             }
             const int64_t b1 = b + stride, b2 = b1 + stride;
@@ -254,6 +314,8 @@ __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const
             __builtin_amdgcn_sched_barrier(0);  // the loads are issued before the computation
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
             __builtin_amdgcn_sched_barrier(0);  // and it is done before the wait for the loads
+            resident_step(a);
+            __builtin_amdgcn_sched_barrier(0);
             hold_block(c);
             a = load_block<T, CPS, S, MASK>(X + b2 * D * R, y + b2 * R, D);
             __builtin_amdgcn_sched_barrier(0);
@@ -268,6 +330,8 @@ __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const
             __builtin_amdgcn_sched_barrier(0);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
             __builtin_amdgcn_sched_barrier(0);
+            resident_step(a);
+            __builtin_amdgcn_sched_barrier(0);
             hold_block(c);
             compute_block<T, CPS, S>(c, N - b1 * R, qv, acc, loss);
         } else {
@@ -277,27 +341,38 @@ __device__ __forceinline__ void stream_blocks_from(BlockRegs<T, CPS, S> a, const
 #pragma unroll 1
         for (;;) {
             const int64_t nx = b + stride;
-            const bool more = nx < nb && !stop_requested<ABORT>(stop, token);
+            const bool stopped = stop_requested<ABORT>(stop, token);
+            const bool more = nx < nb && !stopped;
             const int64_t lb = more ? nx : b;  // a valid block either way
             const BlockRegs<T, CPS, S> nxt = load_block<T, CPS, S, MASK>(X + lb * D * R, y + lb * R, D);
             compute_block<T, CPS, S>(a, N - b * R, qv, acc, loss);
-            if (!more) break;
+            if (!more) {
+                called_off = stopped;
+                break;
+            }
+            resident_step(a);
             a = nxt;
             b = nx;
         }
     }
+    if constexpr (RES) {
+#pragma unroll 1
+        while (uni(!called_off && r < res.count)) resident_step(a);
+    }
 }
 
-template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false>
+template <typename T, int CPS, int S, bool PIPE, bool MASK, bool ABORT = false, bool RES = false>
 __device__ __forceinline__ void stream_blocks(const T* __restrict__ X, const uint8_t* __restrict__ y, int D,
                                               int64_t N, int64_t nb, int64_t first, int64_t stride,
                                               const double (&qv)[CPS], double (&acc)[CPS], double& loss,
-                                              const int* stop = nullptr, int token = 0)
+                                              const int* stop = nullptr, int token = 0,
+                                              const ResidentBlocks& res = ResidentBlocks())
 {
     constexpr int R = BlockShape<T, S>::R;
     if (first >= nb) return;
     const BlockRegs<T, CPS, S> a = load_block<T, CPS, S, MASK>(X + first * D * R, y + first * R, D);
-    stream_blocks_from<T, CPS, S, PIPE, MASK, ABORT>(a, X, y, D, N, nb, first, stride, qv, acc, loss, stop, token);
+    stream_blocks_from<T, CPS, S, PIPE, MASK, ABORT, RES>(a, X, y, D, N, nb, first, stride, qv, acc, loss, stop,
+                                                          token, res);
 }
 
 // Lane that holds column c after reduce_rows<CPS, S>.

@@ -69,9 +69,20 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
                        grid_partial_elems(a.data.D, groups), result, grid_result_elems(a.data.D), sync);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t lds =
-        (size_t)chain_lds_doubles(a.data.D, a.max_depth, a.sub_merge, grid_edge_nodes(a.data.D)) * sizeof(double);
     const void* k = pick_grid_kernel(a.data, sampler_extended(a));
+    // the chain's state, then as many resident blocks a worker as the rest
+    // of the group's LDS holds (at most one fewer than the smallest share)
+    hipFuncAttributes attr;
+    e = hipFuncGetAttributes(&attr, k);
+    if (e != hipSuccess) return e;
+    const size_t chain = grid_resident_offset(a.data.D, a.max_depth, a.sub_merge);
+    const size_t block = (size_t)lds_block_bytes(a.data.dtype, a.data.split, a.data.cols);
+    const size_t used = attr.sharedSizeBytes + chain;
+    int64_t resident = used < sampler::kMaxGroupLds ? (int64_t)((sampler::kMaxGroupLds - used) / ((kGridWaves - 1) * block)) : 0;
+    const int64_t smallest_share = a.data.nb / ((int64_t)groups * (kGridWaves - 1));
+    if (resident > smallest_share - 1) resident = smallest_share > 1 ? smallest_share - 1 : 0;
+    int res = (int)resident;
+    const size_t lds = chain + (size_t)res * (kGridWaves - 1) * block;
     e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     if (at_launch) {
@@ -79,7 +90,7 @@ hipError_t launch_sampler_grid(const SamplerArgs& a, int groups, double* partial
         if (e != hipSuccess) return e;
     }
     SamplerArgs A = a;
-    void* args[] = {&A, &groups, &partials, &result, &sync};
+    void* args[] = {&A, &groups, &res, &partials, &result, &sync};
     return hipLaunchCooperativeKernel(k, dim3(groups), dim3(kGridWaves * kWave), args, (unsigned)lds, stream);
 }
 

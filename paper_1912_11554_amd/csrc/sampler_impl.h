@@ -329,6 +329,30 @@ __device__ __forceinline__ bool wait_slot(const GridCtx& c, const double* p, dou
     }
 }
 
+// A worker's share of the data blocks: first, first + stride, ... < nb.
+// The last res.count of them sit in LDS for the whole launch; the others,
+// those below nb_mem, stream from memory at every evaluation.  Every wave
+// keeps at least one block in memory (the one it loads ahead of the
+// position).
+struct WaveShare {
+    int64_t first, stride, nb_mem;
+    ResidentBlocks res;
+};
+
+__device__ inline WaveShare grid_wave_share(int64_t nb, int groups, int wave, int resident, const char* res_base)
+{
+    WaveShare w;
+    w.stride = (int64_t)groups * (kGridWaves - 1);
+    w.first = (int64_t)blockIdx.x * (kGridWaves - 1) + (wave - 1);
+    const int64_t count = w.first < nb ? (nb - 1 - w.first) / w.stride + 1 : 0;
+    const int nres = count >= 2 ? (int)(count - 1 < resident ? count - 1 : resident) : 0;
+    w.nb_mem = count > 0 ? w.first + (count - nres - 1) * w.stride + 1 : nb;
+    w.res.base = res_base;
+    w.res.count = nres;
+    w.res.first_block = w.first + (count - nres) * w.stride;
+    return w;
+}
+
 // Position of the loss in a result row: right after the D gradient columns
 // when the row has room there (so that it shares their cache lines), else
 // the first slot of the extra lane-row.
@@ -372,7 +396,8 @@ __device__ __forceinline__ int result_pos(int ci, int D, int DPL) { return ci < 
 // and empties nothing, so the next one reuses its step.
 template <typename T, int S, int CPS, int DPL, int NW, bool WORKER>
 __device__ int grid_begin(const GridCtx& c, GridShared<DPL, NW>& sh, const double (&q)[DPL], int cmd_in,
-                          int gen_in, int* gen_out, const BlockRegs<T, CPS, S>* first_block = nullptr)
+                          int gen_in, int* gen_out, const WaveShare* share = nullptr,
+                          const BlockRegs<T, CPS, S>* first_block = nullptr)
 {
     const int l = lane();
     const int wave = threadIdx.x / kWave;
@@ -390,24 +415,21 @@ __device__ int grid_begin(const GridCtx& c, GridShared<DPL, NW>& sh, const doubl
     if (cmd == kCmdExit) return cmd;
     if (WORKER) {
         const int D = c.D;
-        const int G = c.groups;
-        const int g = blockIdx.x;
         double qv[CPS];
         spread_position_lds<CPS, S>(sh.qbuf, D, qv);
         double acc[CPS];
 #pragma unroll
         for (int k = 0; k < CPS; ++k) acc[k] = 0.0;
         double loss = 0.0;
-        const int workers = NW - 1;
+        const WaveShare& ws = *share;
         if constexpr (kGridPrefetch<T>)
-            stream_blocks_from<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>(
-                *first_block, (const T*)c.X, c.y, D, c.N, c.nb, (int64_t)g * workers + (wave - 1),
-                (int64_t)G * workers, qv, acc, loss, &sh.stop, *gen_out);
+            stream_blocks_from<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true, true>(
+                *first_block, (const T*)c.X, c.y, D, c.N, ws.nb_mem, ws.first, ws.stride, qv, acc, loss, &sh.stop,
+                *gen_out, ws.res);
         else
-            stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true>((const T*)c.X, c.y, D, c.N, c.nb,
-                                                                      (int64_t)g * workers + (wave - 1),
-                                                                      (int64_t)G * workers, qv, acc, loss,
-                                                                      &sh.stop, *gen_out);
+            stream_blocks<T, CPS, S, kGridPipe<T>, kGridPipe<T>, true, true>((const T*)c.X, c.y, D, c.N, ws.nb_mem,
+                                                                            ws.first, ws.stride, qv, acc, loss,
+                                                                            &sh.stop, *gen_out, ws.res);
         if constexpr (S <= 8 && CPS == 8) {
             const double col = finish_pass<CPS, S>(acc, loss);
             if (l < D) sh.red[wave][l] = col;
@@ -1318,9 +1340,11 @@ __global__ void __launch_bounds__(kWaveChainsPerGroup * kWave, RESIDENT ? 1 : 3)
 
 template <typename T, int S, int CPS, int DPL, bool EXT>
 __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(SamplerArgs A, int groups,
-                                                                            double* partials, double* result,
-                                                                            GridSync* sync)
+                                                                            int resident, double* partials,
+                                                                            double* result, GridSync* sync)
 {
+    static_assert(LdsBlock<T, CPS, S>::kBytes == lds_block_bytes(sizeof(T) == 8 ? NUTS_F64 : NUTS_F32, S, CPS),
+                  "the host sizes resident blocks as the kernel lays them out");
     extern __shared__ double lds[];
     __shared__ GridShared<DPL, kGridWaves> sh;
     GridCtx c;
@@ -1333,7 +1357,7 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
     c.partials = partials;
     c.result = result;
     c.sync = sync;
-    const int wave = threadIdx.x / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (wave == 0) {
         // published by the first collective's barrier
         if (lane() == 0) __hip_atomic_store(&sh.stop, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1358,8 +1382,18 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
         // controller's step) and every collective starts on a block already
         // in registers.
         constexpr int R = BlockShape<T, S>::R;
-        const int64_t first = (int64_t)blockIdx.x * (kGridWaves - 1) + (wave - 1);
-        const int64_t fb = first < c.nb ? first : 0;  // a valid block either way
+        using LB = LdsBlock<T, CPS, S>;
+        char* res_base = reinterpret_cast<char*>(lds) + grid_resident_offset(c.D, A.max_depth, A.sub_merge) +
+                         (size_t)(wave - 1) * resident * LB::kBytes;
+        const WaveShare share = grid_wave_share(c.nb, groups, wave, resident, res_base);
+        // the resident blocks, loaded once
+#pragma unroll 1
+        for (int r = 0; r < share.res.count; ++r) {
+            const int64_t b = share.res.first_block + r * share.stride;
+            LB::store(res_base + (size_t)r * LB::kBytes,
+                      load_block<T, CPS, S, kGridPipe<T>>((const T*)c.X + b * c.D * R, c.y + b * R, c.D));
+        }
+        const int64_t fb = share.first < c.nb ? share.first : 0;  // a valid block either way
         const T* Xf = (const T*)c.X + fb * c.D * R;
         const uint8_t* yf = c.y + fb * R;
         for (;;) {
@@ -1368,9 +1402,9 @@ __global__ void __launch_bounds__(kGridWaves * kWave, 1) sampler_grid_kernel(Sam
             int cmd;
             if constexpr (kGridPrefetch<T>) {
                 const BlockRegs<T, CPS, S> pre = load_block<T, CPS, S, kGridPipe<T>>(Xf, yf, c.D);
-                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen, &pre);
+                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen, &share, &pre);
             } else {
-                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen);
+                cmd = grid_begin<T, S, CPS, DPL, kGridWaves, true>(c, sh, q, 0, 0, &gen, &share);
             }
             if (cmd == kCmdExit) break;
             if (grid_end<T, S, CPS, DPL, kGridWaves, true>(c, sh, step, gen, false, r, &ab)) step++;

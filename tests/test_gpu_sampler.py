@@ -255,3 +255,34 @@ def test_kernel_time_is_reported(sampler, path):
     assert 0.0 < r1["kernel_ms"] <= wall_ms
     np.testing.assert_array_equal(r0["samples"], r1["samples"])
     assert r0["grad_evals"] == r1["grad_evals"]
+
+
+# Shapes of the grid path with enough row blocks that every worker keeps the
+# last blocks of its share in LDS for the whole launch (the group's LDS
+# beside the chain's state holds two or three of them a worker; each worker
+# has at least four here, over 256 groups of 11 workers), and a ragged last
+# block, which is one of the resident ones.  (D, dtype, rows per block,
+# blocks a worker):
+RESIDENT_SHAPES = [(9, "f32", 128, 4), (9, "f64", 128, 4), (20, "f32", 32, 5), (55, "f64", 8, 6),
+                   (100, "f32", 8, 5), (150, "f64", 2, 5)]
+
+
+@pytest.mark.parametrize("D,dt,R,per_wave", RESIDENT_SHAPES)
+def test_grid_resident_blocks(sampler, orc, D, dt, R, per_wave):
+    N = R * 256 * 11 * per_wave + R // 2 + 1
+    X, y, w = workloads.make_logistic(N, D, w_scale=0.5, key=[75, D], dtype=dt)
+    say("sampler grid resident blocks", N, D, dt)
+    kw = dict(step_size=0.0015 * np.sqrt(581012 / N), max_tree_depth=6, num_warmup=1, num_samples=4,
+              seed=13, init_q=w)
+    r = sampler.sample(X, y, path=2, **kw)
+    ref = orc.nuts(X.astype(np.float64), y, **kw)
+    assert ref["stats"]["num_steps"].sum() >= 8  # trees, not divergences at the first leaf
+    if dt == "f64":
+        H = np.abs(ref["stats"]["energy"]).max()
+        compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-9, accept_atol=1e-12 * H)
+    else:
+        # each row's fp32-evaluated loss carries about 3e-8 absolute error
+        # (random in sign): H - H0 within 5 sqrt(2 N) 3e-8
+        compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-6,
+                      accept_atol=5 * np.sqrt(2 * N) * 3e-8)
+    assert r["grad_evals"] == ref["grad_evals"]
