@@ -27,6 +27,21 @@ struct Block4 {
     uint64_t w0, w1, w2, w3;
 };
 
+// The 128-bit product of a 64-bit constant and x, from the four 32 x 32-bit
+// partial products (each a 64-bit multiply-add on the vector ALU; no sum
+// below overflows 64 bits): the high and low halves share them.
+template <uint64_t A>
+__device__ __forceinline__ void mul128(uint64_t x, uint64_t& hi, uint64_t& lo)
+{
+    constexpr uint32_t aL = (uint32_t)A, aH = (uint32_t)(A >> 32);
+    const uint32_t xL = (uint32_t)x, xH = (uint32_t)(x >> 32);
+    const uint64_t p00 = (uint64_t)aL * xL;
+    const uint64_t t = (uint64_t)aL * xH + (p00 >> 32);
+    const uint64_t u = (uint64_t)aH * xL + (uint32_t)t;
+    hi = (uint64_t)aH * xH + (t >> 32) + (u >> 32);
+    lo = (u << 32) | (uint32_t)p00;
+}
+
 __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                                 uint64_t k0, uint64_t k1)
 {
@@ -36,8 +51,9 @@ __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64
     constexpr uint64_t kWeylB = 0xBB67AE8584CAA73Bull;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint64_t hiA = __umul64hi(kMulA, c0), loA = kMulA * c0;
-        const uint64_t hiB = __umul64hi(kMulB, c2), loB = kMulB * c2;
+        uint64_t hiA, loA, hiB, loB;
+        mul128<kMulA>(c0, hiA, loA);
+        mul128<kMulB>(c2, hiB, loB);
         const uint64_t n0 = hiB ^ c1 ^ k0;
         const uint64_t n2 = hiA ^ c3 ^ k1;
         c0 = n0;
