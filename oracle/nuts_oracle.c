@@ -108,9 +108,14 @@ void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint6
     out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
 }
 
-/* Draw tags: which random quantity a Philox block feeds (reading R8). */
-enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_DIR = 2, ORC_TAG_MERGE = 3, ORC_TAG_LEAF = 4, ORC_TAG_STEP = 5,
-       ORC_TAG_SUBMERGE = 6, ORC_TAG_PREDICT = 7 };
+/* Draw tags: which random quantity a Philox block feeds (reading R8).
+ * ORC_TAG_TREE block b of iteration t (counter {t, TREE << 32, b, 0}) holds
+ * the direction of doubling b (word 0), the merge uniform of doubling b
+ * (word 1) and the uniforms of leaves 2b and 2b + 1 (words 2, 3), leaves
+ * numbered in the order the trajectory generates them: leaf n of doubling j
+ * is number 2^j - 1 + n. */
+enum { ORC_TAG_MOMENTUM = 1, ORC_TAG_TREE = 2, ORC_TAG_STEP = 5, ORC_TAG_SUBMERGE = 6,
+       ORC_TAG_PREDICT = 7 };
 
 static void orc_block(uint64_t seed, uint64_t chain, uint64_t t, uint64_t tag, uint64_t j,
                       uint64_t n, uint64_t out[4])
@@ -154,22 +159,23 @@ void orc_normals(uint64_t seed, uint64_t chain, uint64_t t, int64_t D, double *o
 int orc_direction(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j)
 {
     uint64_t w[4];
-    orc_block(seed, chain, t, ORC_TAG_DIR, j, 0, w);
+    orc_block(seed, chain, t, ORC_TAG_TREE, 0, j, w);
     return (w[0] & 1ULL) ? +1 : -1;
 }
 
 double orc_u_merge(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j)
 {
     uint64_t w[4];
-    orc_block(seed, chain, t, ORC_TAG_MERGE, j, 0, w);
-    return orc_u53(w[0]);
+    orc_block(seed, chain, t, ORC_TAG_TREE, 0, j, w);
+    return orc_u53(w[1]);
 }
 
 double orc_u_leaf(uint64_t seed, uint64_t chain, uint64_t t, uint64_t j, uint64_t n)
 {
+    const uint64_t g = (((uint64_t)1 << j) - 1) + n; /* the leaf's number in the iteration */
     uint64_t w[4];
-    orc_block(seed, chain, t, ORC_TAG_LEAF, j, n, w);
-    return orc_u53(w[0]);
+    orc_block(seed, chain, t, ORC_TAG_TREE, 0, g >> 1, w);
+    return orc_u53(w[2 + (g & 1)]);
 }
 
 /* Reading R22: the uniform of a merge of two halves inside subtree j, named

@@ -66,11 +66,12 @@ __device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64
     return Block4{c0, c1, c2, c3};
 }
 
-// Which quantity a block feeds; part of the counter.
-enum : uint64_t {
-    kTagMomentum = 1, kTagDirection = 2, kTagMerge = 3, kTagLeaf = 4, kTagStepSize = 5, kTagSubMerge = 6,
-    kTagPredict = 7
-};
+// Which quantity a block feeds; part of the counter.  Block b of kTagTree
+// (counter {iteration, kTagTree << 32, b, 0}) holds the direction of
+// doubling b (word 0), the merge uniform of doubling b (word 1) and the
+// uniforms of leaves 2b and 2b + 1 (words 2, 3), leaf n of doubling j being
+// the iteration's leaf number 2^j - 1 + n.
+enum : uint64_t { kTagMomentum = 1, kTagTree = 2, kTagStepSize = 5, kTagSubMerge = 6, kTagPredict = 7 };
 
 // Kept out of line: it is called a few times per iteration, and inlining it
 // would keep its temporaries and constants live across the tree loops.

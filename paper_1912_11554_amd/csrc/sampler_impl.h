@@ -844,24 +844,25 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     }
 
     // An iteration's draws: the momentum's standard normals (component l +
-    // 64 m in lane l) and, one doubling per lane, the direction bit and the
-    // merge uniform.  None depends on the chain's state, so with a
-    // speculative evaluator the next iteration's are drawn while the first
-    // leaf of this one is evaluated, off the path between iterations.
+    // 64 m in lane l) and tree block l (kTagTree): the direction bit and the
+    // merge uniform of doubling l, the uniforms of the iteration's leaves 2l
+    // and 2l + 1.  None depends on the chain's state, so with a speculative
+    // evaluator the next iteration's are drawn while the first leaf of this
+    // one is evaluated, off the path between iterations.
     struct IterDraws {
         double xi[DPL];
         int dir_bit;
         double u_merge;
+        double u_leaf_a, u_leaf_b;
     };
     const auto draw_iteration = [&](uint64_t t, IterDraws& dr) {
 #pragma unroll
         for (int m = 0; m < DPL; ++m) dr.xi[m] = act[m] ? momentum_normal(seed, key_chain, t, l + 64 * m) : 0.0;
-        dr.dir_bit = 0;
-        dr.u_merge = 0.0;
-        if (l < maxd) {
-            dr.dir_bit = (int)(draw(seed, key_chain, t, kTagDirection, (uint64_t)l, 0).w0 & 1ull);
-            dr.u_merge = unit53(draw(seed, key_chain, t, kTagMerge, (uint64_t)l, 0).w0);
-        }
+        const Block4 b = draw(seed, key_chain, t, kTagTree, 0, (uint64_t)l);
+        dr.dir_bit = l < maxd ? (int)(b.w0 & 1ull) : 0;
+        dr.u_merge = l < maxd ? unit53(b.w1) : 0.0;
+        dr.u_leaf_a = unit53(b.w2);
+        dr.u_leaf_b = unit53(b.w3);
     };
     IterDraws next_draws;
     bool have_next = false;
@@ -887,6 +888,10 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
 
         const double u_merge = dr.u_merge;
         const uint64_t dirmask = __ballot(dr.dir_bit);
+        // uniforms of the leaves 128 c .. 128 c + 127 (c = leaf_chunk): lane l
+        // holds those of leaves 128 c + 2 l and 128 c + 2 l + 1
+        double u_la = dr.u_leaf_a, u_lb = dr.u_leaf_b;
+        int64_t leaf_chunk = 0;
 
         nodes.reset(cur);
         // a speculative evaluation: the next leapfrog position, handed to the
@@ -913,7 +918,6 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             int status = kTreeOk;
             depth = j + 1;
             const int64_t nleaf = 1ll << j;
-            double u_leaf = 0.0;
             double u_sm = 0.0;    // merge-structured: uniforms of merges [msub & ~63, + 64)
             int64_t msub = 0;     // merges completed in this subtree
             double rsum[DPL];  // momentum sum over the subtree's leaves so far
@@ -921,10 +925,13 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             for (int m = 0; m < DPL; ++m) rsum[m] = 0.0;
 
             for (int64_t n = 0; n < nleaf; ++n) {
-                if (!smerge && (n & (kWave - 1)) == 0)
-                    u_leaf = (n + l < nleaf)
-                                 ? unit53(draw(seed, key_chain, t, kTagLeaf, (uint64_t)j, (uint64_t)(n + l)).w0)
-                                 : 0.0;
+                const int64_t gleaf = nleaf - 1 + n;  // the leaf's number in the iteration
+                if (!smerge && uni((gleaf >> 7) != leaf_chunk)) {
+                    leaf_chunk = gleaf >> 7;
+                    const Block4 b = draw(seed, key_chain, t, kTagTree, 0, (uint64_t)(leaf_chunk * 64 + l));
+                    u_la = unit53(b.w2);
+                    u_lb = unit53(b.w3);
+                }
                 // leapfrog: half kick, drift, gradient, half kick
                 double ph[DPL];
                 if constexpr (Eval::kSpeculative) {
@@ -1049,7 +1056,8 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 } else {
                     // streaming multinomial choice inside the subtree
                     const double lw = logaddexp(logw, lam);
-                    const double u = __shfl(u_leaf, (int)(n & (kWave - 1)));
+                    const int gi = (int)(gleaf & 127);
+                    const double u = __shfl((gi & 1) ? u_lb : u_la, gi >> 1);
                     if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
                         nodes.set_sprop(z);
                         sprop_idx = e + v * (n + 1);

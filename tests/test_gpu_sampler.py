@@ -143,8 +143,13 @@ def test_covtype_first_iterations(sampler, orc, name):
                        num_warmup=0, num_samples=iters, seed=wl.seed, path=2)
     ref = _oracle_chain(orc, X, y, wl, 0, iters)
     # fp32 data: the per-row exp/log/reciprocal run in fp32 (~1e-6 relative
-    # per row), so positions drift apart at the 1e-8 level over the run
-    compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-9 if wl.dtype == "f64" else 1e-6)
+    # per row), so positions drift apart at the 1e-8 level over the run; the
+    # acceptance statistic averages exp(-(H - H0)) over the leaves, and each
+    # row's fp32-evaluated loss carries ~3e-8 absolute error, a random walk of
+    # sqrt(2 N) 3e-8 = 3.2e-5 in H - H0 at N = 581,012: compared within 1.5e-4
+    # (as in the 50-iteration test below)
+    compare_chain(r["samples"][0], r["stats"][0], ref, atol=1e-9 if wl.dtype == "f64" else 1e-6,
+                  accept_atol=None if wl.dtype == "f64" else 1.5e-4)
 
 
 @pytest.mark.parametrize("name", ["covtype_n581012_d55_f64", "covtype_n581012_d55_f32"])

@@ -95,3 +95,21 @@ def test_direction_and_uniform_draws(orc):
         assert stats.kstest(u, "uniform").pvalue > 1e-3
     # the tags keep the streams apart
     assert orc.u_merge(0, 0, 5, 3) != orc.u_leaf(0, 0, 5, 3, 0)
+
+
+def test_tree_draws_come_from_the_documented_words(orc):
+    # reading R8: block b of tag 2 (counter {t, 2 << 32, b, 0}, key {seed,
+    # chain}) holds the direction of doubling b (word 0, low bit), the merge
+    # uniform of doubling b (word 1) and the uniforms of leaves 2b, 2b + 1
+    # (words 2, 3), leaf n of doubling j being number 2^j - 1 + n; the words
+    # are taken from numpy's Philox, not from the oracle's
+    seed, chain, t = 9, 33, 1234
+    u53 = lambda w: float(int(w) >> 11) * 2.0**-53
+    for j in range(12):
+        w = _numpy_block([t, 2 << 32, j, 0], [seed, chain])
+        assert orc.direction(seed, chain, t, j) == (1 if int(w[0]) & 1 else -1)
+        assert orc.u_merge(seed, chain, t, j) == u53(w[1])
+    for j, n in [(0, 0), (1, 0), (1, 1), (2, 3), (6, 0), (7, 0), (7, 127), (9, 300), (20, 12345)]:
+        g = (1 << j) - 1 + n
+        w = _numpy_block([t, 2 << 32, g >> 1, 0], [seed, chain])
+        assert orc.u_leaf(seed, chain, t, j, n) == u53(w[2 + (g & 1)])
