@@ -126,13 +126,22 @@ struct StageRegs {
 
 __device__ __forceinline__ void load_stage(const BatchView& bv, int64_t st, int tid, StageRegs& r)
 {
+    // the piece offsets are recomputed at every stage: hoisted out of the
+    // stage loop they were kept in scratch memory, and each reload waited for
+    // every load issued before it, so the stage's loads went out one by one
+    int opaque_zero;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
+    tid += opaque_zero;
     const int last = kBatchStageRows * bv.stride / 4 - 1;
     const v4f* src = reinterpret_cast<const v4f*>(bv.X + st * kBatchStageRows * bv.stride);
+    // the labels first: whatever their address waits for (a register
+    // reloaded from scratch waits for every load before it) is then not the
+    // stage's pieces
+    if (tid < kBatchStageRows / 4) r.y = reinterpret_cast<const uint32_t*>(bv.y + st * kBatchStageRows)[tid];
     // unconditional loads (pieces past the stage re-read its last piece and
     // are not stored), so the loop unrolls into straight-line code
 #pragma unroll
     for (int i = 0; i < kStageVecs; ++i) r.v[i] = src[min(tid + i * kWaves * kWave, last)];
-    if (tid < kBatchStageRows / 4) r.y = reinterpret_cast<const uint32_t*>(bv.y + st * kBatchStageRows)[tid];
 }
 
 // Scatter a stage into the LDS geometry: HBM piece q of a row goes to
@@ -142,6 +151,12 @@ __device__ __forceinline__ void store_stage(const StageRegs& r, int tid, float* 
 {
     using G = Geo<KT>;
     constexpr int last = kBatchStageRows * G::HV - 1;
+    // the destinations are recomputed at every stage (a few integer
+    // instructions): hoisted out of the stage loop they were kept in scratch
+    // memory, and each stage waited for their reload before its stores
+    int opaque_zero;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
+    tid += opaque_zero;
 #pragma unroll
     for (int i = 0; i < kStageVecs; ++i) {
         const int idx = tid + i * kWaves * kWave;
