@@ -657,14 +657,61 @@ def cpu_all_cores(f, X, y, w, seconds, scale=1.0):
                 sample=f"{n} evaluations, rows in {cores} fixed chunks, {el:.1f}s")
 
 
+def run_standalone_chains(name, d, chains, stream, launches=200):
+    """The potential kernel alone on a per-chain workload: one position for
+    every chain's data set per call (all data sets in one call, as the
+    sampler evaluates them), back-to-back calls of the allocation-free entry
+    point, HIP events around all of them.  The data sets stream from memory
+    at every call; the sampler holds them in LDS for its whole launch."""
+    import torch
+
+    import workloads
+
+    wl = workloads.WORKLOADS[name]
+    rng = np.random.default_rng(3)
+    W = torch.from_numpy(rng.normal(0.0, 0.1, size=(chains, wl.D))).cuda()
+    U = torch.empty(chains, dtype=torch.float64, device="cuda")
+    G = torch.empty((chains, wl.D), dtype=torch.float64, device="cuda")
+    for _ in range(10):
+        d.potential_grad(W, out_U=U, out_grad=G, no_alloc=True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(launches):
+        d.potential_grad(W, out_U=U, out_grad=G, no_alloc=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) * 1e3 / launches
+    es = 8 if wl.dtype == "f64" else 4
+    gbs = chains * (wl.N * wl.D * es + wl.N) / (us * 1e-6) / 1e9
+    log(f"{name}: standalone gradient pass over {chains} data sets {us:.2f} us per call, "
+        f"{chains / us:.1f} M evals/s, {gbs:.0f} GB/s")
+    return dict(workload=name, entry_point="nuts_data_potential_grad_noalloc", positions_per_call=chains,
+                calls=launches,
+                us_per_call=round(us, 3), evals_per_s=round(chains / (us * 1e-6), 1),
+                achieved_gbs=round(gbs, 1),
+                note="per call: one position for each chain's data set, the data sets read from memory; "
+                     "back-to-back, so launch gaps are included")
+
+
 def sub_line(name, s, stream, cpu_seconds):
     """Another workload's line: its own short protocol, roofline and CPU
-    baseline."""
+    baseline; for per-chain data also the standalone gradient pass over the
+    same data sets."""
+    import workloads
+
     data = load_workload(name)
     warmup, steps = SUB_STEPS[name]
     d, res = run_workload(name, data, s, stream, steps=steps, warmup=warmup)
+    standalone = None
+    if workloads.WORKLOADS[name].per_chain_data:
+        standalone = run_standalone_chains(name, d, res["chains"], stream)
+        standalone["sampler_evals_per_s_by_kernel_time"] = round(res["grad_evals"] / res["kernel_seconds"], 1)
     d.free()
     out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in res.items()}
+    if standalone:
+        out["standalone_grad"] = standalone
     out["roofline"] = roofline(res)
     out["cpu_baseline"] = None if cpu_seconds <= 0 else cpu_baseline(name, data, cpu_seconds)
     return out

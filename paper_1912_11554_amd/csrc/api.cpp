@@ -636,7 +636,7 @@ int nuts_data_potential_grad_noalloc(nuts_handle* h, const nuts_data* d, double 
     if (!is_device_ptr(W) || !is_device_ptr(out_U) || !is_device_ptr(out_grad))
         return fail(h, NUTS_EINVAL, "W, out_U and out_grad must be device memory (this entry point copies nothing)");
     const PotentialPlan plan = plan_potential(d->view, K, h->num_cu);
-    const size_t need = (size_t)K * plan.groups_per_item * plan.width * sizeof(double);
+    const size_t need = plan.items ? 0 : (size_t)K * plan.groups_per_item * plan.width * sizeof(double);
     if (need > kStaticScratchBytes)
         return fail(h, NUTS_EINVAL,
                     "K = %lld positions need %zu bytes of partial sums (%d groups of %d doubles each), more than "

@@ -78,6 +78,8 @@ hipError_t launch_to_blocks(const void* X_rowmajor, const uint8_t* y_in, DataVie
 struct PotentialPlan {
     int groups_per_item;  // G
     int width;            // partial_width(D)
+    bool own_cu;          // G * K groups fit the device once: one group a CU
+    bool items;           // many items with few blocks each: one wave an item, no partial rows
 };
 constexpr int kMaxPotentialItems = 65535;
 constexpr int kMaxPotentialGroups = 256;  // groups per item

@@ -223,6 +223,68 @@ __global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave))
     }
 }
 
+// Many items (K >= kItemMinK) of at most kItemMaxBlocks row blocks and
+// D <= 64 (one lane a column): one wavefront an item, four a group.  The
+// wave streams its item's blocks (the next block's loads in flight while the
+// current one is computed), reduces the rows over the wave (column c in lane
+// c) and writes U and grad U itself: no partial rows, no exchange.  With the
+// multi-group kernel such an item took one group of 8 waves, most of them
+// without a block, one group a CU.
+constexpr int kItemWaves = 4;
+constexpr int64_t kItemMaxBlocks = 32;
+constexpr int64_t kItemMinK = 64;
+
+template <typename T, int S, int CPS>
+__global__ void __launch_bounds__(kItemWaves * kWave) potential_items_kernel(DataView dv,
+                                                                             const double* __restrict__ W, int64_t K,
+                                                                             double prior_scale,
+                                                                             double* __restrict__ out_U,
+                                                                             double* __restrict__ out_grad)
+{
+    constexpr int R = BlockShape<T, S>::R;
+    constexpr bool kPipe = !(sizeof(T) == 8 && S == 1);  // fp64 rows of one lane: one register set
+    const int l = lane();
+    const int64_t k = (int64_t)blockIdx.x * kItemWaves + (int)(threadIdx.x / kWave);
+    if (k >= K) return;  // uniform over the wave
+    const int D = dv.D;
+    const int64_t ds = dv.nds > 1 ? k : 0;
+    const T* X = (const T*)dv.X + ds * dv.nb * (int64_t)D * R;
+    const uint8_t* y = dv.y + ds * dv.nb * R;
+    const double q = l < D ? W[k * D + l] : 0.0;
+    double qv[CPS];
+    spread_position<CPS, S>(q, qv);
+    double acc[CPS];
+#pragma unroll
+    for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
+    double loss = 0.0;
+    stream_blocks<T, CPS, S, kPipe, false>(X, y, D, dv.N, dv.nb, 0, 1, qv, acc, loss);
+    const double col = finish_pass<CPS, S>(acc, loss);
+    const double inv_s2 = 1.0 / (prior_scale * prior_scale);
+    const double prior = wave_sum(0.5 * q * q * inv_s2);
+    if (l < D) out_grad[k * D + l] = col + q * inv_s2;
+    if (l == 0) out_U[k] = loss + prior + (double)D * (log(prior_scale) + kHalfLog2Pi);
+}
+
+template <typename T, int S, int CPS>
+hipError_t enqueue_items(const DataView& dv, double prior_scale, const double* W, int64_t K, double* out_U,
+                         double* out_grad, hipStream_t stream)
+{
+    hipLaunchKernelGGL((potential_items_kernel<T, S, CPS>), dim3((unsigned)((K + kItemWaves - 1) / kItemWaves)),
+                       dim3(kItemWaves * kWave), 0, stream, dv, W, K, prior_scale, out_U, out_grad);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t enqueue_items_shape(const DataView& dv, double prior_scale, const double* W, int64_t K,
+                               double* out_U, double* out_grad, hipStream_t stream)
+{
+    const int D = dv.D;
+    if (D <= 8) return enqueue_items<T, 1, 8>(dv, prior_scale, W, K, out_U, out_grad, stream);
+    if (D <= 16) return enqueue_items<T, 1, 16>(dv, prior_scale, W, K, out_U, out_grad, stream);
+    if (D <= 32) return enqueue_items<T, 4, 8>(dv, prior_scale, W, K, out_U, out_grad, stream);
+    return enqueue_items<T, 8, 8>(dv, prior_scale, W, K, out_U, out_grad, stream);
+}
+
 // The 8-wave shapes use at most 128 registers a lane, so two of their groups
 // would fit in one CU, and the dispatcher does place two groups on one CU
 // while another CU idles (the pass over the 581,012 x 55 fp32 set ran about
@@ -232,11 +294,12 @@ constexpr size_t kOwnCuLds = 96 * 1024;
 
 template <typename T, int S, int CPS>
 hipError_t enqueue(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-                   double* partials, double* out_U, double* out_grad, hipStream_t stream)
+                   bool own_cu, double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
     constexpr int NW = pot_waves<T, S, CPS>();
     size_t lds = (size_t)NW * width * sizeof(double);
-    if (NW == 8 && lds < kOwnCuLds) lds = kOwnCuLds;
+    // with more groups than CUs (many items) the groups share CUs instead
+    if (NW == 8 && own_cu && lds < kOwnCuLds) lds = kOwnCuLds;
     const void* k = (const void*)potential_grad_kernel<T, S, CPS>;
     const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -247,11 +310,11 @@ hipError_t enqueue(const DataView& dv, double prior_scale, const double* W, int6
 
 template <typename T>
 hipError_t enqueue_shape(const DataView& dv, double prior_scale, const double* W, int64_t K, int G, int width,
-                         double* partials, double* out_U, double* out_grad, hipStream_t stream)
+                         bool own_cu, double* partials, double* out_U, double* out_grad, hipStream_t stream)
 {
     const int D = dv.D;
 #define NUTS_POT(S_, C_) \
-    return enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, partials, out_U, out_grad, stream)
+    return enqueue<T, S_, C_>(dv, prior_scale, W, K, G, width, own_cu, partials, out_U, out_grad, stream)
     if (D <= 8) NUTS_POT(1, 8);
     if (D <= 16) NUTS_POT(1, 16);
     if (D <= 32) NUTS_POT(4, 8);
@@ -349,6 +412,8 @@ hipError_t static_workspace_setup(int device, hipStream_t stream, void** out)
 
 PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
 {
+    if (dv.D <= 64 && dv.nb <= kItemMaxBlocks && K >= kItemMinK)
+        return PotentialPlan{1, partial_width(dv.D), false, true};
     // one group per CU over all items, never more groups than the blocks give
     // their waves work
     int64_t want = ((int64_t)num_cu + K - 1) / K;
@@ -356,17 +421,20 @@ PotentialPlan plan_potential(const DataView& dv, int64_t K, int num_cu)
     if (want > most) want = most;
     if (want > kMaxPotentialGroups) want = kMaxPotentialGroups;
     if (want < 1) want = 1;
-    return PotentialPlan{(int)want, partial_width(dv.D)};
+    return PotentialPlan{(int)want, partial_width(dv.D), want * K <= num_cu, false};
 }
 
 hipError_t launch_potential_grad(const DataView& dv, double prior_scale, const double* W, int64_t K,
                                  const PotentialPlan& plan, double* partials, double* out_U, double* out_grad,
                                  hipStream_t stream)
 {
+    if (plan.items)
+        return dv.dtype == NUTS_F64 ? enqueue_items_shape<double>(dv, prior_scale, W, K, out_U, out_grad, stream)
+                                    : enqueue_items_shape<float>(dv, prior_scale, W, K, out_U, out_grad, stream);
     if (dv.dtype == NUTS_F64)
-        return enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U,
+        return enqueue_shape<double>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, plan.own_cu, partials, out_U,
                                      out_grad, stream);
-    return enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, partials, out_U, out_grad,
+    return enqueue_shape<float>(dv, prior_scale, W, K, plan.groups_per_item, plan.width, plan.own_cu, partials, out_U, out_grad,
                                 stream);
 }
 

@@ -97,6 +97,38 @@ def test_batched_shared_and_per_chain(sampler, orc):
         assert np.abs(G[k] - g_ref).max() <= 1e-10 * np.abs(g_ref).max()
 
 
+@pytest.mark.parametrize("dt", ["f64", "f32"])
+@pytest.mark.parametrize("N,D,K,per_chain", [(1, 1, 64, True), (77, 8, 100, True), (130, 9, 4096, True),
+                                             (500, 16, 300, False), (1000, 17, 64, True),
+                                             (257, 32, 70, False), (511, 33, 129, True),
+                                             (500, 64, 65, True), (4000, 55, 64, False)])
+def test_many_small_items(sampler, orc, dt, N, D, K, per_chain):
+    # many positions on data sets of at most 32 row blocks (D <= 64): one
+    # wavefront an item; per-chain data sets or one shared set, ragged row
+    # counts, every item compared with the oracle
+    rng = np.random.default_rng(N * 7 + D + K)
+    if per_chain:
+        nsets = K if K <= 130 else 130
+        sets = [workloads.make_logistic(N, D, w_scale=0.7, key=[76, (N * 1000 + D) * 1000 + c], dtype=dt)[:2]
+                for c in range(nsets)]
+        idx = np.arange(K) % nsets
+        X = np.stack([sets[i][0] for i in idx])
+        y = np.stack([sets[i][1] for i in idx])
+    else:
+        X, y, _ = workloads.make_logistic(N, D, w_scale=0.7, key=[77, N * 1000 + D], dtype=dt)
+    W = 0.5 * rng.normal(size=(K, D))
+    say("potential_grad many items", N, D, K, per_chain, dt)
+    d = sampler.data(X, y, per_chain=per_chain)
+    U, G = d.potential_grad(W)
+    d.free()
+    for k in range(K):
+        Xk, yk = (X[k], y[k]) if per_chain else (X, y)
+        U_ref, g_ref = orc.logistic_potential_grad(Xk.astype(np.float64), yk, W[k])
+        assert abs(U[k] - U_ref) <= RTOL[dt] * abs(U_ref), (k, U[k], U_ref)
+        assert (np.abs(G[k] - g_ref) <= grad_tol(Xk, W[k], g_ref, 1.0, RTOL[dt])).all(), k
+        assert np.abs(G[k] - g_ref).max() <= RTOL[dt] * np.abs(g_ref).max(), k
+
+
 @pytest.mark.parametrize("name", ["covtype_n581012_d55_f64", "covtype_n581012_d55_f32"])
 def test_full_size_covtype(sampler, orc, name):
     wl = workloads.WORKLOADS[name]

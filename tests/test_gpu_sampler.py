@@ -94,6 +94,23 @@ def test_many_chains_per_chain_data_subset(sampler, orc):
         compare_chain(r["samples"][c], r["stats"][c], ref)
 
 
+def test_many_chains_all_4096_first_iterations(sampler, orc):
+    # the whole 4,096-chain workload (own 500 x 9 fp64 data set per chain) in
+    # the launch the benchmark times (LDS-resident data, four chains a
+    # group): every chain compared with the oracle for its first 5 iterations
+    wl = workloads.WORKLOADS["chains4096_n500_d9_f64"]
+    X, y = workloads.make_workload(wl)
+    C, iters = X.shape[0], 5
+    assert C == 4096
+    say("sampler per-chain C=4096, first iterations")
+    r = sampler.sample(X, y, step_size=wl.step_size, max_tree_depth=wl.max_tree_depth,
+                       num_warmup=0, num_samples=iters, num_chains=C, seed=wl.seed, per_chain=True)
+    for c in range(C):
+        ref = _oracle_chain(orc, X[c], y[c], wl, c, iters)
+        compare_chain(r["samples"][c], r["stats"][c], ref)
+    assert r["grad_evals"] == sum(int(r["stats"][c]["num_steps"].sum()) + 1 for c in range(C))
+
+
 def test_shared_data_many_chains(sampler, orc):
     wl = workloads.WORKLOADS["logreg_n1000_d11_f64"]
     X, y = workloads.make_workload(wl)
