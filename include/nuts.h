@@ -111,7 +111,10 @@ void nuts_data_free(nuts_handle* h, nuts_data* d);
  * shared data every row of W is evaluated on the same X; with per-chain data
  * row k uses data set k (K must equal num_datasets).  Writes out_U [K] and
  * out_grad [K][D] (fp64).  U and the gradient are accumulated in fp64 also
- * for fp32 X. */
+ * for fp32 X.  Large data sets are split over several workgroups per
+ * position whose partial sums meet in device memory; many small items
+ * (D <= 64, at most 32 row blocks of the layout each, K >= 64) take one
+ * wavefront each. */
 int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_scale,
                              const double* W, int64_t K, double* out_U, double* out_grad);
 
@@ -130,7 +133,10 @@ int nuts_data_potential_grad(nuts_handle* h, const nuts_data* d, double prior_sc
  *     must fit in the array's 8 MiB (G = groups per position, about
  *     num_CUs / K; one group per position for K >= num_CUs): with D <= 64 up
  *     to about 8 000 positions, with D <= 320 about 2 700; larger requests
- *     fail with NUTS_EINVAL and a message giving the sizes;
+ *     fail with NUTS_EINVAL and a message giving the sizes.  Many small items
+ *     (D <= 64, data sets of at most 32 row blocks, K >= 64) are evaluated
+ *     one wavefront an item and use no partial sums, so only K <= 16384
+ *     applies to them;
  *   - every call on one device shares that device's array (each call leaves
  *     the slots it used empty for the next): calls that overlap on one
  *     device (different streams or handles, or host threads) race and give
