@@ -124,39 +124,47 @@ struct StageRegs {
     uint32_t y;
 };
 
+// RECOMPUTE (the sampler kernel, whose nine waves leave 168 registers a
+// lane): the piece offsets are recomputed at every stage.  Hoisted out of the
+// stage loop they were kept in scratch memory there, and each reload waited
+// for every load issued before it, so the stage's loads went out one by one.
+// Kernels with registers to spare keep them (recomputing cost them time).
+template <bool RECOMPUTE>
 __device__ __forceinline__ void load_stage(const BatchView& bv, int64_t st, int tid, StageRegs& r)
 {
-    // the piece offsets are recomputed at every stage: hoisted out of the
-    // stage loop they were kept in scratch memory, and each reload waited for
-    // every load issued before it, so the stage's loads went out one by one
-    int opaque_zero;
-    asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
-    tid += opaque_zero;
+    if constexpr (RECOMPUTE) {
+        int opaque_zero;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
+        tid += opaque_zero;
+    }
     const int last = kBatchStageRows * bv.stride / 4 - 1;
     const v4f* src = reinterpret_cast<const v4f*>(bv.X + st * kBatchStageRows * bv.stride);
-    // the labels first: whatever their address waits for (a register
-    // reloaded from scratch waits for every load before it) is then not the
-    // stage's pieces
-    if (tid < kBatchStageRows / 4) r.y = reinterpret_cast<const uint32_t*>(bv.y + st * kBatchStageRows)[tid];
+    const uint32_t* ysrc = reinterpret_cast<const uint32_t*>(bv.y + st * kBatchStageRows);
+    // with RECOMPUTE the labels first: whatever their address waits for (a
+    // register reloaded from scratch waits for every load before it) is then
+    // not the stage's pieces
+    if (RECOMPUTE && tid < kBatchStageRows / 4) r.y = ysrc[tid];
     // unconditional loads (pieces past the stage re-read its last piece and
     // are not stored), so the loop unrolls into straight-line code
 #pragma unroll
     for (int i = 0; i < kStageVecs; ++i) r.v[i] = src[min(tid + i * kWaves * kWave, last)];
+    if (!RECOMPUTE && tid < kBatchStageRows / 4) r.y = ysrc[tid];
 }
 
 // Scatter a stage into the LDS geometry: HBM piece q of a row goes to
 // residue q / (KP / 4), half q % (KP / 4); the last piece is the tail.
-template <int KT>
+// RECOMPUTE as for load_stage: the destinations are recomputed at every
+// stage (a few integer instructions) instead of reloaded from scratch.
+template <int KT, bool RECOMPUTE>
 __device__ __forceinline__ void store_stage(const StageRegs& r, int tid, float* xs, float* ys)
 {
     using G = Geo<KT>;
     constexpr int last = kBatchStageRows * G::HV - 1;
-    // the destinations are recomputed at every stage (a few integer
-    // instructions): hoisted out of the stage loop they were kept in scratch
-    // memory, and each stage waited for their reload before its stores
-    int opaque_zero;
-    asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
-    tid += opaque_zero;
+    if constexpr (RECOMPUTE) {
+        int opaque_zero;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(opaque_zero));
+        tid += opaque_zero;
+    }
 #pragma unroll
     for (int i = 0; i < kStageVecs; ++i) {
         const int idx = tid + i * kWaves * kWave;
@@ -415,20 +423,20 @@ __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, 
     };
     if (st0 < st1) {
         StageRegs r;
-        load_stage(bv, st0, tid, r);
-        store_stage<KT>(r, tid, xs, ys);
+        load_stage<false>(bv, st0, tid, r);
+        store_stage<KT, false>(r, tid, xs, ys);
     }
     __syncthreads();
     for (int64_t st = st0; st < st1; ++st) {
         const int b = (int)((st - st0) & 1);
         const bool more = st + 1 < st1;
         StageRegs r;
-        if (more) load_stage(bv, st + 1, tid, r);
+        if (more) load_stage<false>(bv, st + 1, tid, r);
         if (st > st0) flush(st - 1, b ^ 1);
         po.row0 = st * kBatchStageRows;
         compute_stage_ll<KT, PRED, SAMPLE>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, live, loss,
                                            rs + (b * kWaves + widx) * kBatchStageRows, po);
-        if (more) store_stage<KT>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
+        if (more) store_stage<KT, false>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
         __syncthreads();
     }
     if (st1 > st0) flush(st1 - 1, (int)((st1 - 1 - st0) & 1));
@@ -437,8 +445,8 @@ __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, 
 // The stage loop over [st0, st1) with double-buffered LDS stages.  Workers
 // (tid = loader index, 0 .. 511) load and compute; a non-worker wave of the
 // same group passes the same workgroup barriers (1 + st1 - st0 of them) and
-// does nothing else.
-template <int KT, bool WORKER>
+// does nothing else.  RECOMPUTE as for load_stage.
+template <int KT, bool WORKER, bool RECOMPUTE = false>
 __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int64_t st1, int tid, float* xs,
                                            float* ys, const WaveQ& Q, WaveAcc& acc)
 {
@@ -447,17 +455,17 @@ __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int
     } else {
         if (st0 < st1) {
             StageRegs r;
-            load_stage(bv, st0, tid, r);
-            store_stage<KT>(r, tid, xs, ys);
+            load_stage<RECOMPUTE>(bv, st0, tid, r);
+            store_stage<KT, RECOMPUTE>(r, tid, xs, ys);
         }
         __syncthreads();
         for (int64_t st = st0; st < st1; ++st) {
             const int b = (int)((st - st0) & 1);
             const bool more = st + 1 < st1;
             StageRegs r;
-            if (more) load_stage(bv, st + 1, tid, r);
+            if (more) load_stage<RECOMPUTE>(bv, st + 1, tid, r);
             compute_stage<KT>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, acc, tid >= 4 * kWave);
-            if (more) store_stage<KT>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
+            if (more) store_stage<KT, RECOMPUTE>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
             __syncthreads();
         }
     }

@@ -601,7 +601,7 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = tv[k];
         WaveAcc acc;
         batch::zero(acc);
-        batch::stage_loop<KT, true>(c.bv, c.st0, c.st1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
+        batch::stage_loop<KT, true, true>(c.bv, c.st0, c.st1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
         store_partials<KT, true>(c.bv, acc, widx, c.pw, c.P + (tile_base + c.i) * rstride,
                                  c.L + (tile_base + c.i) * kBatchTileChains);
         sampler::drain_memory_ops();
