@@ -708,6 +708,17 @@ def sub_line(name, s, stream, cpu_seconds):
     if workloads.WORKLOADS[name].per_chain_data:
         standalone = run_standalone_chains(name, d, res["chains"], stream)
         standalone["sampler_evals_per_s_by_kernel_time"] = round(res["grad_evals"] / res["kernel_seconds"], 1)
+        # the share of the sampler's vector instructions per evaluation that
+        # are not the evaluation itself (the tree step, the draws), from the
+        # recorded SQ_INSTS_VALU of both kernels on this workload
+        items = recorded_traffic("potential_items_kernel", name, res["chains"])
+        sampler_rec = recorded_traffic(res["kernel"], name, res["grad_evals"])
+        if items and sampler_rec and "valu_instructions_per_eval" in items and \
+                "valu_instructions_per_eval" in sampler_rec:
+            vi, vs = items["valu_instructions_per_eval"], sampler_rec["valu_instructions_per_eval"]
+            standalone["valu_instructions_per_eval"] = vi
+            standalone["sampler_valu_instructions_per_eval"] = vs
+            standalone["sampler_instruction_overhead"] = round(1.0 - vi / vs, 4)
     d.free()
     out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in res.items()}
     if standalone:

@@ -34,6 +34,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # header (the include directive lines are followed, nothing else).
 KERNEL_UNITS = {
     "potential_grad_kernel": ("potential.hip",),
+    "potential_items_kernel": ("potential.hip",),
     "sampler_grid_kernel": ("sampler.hip", "sampler_f32.hip", "sampler_f64.hip", "sampler_ext_f32.hip",
                             "sampler_ext_f64.hip"),
     "sampler_wave_kernel": ("sampler.hip", "sampler_f32.hip", "sampler_f64.hip", "sampler_ext_f32.hip",
@@ -126,6 +127,11 @@ STANDALONE_DISPATCH = {
     "covtype_n581012_d55_f32": "potential_grad_kernel<float, 8, 8>",
     "covtype_n581012_d55_f64": "potential_grad_kernel<double, 8, 8>",
 }
+# the standalone pass beside a per-chain workload's line: one call, one
+# position for every chain's data set
+ITEMS_DISPATCH = {
+    "chains4096_n500_d9_f64": "potential_items_kernel<double, 1, 16>",
+}
 KIB = 1024
 TRAFFIC_NOTE = ("HBM bytes per gradient evaluation of each workload's timed dispatch in a run of bench.py "
                 "(--copy-mb 256) under rocprofv3 --pmc: FETCH_SIZE and WRITE_SIZE (KiB, summed over instances) "
@@ -192,6 +198,10 @@ def traffic_record(fetch_db: str, write_db: str, bench_line: dict) -> dict:
             add(kernel, workload, name, evals)
         if workload in STANDALONE_DISPATCH and bench_line.get("standalone_grad") is not None:
             add("potential_grad_kernel", workload, STANDALONE_DISPATCH[workload], 1)
+    for workload, sub in (bench_line.get("workloads") or {}).items():
+        sa = sub.get("standalone_grad")
+        if sa and workload in ITEMS_DISPATCH:
+            add("potential_items_kernel", workload, ITEMS_DISPATCH[workload], sa["positions_per_call"])
     return entries
 
 
