@@ -300,14 +300,24 @@ __device__ __forceinline__ void ll_terms(float eta, float sgn, float& loss, floa
     p1 = sgn > 0.0f ? sig_t : sig_mt;
 }
 
-// Sum over the 16 positions of a wave (lanes l, l ^ 1, ..., l ^ 15 share the
-// row group l / 16); every lane of the 16 gets the same bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v)
+{
+    // every pattern used here reads a lane of the same row with all rows and
+    // banks enabled
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over the 16 positions of a wave (lanes 16 g .. 16 g + 15, one DPP row,
+// share the row group g): pair butterflies inside the row on DPP moves, so no
+// LDS instruction (as cross-lane shuffles these were over half of the kernel's
+// LDS instructions); every lane of the 16 gets the same bits.
 __device__ __forceinline__ float sum16(float v)
 {
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
-    v += __shfl_xor(v, 8);
+    v += dpp_f32<kDppXor1>(v);
+    v += dpp_f32<kDppXor2>(v);
+    v += dpp_f32<kDppHalfMirror>(v);
+    v += dpp_f32<kDppMirror>(v);
     return v;
 }
 
@@ -340,7 +350,7 @@ __device__ __forceinline__ void predict_rows(const PredictOut& po, int64_t r0, c
 template <int KT, bool PRED, bool SAMPLE>
 __device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, const float* __restrict__ ys,
                                                  const WaveQ& Q, float live, double& loss, float* rs,
-                                                 const PredictOut& po)
+                                                 const PredictOut& po, bool tail)
 {
     using G = Geo<KT>;
     const int l = lane();
@@ -364,12 +374,14 @@ __device__ __forceinline__ void compute_stage_ll(const float* __restrict__ xs, c
                 e1 = mfma(a1[i], Q.q[4 * t + i], e1);
             }
         }
+        if (tail) {  // uniform: the data has tail columns
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const v4f xr0 = *reinterpret_cast<const v4f*>(x0 + (4 * jj + r) * G::RS + 16 * G::GS);
-            const v4f xr1 = *reinterpret_cast<const v4f*>(x1 + (4 * jj + r) * G::RS + 16 * G::GS);
-            e0[r] += ((xr0[0] * Q.qt[0] + xr0[1] * Q.qt[1]) + xr0[2] * Q.qt[2]) + xr0[3] * Q.qt[3];
-            e1[r] += ((xr1[0] * Q.qt[0] + xr1[1] * Q.qt[1]) + xr1[2] * Q.qt[2]) + xr1[3] * Q.qt[3];
+            for (int r = 0; r < 4; ++r) {
+                const v4f xr0 = *reinterpret_cast<const v4f*>(x0 + (4 * jj + r) * G::RS + 16 * G::GS);
+                const v4f xr1 = *reinterpret_cast<const v4f*>(x1 + (4 * jj + r) * G::RS + 16 * G::GS);
+                e0[r] += ((xr0[0] * Q.qt[0] + xr0[1] * Q.qt[1]) + xr0[2] * Q.qt[2]) + xr0[3] * Q.qt[3];
+                e1[r] += ((xr1[0] * Q.qt[0] + xr1[1] * Q.qt[1]) + xr1[2] * Q.qt[2]) + xr1[3] * Q.qt[3];
+            }
         }
         const v4f s0 = *reinterpret_cast<const v4f*>(ys + tp * kTileRows + 4 * jj);
         const v4f s1 = *reinterpret_cast<const v4f*>(ys + (tp + 1) * kTileRows + 4 * jj);
@@ -435,7 +447,7 @@ __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, 
         if (st > st0) flush(st - 1, b ^ 1);
         po.row0 = st * kBatchStageRows;
         compute_stage_ll<KT, PRED, SAMPLE>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, live, loss,
-                                           rs + (b * kWaves + widx) * kBatchStageRows, po);
+                                           rs + (b * kWaves + widx) * kBatchStageRows, po, bv.tc > 0);
         if (more) store_stage<KT, false>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
         __syncthreads();
     }
