@@ -200,7 +200,7 @@ __device__ __forceinline__ void store_stage(const StageRegs& r, int tid, float* 
 // at the stage barrier.
 template <int KT>
 __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, const float* __restrict__ ys,
-                                              const WaveQ& Q, WaveAcc& acc, bool flip)
+                                              const WaveQ& Q, WaveAcc& acc, bool flip, int pair_lo, int pair_hi)
 {
     using G = Geo<KT>;
     const int l = lane();
@@ -213,6 +213,7 @@ __device__ __forceinline__ void compute_stage(const float* __restrict__ xs, cons
 #pragma unroll 1
     for (int step = 0; step < kTiles; step += 2) {
         const int tp = flip ? kTiles - 2 - step : step;
+        if (tp / 2 < pair_lo || tp / 2 >= pair_hi) continue;  // uniform: another group's rows
         const float* x0 = xs + tp * kTileRows * G::RS;
         const float* x1 = x0 + kTileRows * G::RS;
         v4f e0 = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -454,14 +455,28 @@ __device__ __forceinline__ void stage_loop_ll(const BatchView& bv, int64_t st0, 
     if (st1 > st0) flush(st1 - 1, (int)((st1 - 1 - st0) & 1));
 }
 
-// The stage loop over [st0, st1) with double-buffered LDS stages.  Workers
-// (tid = loader index, 0 .. 511) load and compute; a non-worker wave of the
-// same group passes the same workgroup barriers (1 + st1 - st0 of them) and
-// does nothing else.  RECOMPUTE as for load_stage.
+// A group's rows in halves of stages (pairs of 16-row tiles, 32 rows):
+// the 2 ns halves split evenly over the groups, so that no group has more
+// than one half more than another (whole stages left 53 of 128 groups a
+// whole stage more).  A stage whose halves two groups share is loaded by
+// both, each computing its own.
+__host__ __device__ inline void group_halves(int64_t ns, int64_t i, int64_t groups, int64_t* h0, int64_t* h1)
+{
+    *h0 = i * 2 * ns / groups;
+    *h1 = (i + 1) * 2 * ns / groups;
+}
+
+// The stage loop over the halves [h0, h1) (stages h0 / 2 .. (h1 - 1) / 2)
+// with double-buffered LDS stages.  Workers (tid = loader index, 0 .. 511)
+// load and compute; a non-worker wave of the same group passes the same
+// workgroup barriers (one more than the stages) and does nothing else.
+// RECOMPUTE as for load_stage.
 template <int KT, bool WORKER, bool RECOMPUTE = false>
-__device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int64_t st1, int tid, float* xs,
+__device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t h0, int64_t h1, int tid, float* xs,
                                            float* ys, const WaveQ& Q, WaveAcc& acc)
 {
+    const int64_t st0 = h0 / 2;
+    const int64_t st1 = h1 > h0 ? (h1 + 1) / 2 : st0;
     if constexpr (!WORKER) {
         for (int64_t st = st0; st <= st1; ++st) __syncthreads();
     } else {
@@ -476,7 +491,10 @@ __device__ __forceinline__ void stage_loop(const BatchView& bv, int64_t st0, int
             const bool more = st + 1 < st1;
             StageRegs r;
             if (more) load_stage<RECOMPUTE>(bv, st + 1, tid, r);
-            compute_stage<KT>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, acc, tid >= 4 * kWave);
+            // the halves of this stage that are the group's
+            const int lo = (int)(h0 > 2 * st ? h0 - 2 * st : 0);
+            const int hi = (int)(h1 < 2 * st + 2 ? h1 - 2 * st : 2);
+            compute_stage<KT>(xs + b * kStageBuf, ys + b * kBatchStageRows, Q, acc, tid >= 4 * kWave, lo, hi);
             if (more) store_stage<KT, RECOMPUTE>(r, tid, xs + (b ^ 1) * kStageBuf, ys + (b ^ 1) * kBatchStageRows);
             __syncthreads();
         }

@@ -150,9 +150,9 @@ __global__ void __launch_bounds__(batch::kWaves * kWave, 1) batch_pass_kernel(Ba
 
     WaveAcc acc;
     batch::zero(acc);
-    const int64_t st0 = (int64_t)g * bv.ns / groups;
-    const int64_t st1 = (int64_t)(g + 1) * bv.ns / groups;
-    batch::stage_loop<KT, true>(bv, st0, st1, (int)threadIdx.x, xs, ys, Q, acc);
+    int64_t h0, h1;
+    batch::group_halves(bv.ns, g, groups, &h0, &h1);
+    batch::stage_loop<KT, true>(bv, h0, h1, (int)threadIdx.x, xs, ys, Q, acc);
     const int64_t base = (int64_t)t * groups + g;
     store_partials<KT, false>(bv, acc, widx, pw, P + base * kBatchTileChains * pw, L + base * kBatchTileChains);
 }
@@ -440,7 +440,7 @@ struct BatchCtx {
     BatchView bv;
     int tiles, groups;
     int t, i;  // this group's tile and index in the tile
-    int64_t st0, st1;
+    int64_t h0, h1;  // this group's halves of stages (group_halves)
     int pw;
     float* qbuf;
     float* P;
@@ -577,7 +577,7 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
     if (LEADER) {
         WaveQ Q;
         WaveAcc acc;
-        batch::stage_loop<KT, false>(c.bv, c.st0, c.st1, 0, sh.xs, sh.ys, Q, acc);
+        batch::stage_loop<KT, false>(c.bv, c.h0, c.h1, 0, sh.xs, sh.ys, Q, acc);
     } else {
         const int widx = wave - 1;
         const int m = l & 15;
@@ -601,7 +601,7 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         for (int k = 0; k < batch::kTail; ++k) Q.qt[k] = tv[k];
         WaveAcc acc;
         batch::zero(acc);
-        batch::stage_loop<KT, true, true>(c.bv, c.st0, c.st1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
+        batch::stage_loop<KT, true, true>(c.bv, c.h0, c.h1, (int)threadIdx.x - kWave, sh.xs, sh.ys, Q, acc);
         store_partials<KT, true>(c.bv, acc, widx, c.pw, c.P + (tile_base + c.i) * rstride,
                                  c.L + (tile_base + c.i) * kBatchTileChains);
         sampler::drain_memory_ops();
@@ -746,8 +746,7 @@ __global__ void __launch_bounds__(kGroupWaves * kWave, 1) sampler_batch_kernel(S
     c.groups = groups;
     c.t = (int)(blockIdx.x / groups);
     c.i = (int)(blockIdx.x % groups);
-    c.st0 = (int64_t)c.i * bv.ns / groups;
-    c.st1 = (int64_t)(c.i + 1) * bv.ns / groups;
+    batch::group_halves(bv.ns, c.i, groups, &c.h0, &c.h1);
     c.pw = 64 * DPL;
     c.qbuf = qbuf;
     c.P = P;
