@@ -100,14 +100,20 @@ __global__ void __launch_bounds__((pot_waves<T, S, CPS>() * kWave))
     const T* X = (const T*)dv.X + ds * dv.nb * (int64_t)D * R;
     const uint8_t* y = dv.y + ds * dv.nb * R;
 
+    // the first block's loads go out before the position is read, so that
+    // the two round trips overlap
+    const int64_t first = (int64_t)g * NW + wave;
+    BlockRegs<T, CPS, S> a;
+    if (first < dv.nb) a = load_block<T, CPS, S, pot_mask<S, CPS>()>(X + first * D * R, y + first * R, D);
     double qv[CPS];
     spread_position_lds<CPS, S>(W + k * D, D, qv);
     double acc[CPS];
 #pragma unroll
     for (int c = 0; c < CPS; ++c) acc[c] = 0.0;
     double loss = 0.0;
-    stream_blocks<T, CPS, S, pot_pipe<T, S, CPS>(), pot_mask<S, CPS>()>(
-        X, y, D, dv.N, dv.nb, (int64_t)g * NW + wave, (int64_t)G * NW, qv, acc, loss);
+    if (first < dv.nb)
+        stream_blocks_from<T, CPS, S, pot_pipe<T, S, CPS>(), pot_mask<S, CPS>()>(
+            a, X, y, D, dv.N, dv.nb, first, (int64_t)G * NW, qv, acc, loss);
 
     double* row = part + wave * width;
     if constexpr (S <= 8 && CPS == 8) {
