@@ -162,6 +162,19 @@ __device__ __forceinline__ double wave_sum(double v)
     return ((readlane_f64(v, 0) + readlane_f64(v, 16)) + readlane_f64(v, 32)) + readlane_f64(v, 48);
 }
 
+// wave_sum for values that are zero outside lanes 0..15 when `one_row` (a
+// wave-uniform flag): then the first row's sum is the whole sum (adding the
+// other rows' zeros changes at most the sign of a zero result).
+__device__ __forceinline__ double wave_sum_rows(double v, bool one_row)
+{
+    v += pair_move<1>(v);
+    v += pair_move<2>(v);
+    v += pair_move<4>(v);
+    v += pair_move<8>(v);
+    if (one_row) return readlane_f64(v, 0);
+    return ((readlane_f64(v, 0) + readlane_f64(v, 16)) + readlane_f64(v, 32)) + readlane_f64(v, 48);
+}
+
 // ---------------------------------------------------------------------------
 // Logistic row terms.  With s = 1 - 2y and t = s * eta, the row's negative
 // log-likelihood is softplus(t) >= 0 and d/d eta of it is s * sigmoid(t); both
@@ -296,6 +309,22 @@ __device__ __forceinline__ double logaddexp(double a, double b)
     const double e = exp_nonpos(-fabs(a - b));
     const double u = 1.0 + e;
     return fmax(a, b) + log1p_unit(e, u, recip(u));
+}
+
+// logaddexp(a, b) and b's share e^b / (e^a + e^b) of the sum, both from the
+// one exponential: with e = e^-|a - b| the share is 1 / (1 + e) when b >= a
+// and e / (1 + e) otherwise (1 when a = -inf; b is finite).
+__device__ __forceinline__ double logaddexp_share(double a, double b, double& share_b)
+{
+    if (a == -INFINITY) {
+        share_b = 1.0;
+        return b;
+    }
+    const double e = exp_nonpos(-fabs(a - b));
+    const double u = 1.0 + e;
+    const double inv = recip(u);
+    share_b = b >= a ? inv : e * inv;
+    return fmax(a, b) + log1p_unit(e, u, inv);
 }
 
 }  // namespace nuts

@@ -126,20 +126,12 @@ struct EdgeNodes<DPL, true> {
     __device__ Node<DPL> get_prop() const { return load(kProp); }
 };
 
-template <int DPL>
-__device__ __forceinline__ double dot3(const double (&a)[DPL], const double (&b)[DPL], const double (&c)[DPL])
-{
-    double s = 0.0;
-#pragma unroll
-    for (int m = 0; m < DPL; ++m) s += a[m] * b[m] * c[m];
-    return wave_sum(s);
-}
-
 // Endpoint U-turn test on time-ordered ends: (a, b) are the first- and
-// last-generated nodes of a subtree built in direction v.
+// last-generated nodes of a subtree built in direction v.  one_row: D <= 16
+// (the lanes past D hold zeros, see wave_sum_rows).
 template <int DPL>
 __device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (&pa)[DPL], const double (&qb)[DPL],
-                                         const double (&pb)[DPL], int v, const double (&im)[DPL])
+                                         const double (&pb)[DPL], int v, const double (&im)[DPL], bool one_row)
 {
     double sl = 0.0, sr = 0.0;
 #pragma unroll
@@ -150,8 +142,8 @@ __device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (
         sl += dq * im[m] * pL;
         sr += dq * im[m] * pR;
     }
-    const double dl = wave_sum(sl);
-    const double dr = wave_sum(sr);
+    const double dl = wave_sum_rows(sl, one_row);
+    const double dr = wave_sum_rows(sr, one_row);
     return uni((dl < 0.0) || (dr < 0.0));
 }
 
@@ -159,7 +151,7 @@ __device__ __forceinline__ bool is_uturn(const double (&qa)[DPL], const double (
 // with momentum sum rho turns iff rho . M^-1 p <= 0 at either end.
 template <int DPL>
 __device__ __forceinline__ bool is_uturn_gen(const double (&rho)[DPL], const double (&pa)[DPL],
-                                             const double (&pb)[DPL], const double (&im)[DPL])
+                                             const double (&pb)[DPL], const double (&im)[DPL], bool one_row)
 {
     double sa = 0.0, sb = 0.0;
 #pragma unroll
@@ -167,8 +159,8 @@ __device__ __forceinline__ bool is_uturn_gen(const double (&rho)[DPL], const dou
         sa += rho[m] * im[m] * pa[m];
         sb += rho[m] * im[m] * pb[m];
     }
-    const double da = wave_sum(sa);
-    const double db = wave_sum(sb);
+    const double da = wave_sum_rows(sa, one_row);
+    const double db = wave_sum_rows(sb, one_row);
     return uni((da <= 0.0) || (db <= 0.0));
 }
 
@@ -794,6 +786,8 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
     bool act[DPL];
 #pragma unroll
     for (int m = 0; m < DPL; ++m) act[m] = l + 64 * m < D;
+    // every dimension in the first 16 lanes: the tree's sums take one row
+    const bool one_row = uni(D <= 16);
     const int maxd = A.max_depth;
     double eps = A.step_size;
     const uint64_t seed = A.seed;
@@ -881,7 +875,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             cur.p[m] = act[m] ? dr.xi[m] / sqrt(im[m]) : 0.0;
             kin += im[m] * cur.p[m] * cur.p[m];
         }
-        const double H0 = cur.U + 0.5 * wave_sum(kin);
+        const double H0 = cur.U + 0.5 * wave_sum_rows(kin, one_row);
         double rho_traj[DPL];  // momentum sum over the trajectory's points
 #pragma unroll
         for (int m = 0; m < DPL; ++m) rho_traj[m] = cur.p[m];
@@ -990,7 +984,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     for (int m = 0; m < DPL; ++m) rsum[m] += z.p[m];
                 }
 
-                const double dH = (z.U + 0.5 * wave_sum(k2)) - H0;
+                const double dH = (z.U + 0.5 * wave_sum_rows(k2, one_row)) - H0;
                 if (dH == dH) sum_acc += dH > 0.0 ? exp_nonpos(-dH) : 1.0;
                 if (uni(!(dH <= 1000.0))) {
                     status = kTreeDivergent;
@@ -1018,8 +1012,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                         ++msub;
                         const double* lv = stk + (int64_t)k2 * 3 * D;
                         const double* sc = stk_sc + 3 * k2;
-                        const double lw = logaddexp(sc[0], clw);
-                        if (!uni(um < exp_nonpos(clw - lw))) {  // clw <= lw
+                        double share;  // the later block's share of the weight
+                        const double lw = logaddexp_share(sc[0], clw, share);
+                        if (!uni(um < share)) {
 #pragma unroll
                             for (int m = 0; m < DPL; ++m) {
                                 cp.q[m] = act[m] ? lv[l + 64 * m] : 0.0;
@@ -1055,10 +1050,11 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     }
                 } else {
                     // streaming multinomial choice inside the subtree
-                    const double lw = logaddexp(logw, lam);
+                    double share;  // the leaf's share of the subtree's weight
+                    const double lw = logaddexp_share(logw, lam, share);
                     const int gi = (int)(gleaf & 127);
                     const double u = __shfl((gi & 1) ? u_lb : u_la, gi >> 1);
-                    if (uni(u < exp_nonpos(lam - lw))) {  // lam <= lw
+                    if (uni(u < share)) {
                         nodes.set_sprop(z);
                         sprop_idx = e + v * (n + 1);
                     }
@@ -1095,9 +1091,9 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                             double rho[DPL];
 #pragma unroll
                             for (int m = 0; m < DPL; ++m) rho[m] = rsum[m] - sq[m];
-                            t_ = is_uturn_gen<DPL>(rho, sp, z.p, im);
+                            t_ = is_uturn_gen<DPL>(rho, sp, z.p, im, one_row);
                         } else {
-                            t_ = is_uturn<DPL>(sq, sp, z.q, z.p, v, im);
+                            t_ = is_uturn<DPL>(sq, sp, z.q, z.p, v, im, one_row);
                         }
                         if (t_) {
                             turned = true;
@@ -1138,11 +1134,12 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 const Node<DPL> other = nodes.edge(v < 0);
                 const Node<DPL>& le = v > 0 ? other : z;
                 const Node<DPL>& ri = v > 0 ? z : other;
-                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, le.p, ri.p, im)
-                                : is_uturn<DPL>(le.q, le.p, ri.q, ri.p, 1, im);
+                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, le.p, ri.p, im, one_row)
+                                : is_uturn<DPL>(le.q, le.p, ri.q, ri.p, 1, im, one_row);
             } else {
-                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, nodes.left.p, nodes.right.p, im)
-                                : is_uturn<DPL>(nodes.left.q, nodes.left.p, nodes.right.q, nodes.right.p, 1, im);
+                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, nodes.left.p, nodes.right.p, im, one_row)
+                                : is_uturn<DPL>(nodes.left.q, nodes.left.p, nodes.right.q, nodes.right.p, 1, im,
+                                                one_row);
             }
             if (traj_turn) {
                 turning = 1;
