@@ -99,7 +99,10 @@ __device__ __noinline__ double momentum_normal(uint64_t seed, uint64_t chain, ui
     const double ub = unit53(second_pair ? b.w3 : b.w1);
     const double r = sqrt(-2.0 * log(1.0 - ua));
     const double th = 6.283185307179586476925286766559 * ub;
-    return (i & 1) ? r * sin(th) : r * cos(th);
+    // both from one argument reduction (the lanes of a wave want either)
+    double sn, cs;
+    sincos(th, &sn, &cs);
+    return (i & 1) ? r * sn : r * cs;
 }
 
 // ---------------------------------------------------------------------------

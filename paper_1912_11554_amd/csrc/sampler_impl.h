@@ -1008,7 +1008,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                                        ? unit53(draw(seed, key_chain, t, kTagSubMerge, (uint64_t)j,
                                                      (uint64_t)(msub + l)).w0)
                                        : 0.0;
-                        const double um = __shfl(u_sm, (int)(msub & (kWave - 1)));
+                        const double um = readlane_f64(u_sm, (int)(msub & (kWave - 1)));
                         ++msub;
                         const double* lv = stk + (int64_t)k2 * 3 * D;
                         const double* sc = stk_sc + 3 * k2;
@@ -1053,7 +1053,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                     double share;  // the leaf's share of the subtree's weight
                     const double lw = logaddexp_share(logw, lam, share);
                     const int gi = (int)(gleaf & 127);
-                    const double u = __shfl((gi & 1) ? u_lb : u_la, gi >> 1);
+                    const double u = readlane_f64((gi & 1) ? u_lb : u_la, gi >> 1);
                     if (uni(u < share)) {
                         nodes.set_sprop(z);
                         sprop_idx = e + v * (n + 1);
@@ -1114,7 +1114,7 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
                 break;
             }
             // biased progressive choice between trajectory and new subtree
-            const double um = __shfl(u_merge, j);
+            const double um = readlane_f64(u_merge, j);
             const double dw = logw - logw_traj;
             if (uni(um < (dw >= 0.0 ? 1.0 : exp_nonpos(dw)))) {
                 nodes.accept_sprop();
