@@ -377,14 +377,14 @@ def roofline(res):
                 "valu_instructions_per_eval": traffic["valu_instructions_per_eval"],
                 "bytes_per_eval": res["bytes_per_eval"], "algorithmic_gbs": round(res["achieved_gbs"], 1)}
     if kernel == "sampler_wave_kernel":
-        # no instruction count recorded for this build of the kernel: the
+        # no instruction count recorded for these kernel sources: the
         # algorithmic flops (4 N D per evaluation) against the vector peak of
         # the kernel's arithmetic type; the data sit in LDS, so HBM is no bound
         peak = VECTOR_PEAK_TFLOPS[res["dtype"]]
         return {"kernel": kernel, "bound": "alu", "achieved": round(res["achieved_tflops"], 3), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(res["achieved_tflops"] / peak, 4),
                 "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
-                "flops_per_eval": res["flops_per_eval"], "note": "no instruction count recorded for this build"}
+                "flops_per_eval": res["flops_per_eval"], "note": "no instruction count recorded for these kernel sources"}
     return {"kernel": kernel, "bound": "hbm", "achieved": round(res["achieved_gbs"], 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(res["achieved_gbs"] / HBM_PEAK_GBS, 4),
             "traffic": traffic and traffic["bytes"], "traffic_detail": traffic,
@@ -759,7 +759,7 @@ def main():
     ap.add_argument("--hmm-only", action="store_true", help="run the HMM measurement alone")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
