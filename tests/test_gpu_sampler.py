@@ -79,6 +79,20 @@ def test_wide_models(sampler, orc, D, path):
     compare_chain(r["samples"][0], r["stats"][0], ref)
 
 
+@pytest.mark.parametrize("D", [16, 17])
+@pytest.mark.parametrize("path", [1, 2])
+def test_tree_sums_either_side_of_one_row(sampler, orc, D, path):
+    # with D <= 16 the tree's sums over dimensions take the first 16 lanes
+    # only; D = 16 and D = 17 sit either side of that switch
+    N = 400
+    X, y, _ = workloads.make_logistic(N, D, w_scale=0.5, key=[62, D])
+    say("sampler one-row boundary", N, D, "path", path)
+    r = sampler.sample(X, y, step_size=0.05, max_tree_depth=6, num_warmup=2, num_samples=10, seed=11,
+                       path=path)
+    ref = orc.nuts(X, y, step_size=0.05, max_tree_depth=6, num_warmup=2, num_samples=10, seed=11)
+    compare_chain(r["samples"][0], r["stats"][0], ref)
+
+
 def test_many_chains_per_chain_data_subset(sampler, orc):
     # 256 chains of the 4096-chain workload (own data per chain); every chain
     # compared with the oracle for its first 50 iterations
