@@ -613,15 +613,20 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
     }
     __syncthreads();  // every group of the tile is in
     const int status = sh.cmd;
-    if (host) {
-        // this wave's share of the groups, in group order
+    if (LEADER && host) {
+        // the leader keeps its registers for the tree state (sixteen loads in
+        // flight would push it into scratch memory): its row of sums is zero
+#pragma unroll
+        for (int mm = 0; mm <= DPL; ++mm) sh.red[0][mm * 64 + l] = 0.0;
+    } else if (host) {
+        // this worker's share of the groups, in group order
         const float* src = c.P + tile_base * rstride + (int64_t)c.i * c.pw;
         const double* lsrc = c.L + tile_base * kBatchTileChains + c.i;
         // Lane l adds columns 4 l .. 4 l + 3 with 16-byte loads at agent
         // scope (buffer loads with the sc1 bit); every load of a wave's share
-        // in flight at once: one round trip for up to 16 groups per wave (144
-        // groups of 9 waves); a group past the last re-reads the wave's first
-        // group and is not added.  (4-byte loads of the same rows took three
+        // in flight at once: one round trip for up to 16 groups per wave (128
+        // groups of the 8 workers); a group past the last re-reads the wave's
+        // first group and is not added.  (4-byte loads of the same rows took three
         // times as long: the gather is bound by the count of uncached
         // requests, not by bytes.)
         const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -631,19 +636,20 @@ __device__ int batch_collective(const BatchCtx& c, BatchShared<DPL>& sh, unsigne
         double s4[4] = {0.0, 0.0, 0.0, 0.0};
         double sl = 0.0;
         constexpr int B = 16;
-        for (int g0 = wave; g0 < c.groups; g0 += B * kGroupWaves) {
+        constexpr int NWK = kGroupWaves - 1;  // the workers
+        for (int g0 = wave - 1; g0 < c.groups; g0 += B * NWK) {
             batch::v4f v[B];
             double lv[B];
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const int gg = g0 + b * kGroupWaves;
+                const int gg = g0 + b * NWK;
                 const int gq = gg < c.groups ? gg : g0;
                 v[b] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)((gq * rstride + 4 * lc) * 4), 0, kCachePolicyAgent);
                 lv[b] = l == 0 ? sampler::load_shared(lsrc + (int64_t)gq * kBatchTileChains) : 0.0;
             }
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                if (g0 + b * kGroupWaves < c.groups) {
+                if (g0 + b * NWK < c.groups) {
 #pragma unroll
                     for (int k = 0; k < 4; ++k) s4[k] += (double)v[b][k];
                     sl += lv[b];
