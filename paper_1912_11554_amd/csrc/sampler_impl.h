@@ -1130,12 +1130,15 @@ __device__ void run_chain(const SamplerArgs& A, Eval& ev, int64_t chain, double*
             }
             bool traj_turn;
             if constexpr (Eval::kNodesInLds) {
-                // the edge just extended is z, the other one is read back
+                // the edge just extended is z, the other one is read back; the
+                // pair (other, z) is the trajectory's ends in the order of a
+                // subtree built in direction v, which is_uturn puts in time
+                // order element by element (is_uturn_gen is symmetric in its
+                // ends).  (References chosen between the two nodes at run
+                // time put both in scratch memory.)
                 const Node<DPL> other = nodes.edge(v < 0);
-                const Node<DPL>& le = v > 0 ? other : z;
-                const Node<DPL>& ri = v > 0 ? z : other;
-                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, le.p, ri.p, im, one_row)
-                                : is_uturn<DPL>(le.q, le.p, ri.q, ri.p, 1, im, one_row);
+                traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, other.p, z.p, im, one_row)
+                                : is_uturn<DPL>(other.q, other.p, z.q, z.p, v, im, one_row);
             } else {
                 traj_turn = gen ? is_uturn_gen<DPL>(rho_traj, nodes.left.p, nodes.right.p, im, one_row)
                                 : is_uturn<DPL>(nodes.left.q, nodes.left.p, nodes.right.q, nodes.right.p, 1, im,
